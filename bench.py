@@ -1,0 +1,242 @@
+#!/usr/bin/env python3
+"""Benchmark: one paper-scale PPO optimizer step on one MI355X.
+
+Workload: the full optimizer step of OpenAI Five's method at the paper's LSTM
+size -- GAE over 128 segments of 256 steps, the cut into 2048 samples of 16
+steps, the 4096-unit LSTM forward pass (input width 4096), four categorical
+heads (30, 8, 32, 4) plus a value head with the PPO loss and its gradient,
+truncated BPTT, and Adam with the +-5 sqrt(v) clip over every parameter
+(fp32 master weights, bf16 GEMM operands).  Inputs are synthetic and resident
+in device memory before the timed region; the behaviour-policy data (actions,
+log-probabilities, values) come from an untimed pass of the same library with
+perturbed weights.
+
+Prints one JSON line: timesteps/s (B*T per step), the roofline of the
+dominant kernel (device time from HIP events recorded by the library on the
+launch stream during the timed region), per-site kernel times, and the CPU
+oracle timed on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "PPO train timesteps/sec at LSTM H=4096,T=16 (1 GPU); % bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def gpu_behaviour(st, inp):
+    """Untimed: actions, log-probabilities and values of a perturbed policy,
+    produced by the library itself (forward pass + sampler)."""
+    import torch
+    from paper_1912_06680_amd import o5
+    from paper_1912_06680_amd.step import PARAM_ORDER
+    cfg = st.cfg
+    T, B, D, H, L, S = cfg.T, cfg.B, cfg.D, cfg.H, cfg.L, cfg.S
+    J = L // T
+    st.load_params({k: inp[k] + inp["noise_" + k] for k in PARAM_ORDER})
+    st.load_x(inp["x"])
+    dev = st.p32.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    st.h0.copy_(torch.from_numpy(inp["h0"]))
+    st.c0.copy_(torch.from_numpy(inp["c0"]))
+    st.dones.copy_(torch.from_numpy(inp["dones"]))
+    zeros = torch.zeros((L, S), **f32)
+    o5.o5_segments_to_samples(L, S, T, zeros, zeros, st.dones, st.adv_s, st.ret_s, st.reset)
+    o5.o5_lstm_fwd(st.dt, T, B, D, H, st.x, st.W["Wx"], st.W["Wh"], st.P["b"], st.h0, st.c0, st.reset,
+                   st.h, st.c, None, st.ws)
+    N = T * B
+    val = torch.empty(N, **f32)
+    sws = torch.empty(max(o5.o5_policy_sample_workspace_bytes(st.dt, N, H, st.heads), 256),
+                      dtype=torch.uint8, device=dev)
+    o5.o5_policy_sample(st.dt, N, H, st.heads, st.h, st.W["Wp"], st.P["bp"], 1, 0, st.act, st.logp_old, val, sws)
+    values = torch.empty((L + 1, S), **f32)
+    values[:L] = val.view(T, S, J).permute(2, 0, 1).reshape(L, S)
+    last = torch.arange(S, device=dev) * J + (J - 1)
+    hT = st.h[T - 1, last].float().contiguous()
+    cT = st.c[T - 1, last].contiguous()
+    xb32 = torch.from_numpy(inp["x_boot"]).to(dev)
+    xb = torch.empty_like(xb32, dtype=st.x.dtype)
+    if st.bf16:
+        o5.o5_f32_to_bf16(xb32.numel(), xb32, xb)
+    else:
+        xb.copy_(xb32)
+    hb = torch.empty((1, S, H), dtype=st.h.dtype, device=dev)
+    cb = torch.empty((1, S, H), **f32)
+    bws = torch.empty(max(o5.o5_lstm_fwd_workspace_bytes(st.dt, 1, S, D, H), 256), dtype=torch.uint8, device=dev)
+    o5.o5_lstm_fwd(st.dt, 1, S, D, H, xb, st.W["Wx"], st.W["Wh"], st.P["b"], hT, cT, None, hb, cb, None, bws)
+    act_b = torch.empty((S, len(st.heads)), dtype=torch.int32, device=dev)
+    lp_b = torch.empty(S, **f32)
+    vb = torch.empty(S, **f32)
+    o5.o5_policy_sample(st.dt, S, H, st.heads, hb, st.W["Wp"], st.P["bp"], 1, 1, act_b, lp_b, vb, sws)
+    values[L] = vb
+    st.values.copy_(values)
+    st.rewards.copy_(torch.from_numpy(inp["rewards"]))
+    torch.cuda.synchronize()
+
+
+def cpu_baseline(cfg, target_s=15.0):
+    """Time the CPU oracle's composed step on a bounded sample: the same
+    per-sample shapes (T, D, H, heads, segment length) with fewer segments."""
+    from oracle.step import ppo_step
+    from paper_1912_06680_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+
+    def run(nb):
+        # nb samples, each its own GAE segment of T steps (same per-timestep work)
+        sub = synth.scaled(cfg, S=nb, B=nb, L=cfg.T)
+        inp = synth.make_inputs(sub, 1)
+        rng = np.random.default_rng(2)
+        N = sub.T * sub.B
+        act = np.stack([rng.integers(0, n, N) for n in sub.head_sizes], axis=1)
+        logp_old = -np.log(np.prod(sub.head_sizes)) + rng.normal(0, 0.05, N)
+        values = rng.standard_normal((sub.L + 1, sub.S))
+        params = {k: inp[k] for k in ("Wx", "Wh", "b", "Wp", "bp")}
+        t0 = time.perf_counter()
+        ppo_step(params, inp["x"], inp["h0"], inp["c0"], inp["rewards"], inp["dones"], values, act, logp_old,
+                 sub.head_sizes, sub.T, sub.gamma, sub.lam, sub.clip_eps, sub.vf_coef, sub.ent_coef, None, sub.lr,
+                 sub.beta1, sub.beta2, sub.adam_eps, sub.clip_k, 1, bf16=sub.dtype == "bf16")
+        return time.perf_counter() - t0, sub
+
+    nb = 4
+    dt, sub = run(nb)
+    if dt < target_s / 3:
+        nb = int(max(nb, min(cfg.B, round(nb * target_s / dt))))
+        if nb > 4:
+            dt, sub = run(nb)
+    return {"value": sub.B * sub.T / dt, "unit": "timesteps/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{sub.B} samples x T={sub.T} (D=H={sub.H}, heads {tuple(sub.head_sizes)}, each sample "
+                      f"its own GAE segment), one full step of the fp64 NumPy oracle incl. Adam over all "
+                      f"{synth.n_params(sub)} params, {dt:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="full4096")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU path "
+              "(gradient all-reduce before Adam) is not built", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1912_06680_amd import o5, synth
+    from paper_1912_06680_amd.step import PARAM_ORDER, PPOStep
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    o5.lib()  # fail loudly if the library is missing
+    cfg = synth.CONFIGS[args.config]
+    T, B, D, H = cfg.T, cfg.B, cfg.D, cfg.H
+    log(f"config {cfg.name}: B={B} T={T} D={D} H={H} heads={cfg.head_sizes} L={cfg.L} S={cfg.S} {cfg.dtype}")
+    inp = synth.make_inputs(cfg, 0)
+    st = PPOStep(cfg)
+    gpu_behaviour(st, inp)
+    st.load_params({k: inp[k] for k in PARAM_ORDER})
+    st.m.zero_()
+    st.v.zero_()
+    torch.cuda.synchronize()
+    log("inputs resident; warmup")
+    for _ in range(args.warmup):
+        st.run()
+    torch.cuda.synchronize()
+    log(f"timing {args.steps} steps")
+    o5.o5_ktimer_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        st.run()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    o5.o5_ktimer_enable(False)
+    ms_step = elapsed * 1e3 / args.steps
+    value = B * T * args.steps / elapsed
+    stats = st.stats.cpu().numpy().tolist()
+    log(f"{ms_step:.3f} ms/step, {value:.0f} timesteps/s, loss {stats[0]:.5f}")
+
+    # per-site device time and algorithmic work per launch
+    A1 = sum(cfg.head_sizes) + 1
+    n = st.n_params
+    flops = {
+        "lstm_fwd_gemm": 2.0 * B * 4 * H * (D + H),
+        "lstm_dh_gemm": 2.0 * B * H * 4 * H,
+        "lstm_dw_gemm": 2.0 * 4 * H * (D + H) * T * B,
+    }
+    bytes_ = {
+        "lstm_fwd_cell": 34.0 * B * H,
+        "lstm_bwd_cell": 40.0 * B * H,
+        "adam_step": 30.0 * n,
+        "gae": 17.0 * cfg.L * cfg.S + 4.0 * cfg.S,
+        "ppo_loss_grad": (2 * 2.0 * H + 4.0 * H + 4.0 * A1 + 16.0) * T * B,
+    }
+    kernels = {}
+    for site, name in enumerate(o5.KTIMER_SITES):
+        tot, cnt = o5.o5_ktimer_read(site)
+        if cnt == 0:
+            continue
+        per = tot / cnt
+        k = {"ms_per_launch": round(per, 5), "launches_per_step": cnt / args.steps,
+             "ms_per_step": round(tot / args.steps, 4)}
+        if name in flops:
+            k["tflops"] = round(flops[name] / (per * 1e-3) / 1e12, 2)
+            k["frac_mfma_peak"] = round(k["tflops"] / PEAK_BF16_TFLOPS, 4)
+        if name in bytes_:
+            k["gbs"] = round(bytes_[name] / (per * 1e-3) / 1e9, 1)
+            k["frac_hbm_peak"] = round(k["gbs"] / PEAK_HBM_GBS, 4)
+        kernels[name] = k
+    gemm_ms = sum(kernels[s]["ms_per_step"] for s in flops if s in kernels)
+    gemm_flop = sum(flops[s] * kernels[s]["launches_per_step"] for s in flops if s in kernels)
+    lstm_gemm_tflops = gemm_flop / (gemm_ms * 1e-3) / 1e12 if gemm_ms > 0 else 0.0
+    dom = max(flops, key=lambda s: kernels.get(s, {}).get("ms_per_step", 0.0))
+    dk = kernels[dom]
+    roofline = {"bound": "mfma", "achieved": dk["tflops"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(dk["tflops"] / PEAK_BF16_TFLOPS, 4), "traffic": None, "kernel": dom,
+                "flop_per_launch": flops[dom], "ms_per_launch": dk["ms_per_launch"]}
+    step_flop = 2.0 * T * B * 4 * H * (D + H) + 2.0 * 4 * H * ((T - 1) * B * H + T * B * H + T * B * D) + \
+        3 * 2.0 * T * B * A1 * H
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        cpu = cpu_baseline(cfg)
+        log(f"cpu oracle: {cpu['value']:.1f} timesteps/s ({cpu['sample']})")
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "timesteps/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"full PPO optimizer step: B={B} samples x T={T}, LSTM D={D} H={H}, heads "
+                               f"{list(cfg.head_sizes)} + value, GAE {cfg.S} segments x {cfg.L} steps, Adam over "
+                               f"{n} params", "global_batch": B * T, "seq_len": T, "parallelism": "none (1 GPU)"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "lstm_gemm_mfma_frac": round(lstm_gemm_tflops / PEAK_BF16_TFLOPS, 4),
+        "lstm_gemm_tflops": round(lstm_gemm_tflops, 2),
+        "step_tflops": round(step_flop / (ms_step * 1e-3) / 1e12, 2),
+        "kernels": kernels,
+        "loss_stats": [round(s, 6) for s in stats],
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,286 @@
+/*
+ * o5.h -- C ABI of libo5: one PPO optimizer step on a single-layer LSTM
+ * policy, after "Dota 2 with Large Scale Deep Reinforcement Learning"
+ * (OpenAI Five, arXiv:1912.06680), on AMD Instinct MI355X (gfx950).
+ *
+ * The paper's optimizer trains a central single-layer 4096-unit LSTM whose
+ * state feeds linear policy and value heads, with PPO and generalized
+ * advantage estimation, Adam, truncated backpropagation through time over
+ * 16-timestep samples, and a per-parameter gradient clip to +-5 sqrt(v)
+ * (section "Training System", subsections "Playing Dota using AI" and
+ * "Optimizing the Policy"; Table "Hyperparameters").  Each call below is one
+ * step of that computation.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every pointer argument is a DEVICE pointer unless marked "host".  All
+ *   device buffers belong to the caller; the library never allocates device
+ *   memory, never keeps a pointer after it returns and never synchronises
+ *   the stream.  Scratch space is passed in as (ws, ws_bytes); the matching
+ *   *_workspace_bytes() query gives the size needed.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *   Work is enqueued in order on that stream; calls on different streams
+ *   with disjoint buffers are independent.
+ * - Arguments are validated on the host before anything is enqueued.  On
+ *   error the call returns a nonzero O5_E_* code, enqueues nothing, leaves
+ *   every output untouched and records a message for o5_last_error() (per
+ *   calling thread).  Faults raised by the device while running enqueued
+ *   work surface at the caller's next synchronisation, as for any HIP call.
+ * - Device pointers must be 16-byte aligned.  Outputs are overwritten, never
+ *   accumulated into; inputs and outputs must not overlap except where a
+ *   call says so (o5_adam_step updates p, m, v in place).
+ * - Results are deterministic: identical inputs on the same GPU give
+ *   bitwise identical outputs (no floating-point atomics).
+ * - Layouts are row-major and time-major: [T, B, D] means element
+ *   (t, b, d) at index (t * B + b) * D + d.  LSTM gate blocks are ordered
+ *   (i, f, g, o): row g * H + j of a [4H, .] weight holds gate g of unit j.
+ * - bf16 buffers hold IEEE bfloat16 bit patterns (uint16).
+ */
+#ifndef O5_H
+#define O5_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define O5_VERSION 100 /* 1.0.0 */
+
+enum {
+  O5_OK = 0,
+  O5_E_NULL = 1,      /* a required pointer is NULL */
+  O5_E_SHAPE = 2,     /* a size is out of range or inconsistent */
+  O5_E_DTYPE = 3,     /* unknown o5_dtype */
+  O5_E_ALIGN = 4,     /* a device pointer is not 16-byte aligned */
+  O5_E_WORKSPACE = 5, /* ws is NULL or ws_bytes is below the query */
+  O5_E_HIP = 6,       /* the HIP runtime refused a launch */
+  O5_E_ARG = 7        /* another argument is out of range */
+};
+
+/* Arithmetic type of the GEMM inputs (x, weights, hidden state).  Cell
+ * state, gradients, optimizer state, advantages and losses are always fp32;
+ * GEMMs always accumulate in fp32. */
+typedef enum { O5_F32 = 0, O5_BF16 = 1 } o5_dtype;
+
+/* O5_VERSION of the loaded library. */
+int o5_version(void);
+/* Static description of a status code (never NULL). */
+const char* o5_status_str(int status);
+/* Message of the calling thread's last failed call ("" if none). */
+const char* o5_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * o5_lstm_fwd -- T steps of the single-layer LSTM over a minibatch of B
+ * samples, each started from its stored rollout state (section "Training
+ * System": a single-layer 4096-unit LSTM of the forget-gate kind (Gers et
+ * al. 1999); subsection "Optimizing the Policy": samples of 16 timesteps).
+ *
+ *   h~ = (1 - reset[t,b]) h_{t-1},  c~ = (1 - reset[t,b]) c_{t-1}
+ *   a  = W_x x_t + W_h h~ + b;  i, f, o = sigmoid(a_i, a_f, a_o);  g = tanh(a_g)
+ *   c_t = f c~ + i g;  h_t = o tanh(c_t)            (h_{-1} = h0, c_{-1} = c0)
+ *
+ * dt       GEMM input type: x, Wx, Wh and the output h are fp32 (O5_F32) or
+ *          bf16 (O5_BF16).
+ * T, B     steps and samples, >= 1.  D, H: input width and hidden units,
+ *          multiples of 64, <= 65536.
+ * x        [T, B, D] dt.   Wx [4H, D] dt.   Wh [4H, H] dt.   b [4H] fp32.
+ * h0, c0   [B, H] fp32, the start state of each sample.
+ * reset    [T, B] uint8 or NULL (no resets): nonzero zeroes the carried
+ *          state before step t of sample b.
+ * h        out [T, B, H] dt.   c: out [T, B, H] fp32.
+ * gates    out [T, B, 4H] dt, the post-activation (i, f, g, o) that
+ *          o5_lstm_bptt needs; NULL for inference (nothing saved).
+ * ws       scratch of o5_lstm_fwd_workspace_bytes(dt, T, B, D, H) bytes.
+ * ------------------------------------------------------------------------ */
+size_t o5_lstm_fwd_workspace_bytes(o5_dtype dt, int T, int B, int D, int H);
+int o5_lstm_fwd(o5_dtype dt, int T, int B, int D, int H,
+                const void* x, const void* Wx, const void* Wh, const float* b,
+                const float* h0, const float* c0, const uint8_t* reset,
+                void* h, float* c, void* gates,
+                void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * o5_lstm_bptt -- truncated backpropagation through time over the T steps
+ * of one o5_lstm_fwd call (subsection "Optimizing the Policy": BPTT over
+ * samples of 16 timesteps).  It differentiates
+ *     J = sum_t <dh[t], h[t]> + <dhT, h[T-1]> + <dcT, c[T-1]>
+ * with respect to the weights; no gradient flows into h0 or c0 (the
+ * truncation).
+ *
+ * x, Wx, Wh, h0, c0, reset, h, c, gates: exactly as given to / produced by
+ *          o5_lstm_fwd (gates must not be NULL).
+ * dh       [T, B, H] fp32: gradient arriving at every step's output h[t]
+ *          (from the heads).
+ * dhT, dcT [B, H] fp32 or NULL (= 0): gradient arriving at the final state.
+ * dWx      out [4H, D] fp32.   dWh: out [4H, H] fp32.   db: out [4H] fp32.
+ * dx       out [T, B, D] dt, or NULL to skip the input gradient.
+ * ws       scratch of o5_lstm_bptt_workspace_bytes(dt, T, B, D, H) bytes.
+ * ------------------------------------------------------------------------ */
+size_t o5_lstm_bptt_workspace_bytes(o5_dtype dt, int T, int B, int D, int H);
+int o5_lstm_bptt(o5_dtype dt, int T, int B, int D, int H,
+                 const void* x, const void* Wx, const void* Wh,
+                 const float* h0, const float* c0, const uint8_t* reset,
+                 const void* h, const float* c, const void* gates,
+                 const float* dh, const float* dhT, const float* dcT,
+                 float* dWx, float* dWh, float* db, void* dx,
+                 void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * o5_gae -- generalized advantage estimation over S rollout segments of L
+ * steps (subsection "Optimizing the Policy": PPO with GAE, advantages
+ * smoothed over 256-step segments; Table "Hyperparameters": lambda = 0.95).
+ *
+ *   delta_t = r_t + gamma (1 - done_t) v_{t+1} - v_t
+ *   adv_t   = delta_t + gamma lambda (1 - done_t) adv_{t+1}    (adv_L = 0)
+ *   ret_t   = adv_t + v_t
+ *
+ * L, S     >= 1.
+ * r        [L, S] fp32 rewards.   v: [L+1, S] fp32 values, row L the
+ *          bootstrap value after the segment.   done: [L, S] uint8, nonzero
+ *          marks transition t terminal.
+ * gamma, lambda in [0, 1].
+ * adv, ret out [L, S] fp32.
+ * ------------------------------------------------------------------------ */
+int o5_gae(int L, int S, const float* r, const float* v, const uint8_t* done,
+           float gamma, float lambda, float* adv, float* ret, void* stream);
+
+/* ------------------------------------------------------------------------
+ * o5_segments_to_samples -- cut each of S segments of L steps into L/T
+ * samples of T steps, the unit truncated BPTT runs on (Figure "Timescales
+ * and Staleness": a segment is subdivided into samples of 16 policy
+ * actions).  Sample b = s * (L/T) + j holds segment steps T*j .. T*j+T-1.
+ *
+ * L, S, T  >= 1, T divides L.
+ * adv, ret [L, S] fp32.   done: [L, S] uint8.
+ * adv_s, ret_s out [T, B] fp32 (B = S*L/T).
+ * reset    out [T, B] uint8: reset[0, b] = 0 and reset[t, b] = (done at the
+ *          previous step of the same sample != 0) for t >= 1.
+ * ------------------------------------------------------------------------ */
+int o5_segments_to_samples(int L, int S, int T, const float* adv, const float* ret,
+                           const uint8_t* done, float* adv_s, float* ret_s,
+                           uint8_t* reset, void* stream);
+
+/* ------------------------------------------------------------------------
+ * o5_ppo_loss_grad -- policy and value heads, PPO loss and its gradient
+ * (appendix "Neural Network Architecture": the action logits and the value
+ * are linear projections of the LSTM state, sharing the network and its
+ * gradients; appendix "Action Space": a factorised action with masking of
+ * ignored parameter heads; subsection "Optimizing the Policy" and Table
+ * "Hyperparameters": PPO clipping 0.2, value loss weight 1.0; appendix
+ * "Exploration", "Loss function": entropy bonus c S[pi], c = 0.01).
+ *
+ *   z = h Wp^T + bp;  head k = columns [o_k, o_k + n_k); value V = z[:, A]
+ *   logpi = sum_k m_k log softmax(z_k)[a_k];  r = exp(logpi - logp_old)
+ *   L = -mean min(r A, clip(r, 1-eps, 1+eps) A) + vf_coef mean (V - R)^2
+ *       - ent_coef mean sum_k m_k S_k
+ *
+ * dt       type of h and Wp.   N: rows (timesteps), >= 1.   H: multiple of
+ *          64.   K: heads, 1..8.   head_sizes: host [K], each >= 1, with
+ *          A + 1 = sum + 1 <= 1024.
+ * h        [N, H] dt.   Wp: [A+1, H] dt, last row the value head.   bp:
+ *          [A+1] fp32.
+ * act      [N, K] int32, action index within each head (0 <= a < n_k).
+ * logp_old, adv, ret [N] fp32 (behaviour log-probability of the joint
+ *          action, advantage, value target).
+ * head_mask [N, K] uint8 or NULL (all heads count).
+ * hp       {clip_eps, vf_coef, ent_coef}.
+ * stats    out [8] fp32: total, pg, vf, ent, clipfrac (mean |r-1| > eps),
+ *          approx_kl (mean (r - 1) - log r), mean_ratio, nonfinite (rows
+ *          whose loss term is not finite).
+ * dh       out [N, H] fp32 = dL/dh.   dWp: out [A+1, H] fp32.   dbp: out
+ *          [A+1] fp32.
+ * ws       scratch of o5_ppo_loss_grad_workspace_bytes(...) bytes.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  float clip_eps; /* 0.2 */
+  float vf_coef;  /* 1.0 */
+  float ent_coef; /* 0.01 */
+} o5_ppo_hp;
+
+size_t o5_ppo_loss_grad_workspace_bytes(o5_dtype dt, int N, int H, int K,
+                                        const int* head_sizes);
+int o5_ppo_loss_grad(o5_dtype dt, int N, int H, int K, const int* head_sizes,
+                     const void* h, const void* Wp, const float* bp,
+                     const int32_t* act, const float* logp_old, const float* adv,
+                     const float* ret, const uint8_t* head_mask, o5_ppo_hp hp,
+                     float* stats, float* dh, float* dWp, float* dbp,
+                     void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * o5_adam_step -- Adam with the per-parameter clip of each gradient element
+ * to +-clip_k sqrt(v) (subsection "Optimizing the Policy"; Table
+ * "Hyperparameters": beta1 0.9, beta2 0.999, learning rate 5e-5):
+ *
+ *   v = b2 v + (1-b2) g^2;  vh = v / (1 - b2^step)
+ *   g' = clamp(g, -clip_k sqrt(vh), clip_k sqrt(vh))     (clip_k <= 0: g' = g)
+ *   m = b1 m + (1-b1) g';   mh = m / (1 - b1^step)
+ *   p = p - lr mh / (sqrt(vh) + eps)
+ *
+ * n        elements (>= 1).   p, m, v: [n] fp32, updated in place.   g: [n]
+ *          fp32.   p_bf16: out [n] bf16 copy of the new p, or NULL.
+ * step     1-based step counter (>= 1).
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  float lr;     /* 5e-5 */
+  float beta1;  /* 0.9 */
+  float beta2;  /* 0.999 */
+  float eps;    /* 1e-8 */
+  float clip_k; /* 5; <= 0 turns the clip off */
+} o5_adam_hp;
+
+int o5_adam_step(size_t n, float* p, float* m, float* v, const float* g,
+                 uint16_t* p_bf16, o5_adam_hp hp, int step, void* stream);
+
+/* ------------------------------------------------------------------------
+ * o5_policy_sample -- rollout inference heads: logits and value from the
+ * LSTM state, then one action per head sampled from its categorical
+ * distribution (section "Training System", subsection "Playing Dota using
+ * AI": an action is sampled from the output distribution every timestep).
+ * The draw is Gumbel-max, a = argmax_a (z_a + G_a), G = -ln(-ln U), with U
+ * from Philox4x64-10 (Salmon et al., SC'11): the noise for logit a of head
+ * k in row b is word (a mod 4) of the block with counter
+ * (a div 4, k, b, counter) and key (seed, 0); U = ((word >> 40) + 0.5)/2^24.
+ * Ties go to the lowest index.
+ *
+ * dt, B, H, K, head_sizes, h [B, H], Wp, bp: as for o5_ppo_loss_grad.
+ * act      out [B, K] int32.   logp: out [B] fp32, joint log-probability
+ *          of the sampled action.   value: out [B] fp32.
+ * ws       scratch of o5_policy_sample_workspace_bytes(...) bytes.
+ * ------------------------------------------------------------------------ */
+size_t o5_policy_sample_workspace_bytes(o5_dtype dt, int B, int H, int K,
+                                        const int* head_sizes);
+int o5_policy_sample(o5_dtype dt, int B, int H, int K, const int* head_sizes,
+                     const void* h, const void* Wp, const float* bp,
+                     uint64_t seed, uint64_t counter,
+                     int32_t* act, float* logp, float* value,
+                     void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * o5_f32_to_bf16 -- round n fp32 values to bfloat16 (nearest, ties to
+ * even; NaN stays NaN).  Used to build the bf16 GEMM operands.
+ * ------------------------------------------------------------------------ */
+int o5_f32_to_bf16(size_t n, const float* src, uint16_t* dst, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Kernel timing (instrumentation for benchmarks, not thread-safe).
+ * o5_ktimer_enable(1) clears previous records and starts recording a pair
+ * of hipEvents on the caller's stream around every launch site listed
+ * below; o5_ktimer_enable(0) stops recording (records are kept until the
+ * next enable).  o5_ktimer_read waits for the recorded events of one site
+ * and returns the summed device time in milliseconds and the number of
+ * launches.  Sites: 0 lstm_fwd_gemm, 1 lstm_fwd_cell, 2 lstm_dh_gemm,
+ * 3 lstm_bwd_cell, 4 lstm_dw_gemm, 5 lstm_dx_gemm, 6 ppo_loss_grad (whole
+ * call), 7 adam_step, 8 gae, 9 policy_sample (whole call).
+ * o5_ktimer_site_name returns the site's name ("" if out of range).
+ * ------------------------------------------------------------------------ */
+int o5_ktimer_enable(int on);
+int o5_ktimer_read(int site, double* total_ms, int* launches);
+const char* o5_ktimer_site_name(int site);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* O5_H */

@@ -1,0 +1,159 @@
+// Status strings, per-thread error messages, fp32 -> bf16 conversion.
+#include "common.h"
+
+#include <utility>
+#include <vector>
+
+namespace o5 {
+
+static thread_local char g_last_error[512] = "";
+
+void set_error(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+}
+
+void clear_error() { g_last_error[0] = '\0'; }
+
+int check_launch(const char* where) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    set_error("%s: kernel launch failed: %s", where, hipGetErrorString(e));
+    return O5_E_HIP;
+  }
+  return O5_OK;
+}
+
+// ----------------------------------------------------------- kernel timer
+// Events are recorded on the caller's stream around each timed launch site;
+// elapsed times are read (and the events returned to the pool) by
+// o5_ktimer_read.  Host-side state only; meant for single-threaded
+// benchmarking.
+namespace {
+struct KTimer {
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> done[kSiteCount];
+  hipEvent_t open[kSiteCount] = {};
+  hipEvent_t get() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+KTimer g_kt;
+const char* kSiteNames[kSiteCount] = {"lstm_fwd_gemm", "lstm_fwd_cell", "lstm_dh_gemm", "lstm_bwd_cell",
+                                      "lstm_dw_gemm",  "lstm_dx_gemm",  "ppo_loss_grad", "adam_step",
+                                      "gae",           "policy_sample"};
+}  // namespace
+
+void ktimer_begin(int site, hipStream_t s) {
+  if (!g_kt.on) return;
+  hipEvent_t e = g_kt.get();
+  if (e && hipEventRecord(e, s) == hipSuccess) g_kt.open[site] = e;
+}
+
+void ktimer_end(int site, hipStream_t s) {
+  if (!g_kt.on || !g_kt.open[site]) return;
+  hipEvent_t e = g_kt.get();
+  if (e && hipEventRecord(e, s) == hipSuccess) g_kt.done[site].emplace_back(g_kt.open[site], e);
+  g_kt.open[site] = nullptr;
+}
+
+// 8 elements per thread: two float4 loads, one 16-byte store.
+__global__ void __launch_bounds__(256) f32_to_bf16_kernel(size_t n, const float* __restrict__ src,
+                                                          uint16_t* __restrict__ dst) {
+  const size_t n8 = n / 8;
+  const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
+  for (size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n8; i += stride) {
+    const float4 a = reinterpret_cast<const float4*>(src)[2 * i];
+    const float4 b = reinterpret_cast<const float4*>(src)[2 * i + 1];
+    uint4 o;
+    o.x = f32_to_bf16_bits(a.x) | (static_cast<uint32_t>(f32_to_bf16_bits(a.y)) << 16);
+    o.y = f32_to_bf16_bits(a.z) | (static_cast<uint32_t>(f32_to_bf16_bits(a.w)) << 16);
+    o.z = f32_to_bf16_bits(b.x) | (static_cast<uint32_t>(f32_to_bf16_bits(b.y)) << 16);
+    o.w = f32_to_bf16_bits(b.z) | (static_cast<uint32_t>(f32_to_bf16_bits(b.w)) << 16);
+    reinterpret_cast<uint4*>(dst)[i] = o;
+  }
+  // tail (fewer than 8 elements), handled by the first block
+  if (blockIdx.x == 0) {
+    const size_t t = n8 * 8 + threadIdx.x;
+    if (t < n) dst[t] = f32_to_bf16_bits(src[t]);
+  }
+}
+
+}  // namespace o5
+
+using namespace o5;
+
+extern "C" int o5_version(void) { return O5_VERSION; }
+
+extern "C" const char* o5_status_str(int status) {
+  switch (status) {
+    case O5_OK: return "O5_OK: success";
+    case O5_E_NULL: return "O5_E_NULL: a required pointer is NULL";
+    case O5_E_SHAPE: return "O5_E_SHAPE: a size is out of range or inconsistent";
+    case O5_E_DTYPE: return "O5_E_DTYPE: unknown dtype";
+    case O5_E_ALIGN: return "O5_E_ALIGN: a device pointer is not 16-byte aligned";
+    case O5_E_WORKSPACE: return "O5_E_WORKSPACE: workspace missing or too small";
+    case O5_E_HIP: return "O5_E_HIP: the HIP runtime refused a launch";
+    case O5_E_ARG: return "O5_E_ARG: an argument is out of range";
+    default: return "unknown o5 status";
+  }
+}
+
+extern "C" const char* o5_last_error(void) { return o5::g_last_error; }
+
+extern "C" int o5_ktimer_enable(int on) {
+  for (int i = 0; i < kSiteCount; ++i) {
+    for (auto& pr : g_kt.done[i]) {
+      g_kt.pool.push_back(pr.first);
+      g_kt.pool.push_back(pr.second);
+    }
+    g_kt.done[i].clear();
+    g_kt.open[i] = nullptr;
+  }
+  g_kt.on = on != 0;
+  return O5_OK;
+}
+
+extern "C" int o5_ktimer_read(int site, double* total_ms, int* launches) {
+  O5_CHECK(site >= 0 && site < kSiteCount, O5_E_ARG, "o5_ktimer_read: site %d out of range", site);
+  O5_CHECK(total_ms != nullptr && launches != nullptr, O5_E_NULL, "o5_ktimer_read: NULL output");
+  double t = 0.0;
+  for (auto& pr : g_kt.done[site]) {
+    float ms = 0.0f;
+    if (hipEventSynchronize(pr.second) != hipSuccess || hipEventElapsedTime(&ms, pr.first, pr.second) != hipSuccess) {
+      set_error("o5_ktimer_read: event query failed");
+      return O5_E_HIP;
+    }
+    t += ms;
+  }
+  *total_ms = t;
+  *launches = static_cast<int>(g_kt.done[site].size());
+  return O5_OK;
+}
+
+extern "C" const char* o5_ktimer_site_name(int site) {
+  return (site >= 0 && site < kSiteCount) ? kSiteNames[site] : "";
+}
+
+extern "C" int o5_f32_to_bf16(size_t n, const float* src, uint16_t* dst, void* stream) {
+  O5_CHECK(n >= 1, O5_E_SHAPE, "o5_f32_to_bf16: n must be >= 1");
+  O5_PTR(src, "src");
+  O5_PTR(dst, "dst");
+  size_t n8 = n / 8;
+  size_t blocks = (n8 + 255) / 256;
+  if (blocks < 1) blocks = 1;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(f32_to_bf16_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                     as_stream(stream), n, src, dst);
+  return check_launch("o5_f32_to_bf16");
+}

@@ -1,0 +1,101 @@
+// Shared host/device helpers of libo5: error reporting, argument checks,
+// bf16 conversion, launch helpers.  gfx950 (CDNA4) only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstddef>
+#include <cstdint>
+#include <cstdio>
+
+#include "../../include/o5.h"
+
+namespace o5 {
+
+// ---------------------------------------------------------------- errors
+void set_error(const char* fmt, ...);
+void clear_error();
+
+#define O5_CHECK(cond, code, ...)          \
+  do {                                     \
+    if (!(cond)) {                         \
+      ::o5::set_error(__VA_ARGS__);        \
+      return (code);                       \
+    }                                      \
+  } while (0)
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+#define O5_PTR(p, name)                                                        \
+  do {                                                                         \
+    O5_CHECK((p) != nullptr, O5_E_NULL, "%s: argument '%s' is NULL", __func__, name); \
+    O5_CHECK(::o5::aligned16(p), O5_E_ALIGN, "%s: '%s' is not 16-byte aligned", __func__, name); \
+  } while (0)
+
+#define O5_OPT_PTR(p, name)                                                    \
+  do {                                                                         \
+    if ((p) != nullptr)                                                        \
+      O5_CHECK(::o5::aligned16(p), O5_E_ALIGN, "%s: '%s' is not 16-byte aligned", __func__, name); \
+  } while (0)
+
+// Returns O5_OK, or O5_E_HIP with a message if the last launch failed.
+int check_launch(const char* where);
+
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+// ------------------------------------------------------- kernel timing
+// Launch sites whose device time o5_ktimer_* can report (see o5.h).
+enum KSite {
+  kSiteLstmFwdGemm = 0,
+  kSiteLstmFwdCell,
+  kSiteLstmDhGemm,
+  kSiteLstmBwdCell,
+  kSiteLstmDwGemm,
+  kSiteLstmDxGemm,
+  kSitePpo,
+  kSiteAdam,
+  kSiteGae,
+  kSiteSample,
+  kSiteCount
+};
+// When timing is on, record an event on `s` before / after a launch site.
+void ktimer_begin(int site, hipStream_t s);
+void ktimer_end(int site, hipStream_t s);
+
+inline size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
+
+// ------------------------------------------------------------------ bf16
+// Round-to-nearest-even fp32 -> bf16 bits; NaN keeps a quiet NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x0040u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// ------------------------------------------------------------- activations
+__device__ __forceinline__ float sigmoid_f(float a) { return 1.0f / (1.0f + __expf(-a)); }
+__device__ __forceinline__ float tanh_f(float a) { return tanhf(a); }
+
+// Element type tags used by templates: float (fp32 path) or uint16_t
+// holding bf16 bits (bf16 path).
+template <typename E> struct elem;
+template <> struct elem<float> {
+  __device__ __forceinline__ static float to_f32(float v) { return v; }
+  __device__ __forceinline__ static float from_f32(float v) { return v; }
+};
+template <> struct elem<uint16_t> {
+  __device__ __forceinline__ static float to_f32(uint16_t v) { return bf16_bits_to_f32(v); }
+  __device__ __forceinline__ static uint16_t from_f32(float v) { return f32_to_bf16_bits(v); }
+};
+
+inline size_t dtype_size(o5_dtype dt) { return dt == O5_BF16 ? 2 : 4; }
+
+}  // namespace o5

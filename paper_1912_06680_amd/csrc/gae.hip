@@ -1,0 +1,185 @@
+// Generalized advantage estimation over rollout segments, and the cut of
+// segments into 16-step samples (subsection "Optimizing the Policy"; Figure
+// "Timescales and Staleness").
+//
+// GAE is the reverse linear recurrence  A_t = delta_t + c_t A_{t+1}  with
+// c_t = gamma lambda (1 - done_t) and A_L = 0.  Two kernels:
+//  * lane per segment (large S): each lane walks its segment backwards;
+//    at every step a wave reads 64 consecutive segments, so every load and
+//    store is coalesced and the kernel streams at HBM rate.
+//  * wave per segment (small S): the 64 lanes of a wave split the segment
+//    into 64 chunks, reduce each chunk to an affine map A_in -> alpha + beta
+//    A_in, combine the maps with a wavefront suffix scan (shuffles), then
+//    replay their chunk from the correct carry-in.  This cuts the serial
+//    dependency from L to L/64 + log2(64) steps.
+#include "common.h"
+
+namespace o5 {
+
+constexpr int kGaeLaneUnroll = 16;
+
+__global__ void __launch_bounds__(256) gae_lane_per_segment(int L, int S, const float* __restrict__ r,
+                                                            const float* __restrict__ v,
+                                                            const uint8_t* __restrict__ done, float gamma,
+                                                            float gl, float* __restrict__ adv,
+                                                            float* __restrict__ ret) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= S) return;
+  const size_t S_ = static_cast<size_t>(S);
+  float carry = 0.0f;
+  float vnext = v[static_cast<size_t>(L) * S_ + s];
+  int t_hi = L - 1;
+  // full chunks: issue all loads of a chunk first, then run the recurrence
+  while (t_hi + 1 >= kGaeLaneUnroll) {
+    float rr[kGaeLaneUnroll], vv[kGaeLaneUnroll];
+    uint8_t dd[kGaeLaneUnroll];
+#pragma unroll
+    for (int u = 0; u < kGaeLaneUnroll; ++u) {
+      const size_t idx = static_cast<size_t>(t_hi - u) * S_ + s;
+      rr[u] = r[idx];
+      vv[u] = v[idx];
+      dd[u] = done[idx];
+    }
+#pragma unroll
+    for (int u = 0; u < kGaeLaneUnroll; ++u) {
+      const float nd = dd[u] ? 0.0f : 1.0f;
+      const float delta = rr[u] + gamma * nd * vnext - vv[u];
+      carry = delta + gl * nd * carry;
+      const size_t idx = static_cast<size_t>(t_hi - u) * S_ + s;
+      adv[idx] = carry;
+      ret[idx] = carry + vv[u];
+      vnext = vv[u];
+    }
+    t_hi -= kGaeLaneUnroll;
+  }
+  for (; t_hi >= 0; --t_hi) {
+    const size_t idx = static_cast<size_t>(t_hi) * S_ + s;
+    const float vt = v[idx];
+    const float nd = done[idx] ? 0.0f : 1.0f;
+    const float delta = r[idx] + gamma * nd * vnext - vt;
+    carry = delta + gl * nd * carry;
+    adv[idx] = carry;
+    ret[idx] = carry + vt;
+    vnext = vt;
+  }
+}
+
+// One wave (64 lanes) per segment; blockDim = 256 holds 4 segments.
+__global__ void __launch_bounds__(256) gae_wave_per_segment(int L, int S, const float* __restrict__ r,
+                                                            const float* __restrict__ v,
+                                                            const uint8_t* __restrict__ done, float gamma,
+                                                            float gl, float* __restrict__ adv,
+                                                            float* __restrict__ ret) {
+  const int lane = threadIdx.x & 63;
+  const int s = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (s >= S) return;  // whole wave exits together
+  const size_t S_ = static_cast<size_t>(S);
+  const int q = (L + 63) / 64;             // steps per lane
+  const int t0 = lane * q;                 // this lane's chunk [t0, t1)
+  const int t1 = min(t0 + q, L);
+
+  // 1) reduce the chunk to A(t0) = alpha + beta * A(t1), with A(t1) unknown
+  float alpha = 0.0f, beta = 1.0f;
+  for (int t = t1 - 1; t >= t0; --t) {
+    const size_t idx = static_cast<size_t>(t) * S_ + s;
+    const float nd = done[idx] ? 0.0f : 1.0f;
+    const float delta = r[idx] + gamma * nd * v[idx + S_] - v[idx];
+    const float c = gl * nd;
+    alpha = delta + c * alpha;
+    beta = c * beta;
+  }
+  // 2) suffix scan of the maps: lane j ends with F_j = f_j o f_{j+1} o ... o f_63
+  for (int d = 1; d < 64; d <<= 1) {
+    const float a2 = __shfl_down(alpha, d, 64);
+    const float b2 = __shfl_down(beta, d, 64);
+    if (lane + d < 64) {
+      alpha = alpha + beta * a2;
+      beta = beta * b2;
+    }
+  }
+  // carry-in of lane j is A at the start of chunk j+1, i.e. F_{j+1}(0)
+  float carry = __shfl_down(alpha, 1, 64);
+  if (lane == 63) carry = 0.0f;
+  // 3) replay the chunk from its carry-in
+  for (int t = t1 - 1; t >= t0; --t) {
+    const size_t idx = static_cast<size_t>(t) * S_ + s;
+    const float vt = v[idx];
+    const float nd = done[idx] ? 0.0f : 1.0f;
+    const float delta = r[idx] + gamma * nd * v[idx + S_] - vt;
+    carry = delta + gl * nd * carry;
+    adv[idx] = carry;
+    ret[idx] = carry + vt;
+  }
+}
+
+// One thread per (t, b) of the sample layout.
+__global__ void __launch_bounds__(256) segments_to_samples_kernel(int L, int S, int T,
+                                                                  const float* __restrict__ adv,
+                                                                  const float* __restrict__ ret,
+                                                                  const uint8_t* __restrict__ done,
+                                                                  float* __restrict__ adv_s,
+                                                                  float* __restrict__ ret_s,
+                                                                  uint8_t* __restrict__ reset) {
+  const int J = L / T;
+  const int B = S * J;
+  const size_t total = static_cast<size_t>(T) * B;
+  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const int t = static_cast<int>(i / B);
+  const int b = static_cast<int>(i % B);
+  const int s = b / J;
+  const int j = b % J;
+  const size_t src = static_cast<size_t>(T * j + t) * S + s;
+  adv_s[i] = adv[src];
+  ret_s[i] = ret[src];
+  reset[i] = (t > 0 && done[src - S] != 0) ? 1 : 0;
+}
+
+}  // namespace o5
+
+using namespace o5;
+
+// Segments per launch below which the wave-per-segment scan is used.
+static constexpr int kGaeWaveScanMaxS = 4096;
+
+extern "C" int o5_gae(int L, int S, const float* r, const float* v, const uint8_t* done, float gamma,
+                      float lambda, float* adv, float* ret, void* stream) {
+  O5_CHECK(L >= 1 && S >= 1, O5_E_SHAPE, "o5_gae: L=%d and S=%d must be >= 1", L, S);
+  O5_CHECK(static_cast<long long>(L + 1) * S < (1ll << 40), O5_E_SHAPE, "o5_gae: L*S too large");
+  O5_CHECK(gamma >= 0.0f && gamma <= 1.0f && lambda >= 0.0f && lambda <= 1.0f, O5_E_ARG,
+           "o5_gae: gamma=%g and lambda=%g must lie in [0, 1]", gamma, lambda);
+  O5_PTR(r, "r");
+  O5_PTR(v, "v");
+  O5_PTR(done, "done");
+  O5_PTR(adv, "adv");
+  O5_PTR(ret, "ret");
+  const float gl = gamma * lambda;
+  ktimer_begin(kSiteGae, as_stream(stream));
+  if (S <= kGaeWaveScanMaxS) {
+    hipLaunchKernelGGL(gae_wave_per_segment, dim3((S + 3) / 4), dim3(256), 0, as_stream(stream), L, S,
+                       r, v, done, gamma, gl, adv, ret);
+  } else {
+    hipLaunchKernelGGL(gae_lane_per_segment, dim3((S + 255) / 256), dim3(256), 0, as_stream(stream), L,
+                       S, r, v, done, gamma, gl, adv, ret);
+  }
+  ktimer_end(kSiteGae, as_stream(stream));
+  return check_launch("o5_gae");
+}
+
+extern "C" int o5_segments_to_samples(int L, int S, int T, const float* adv, const float* ret,
+                                      const uint8_t* done, float* adv_s, float* ret_s, uint8_t* reset,
+                                      void* stream) {
+  O5_CHECK(L >= 1 && S >= 1 && T >= 1 && L % T == 0, O5_E_SHAPE,
+           "o5_segments_to_samples: need L, S, T >= 1 and T | L (L=%d S=%d T=%d)", L, S, T);
+  O5_CHECK(static_cast<long long>(L) * S < (1ll << 40), O5_E_SHAPE, "o5_segments_to_samples: too large");
+  O5_PTR(adv, "adv");
+  O5_PTR(ret, "ret");
+  O5_PTR(done, "done");
+  O5_PTR(adv_s, "adv_s");
+  O5_PTR(ret_s, "ret_s");
+  O5_PTR(reset, "reset");
+  const size_t total = static_cast<size_t>(L) * S;
+  hipLaunchKernelGGL(segments_to_samples_kernel, dim3(static_cast<unsigned>((total + 255) / 256)),
+                     dim3(256), 0, as_stream(stream), L, S, T, adv, ret, done, adv_s, ret_s, reset);
+  return check_launch("o5_segments_to_samples");
+}

@@ -1,0 +1,395 @@
+// LSTM forward pass and truncated BPTT over one minibatch of 16-step samples
+// (section "Training System": a single-layer 4096-unit forget-gate LSTM;
+// subsection "Optimizing the Policy": truncated BPTT over 16 timesteps).
+//
+// Forward, for t = 0 .. T-1:
+//   GEMM  P_t = [x_t | h~_{t-1}] . [W_x | W_h]^T          (M = B, N = 4H, K = D + H)
+//   cell  a = P_t + b; (i, f, g, o); c_t = f c~ + i g; h_t = o tanh(c_t)
+// The concatenated-K GEMM reads x_t and the previous hidden state directly,
+// so no [T, B, 4H] input projection ever goes through HBM; the reset mask is
+// applied to the hidden-state half of each A row as it is loaded.
+//
+// Backward, for t = T-1 .. 0:
+//   GEMM  R = dG_{t+1} . W_h                               (M = B, N = H, K = 4H)
+//   cell  dh = dh_heads[t] + (1 - reset[t+1]) R;  dG_t and the carried dc;
+//         per-block column sums of dG_t for the bias gradient
+// then once:
+//   GEMM  [dW_x | dW_h] = dG^T . [x | h~_prev]             (M = 4H, N = D + H, K = T B)
+//   GEMM  dx = dG . W_x                                     (M = T B, N = D, K = 4H), optional
+//   db    = fixed-order sum of the per-block column sums.
+//
+// fp32 path: the FMA engine; bf16 path: the MFMA engine, with h, the saved
+// gates and dG stored in bf16 and everything else in fp32.
+#include "gemm.h"
+#include "reduce.h"
+
+namespace o5 {
+
+// ------------------------------------------------------- pointwise kernels
+
+constexpr int kPwCols = 64;  // hidden units per block
+constexpr int kPwRowGroups = 4;
+constexpr int kPwRows = 32;  // batch rows per block (8 per row group)
+
+// Forward cell for one step.  pre: [S][B][4H] partial GEMM sums.
+template <typename E>
+__global__ void __launch_bounds__(256) lstm_fwd_cell(int B, int H, int S, const float* __restrict__ pre,
+                                                     const float* __restrict__ bias, const float* __restrict__ c_prev,
+                                                     const uint8_t* __restrict__ reset_t, E* __restrict__ h_out,
+                                                     float* __restrict__ c_out, E* __restrict__ gates_out) {
+  const int j = blockIdx.x * kPwCols + (threadIdx.x & 63);
+  const int rg = threadIdx.x >> 6;
+  if (j >= H) return;
+  const size_t G = 4 * static_cast<size_t>(H);
+  const size_t sstride = static_cast<size_t>(B) * G;
+  const float bi = bias[j], bf = bias[H + j], bg = bias[2 * H + j], bo = bias[3 * H + j];
+  for (int r = rg; r < kPwRows; r += kPwRowGroups) {
+    const int b = blockIdx.y * kPwRows + r;
+    if (b >= B) break;
+    const size_t row = static_cast<size_t>(b) * G;
+    float ai = bi, af = bf, ag = bg, ao = bo;
+    for (int s = 0; s < S; ++s) {
+      const float* p = pre + s * sstride + row;
+      ai += p[j];
+      af += p[H + j];
+      ag += p[2 * H + j];
+      ao += p[3 * H + j];
+    }
+    const float keep = (reset_t && reset_t[b]) ? 0.0f : 1.0f;
+    const size_t hj = static_cast<size_t>(b) * H + j;
+    const float cp = keep * c_prev[hj];
+    const float ig = sigmoid_f(ai), fg = sigmoid_f(af), gg = tanh_f(ag), og = sigmoid_f(ao);
+    const float c = fg * cp + ig * gg;
+    const float h = og * tanh_f(c);
+    c_out[hj] = c;
+    h_out[hj] = elem<E>::from_f32(h);
+    if (gates_out) {
+      E* gp = gates_out + row;
+      gp[j] = elem<E>::from_f32(ig);
+      gp[H + j] = elem<E>::from_f32(fg);
+      gp[2 * H + j] = elem<E>::from_f32(gg);
+      gp[3 * H + j] = elem<E>::from_f32(og);
+    }
+  }
+}
+
+// Backward cell for step t.  rec: [S][B][H] partial sums of dG_{t+1} W_h (or
+// NULL at t = T-1).  dc: in = dc arriving at c_t, out = dc for c_{t-1}.
+template <typename E>
+__global__ void __launch_bounds__(256) lstm_bwd_cell(
+    int B, int H, int S, const float* __restrict__ rec, const uint8_t* __restrict__ reset_next,
+    const float* __restrict__ dh_t, const float* __restrict__ dh_extra, const float* dc_in,
+    float* dc_out, const E* __restrict__ gates_t, const float* __restrict__ c_t,
+    const float* __restrict__ c_prev, const uint8_t* __restrict__ reset_t, E* __restrict__ dG_t,
+    float* __restrict__ db_part) {
+  __shared__ float red[kPwRowGroups][4][kPwCols];
+  const int jl = threadIdx.x & 63;
+  const int j = blockIdx.x * kPwCols + jl;
+  const int rg = threadIdx.x >> 6;
+  const size_t G = 4 * static_cast<size_t>(H);
+  const size_t sstride = static_cast<size_t>(B) * H;
+  float sdi = 0.f, sdf = 0.f, sdg = 0.f, sdo = 0.f;
+  if (j < H) {
+    for (int r = rg; r < kPwRows; r += kPwRowGroups) {
+      const int b = blockIdx.y * kPwRows + r;
+      if (b >= B) break;
+      const size_t hj = static_cast<size_t>(b) * H + j;
+      const size_t row = static_cast<size_t>(b) * G;
+      float dh = dh_t[hj];
+      if (dh_extra) dh += dh_extra[hj];
+      if (rec) {
+        float acc = 0.0f;
+        for (int s = 0; s < S; ++s) acc += rec[s * sstride + hj];
+        const float keep_n = (reset_next && reset_next[b]) ? 0.0f : 1.0f;
+        dh += keep_n * acc;
+      }
+      const float dcin = dc_in ? dc_in[hj] : 0.0f;
+      const float ig = elem<E>::to_f32(gates_t[row + j]);
+      const float fg = elem<E>::to_f32(gates_t[row + H + j]);
+      const float gg = elem<E>::to_f32(gates_t[row + 2 * H + j]);
+      const float og = elem<E>::to_f32(gates_t[row + 3 * H + j]);
+      const float tc = tanh_f(c_t[hj]);
+      const float keep = (reset_t && reset_t[b]) ? 0.0f : 1.0f;
+      const float cp = keep * c_prev[hj];
+      const float dc = dcin + dh * og * (1.0f - tc * tc);
+      const float dai = dc * gg * ig * (1.0f - ig);
+      const float daf = dc * cp * fg * (1.0f - fg);
+      const float dag = dc * ig * (1.0f - gg * gg);
+      const float dao = dh * tc * og * (1.0f - og);
+      dc_out[hj] = keep * dc * fg;
+      dG_t[row + j] = elem<E>::from_f32(dai);
+      dG_t[row + H + j] = elem<E>::from_f32(daf);
+      dG_t[row + 2 * H + j] = elem<E>::from_f32(dag);
+      dG_t[row + 3 * H + j] = elem<E>::from_f32(dao);
+      sdi += dai;
+      sdf += daf;
+      sdg += dag;
+      sdo += dao;
+    }
+  }
+  red[rg][0][jl] = sdi;
+  red[rg][1][jl] = sdf;
+  red[rg][2][jl] = sdg;
+  red[rg][3][jl] = sdo;
+  __syncthreads();
+  if (rg == 0 && j < H) {
+    float* out = db_part + static_cast<size_t>(blockIdx.y) * G;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      float s = 0.0f;
+#pragma unroll
+      for (int q = 0; q < kPwRowGroups; ++q) s += red[q][g][jl];
+      out[g * H + j] = s;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- layouts
+
+struct FwdWs {
+  size_t pre, h0e, total;
+  GemmPlan plan;
+};
+
+static FwdWs fwd_ws(o5_dtype dt, int T, int B, int D, int H) {
+  (void)T;
+  FwdWs w;
+  w.plan = plan_gemm(dt == O5_BF16, B, 4 * H, D + H);
+  size_t o = 0;
+  w.pre = o;
+  o += align_up(static_cast<size_t>(w.plan.splits) * B * 4 * H * sizeof(float));
+  w.h0e = o;
+  o += align_up(static_cast<size_t>(B) * H * dtype_size(dt));
+  w.total = o;
+  return w;
+}
+
+struct BwdWs {
+  size_t dG, dc, rec, h0e, dbpart, total;
+  int nbc;
+  GemmPlan plan_dh, plan_dw, plan_dx;
+};
+
+static BwdWs bwd_ws(o5_dtype dt, int T, int B, int D, int H) {
+  BwdWs w;
+  const bool bf = dt == O5_BF16;
+  w.plan_dh = plan_gemm(bf, B, H, 4 * H);
+  w.plan_dw = plan_gemm(bf, 4 * H, D + H, T * B);
+  w.plan_dw.splits = 1;  // dW is written directly (M x N tiles are plentiful)
+  w.plan_dx = plan_gemm(bf, T * B, D, 4 * H);
+  w.plan_dx.splits = 1;
+  w.nbc = cdiv(B, kPwRows);
+  size_t o = 0;
+  w.dG = o;
+  o += align_up(static_cast<size_t>(T) * B * 4 * H * dtype_size(dt));
+  w.dc = o;
+  o += align_up(static_cast<size_t>(B) * H * sizeof(float));
+  w.rec = o;
+  o += align_up(static_cast<size_t>(w.plan_dh.splits) * B * H * sizeof(float));
+  w.h0e = o;
+  o += align_up(static_cast<size_t>(B) * H * dtype_size(dt));
+  w.dbpart = o;
+  o += align_up(static_cast<size_t>(T) * w.nbc * 4 * H * sizeof(float));
+  w.total = o;
+  return w;
+}
+
+static int check_dims(const char* fn, o5_dtype dt, int T, int B, int D, int H) {
+  O5_CHECK(dt == O5_F32 || dt == O5_BF16, O5_E_DTYPE, "%s: unknown dtype %d", fn, static_cast<int>(dt));
+  O5_CHECK(T >= 1 && B >= 1, O5_E_SHAPE, "%s: T=%d and B=%d must be >= 1", fn, T, B);
+  O5_CHECK(D >= 64 && H >= 64 && D % 64 == 0 && H % 64 == 0 && D <= 65536 && H <= 65536, O5_E_SHAPE,
+           "%s: D=%d and H=%d must be positive multiples of 64 (<= 65536)", fn, D, H);
+  O5_CHECK(static_cast<long long>(T) * B * 4 * H < (1ll << 31) && static_cast<long long>(T) * B * D < (1ll << 31),
+           O5_E_SHAPE, "%s: T*B*4H and T*B*D must stay below 2^31", fn);
+  return O5_OK;
+}
+
+// ------------------------------------------------------------- forward
+
+template <typename E>
+static int lstm_fwd_impl(int T, int B, int D, int H, const E* x, const E* Wx, const E* Wh, const float* bias,
+                         const float* h0, const float* c0, const uint8_t* reset, E* h, float* c, E* gates, char* ws,
+                         const FwdWs& w, hipStream_t s) {
+  const size_t BH = static_cast<size_t>(B) * H;
+  float* pre = reinterpret_cast<float*>(ws + w.pre);
+  const E* h0e;
+  if constexpr (sizeof(E) == 2) {
+    E* tmp = reinterpret_cast<E*>(ws + w.h0e);
+    const int st = o5_f32_to_bf16(BH, h0, reinterpret_cast<uint16_t*>(tmp), s);
+    if (st != O5_OK) return st;
+    h0e = tmp;
+  } else {
+    h0e = h0;
+  }
+  const dim3 pw_grid(cdiv(H, kPwCols), cdiv(B, kPwRows));
+  for (int t = 0; t < T; ++t) {
+    const E* hprev = t == 0 ? h0e : h + (t - 1) * BH;
+    const uint8_t* rt = reset ? reset + static_cast<size_t>(t) * B : nullptr;
+    KRows2<E> al{x + static_cast<size_t>(t) * B * D, hprev, rt, D, H, D, D + H, B};
+    KRows2<E> bl{Wx, Wh, nullptr, D, H, D, D + H, 4 * H};
+    EpiStoreF32 epi{pre, 4 * H, static_cast<size_t>(B) * 4 * H};
+    ktimer_begin(kSiteLstmFwdGemm, s);
+    run_gemm(w.plan, al, bl, epi, B, 4 * H, D + H, s);
+    ktimer_end(kSiteLstmFwdGemm, s);
+    const float* cprev = t == 0 ? c0 : c + (t - 1) * BH;
+    E* gt = gates ? gates + static_cast<size_t>(t) * B * 4 * H : nullptr;
+    ktimer_begin(kSiteLstmFwdCell, s);
+    hipLaunchKernelGGL(lstm_fwd_cell<E>, pw_grid, dim3(256), 0, s, B, H, w.plan.splits, pre, bias, cprev, rt,
+                       h + t * BH, c + t * BH, gt);
+    ktimer_end(kSiteLstmFwdCell, s);
+  }
+  return check_launch("o5_lstm_fwd");
+}
+
+// ------------------------------------------------------------ backward
+
+template <typename E>
+static int lstm_bptt_impl(int T, int B, int D, int H, const E* x, const E* Wx, const E* Wh, const float* h0,
+                          const float* c0, const uint8_t* reset, const E* h, const float* c, const E* gates,
+                          const float* dh, const float* dhT, const float* dcT, float* dWx, float* dWh, float* db,
+                          E* dx, char* ws, const BwdWs& w, hipStream_t s) {
+  const size_t BH = static_cast<size_t>(B) * H;
+  const size_t BG = static_cast<size_t>(B) * 4 * H;
+  E* dG = reinterpret_cast<E*>(ws + w.dG);
+  float* dc = reinterpret_cast<float*>(ws + w.dc);
+  float* rec = reinterpret_cast<float*>(ws + w.rec);
+  float* dbpart = reinterpret_cast<float*>(ws + w.dbpart);
+  const E* h0e;
+  if constexpr (sizeof(E) == 2) {
+    E* tmp = reinterpret_cast<E*>(ws + w.h0e);
+    const int st = o5_f32_to_bf16(BH, h0, reinterpret_cast<uint16_t*>(tmp), s);
+    if (st != O5_OK) return st;
+    h0e = tmp;
+  } else {
+    h0e = h0;
+  }
+  const dim3 pw_grid(cdiv(H, kPwCols), w.nbc);
+  for (int t = T - 1; t >= 0; --t) {
+    const float* recp = nullptr;
+    if (t < T - 1) {
+      // R = dG_{t+1} . W_h :  A(i=b, k=n) = dG_{t+1}[b, n];  B(j, k=n) = W_h[n, j]
+      KRows2<E> al{dG + (t + 1) * BG, nullptr, nullptr, 4 * H, 0, 4 * H, 4 * H, B};
+      ICols2<E> bl{Wh, nullptr, nullptr, nullptr, H, 0, H, H, 4 * H, 0};
+      EpiStoreF32 epi{rec, H, BH};
+      ktimer_begin(kSiteLstmDhGemm, s);
+      run_gemm(w.plan_dh, al, bl, epi, B, H, 4 * H, s);
+      ktimer_end(kSiteLstmDhGemm, s);
+      recp = rec;
+    }
+    const uint8_t* rt = reset ? reset + static_cast<size_t>(t) * B : nullptr;
+    const uint8_t* rn = (reset && t < T - 1) ? reset + static_cast<size_t>(t + 1) * B : nullptr;
+    const float* dcin = t == T - 1 ? dcT : dc;
+    const float* dhx = t == T - 1 ? dhT : nullptr;
+    const float* cprev = t == 0 ? c0 : c + (t - 1) * BH;
+    ktimer_begin(kSiteLstmBwdCell, s);
+    hipLaunchKernelGGL(lstm_bwd_cell<E>, pw_grid, dim3(256), 0, s, B, H, w.plan_dh.splits, recp, rn, dh + t * BH, dhx,
+                       dcin, dc, gates + t * BG, c + t * BH, cprev, rt, dG + t * BG,
+                       dbpart + static_cast<size_t>(t) * w.nbc * 4 * H);
+    ktimer_end(kSiteLstmBwdCell, s);
+  }
+  // [dW_x | dW_h] = dG^T . [x | h~_prev] over the T*B rows r = t*B + b
+  {
+    const int R = T * B;
+    ICols2<E> al{dG, nullptr, nullptr, nullptr, 4 * H, 0, 4 * H, 4 * H, R, 0};
+    ICols2<E> bl{x, h0e, h, reset, D, H, D, D + H, R, B};
+    EpiStoreF32Split2 epi{dWx, dWh, D, H, D};
+    ktimer_begin(kSiteLstmDwGemm, s);
+    run_gemm(w.plan_dw, al, bl, epi, 4 * H, D + H, R, s);
+    ktimer_end(kSiteLstmDwGemm, s);
+  }
+  hipLaunchKernelGGL(colsum_rows, dim3(cdiv(4 * H, 256)), dim3(256), 0, s, T * w.nbc, 4 * H, dbpart, db);
+  if (dx) {
+    // dx = dG . W_x :  A(i=r, k=n) = dG[r, n];  B(j=d, k=n) = W_x[n, d]
+    const int R = T * B;
+    KRows2<E> al{dG, nullptr, nullptr, 4 * H, 0, 4 * H, 4 * H, R};
+    ICols2<E> bl{Wx, nullptr, nullptr, nullptr, D, 0, D, D, 4 * H, 0};
+    EpiStoreElem<E> epi{dx, D};
+    ktimer_begin(kSiteLstmDxGemm, s);
+    run_gemm(w.plan_dx, al, bl, epi, R, D, 4 * H, s);
+    ktimer_end(kSiteLstmDxGemm, s);
+  }
+  return check_launch("o5_lstm_bptt");
+}
+
+}  // namespace o5
+
+using namespace o5;
+
+extern "C" size_t o5_lstm_fwd_workspace_bytes(o5_dtype dt, int T, int B, int D, int H) {
+  if (check_dims("o5_lstm_fwd_workspace_bytes", dt, T, B, D, H) != O5_OK) return 0;
+  return fwd_ws(dt, T, B, D, H).total;
+}
+
+extern "C" int o5_lstm_fwd(o5_dtype dt, int T, int B, int D, int H, const void* x, const void* Wx, const void* Wh,
+                           const float* b, const float* h0, const float* c0, const uint8_t* reset, void* h, float* c,
+                           void* gates, void* ws, size_t ws_bytes, void* stream) {
+  int st = check_dims("o5_lstm_fwd", dt, T, B, D, H);
+  if (st != O5_OK) return st;
+  O5_PTR(x, "x");
+  O5_PTR(Wx, "Wx");
+  O5_PTR(Wh, "Wh");
+  O5_PTR(b, "b");
+  O5_PTR(h0, "h0");
+  O5_PTR(c0, "c0");
+  O5_OPT_PTR(reset, "reset");
+  O5_PTR(h, "h");
+  O5_PTR(c, "c");
+  O5_OPT_PTR(gates, "gates");
+  const FwdWs w = fwd_ws(dt, T, B, D, H);
+  O5_CHECK(ws != nullptr && ws_bytes >= w.total, O5_E_WORKSPACE, "o5_lstm_fwd: workspace needs %zu bytes, got %zu",
+           w.total, ws ? ws_bytes : static_cast<size_t>(0));
+  O5_CHECK(aligned16(ws), O5_E_ALIGN, "o5_lstm_fwd: ws is not 16-byte aligned");
+  char* wsp = static_cast<char*>(ws);
+  hipStream_t s = as_stream(stream);
+  if (dt == O5_BF16)
+    return lstm_fwd_impl<uint16_t>(T, B, D, H, static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(Wx),
+                                   static_cast<const uint16_t*>(Wh), b, h0, c0, reset, static_cast<uint16_t*>(h), c,
+                                   static_cast<uint16_t*>(gates), wsp, w, s);
+  return lstm_fwd_impl<float>(T, B, D, H, static_cast<const float*>(x), static_cast<const float*>(Wx),
+                              static_cast<const float*>(Wh), b, h0, c0, reset, static_cast<float*>(h), c,
+                              static_cast<float*>(gates), wsp, w, s);
+}
+
+extern "C" size_t o5_lstm_bptt_workspace_bytes(o5_dtype dt, int T, int B, int D, int H) {
+  if (check_dims("o5_lstm_bptt_workspace_bytes", dt, T, B, D, H) != O5_OK) return 0;
+  return bwd_ws(dt, T, B, D, H).total;
+}
+
+extern "C" int o5_lstm_bptt(o5_dtype dt, int T, int B, int D, int H, const void* x, const void* Wx, const void* Wh,
+                            const float* h0, const float* c0, const uint8_t* reset, const void* h, const float* c,
+                            const void* gates, const float* dh, const float* dhT, const float* dcT, float* dWx,
+                            float* dWh, float* db, void* dx, void* ws, size_t ws_bytes, void* stream) {
+  int st = check_dims("o5_lstm_bptt", dt, T, B, D, H);
+  if (st != O5_OK) return st;
+  O5_PTR(x, "x");
+  O5_PTR(Wx, "Wx");
+  O5_PTR(Wh, "Wh");
+  O5_PTR(h0, "h0");
+  O5_PTR(c0, "c0");
+  O5_OPT_PTR(reset, "reset");
+  O5_PTR(h, "h");
+  O5_PTR(c, "c");
+  O5_PTR(gates, "gates");
+  O5_PTR(dh, "dh");
+  O5_OPT_PTR(dhT, "dhT");
+  O5_OPT_PTR(dcT, "dcT");
+  O5_PTR(dWx, "dWx");
+  O5_PTR(dWh, "dWh");
+  O5_PTR(db, "db");
+  O5_OPT_PTR(dx, "dx");
+  const BwdWs w = bwd_ws(dt, T, B, D, H);
+  O5_CHECK(ws != nullptr && ws_bytes >= w.total, O5_E_WORKSPACE,
+           "o5_lstm_bptt: workspace needs %zu bytes, got %zu", w.total, ws ? ws_bytes : static_cast<size_t>(0));
+  O5_CHECK(aligned16(ws), O5_E_ALIGN, "o5_lstm_bptt: ws is not 16-byte aligned");
+  char* wsp = static_cast<char*>(ws);
+  hipStream_t s = as_stream(stream);
+  if (dt == O5_BF16)
+    return lstm_bptt_impl<uint16_t>(T, B, D, H, static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(Wx),
+                                    static_cast<const uint16_t*>(Wh), h0, c0, reset,
+                                    static_cast<const uint16_t*>(h), c, static_cast<const uint16_t*>(gates), dh, dhT,
+                                    dcT, dWx, dWh, db, static_cast<uint16_t*>(dx), wsp, w, s);
+  return lstm_bptt_impl<float>(T, B, D, H, static_cast<const float*>(x), static_cast<const float*>(Wx),
+                               static_cast<const float*>(Wh), h0, c0, reset, static_cast<const float*>(h), c,
+                               static_cast<const float*>(gates), dh, dhT, dcT, dWx, dWh, db,
+                               static_cast<float*>(dx), wsp, w, s);
+}

@@ -1,0 +1,85 @@
+"""The C ABI on the CPU: libo5.so loads, exports every function include/o5.h
+declares, and rejects bad arguments on the host before anything is enqueued
+(no GPU needed: these calls fail validation before any HIP call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1912_06680_amd import o5
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "o5.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(o5_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(o5.LIB_PATH):
+        pytest.skip("libo5.so not built")
+    return o5.lib()
+
+
+def test_header_declares_the_binding_table():
+    assert _declared_functions() == sorted(o5.EXPORTED)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+    assert o5.o5_version() == 100
+    assert o5.o5_status_str(0).startswith("O5_OK")
+    assert o5.o5_status_str(5).startswith("O5_E_WORKSPACE")
+
+
+def test_host_validation_errors(lib):
+    L = lib
+    # NULL pointers are rejected with O5_E_NULL
+    st = L.o5_gae(16, 8, None, None, None, 0.99, 0.95, None, None, None)
+    assert st == 1 and "NULL" in o5.o5_last_error()
+    # shapes
+    assert L.o5_gae(0, 8, 16, 16, 16, 0.99, 0.95, 16, 16, None) == 2
+    assert L.o5_segments_to_samples(10, 2, 3, 16, 16, 16, 16, 16, 16, None) == 2
+    # misaligned pointer
+    assert L.o5_gae(16, 8, 0x1001, 16, 16, 0.99, 0.95, 16, 16, None) == 4
+    # argument range
+    assert L.o5_gae(16, 8, 16, 16, 16, 1.5, 0.95, 16, 16, None) == 7
+    hp = o5.AdamHp(1e-3, 0.9, 0.999, 1e-8, 5.0)
+    assert L.o5_adam_step(10, 16, 16, 16, 16, None, hp, 0, None) == 7
+    # dtype and LSTM shapes
+    assert L.o5_lstm_fwd(9, 1, 1, 64, 64, *([16] * 11), 1 << 20, None) == 3
+    assert L.o5_lstm_fwd(0, 1, 1, 60, 64, *([16] * 11), 1 << 20, None) == 2
+    # workspace too small
+    need = L.o5_lstm_fwd_workspace_bytes(1, 16, 8, 64, 128)
+    assert need > 0
+    assert L.o5_lstm_fwd(1, 16, 8, 64, 128, *([16] * 11), need - 1, None) == 5
+    # heads
+    heads = (ctypes.c_int * 2)(3, 0)
+    assert L.o5_ppo_loss_grad_workspace_bytes(0, 8, 64, 2, heads) == 0
+    assert "head_sizes[1]" in o5.o5_last_error()
+
+
+def test_workspace_queries_are_positive(lib):
+    for dt in (0, 1):
+        assert o5.o5_lstm_fwd_workspace_bytes(dt, 16, 2048, 4096, 4096) > 0
+        assert o5.o5_lstm_bptt_workspace_bytes(dt, 16, 2048, 4096, 4096) > 0
+        assert o5.o5_ppo_loss_grad_workspace_bytes(dt, 32768, 4096, (30, 8, 32, 4)) > 0
+        assert o5.o5_policy_sample_workspace_bytes(dt, 4096, 4096, (30, 8, 32, 4)) > 0
+
+
+def test_binding_arity_matches_header():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    found = 0
+    for m in re.finditer(r"\b(o5_[a-z0-9_]+)\s*\(([^;{]*?)\)\s*;", text):
+        name, args = m.group(1), m.group(2).strip()
+        n = 0 if args in ("void", "") else args.count(",") + 1
+        assert len(o5._SIGS[name][1]) == n, name
+        found += 1
+    assert found == len(o5.EXPORTED)

@@ -1,0 +1,161 @@
+"""GPU parity: o5_lstm_fwd and o5_lstm_bptt against the fp64 oracle.
+
+fp32 path: every input fp32, tolerance 1e-4.  bf16 path: the oracle takes
+the bf16-rounded x, W_x, W_h; the GPU keeps h, the saved gates and dG in bf16
+and accumulates in fp32; tolerance 3e-2.  Shapes span several tiles with
+ragged edges in B and in the 4H / D+H dimensions, resets inside samples, and
+the paper-scale shape (B=1024, T=16, D=H=4096) on sampled rows.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle.bf16 import round_to_bf16
+from oracle.lstm import lstm_bptt, lstm_forward
+from paper_1912_06680_amd import o5
+from tests.gpu_util import (TOL_BF16, TOL_F32, assert_close, banner, dev, dev_dt, dev_f32, empty_dt, host,
+                            need_gpu, workspace)
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(T, B, D, H, seed, state_std=0.1, p_reset=0.0):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    bound = 1.0 / np.sqrt(H)
+    Wx = ((rng.random((4 * H, D), dtype=np.float32) * 2 - 1) * bound).astype(np.float32)
+    Wh = ((rng.random((4 * H, H), dtype=np.float32) * 2 - 1) * bound).astype(np.float32)
+    b = ((rng.random(4 * H, dtype=np.float32) * 2 - 1) * bound).astype(np.float32)
+    x = rng.standard_normal((T, B, D), dtype=np.float32)
+    h0 = (rng.standard_normal((B, H), dtype=np.float32) * state_std).astype(np.float32)
+    c0 = (rng.standard_normal((B, H), dtype=np.float32) * state_std).astype(np.float32)
+    reset = (rng.random((T, B)) < p_reset).astype(np.uint8) if p_reset > 0 else None
+    dh = rng.standard_normal((T, B, H), dtype=np.float32)
+    dhT = rng.standard_normal((B, H), dtype=np.float32)
+    dcT = rng.standard_normal((B, H), dtype=np.float32)
+    return dict(Wx=Wx, Wh=Wh, b=b, x=x, h0=h0, c0=c0, reset=reset, dh=dh, dhT=dhT, dcT=dcT)
+
+
+def _run_gpu(inp, T, B, D, H, bf16, with_final=True, want_dx=True):
+    dt = o5.O5_BF16 if bf16 else o5.O5_F32
+    x, Wx, Wh = dev_dt(inp["x"], bf16), dev_dt(inp["Wx"], bf16), dev_dt(inp["Wh"], bf16)
+    b, h0, c0 = dev_f32(inp["b"]), dev_f32(inp["h0"]), dev_f32(inp["c0"])
+    reset = dev(inp["reset"]) if inp["reset"] is not None else None
+    h = empty_dt((T, B, H), bf16)
+    c = torch.empty((T, B, H), dtype=torch.float32, device="cuda")
+    gates = empty_dt((T, B, 4 * H), bf16)
+    ws = workspace(max(o5.o5_lstm_fwd_workspace_bytes(dt, T, B, D, H),
+                       o5.o5_lstm_bptt_workspace_bytes(dt, T, B, D, H)))
+    o5.o5_lstm_fwd(dt, T, B, D, H, x, Wx, Wh, b, h0, c0, reset, h, c, gates, ws)
+    dWx = torch.empty((4 * H, D), dtype=torch.float32, device="cuda")
+    dWh = torch.empty((4 * H, H), dtype=torch.float32, device="cuda")
+    db = torch.empty(4 * H, dtype=torch.float32, device="cuda")
+    dx = empty_dt((T, B, D), bf16) if want_dx else None
+    dhT = dev_f32(inp["dhT"]) if with_final else None
+    dcT = dev_f32(inp["dcT"]) if with_final else None
+    o5.o5_lstm_bptt(dt, T, B, D, H, x, Wx, Wh, h0, c0, reset, h, c, gates, dev_f32(inp["dh"]), dhT, dcT,
+                    dWx, dWh, db, dx, ws)
+    return dict(h=h, c=c, gates=gates, dWx=dWx, dWh=dWh, db=db, dx=dx)
+
+
+def _oracle(inp, bf16, with_final=True):
+    rnd = round_to_bf16 if bf16 else (lambda a: np.asarray(a, np.float64))
+    x, Wx, Wh = rnd(inp["x"]), rnd(inp["Wx"]), rnd(inp["Wh"])
+    h, c, gates = lstm_forward(x, Wx, Wh, inp["b"], inp["h0"], inp["c0"], inp["reset"])
+    dWx, dWh, db, dx = lstm_bptt(x, Wx, Wh, inp["h0"], inp["c0"], inp["reset"], h, c, gates, inp["dh"],
+                                 inp["dhT"] if with_final else None, inp["dcT"] if with_final else None,
+                                 want_dx=True)
+    return dict(h=h, c=c, gates=gates, dWx=dWx, dWh=dWh, db=db, dx=dx)
+
+
+CASES = [
+    # name, T, B, D, H, bf16, p_reset
+    ("f32-tiny", 16, 8, 64, 128, False, 0.0),
+    ("f32-ragged-reset", 5, 7, 64, 64, False, 0.2),
+    ("f32-mid", 16, 256, 1024, 1024, False, 0.005),
+    ("bf16-ragged-reset", 3, 300, 128, 192, True, 0.2),
+    ("bf16-mid", 16, 256, 1024, 1024, True, 0.005),
+    ("bf16-tall", 4, 520, 256, 320, True, 0.05),
+]
+
+
+@pytest.mark.parametrize("name,T,B,D,H,bf16,p_reset", CASES, ids=[c[0] for c in CASES])
+def test_lstm_fwd_bptt_matches_oracle(name, T, B, D, H, bf16, p_reset):
+    need_gpu()
+    banner(f"lstm {name} T={T} B={B} D={D} H={H} bf16={bf16}")
+    inp = _inputs(T, B, D, H, seed=T * 1000 + B + H, p_reset=p_reset)
+    got = _run_gpu(inp, T, B, D, H, bf16)
+    ref = _oracle(inp, bf16)
+    tol = TOL_BF16 if bf16 else TOL_F32
+    for k in ("h", "c", "gates", "dWx", "dWh", "db", "dx"):
+        assert_close(k, host(got[k]), ref[k], tol)
+
+
+def test_lstm_without_final_state_gradient_and_dx():
+    need_gpu()
+    banner("lstm f32 no dhT/dcT, no dx")
+    T, B, D, H = 4, 9, 64, 64
+    inp = _inputs(T, B, D, H, seed=5, p_reset=0.3)
+    got = _run_gpu(inp, T, B, D, H, False, with_final=False, want_dx=False)
+    ref = _oracle(inp, False, with_final=False)
+    for k in ("dWx", "dWh", "db"):
+        assert_close(k, host(got[k]), ref[k], TOL_F32)
+
+
+def test_lstm_inference_without_gates_and_determinism():
+    need_gpu()
+    banner("lstm bf16 inference (gates=NULL) and determinism")
+    T, B, D, H = 2, 64, 256, 256
+    inp = _inputs(T, B, D, H, seed=9)
+    dt = o5.O5_BF16
+    x, Wx, Wh = dev_dt(inp["x"], True), dev_dt(inp["Wx"], True), dev_dt(inp["Wh"], True)
+    b, h0, c0 = dev_f32(inp["b"]), dev_f32(inp["h0"]), dev_f32(inp["c0"])
+    ws = workspace(o5.o5_lstm_fwd_workspace_bytes(dt, T, B, D, H))
+    outs = []
+    for _ in range(2):
+        h = empty_dt((T, B, H), True)
+        c = torch.empty((T, B, H), dtype=torch.float32, device="cuda")
+        o5.o5_lstm_fwd(dt, T, B, D, H, x, Wx, Wh, b, h0, c0, None, h, c, None, ws)
+        outs.append((host(h), host(c)))
+    assert np.array_equal(outs[0][0], outs[1][0]) and np.array_equal(outs[0][1], outs[1][1])
+    ref = _oracle(inp, True)
+    assert_close("h", outs[0][0], ref["h"], TOL_BF16)
+
+
+def test_lstm_paper_scale_sampled_rows():
+    """B=1024, T=16, D=H=4096 in the benchmark's launch configuration.
+
+    Forward: rows are independent, so the oracle recomputes 3 sampled rows.
+    BPTT: the upstream gradient is nonzero only on those rows, so every
+    weight gradient is the sum over those rows alone, which the oracle
+    computes exactly."""
+    need_gpu()
+    T, B, D, H = 16, 1024, 4096, 4096
+    banner(f"lstm paper-scale sampled rows T={T} B={B} D={D} H={H}")
+    rng = np.random.Generator(np.random.PCG64(0))
+    bound = 1.0 / np.sqrt(H)
+    inp = dict(
+        Wx=((rng.random((4 * H, D), dtype=np.float32) * 2 - 1) * bound).astype(np.float32),
+        Wh=((rng.random((4 * H, H), dtype=np.float32) * 2 - 1) * bound).astype(np.float32),
+        b=((rng.random(4 * H, dtype=np.float32) * 2 - 1) * bound).astype(np.float32),
+        x=rng.standard_normal((T, B, D), dtype=np.float32),
+        h0=(rng.standard_normal((B, H), dtype=np.float32) * 0.1).astype(np.float32),
+        c0=(rng.standard_normal((B, H), dtype=np.float32) * 0.1).astype(np.float32),
+        reset=None,
+    )
+    rows = np.array([0, 517, 1023])
+    dh = np.zeros((T, B, H), np.float32)
+    dh[:, rows] = rng.standard_normal((T, len(rows), H), dtype=np.float32)
+    inp["dh"] = dh
+    inp["dhT"] = None
+    inp["dcT"] = None
+    got = _run_gpu(inp, T, B, D, H, True, with_final=False, want_dx=False)
+    sub = dict(inp)
+    sub["x"] = inp["x"][:, rows]
+    sub["h0"] = inp["h0"][rows]
+    sub["c0"] = inp["c0"][rows]
+    sub["dh"] = dh[:, rows]
+    ref = _oracle(sub, True, with_final=False)
+    assert_close("h[rows]", host(got["h"])[:, rows], ref["h"], TOL_BF16)
+    assert_close("c[rows]", host(got["c"])[:, rows], ref["c"], TOL_BF16)
+    for k in ("dWx", "dWh", "db"):
+        assert_close(k, host(got[k]), ref[k], TOL_BF16)

@@ -1,0 +1,169 @@
+"""GPU parity: o5_ppo_loss_grad and o5_policy_sample against the fp64 oracle."""
+import numpy as np
+import pytest
+import torch
+
+from oracle.bf16 import round_to_bf16
+from oracle.philox import gumbel_max_sample
+from oracle.ppo import STAT_NAMES, head_logprob_entropy, heads_forward, ppo_loss_grad
+from paper_1912_06680_amd import o5
+from tests.gpu_util import (TOL_BF16, TOL_F32, assert_close, banner, dev, dev_dt, dev_f32, host, need_gpu,
+                            workspace)
+
+pytestmark = pytest.mark.gpu
+
+HEADS = (30, 8, 32, 4)
+KINKS = (np.log(1.2), np.log(0.8))
+
+
+def _inputs(N, H, heads, seed, bf16, with_mask):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    A1 = sum(heads) + 1
+    bound = 1.0 / np.sqrt(H)
+    h = np.tanh(rng.standard_normal((N, H), dtype=np.float32)).astype(np.float32)
+    Wp = ((rng.random((A1, H), dtype=np.float32) * 2 - 1) * bound * 4).astype(np.float32)
+    bp = ((rng.random(A1, dtype=np.float32) * 2 - 1) * bound).astype(np.float32)
+    act = np.stack([rng.integers(0, n, N) for n in heads], axis=1).astype(np.int32)
+    adv = rng.standard_normal(N, dtype=np.float32)
+    ret = rng.standard_normal(N, dtype=np.float32)
+    mask = (rng.random((N, len(heads))) < 0.8).astype(np.uint8) if with_mask else None
+    # behaviour log-probabilities: the oracle's current log-probability shifted
+    # by U(-0.4, 0.4), kept >= 0.01 away from the clip kinks log(1.2), log(0.8)
+    hh = round_to_bf16(h) if bf16 else h.astype(np.float64)
+    ww = round_to_bf16(Wp) if bf16 else Wp.astype(np.float64)
+    z = heads_forward(hh, ww, bp)
+    logp, _, _ = head_logprob_entropy(z, act, heads)
+    m = np.ones_like(logp) if mask is None else mask.astype(np.float64)
+    logpi = (m * logp).sum(axis=1)
+    shift = rng.uniform(-0.4, 0.4, N)
+    for kk in KINKS:   # r = exp(-shift); keep -shift away from the kinks
+        near = np.abs(-shift - kk) < 0.01
+        shift[near] += 0.03
+    logp_old = (logpi + shift).astype(np.float32)
+    return dict(h=h, Wp=Wp, bp=bp, act=act, adv=adv, ret=ret, mask=mask, logp_old=logp_old, hh=hh, ww=ww)
+
+
+PPO_CASES = [
+    ("f32-small", 64, 64, HEADS, False, False),
+    ("f32-mask-ragged", 1001, 128, (5, 3, 7), False, True),
+    ("bf16-mid", 4096, 1024, HEADS, True, True),
+    ("bf16-one-head", 333, 192, (8,), True, False),
+]
+
+
+@pytest.mark.parametrize("name,N,H,heads,bf16,with_mask", PPO_CASES, ids=[c[0] for c in PPO_CASES])
+def test_ppo_loss_grad_matches_oracle(name, N, H, heads, bf16, with_mask):
+    need_gpu()
+    banner(f"ppo {name} N={N} H={H} heads={heads} bf16={bf16}")
+    inp = _inputs(N, H, heads, seed=N + H, bf16=bf16, with_mask=with_mask)
+    stats_ref, dh_ref, dWp_ref, dbp_ref, _ = ppo_loss_grad(
+        inp["hh"], inp["ww"], inp["bp"], inp["act"], inp["logp_old"], inp["adv"], inp["ret"], heads,
+        0.2, 1.0, 0.01, inp["mask"])
+    dt = o5.O5_BF16 if bf16 else o5.O5_F32
+    A1 = sum(heads) + 1
+    stats = torch.empty(8, dtype=torch.float32, device="cuda")
+    dh = torch.empty((N, H), dtype=torch.float32, device="cuda")
+    dWp = torch.empty((A1, H), dtype=torch.float32, device="cuda")
+    dbp = torch.empty(A1, dtype=torch.float32, device="cuda")
+    ws = workspace(o5.o5_ppo_loss_grad_workspace_bytes(dt, N, H, heads))
+    mask = dev(inp["mask"]) if inp["mask"] is not None else None
+    o5.o5_ppo_loss_grad(dt, N, H, heads, dev_dt(inp["h"], bf16), dev_dt(inp["Wp"], bf16), dev_f32(inp["bp"]),
+                        dev(inp["act"]), dev_f32(inp["logp_old"]), dev_f32(inp["adv"]), dev_f32(inp["ret"]),
+                        mask, 0.2, 1.0, 0.01, stats, dh, dWp, dbp, ws)
+    tol = TOL_BF16 if bf16 else TOL_F32
+    st = host(stats)
+    for i, name_ in enumerate(STAT_NAMES):
+        ref = stats_ref[name_]
+        e = abs(st[i] - ref) / max(abs(ref), 1e-6)
+        print(f"    stat {name_}: gpu={st[i]:.6g} ref={ref:.6g} rel={e:.2e}", flush=True)
+        assert e <= tol, name_
+    assert_close("dh", host(dh), dh_ref, tol)
+    assert_close("dWp", host(dWp), dWp_ref, tol)
+    assert_close("dbp", host(dbp), dbp_ref, tol)
+
+
+def test_ppo_ratio_one_invariant_on_gpu():
+    """logp_old = logpi makes every ratio 1: pg = -mean(A) and clipfrac = 0."""
+    need_gpu()
+    banner("ppo ratio=1 invariant")
+    N, H = 512, 64
+    inp = _inputs(N, H, HEADS, seed=1, bf16=False, with_mask=False)
+    z = heads_forward(inp["hh"], inp["ww"], inp["bp"])
+    logp, _, _ = head_logprob_entropy(z, inp["act"], HEADS)
+    logp_old = logp.sum(axis=1).astype(np.float32)
+    stats = torch.empty(8, dtype=torch.float32, device="cuda")
+    dh = torch.empty((N, H), dtype=torch.float32, device="cuda")
+    dWp = torch.empty((sum(HEADS) + 1, H), dtype=torch.float32, device="cuda")
+    dbp = torch.empty(sum(HEADS) + 1, dtype=torch.float32, device="cuda")
+    ws = workspace(o5.o5_ppo_loss_grad_workspace_bytes(0, N, H, HEADS))
+    o5.o5_ppo_loss_grad(0, N, H, HEADS, dev_f32(inp["h"]), dev_f32(inp["Wp"]), dev_f32(inp["bp"]), dev(inp["act"]),
+                        dev_f32(logp_old), dev_f32(inp["adv"]), dev_f32(inp["ret"]), None, 0.2, 1.0, 0.01, stats, dh,
+                        dWp, dbp, ws)
+    st = host(stats)
+    assert abs(st[1] - (-inp["adv"].astype(np.float64).mean())) < 1e-5
+    assert st[4] == 0.0 and abs(st[6] - 1.0) < 1e-5
+
+
+SAMPLE_CASES = [("f32", 512, 256, False), ("bf16", 1000, 512, True)]
+
+
+@pytest.mark.parametrize("name,B,H,bf16", SAMPLE_CASES, ids=[c[0] for c in SAMPLE_CASES])
+def test_policy_sample_matches_oracle(name, B, H, bf16):
+    need_gpu()
+    banner(f"policy_sample {name} B={B} H={H}")
+    inp = _inputs(B, H, HEADS, seed=B, bf16=bf16, with_mask=False)
+    seed, counter = 12345, 7
+    act_ref, logp_ref, v_ref, scores = gumbel_max_sample(heads_forward(inp["hh"], inp["ww"], inp["bp"]), HEADS,
+                                                          seed, counter)
+    dt = o5.O5_BF16 if bf16 else o5.O5_F32
+    act = torch.empty((B, len(HEADS)), dtype=torch.int32, device="cuda")
+    logp = torch.empty(B, dtype=torch.float32, device="cuda")
+    value = torch.empty(B, dtype=torch.float32, device="cuda")
+    ws = workspace(o5.o5_policy_sample_workspace_bytes(dt, B, H, HEADS))
+    o5.o5_policy_sample(dt, B, H, HEADS, dev_dt(inp["h"], bf16), dev_dt(inp["Wp"], bf16), dev_f32(inp["bp"]), seed,
+                        counter, act, logp, value, ws)
+    a = act.cpu().numpy()
+    # unique where the oracle's best score leads the runner-up by > 1e-4
+    agree = np.ones(B, bool)
+    for k in range(len(HEADS)):
+        s = np.sort(scores[k], axis=1)
+        clear = (s[:, -1] - s[:, -2]) > 1e-4
+        mism = (a[:, k] != act_ref[:, k])
+        assert not np.any(mism & clear), f"head {k}: {np.sum(mism & clear)} clear-cut mismatches"
+        # near ties: the GPU's choice must be one of the near-maximal logits
+        for b in np.where(mism)[0]:
+            assert scores[k][b, a[b, k]] >= s[b, -1] - 1e-4
+        agree &= ~mism
+    assert agree.mean() > 0.99
+    tol = TOL_BF16 if bf16 else TOL_F32
+    assert_close("logp", host(logp)[agree], logp_ref[agree], tol)
+    assert_close("value", host(value), v_ref, tol)
+
+
+def test_policy_sample_frequencies_follow_softmax():
+    """Property at any size: with identical rows, the sampled actions follow
+    softmax(z) (chi-square), and another counter gives other draws."""
+    need_gpu()
+    banner("policy_sample frequencies")
+    from scipy import stats as sstats
+    B, H = 100000, 64
+    rng = np.random.Generator(np.random.PCG64(3))
+    heads = (6, 3)
+    h_row = rng.standard_normal(H, dtype=np.float32) * 0.5
+    Wp = rng.standard_normal((10, H), dtype=np.float32) * 0.3
+    bp = np.zeros(10, np.float32)
+    h = np.broadcast_to(h_row, (B, H)).copy()
+    act = torch.empty((B, 2), dtype=torch.int32, device="cuda")
+    logp = torch.empty(B, dtype=torch.float32, device="cuda")
+    value = torch.empty(B, dtype=torch.float32, device="cuda")
+    ws = workspace(o5.o5_policy_sample_workspace_bytes(0, B, H, heads))
+    o5.o5_policy_sample(0, B, H, heads, dev_f32(h), dev_f32(Wp), dev_f32(bp), 99, 0, act, logp, value, ws)
+    a = act.cpu().numpy()
+    z = Wp.astype(np.float64) @ h_row.astype(np.float64)
+    off = 0
+    for k, n in enumerate(heads):
+        p = np.exp(z[off:off + n] - z[off:off + n].max())
+        p /= p.sum()
+        counts = np.bincount(a[:, k], minlength=n)
+        assert sstats.chisquare(counts, B * p).pvalue > 1e-3
+        off += n
