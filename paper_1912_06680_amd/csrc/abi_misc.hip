@@ -112,6 +112,10 @@ extern "C" const char* o5_status_str(int status) {
 extern "C" const char* o5_last_error(void) { return o5::g_last_error; }
 
 extern "C" int o5_ktimer_enable(int on) {
+  if (!on) {  // stop recording; keep what was recorded
+    g_kt.on = false;
+    return O5_OK;
+  }
   for (int i = 0; i < kSiteCount; ++i) {
     for (auto& pr : g_kt.done[i]) {
       g_kt.pool.push_back(pr.first);
@@ -120,7 +124,7 @@ extern "C" int o5_ktimer_enable(int on) {
     g_kt.done[i].clear();
     g_kt.open[i] = nullptr;
   }
-  g_kt.on = on != 0;
+  g_kt.on = true;
   return O5_OK;
 }
 

@@ -7,23 +7,27 @@
 //   weights  dW    = dG^T . [x | h~_prev]                   (A, B I-contiguous)
 //   input    dx    = dG . W_x                               (B I-contiguous)
 // A loader reports whether its reduction index k is the contiguous one
-// (kKMajor) and hands out elements (fp32 engine) or 8-element 16-byte
-// vectors (bf16 MFMA engine), returning zeros outside the matrix.
+// (kKMajor), hands out single elements to the fp32 engine (at) and, for
+// the bf16 engine, has a per-thread Tile state that precomputes everything
+// that does not change along K (row offsets, masks, sources) so that the
+// K loop issues plain 16-byte loads with no branches.
 //
 // bf16 engine (gfx950 MFMA, v_mfma_f32_32x32x16_bf16, fp32 accumulate):
 //  * block tile BM x BN, K tile 64, waves arranged (BM/WM) x (BN/WN), each
-//    wave owning WM x WN = (WM/32) x (WN/32) MFMA blocks;
-//  * both tiles staged in LDS as [row][64 k] bf16, double buffered, with the
-//    16-byte chunk index XOR-swizzled by (row >> 1) & 7 so that the 16 lanes
-//    of a fragment read (16 consecutive rows, same chunk) hit 16 distinct
-//    16-byte bank groups;
+//    wave owning (WM/32) x (WN/32) MFMA blocks;
+//  * both tiles staged in LDS as [row][64 k] bf16, double buffered, the
+//    16-byte chunk index XOR-swizzled by (row >> 1) & 7 so that 16
+//    consecutive rows read at one chunk hit 16 distinct 16-byte bank groups;
 //  * operands whose contiguous index is not k are loaded as 8x8 blocks and
-//    transposed in registers (v_perm) before the LDS store, so the MFMA
-//    fragment reads are always single 16-byte LDS reads;
-//  * global loads of tile kt+1 are in flight while tile kt is multiplied;
-//  * tiles are numbered so that the M-tiles sharing one B tile run
-//    back-to-back on one XCD (blocks are dealt round-robin to the 8 XCDs),
-//    which keeps the weight tile in that XCD's L2;
+//    transposed in registers (v_perm) before the LDS store, so MFMA fragment
+//    reads are always single 16-byte LDS reads;
+//  * global loads of tile kt+1 are in flight while tile kt is multiplied,
+//    and the fragments of k-step kk+1 are read from LDS while the MFMAs of
+//    k-step kk run;
+//  * blocks are dealt round-robin to the 8 XCDs; each XCD gets a contiguous
+//    run of tiles ordered in groups of 8 M-tiles (M-tile fastest), so the
+//    ~32 blocks an XCD runs at once cover 8 M-tiles x 4 N-tiles and share
+//    both operands in that XCD's L2;
 //  * optional split-K over gridDim.z; split z writes its partial sums to
 //    its own slice (the caller reduces the slices in a fixed order).
 #pragma once
@@ -35,6 +39,43 @@ namespace o5 {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
+__device__ __forceinline__ uint4 zero4() { return make_uint4(0u, 0u, 0u, 0u); }
+__device__ __forceinline__ uint4 sel4(bool keep, uint4 v) { return keep ? v : zero4(); }
+
+// LDS byte offset of 16-byte chunk `chunk` (0..7) of tile row `row`
+// (a row is 64 bf16 = 128 bytes).
+__device__ __forceinline__ int lds_off(int row, int chunk) {
+  return row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4);
+}
+
+// Transpose an 8 x 8 block of 16-bit values held as 8 rows of 4 dwords:
+// in[r] = elements (r, 0..7) -> out[c] = elements (0..7, c).
+__device__ __forceinline__ void transpose8x8_b16(const uint4 (&in)[8], uint4 (&out)[8]) {
+  // v_perm_b32(hi_src, lo_src, sel): bytes 0-3 from lo_src, 4-7 from hi_src
+  const uint32_t kLo = 0x05040100u;  // (lo.lo16, hi.lo16)
+  const uint32_t kHi = 0x07060302u;  // (lo.hi16, hi.hi16)
+#pragma unroll
+  for (int c2 = 0; c2 < 4; ++c2) {  // pair of output columns 2*c2, 2*c2+1
+    uint32_t w[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const uint4 v = in[r];
+      w[r] = c2 == 0 ? v.x : c2 == 1 ? v.y : c2 == 2 ? v.z : v.w;
+    }
+    uint4 lo, hi;
+    lo.x = __builtin_amdgcn_perm(w[1], w[0], kLo);
+    lo.y = __builtin_amdgcn_perm(w[3], w[2], kLo);
+    lo.z = __builtin_amdgcn_perm(w[5], w[4], kLo);
+    lo.w = __builtin_amdgcn_perm(w[7], w[6], kLo);
+    hi.x = __builtin_amdgcn_perm(w[1], w[0], kHi);
+    hi.y = __builtin_amdgcn_perm(w[3], w[2], kHi);
+    hi.z = __builtin_amdgcn_perm(w[5], w[4], kHi);
+    hi.w = __builtin_amdgcn_perm(w[7], w[6], kHi);
+    out[2 * c2] = lo;
+    out[2 * c2 + 1] = hi;
+  }
+}
+
 // ------------------------------------------------------------------ loaders
 
 // (i, k) -> K-contiguous rows, two segments along k: k < K0 reads p0[i*ld0 + k],
@@ -43,6 +84,7 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 template <typename E>
 struct KRows2 {
   static constexpr bool kKMajor = true;
+  static constexpr bool kBf16 = sizeof(E) == 2;
   const E* p0;
   const E* p1;
   const uint8_t* mask1;
@@ -54,13 +96,50 @@ struct KRows2 {
     if (mask1 && mask1[i]) return 0.0f;
     return elem<E>::to_f32(p1[static_cast<size_t>(i) * ld1 + (k - K0)]);
   }
-  // 8 consecutive k starting at k (k % 8 == 0, K0 % 8 == 0); bf16 only
-  __device__ __forceinline__ uint4 vec(int i, int k) const {
-    if (i >= rows || k >= K) return make_uint4(0, 0, 0, 0);
-    if (k < K0) return *reinterpret_cast<const uint4*>(p0 + static_cast<size_t>(i) * ld0 + k);
-    if (mask1 && mask1[i]) return make_uint4(0, 0, 0, 0);
-    return *reinterpret_cast<const uint4*>(p1 + static_cast<size_t>(i) * ld1 + (k - K0));
-  }
+
+  // Per-thread state of the bf16 engine for a ROWS x 64 tile loaded by NT
+  // threads: thread t always loads chunk (t & 7) of rows (t >> 3) + u*NT/8.
+  // Requires K0 % 64 == 0 (a K tile never straddles the two sources),
+  // K % 8 == 0 and rows * ld < 2^31; bf16 only.
+  template <int ROWS, int NT>
+  struct Tile {
+    static constexpr int kPer = ROWS * 8 / NT;
+    static constexpr int kVecs = kPer;
+    static_assert(ROWS * 8 % NT == 0, "tile/threads mismatch");
+    int off0[kPer], off1[kPer];  // element offset of each row in p0 / p1; < 0 -> zeros
+    int chunk;
+
+    __device__ __forceinline__ void init(const KRows2& l, int row0, int tid) {
+      chunk = (tid & 7) * 8;
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int row = row0 + (tid >> 3) + u * (NT / 8);
+        const bool valid = row < l.rows;
+        const bool masked = valid && l.mask1 != nullptr && l.mask1[row] != 0;
+        off0[u] = valid ? row * l.ld0 : -1;
+        off1[u] = (valid && !masked) ? row * l.ld1 : -1;
+      }
+    }
+    __device__ __forceinline__ void load(const KRows2& l, int k0, uint4 (&r)[kVecs]) const {
+      const bool seg0 = k0 < l.K0;  // uniform over the block
+      const bool kok = k0 + chunk < l.K;
+      const E* base = seg0 ? l.p0 + k0 : l.p1 + (k0 - l.K0);
+      const int kc = kok ? chunk : 0;  // k0 itself is always inside the row
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int off = seg0 ? off0[u] : off1[u];
+        const uint4 v = *reinterpret_cast<const uint4*>(base + (off < 0 ? 0 : off) + kc);
+        r[u] = sel4(off >= 0 && kok, v);
+      }
+    }
+    __device__ __forceinline__ void store(char* lds, int tid, const uint4 (&r)[kVecs]) const {
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int row = (tid >> 3) + u * (NT / 8);
+        *reinterpret_cast<uint4*>(lds + lds_off(row, tid & 7)) = r[u];
+      }
+    }
+  };
 };
 
 // (i, k) -> I-contiguous rows indexed by k, two segments along i:
@@ -73,6 +152,7 @@ struct KRows2 {
 template <typename E>
 struct ICols2 {
   static constexpr bool kKMajor = false;
+  static constexpr bool kBf16 = sizeof(E) == 2;
   const E* p0;
   const E* p1a;
   const E* p1b;
@@ -88,13 +168,100 @@ struct ICols2 {
     if (mask1 && mask1[k]) return 0.0f;
     return elem<E>::to_f32(row1(k)[i - I0]);
   }
-  // 8 consecutive i starting at i (i % 8 == 0, I0 % 8 == 0); bf16 only
-  __device__ __forceinline__ uint4 vec(int i, int k) const {
-    if (i >= I || k >= K) return make_uint4(0, 0, 0, 0);
-    if (i < I0) return *reinterpret_cast<const uint4*>(p0 + static_cast<size_t>(k) * ld0 + i);
-    if (mask1 && mask1[k]) return make_uint4(0, 0, 0, 0);
-    return *reinterpret_cast<const uint4*>(row1(k) + (i - I0));
-  }
+
+  // Per-thread state of the bf16 engine for a ROWS x 64 tile: the tile holds
+  // (ROWS/8) x 8 blocks of 8 i x 8 k; thread t loads block (i-chunk t >> 3,
+  // k-chunk t & 7) (+ NT/8 i-chunks per extra block), i.e. 8 rows k of 8
+  // consecutive i, and transposes them before the LDS store.  Requires
+  // I0 % 8 == 0 and I % 8 == 0; bf16 only.
+  template <int ROWS, int NT>
+  struct Tile {
+    static constexpr int kBlocks = ROWS;  // (ROWS/8) i-chunks x 8 k-chunks
+    static constexpr int kPer = kBlocks >= NT ? kBlocks / NT : 1;
+    static constexpr int kVecs = kPer * 8;
+    static_assert(kBlocks >= NT ? kBlocks % NT == 0 : NT % kBlocks == 0, "tile/threads mismatch");
+    int col[kPer];   // column inside its source (0 when the block is idle or out of range)
+    uint32_t flags;  // bit u: block u active and in range; bit 8+u: block u reads the second source
+    int kc;
+
+    __device__ __forceinline__ void init(const ICols2& l, int row0, int tid) {
+      kc = (tid & 7) * 8;
+      flags = 0;
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int blk = tid + u * NT;
+        const int i = row0 + (blk >> 3) * 8;
+        const bool ok = blk < kBlocks && i < l.I;
+        const bool second = ok && i >= l.I0;
+        col[u] = ok ? (second ? i - l.I0 : i) : 0;
+        flags |= (ok ? 1u : 0u) << u;
+        flags |= (second ? 1u : 0u) << (8 + u);
+      }
+    }
+    __device__ __forceinline__ void load(const ICols2& l, int k0, uint4 (&r)[kVecs]) const {
+      if constexpr (kBlocks < NT) {
+        if ((flags & 1u) == 0u) return;  // idle or out-of-range block: store() skips it too
+      }
+      const int kb = k0 + kc;  // first of this thread's 8 rows k
+      // reset mask of the 8 rows (applies to the second source only)
+      uint32_t mlo = 0, mhi = 0;
+      if (l.mask1 != nullptr) {
+        if (kb + 8 <= l.K) {
+          const uint2 m = *reinterpret_cast<const uint2*>(l.mask1 + kb);
+          mlo = m.x;
+          mhi = m.y;
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const uint32_t b = (kb + j < l.K) ? l.mask1[kb + j] : 0u;
+            if (j < 4)
+              mlo |= b << (8 * j);
+            else
+              mhi |= b << (8 * (j - 4));
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const bool ok = (flags >> u) & 1u;
+        const bool second = (flags >> (8 + u)) & 1u;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int k = kb + j;
+          const bool kin = k < l.K;
+          const int kk = kin ? k : l.K - 1;  // clamped row: always a valid address
+          const E* p;
+          if (!second) {
+            p = l.p0 + static_cast<size_t>(kk) * l.ld0 + col[u];
+          } else {
+            p = (kk < l.kswitch ? l.p1a + static_cast<size_t>(kk) * l.ld1
+                                : l.p1b + static_cast<size_t>(kk - l.kswitch) * l.ld1) + col[u];
+          }
+          const uint32_t mb = (j < 4 ? mlo >> (8 * j) : mhi >> (8 * (j - 4))) & 0xffu;
+          const bool keep = ok && kin && !(second && mb != 0u);
+          r[u * 8 + j] = sel4(keep, *reinterpret_cast<const uint4*>(p));
+        }
+      }
+    }
+    __device__ __forceinline__ void store(char* lds, int tid, const uint4 (&r)[kVecs]) const {
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int blk = tid + u * NT;
+        if (blk < kBlocks) {
+          if constexpr (kBlocks < NT) {
+            if ((flags & 1u) == 0u) continue;  // not loaded: leave the rows as they are
+          }
+          uint4 in[8], out[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) in[j] = r[u * 8 + j];
+          transpose8x8_b16(in, out);  // out[c] = the 8 k-values of tile row (blk>>3)*8 + c
+#pragma unroll
+          for (int c = 0; c < 8; ++c)
+            *reinterpret_cast<uint4*>(lds + lds_off((blk >> 3) * 8 + c, blk & 7)) = out[c];
+        }
+      }
+    }
+  };
 };
 
 // ------------------------------------------------------------ epilogues
@@ -188,110 +355,47 @@ __global__ void __launch_bounds__(256) gemm_f32_fma(AL al, BL bl, Epi epi, int M
 
 // ------------------------------------------------------ bf16 MFMA engine
 
-// LDS byte offset of 16-byte chunk `chunk` (0..7) of tile row `row`
-// (a row is 64 bf16 = 128 bytes).
-__device__ __forceinline__ int lds_off(int row, int chunk) {
-  return row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4);
-}
+constexpr int kGroupM = 8;
 
-// Transpose an 8 x 8 block of 16-bit values held as 8 rows of 4 dwords:
-// in[r] = elements (r, 0..7) -> out[c] = elements (0..7, c).
-__device__ __forceinline__ void transpose8x8_b16(const uint4 (&in)[8], uint4 (&out)[8]) {
-  // v_perm_b32(hi_src, lo_src, sel): bytes 0-3 from lo_src, 4-7 from hi_src
-  const uint32_t kLo = 0x05040100u;  // (lo.lo16, hi.lo16)
-  const uint32_t kHi = 0x07060302u;  // (lo.hi16, hi.hi16)
-#pragma unroll
-  for (int c2 = 0; c2 < 4; ++c2) {  // pair of output columns 2*c2, 2*c2+1
-    uint32_t w[8];
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const uint4 v = in[r];
-      w[r] = c2 == 0 ? v.x : c2 == 1 ? v.y : c2 == 2 ? v.z : v.w;
-    }
-    uint4 lo, hi;
-    lo.x = __builtin_amdgcn_perm(w[1], w[0], kLo);
-    lo.y = __builtin_amdgcn_perm(w[3], w[2], kLo);
-    lo.z = __builtin_amdgcn_perm(w[5], w[4], kLo);
-    lo.w = __builtin_amdgcn_perm(w[7], w[6], kLo);
-    hi.x = __builtin_amdgcn_perm(w[1], w[0], kHi);
-    hi.y = __builtin_amdgcn_perm(w[3], w[2], kHi);
-    hi.z = __builtin_amdgcn_perm(w[5], w[4], kHi);
-    hi.w = __builtin_amdgcn_perm(w[7], w[6], kHi);
-    out[2 * c2] = lo;
-    out[2 * c2 + 1] = hi;
-  }
-}
-
-template <int ROWS, int NT, class L>
-struct TileLoader {
-  // K-major: ROWS rows x 8 chunks of 8 k = ROWS*8 vectors, kPer per thread.
-  // I-major: (ROWS/8) x 8 blocks of 8 i x 8 k = ROWS blocks, kPer per thread
-  // (threads past the last block idle when ROWS < NT).
-  static constexpr int kItems = L::kKMajor ? ROWS * 8 : ROWS;
-  static constexpr int kPer = kItems >= NT ? kItems / NT : 1;
-  static constexpr int kVecs = L::kKMajor ? kPer : kPer * 8;
-  static_assert(kItems >= NT ? kItems % NT == 0 : NT % kItems == 0, "tile/threads mismatch");
-  uint4 r[kVecs];
-
-  __device__ __forceinline__ bool active(int item) const { return kItems >= NT || item < kItems; }
-
-  __device__ __forceinline__ void load(const L& l, int row0, int k0, int tid) {
-    if constexpr (L::kKMajor) {
-#pragma unroll
-      for (int u = 0; u < kPer; ++u) {
-        const int v = tid + u * NT;
-        if (active(v)) r[u] = l.vec(row0 + (v >> 3), k0 + ((v & 7) << 3));
-      }
-    } else {
-#pragma unroll
-      for (int u = 0; u < kPer; ++u) {
-        const int blk = tid + u * NT;
-        const int kc = blk & 7, ic = blk >> 3;
-        if (active(blk)) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) r[u * 8 + j] = l.vec(row0 + ic * 8, k0 + kc * 8 + j);
-        }
-      }
-    }
-  }
-  __device__ __forceinline__ void store(char* lds, int tid) {
-    if constexpr (L::kKMajor) {
-#pragma unroll
-      for (int u = 0; u < kPer; ++u) {
-        const int v = tid + u * NT;
-        if (active(v)) *reinterpret_cast<uint4*>(lds + lds_off(v >> 3, v & 7)) = r[u];
-      }
-    } else {
-#pragma unroll
-      for (int u = 0; u < kPer; ++u) {
-        const int blk = tid + u * NT;
-        const int kc = blk & 7, ic = blk >> 3;
-        if (active(blk)) {
-          uint4 in[8], out[8];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) in[j] = r[u * 8 + j];
-          transpose8x8_b16(in, out);  // out[c] = the 8 k-values of tile row ic*8 + c
-#pragma unroll
-          for (int c = 0; c < 8; ++c) *reinterpret_cast<uint4*>(lds + lds_off(ic * 8 + c, kc)) = out[c];
-        }
-      }
-    }
-  }
-};
-
-// Map the linear block id to a (tile_m, tile_n) pair: blocks are dealt
-// round-robin to the 8 XCDs, so give each XCD a contiguous run of tiles,
-// M-tile fastest (consecutive tiles share the same B tile).
+// Map the linear block id to a (tile_m, tile_n) pair.  Blocks are dealt
+// round-robin to the 8 XCDs, so each XCD first gets a contiguous run of
+// tiles (when the tile count is a multiple of 8); tiles are then numbered in
+// groups of kGroupM M-tiles with the M-tile fastest.
 __device__ __forceinline__ void xcd_tile(int pid, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int nt = tiles_m * tiles_n;
   int tile = pid;
   if ((nt & 7) == 0) tile = (pid & 7) * (nt >> 3) + (pid >> 3);
-  tm = tile % tiles_m;
-  tn = tile / tiles_m;
+  const int gsz = kGroupM * tiles_n;
+  const int g = tile / gsz;
+  const int first_m = g * kGroupM;
+  const int gm = min(tiles_m - first_m, kGroupM);
+  const int in = tile - g * gsz;
+  tm = first_m + in % gm;
+  tn = in / gm;
+}
+
+template <int MB, int NB>
+__device__ __forceinline__ void read_frags(const char* a_s, const char* b_s, int wm0, int wn0, int frow, int fchunk,
+                                           bf16x8_t (&af)[MB], bf16x8_t (&bfr)[NB]) {
+#pragma unroll
+  for (int a = 0; a < MB; ++a)
+    af[a] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(a_s + lds_off(wm0 + a * 32 + frow, fchunk)));
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+    bfr[b] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(b_s + lds_off(wn0 + b * 32 + frow, fchunk)));
+}
+
+template <int MB, int NB>
+__device__ __forceinline__ void mfma_block(const bf16x8_t (&af)[MB], const bf16x8_t (&bfr)[NB],
+                                           f32x16_t (&acc)[MB][NB]) {
+#pragma unroll
+  for (int a = 0; a < MB; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
 }
 
 template <int BM, int BN, int WM, int WN, class AL, class BL, class Epi>
-__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64, 1)
     gemm_bf16_mfma(AL al, BL bl, Epi epi, int M, int N, int K, int ktiles_per_split) {
   constexpr int BK = 64;
   constexpr int WAVES_N = BN / WN;
@@ -299,6 +403,8 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
   constexpr int MB = WM / 32, NB = WN / 32;
   constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
   __shared__ __attribute__((aligned(16))) char smem[2 * (A_BYTES + B_BYTES)];
+  using ATile = typename AL::template Tile<BM, NT>;
+  using BTile = typename BL::template Tile<BN, NT>;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -319,52 +425,54 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.0f;
 
-  TileLoader<BM, NT, AL> la;
-  TileLoader<BN, NT, BL> lb;
+  ATile ta;
+  BTile tb;
+  // the B operand uses a rotated thread index, so that when a tile has fewer
+  // 8x8 blocks than threads the A and B loads land on different waves
+  const int tidb = (tid + NT / 2) % NT;
+  ta.init(al, m0, tid);
+  tb.init(bl, n0, tidb);
+  uint4 ra[ATile::kVecs], rb[BTile::kVecs];
+
   // buffer b of A at smem + b*A_BYTES, of B at smem + 2*A_BYTES + b*B_BYTES
   if (kt0 < kt1) {
-    la.load(al, m0, kt0 * BK, tid);
-    lb.load(bl, n0, kt0 * BK, tid);
-    la.store(smem, tid);
-    lb.store(smem + 2 * A_BYTES, tid);
+    ta.load(al, kt0 * BK, ra);
+    tb.load(bl, kt0 * BK, rb);
+    ta.store(smem, tid, ra);
+    tb.store(smem + 2 * A_BYTES, tidb, rb);
   }
   __syncthreads();
 
-  const int frow = lane & 31, fchunk = lane >> 5;
+  const int frow = lane & 31, fhalf = lane >> 5;
   for (int kt = kt0; kt < kt1; ++kt) {
     const int buf = (kt - kt0) & 1;
     const bool more = kt + 1 < kt1;
     if (more) {
-      la.load(al, m0, (kt + 1) * BK, tid);
-      lb.load(bl, n0, (kt + 1) * BK, tid);
+      ta.load(al, (kt + 1) * BK, ra);
+      tb.load(bl, (kt + 1) * BK, rb);
     }
     const char* a_s = smem + buf * A_BYTES;
     const char* b_s = smem + 2 * A_BYTES + buf * B_BYTES;
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8_t af[MB], bfr[NB];
-#pragma unroll
-      for (int a = 0; a < MB; ++a)
-        af[a] = __builtin_bit_cast(bf16x8_t,
-                                   *reinterpret_cast<const uint4*>(a_s + lds_off(wm0 + a * 32 + frow, kk * 2 + fchunk)));
-#pragma unroll
-      for (int b = 0; b < NB; ++b)
-        bfr[b] = __builtin_bit_cast(bf16x8_t,
-                                    *reinterpret_cast<const uint4*>(b_s + lds_off(wn0 + b * 32 + frow, kk * 2 + fchunk)));
-#pragma unroll
-      for (int a = 0; a < MB; ++a)
-#pragma unroll
-        for (int b = 0; b < NB; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
-    }
+    bf16x8_t af0[MB], bf0[NB], af1[MB], bf1[NB];
+    // fragments of k-step kk+1 are read while the MFMAs of k-step kk run
+    read_frags<MB, NB>(a_s, b_s, wm0, wn0, frow, 0 + fhalf, af0, bf0);
+    read_frags<MB, NB>(a_s, b_s, wm0, wn0, frow, 2 + fhalf, af1, bf1);
+    mfma_block<MB, NB>(af0, bf0, acc);
+    read_frags<MB, NB>(a_s, b_s, wm0, wn0, frow, 4 + fhalf, af0, bf0);
+    mfma_block<MB, NB>(af1, bf1, acc);
+    read_frags<MB, NB>(a_s, b_s, wm0, wn0, frow, 6 + fhalf, af1, bf1);
+    mfma_block<MB, NB>(af0, bf0, acc);
+    mfma_block<MB, NB>(af1, bf1, acc);
     if (more) {
-      la.store(smem + (buf ^ 1) * A_BYTES, tid);
-      lb.store(smem + 2 * A_BYTES + (buf ^ 1) * B_BYTES, tid);
+      ta.store(smem + (buf ^ 1) * A_BYTES, tid, ra);
+      tb.store(smem + 2 * A_BYTES + (buf ^ 1) * B_BYTES, tidb, rb);
     }
     __syncthreads();
   }
 
   // accumulator layout of a 32 x 32 block: lane holds column (lane & 31);
   // register e holds row 8*(e/4) + 4*(lane/32) + (e%4)
+  const bool full = m0 + BM <= M && n0 + BN <= N;
 #pragma unroll
   for (int a = 0; a < MB; ++a)
 #pragma unroll
@@ -373,7 +481,7 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
       for (int e = 0; e < 16; ++e) {
         const int i = m0 + wm0 + a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
         const int j = n0 + wn0 + b * 32 + (lane & 31);
-        if (i < M && j < N) epi(i, j, acc[a][b][e], split);
+        if (full || (i < M && j < N)) epi(i, j, acc[a][b][e], split);
       }
 }
 
@@ -388,8 +496,11 @@ inline void launch_gemm_f32(const AL& al, const BL& bl, const Epi& epi, int M, i
   hipLaunchKernelGGL((gemm_f32_fma<AL, BL, Epi>), grid, dim3(256), 0, s, al, bl, epi, M, N, K, kps);
 }
 
-// Tile configurations of the bf16 engine.
-enum class BfTile { k256x256, k128x128 };
+// Tile configurations of the bf16 engine: block tile, waves (x 64 threads).
+//   k256x256   256 x 256, 4 waves of 128 x 128 (one wave per SIMD)
+//   k256x256w8 256 x 256, 8 waves of 128 x 64 (two waves per SIMD)
+//   k128x128   128 x 128, 4 waves of 64 x 64
+enum class BfTile { k256x256, k256x256w8, k128x128 };
 
 template <class AL, class BL, class Epi>
 inline void launch_gemm_bf16(const AL& al, const BL& bl, const Epi& epi, int M, int N, int K, int splits,
@@ -399,6 +510,10 @@ inline void launch_gemm_bf16(const AL& al, const BL& bl, const Epi& epi, int M, 
   if (tile == BfTile::k256x256) {
     const unsigned tiles = ((M + 255) / 256) * ((N + 255) / 256);
     hipLaunchKernelGGL((gemm_bf16_mfma<256, 256, 128, 128, AL, BL, Epi>), dim3(tiles, 1, splits), dim3(256), 0, s,
+                       al, bl, epi, M, N, K, kps);
+  } else if (tile == BfTile::k256x256w8) {
+    const unsigned tiles = ((M + 255) / 256) * ((N + 255) / 256);
+    hipLaunchKernelGGL((gemm_bf16_mfma<256, 256, 128, 64, AL, BL, Epi>), dim3(tiles, 1, splits), dim3(512), 0, s,
                        al, bl, epi, M, N, K, kps);
   } else {
     const unsigned tiles = ((M + 127) / 128) * ((N + 127) / 128);
@@ -419,8 +534,22 @@ inline int cdiv(long long a, long long b) { return static_cast<int>((a + b - 1) 
 
 // Choose tile shape and split-K so the launch has >= ~256 blocks (one per
 // CU) while every split keeps a reasonable number of K tiles.
+// Tile variant used for 256 x 256 blocks; O5_BF16_TILE=w4|w8|128 overrides
+// the choice (for tuning runs).
+inline int bf16_tile_override() {
+  static const int v = [] {
+    const char* e = std::getenv("O5_BF16_TILE");
+    if (!e) return 0;
+    if (e[0] == 'w' && e[1] == '4') return 1;
+    if (e[0] == 'w' && e[1] == '8') return 2;
+    if (e[0] == '1') return 3;
+    return 0;
+  }();
+  return v;
+}
+
 inline GemmPlan plan_gemm(bool bf16, int M, int N, int K) {
-  GemmPlan p{bf16, BfTile::k256x256, 1};
+  GemmPlan p{bf16, BfTile::k256x256w8, 1};
   if (!bf16) {
     const int tiles = cdiv(M, 64) * cdiv(N, 64);
     const int nkt = cdiv(K, 16);
@@ -431,10 +560,11 @@ inline GemmPlan plan_gemm(bool bf16, int M, int N, int K) {
   }
   const int nkt = cdiv(K, 64);
   const int t256 = cdiv(M, 256) * cdiv(N, 256);
-  if (t256 >= 64) {
+  const int ov = bf16_tile_override();
+  if (t256 >= 64 && ov != 3) {
     int s = cdiv(256, t256);
     s = std::min(s, std::max(1, nkt / 16));
-    p.tile = BfTile::k256x256;
+    p.tile = ov == 1 ? BfTile::k256x256 : BfTile::k256x256w8;
     p.splits = std::max(1, std::min(s, 8));
     return p;
   }
@@ -449,10 +579,13 @@ inline GemmPlan plan_gemm(bool bf16, int M, int N, int K) {
 template <class AL, class BL, class Epi>
 inline void run_gemm(const GemmPlan& p, const AL& al, const BL& bl, const Epi& epi, int M, int N, int K,
                      hipStream_t s) {
-  if (p.bf16)
-    launch_gemm_bf16(al, bl, epi, M, N, K, p.splits, p.tile, s);
-  else
-    launch_gemm_f32(al, bl, epi, M, N, K, p.splits, s);
+  if constexpr (AL::kBf16 && BL::kBf16) {
+    if (p.bf16) {
+      launch_gemm_bf16(al, bl, epi, M, N, K, p.splits, p.tile, s);
+      return;
+    }
+  }
+  launch_gemm_f32(al, bl, epi, M, N, K, p.splits, s);
 }
 
 }  // namespace o5

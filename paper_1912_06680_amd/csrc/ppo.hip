@@ -12,6 +12,10 @@
 //   dh  = dz Wp                         GEMM  (M = N, N = H, K = A+1)
 //   dWp = dz^T h                        GEMM  (M = A+1, N = H, K = N), split-K
 //   dbp, stats: fixed-order column sums.
+// On the bf16 path the two gradient products run on the MFMA engine: dz is
+// written as a pair of bf16 terms hi = bf16(dz), lo = bf16(dz - hi) (relative
+// error ~2^-16) laid side by side along K, against the bf16 operand repeated
+// twice, so the product keeps nearly fp32 accuracy.
 // Every reduction has a fixed order, so results are bitwise reproducible.
 #include "gemm.h"
 #include "heads.h"
@@ -33,7 +37,9 @@ __global__ void __launch_bounds__(256) ppo_rows(int N, int A1, int S, const floa
                                                 const float* __restrict__ logp_old, const float* __restrict__ adv,
                                                 const float* __restrict__ ret, const uint8_t* __restrict__ mask,
                                                 HeadsMeta hm, float clip_eps, float vf_coef, float ent_coef,
-                                                float invN, float* __restrict__ dz, float* __restrict__ rowstats) {
+                                                float invN, float* __restrict__ dz, float* __restrict__ rowstats,
+                                                uint16_t* __restrict__ dz_hi, uint16_t* __restrict__ dz_lo,
+                                                int ld_hilo) {
   const int n = blockIdx.x * blockDim.x + threadIdx.x;
   if (n >= N) return;
   float* zr = dz + static_cast<size_t>(n) * A1;
@@ -84,6 +90,16 @@ __global__ void __launch_bounds__(256) ppo_rows(int N, int A1, int S, const floa
     }
   }
   zr[hm.A] = 2.0f * vf_coef * verr * invN;
+  if (dz_hi != nullptr) {  // bf16 pair (hi, lo) of the row, zero-padded to ld_hilo
+    uint16_t* hr = dz_hi + static_cast<size_t>(n) * ld_hilo;
+    uint16_t* lr = dz_lo + static_cast<size_t>(n) * ld_hilo;
+    for (int a = 0; a < ld_hilo; ++a) {
+      const float v = a < A1 ? zr[a] : 0.0f;
+      const uint16_t hb = f32_to_bf16_bits(v);
+      hr[a] = hb;
+      lr[a] = f32_to_bf16_bits(v - bf16_bits_to_f32(hb));
+    }
+  }
   const float row_loss = -surr + vf_coef * verr * verr - ent_coef * ent;
   float* st = rowstats + static_cast<size_t>(n) * kStatCols;
   st[0] = surr;
@@ -94,6 +110,16 @@ __global__ void __launch_bounds__(256) ppo_rows(int N, int A1, int S, const floa
   st[5] = ratio;
   st[6] = isfinite(row_loss) ? 0.0f : 1.0f;
   st[7] = 0.0f;
+}
+
+// dst [R, H] bf16 = src [A1, H] with rows A1..R-1 zero.
+__global__ void __launch_bounds__(256) pad_rows_bf16(int A1, int R, int H, const uint16_t* __restrict__ src,
+                                                     uint16_t* __restrict__ dst) {
+  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const size_t total = static_cast<size_t>(R) * H;
+  if (i >= total) return;
+  const int r = static_cast<int>(i / H);
+  dst[i] = r < A1 ? src[i] : static_cast<uint16_t>(0);
 }
 
 __global__ void ppo_finalize(const float* __restrict__ sums, float invN, float vf_coef, float ent_coef,
@@ -111,16 +137,20 @@ __global__ void ppo_finalize(const float* __restrict__ sums, float invN, float v
 }
 
 struct PpoWs {
-  size_t zpart, dz, rowstats, wpart, dbpart, spart, ssum, total;
-  GemmPlan plan_z, plan_w;
-  int nchunk, A1;
+  size_t zpart, dz, rowstats, wpart, dbpart, spart, ssum, dzhi, dzlo, wpad, total;
+  GemmPlan plan_z, plan_w, plan_h;
+  int nchunk, A1, A1p;
 };
 
 static PpoWs ppo_ws(o5_dtype dt, int N, int H, int A1) {
   PpoWs w;
+  const bool bf = dt == O5_BF16;
   w.A1 = A1;
-  w.plan_z = plan_gemm(dt == O5_BF16, N, A1, H);
-  w.plan_w = plan_gemm(false, A1, H, N);
+  w.A1p = cdiv(A1, 64) * 64;  // padded logit count: a multiple of the K tile
+  w.plan_z = plan_gemm(bf, N, A1, H);
+  w.plan_w = bf ? plan_gemm(true, A1, H, 2 * N) : plan_gemm(false, A1, H, N);
+  w.plan_h = bf ? plan_gemm(true, N, H, 2 * w.A1p) : GemmPlan{false, BfTile::k128x128, 1};
+  w.plan_h.splits = 1;
   w.nchunk = cdiv(N, kRowsPerChunk);
   size_t o = 0;
   w.zpart = o;
@@ -137,6 +167,15 @@ static PpoWs ppo_ws(o5_dtype dt, int N, int H, int A1) {
   o += align_up(static_cast<size_t>(w.nchunk) * kStatCols * 4);
   w.ssum = o;
   o += align_up(kStatCols * 4);
+  w.dzhi = w.dzlo = w.wpad = 0;
+  if (bf) {
+    w.dzhi = o;
+    o += align_up(static_cast<size_t>(N) * w.A1p * 2);
+    w.dzlo = o;
+    o += align_up(static_cast<size_t>(N) * w.A1p * 2);
+    w.wpad = o;
+    o += align_up(static_cast<size_t>(w.A1p) * H * 2);
+  }
   w.total = o;
   return w;
 }
@@ -179,22 +218,47 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
     EpiLogits epi{{zpart, A1, static_cast<size_t>(N) * A1}};
     run_gemm(w.plan_z, al, bl, epi, N, A1, H, s);
   }
+  uint16_t* dzhi = nullptr;
+  uint16_t* dzlo = nullptr;
+  if constexpr (sizeof(E) == 2) {
+    dzhi = reinterpret_cast<uint16_t*>(ws + w.dzhi);
+    dzlo = reinterpret_cast<uint16_t*>(ws + w.dzlo);
+  }
   hipLaunchKernelGGL(ppo_rows, dim3(cdiv(N, 256)), dim3(256), 0, s, N, A1, w.plan_z.splits, zpart, bp, act, logp_old,
-                     adv, ret, mask, hm, hp.clip_eps, hp.vf_coef, hp.ent_coef, invN, dz, rowstats);
-  {  // dh = dz Wp  (fp32 FMA engine: dz stays fp32)
-    KRows2<float> al{dz, nullptr, nullptr, A1, 0, A1, A1, N};
-    ICols2<E> bl{Wp, nullptr, nullptr, nullptr, H, 0, H, H, A1, 0};
-    EpiStoreF32 epi{dh, H, 0};
-    launch_gemm_f32(al, bl, epi, N, H, A1, 1, s);
+                     adv, ret, mask, hm, hp.clip_eps, hp.vf_coef, hp.ent_coef, invN, dz, rowstats, dzhi, dzlo, w.A1p);
+  if constexpr (sizeof(E) == 2) {
+    const int A1p = w.A1p;
+    uint16_t* wpad = reinterpret_cast<uint16_t*>(ws + w.wpad);
+    hipLaunchKernelGGL(pad_rows_bf16, dim3(cdiv(static_cast<long long>(A1p) * H, 256)), dim3(256), 0, s, A1, A1p, H,
+                       Wp, wpad);
+    {  // dh = [dz_hi | dz_lo] . [Wp ; Wp]  (K = 2 A1p)
+      KRows2<uint16_t> al{dzhi, dzlo, nullptr, A1p, A1p, A1p, 2 * A1p, N};
+      ICols2<uint16_t> bl{wpad, wpad, wpad, nullptr, H, H, 0, H, 2 * A1p, A1p};
+      EpiStoreF32 epi{dh, H, 0};
+      run_gemm(w.plan_h, al, bl, epi, N, H, 2 * A1p, s);
+    }
+    {  // dWp = [dz_hi ; dz_lo]^T . [h ; h]  (K = 2N), split over K, fixed-order sum
+      ICols2<uint16_t> al{dzhi, dzhi, dzlo, nullptr, A1p, A1p, 0, A1p, 2 * N, N};
+      ICols2<uint16_t> bl{h, h, h, nullptr, H, H, 0, H, 2 * N, N};
+      EpiStoreF32 epi{wpart, H, static_cast<size_t>(A1) * H};
+      run_gemm(w.plan_w, al, bl, epi, A1, H, 2 * N, s);
+    }
+  } else {
+    {  // dh = dz Wp  (fp32 FMA engine)
+      KRows2<float> al{dz, nullptr, nullptr, A1, 0, A1, A1, N};
+      ICols2<E> bl{Wp, nullptr, nullptr, nullptr, H, 0, H, H, A1, 0};
+      EpiStoreF32 epi{dh, H, 0};
+      launch_gemm_f32(al, bl, epi, N, H, A1, 1, s);
+    }
+    {  // dWp = dz^T h, split over rows
+      ICols2<float> al{dz, nullptr, nullptr, nullptr, A1, 0, A1, A1, N, 0};
+      ICols2<E> bl{h, nullptr, nullptr, nullptr, H, 0, H, H, N, 0};
+      EpiStoreF32 epi{wpart, H, static_cast<size_t>(A1) * H};
+      launch_gemm_f32(al, bl, epi, A1, H, N, w.plan_w.splits, s);
+    }
   }
-  {  // dWp = dz^T h, split over rows, then a fixed-order sum of the splits
-    ICols2<float> al{dz, nullptr, nullptr, nullptr, A1, 0, A1, A1, N, 0};
-    ICols2<E> bl{h, nullptr, nullptr, nullptr, H, 0, H, H, N, 0};
-    EpiStoreF32 epi{wpart, H, static_cast<size_t>(A1) * H};
-    launch_gemm_f32(al, bl, epi, A1, H, N, w.plan_w.splits, s);
-    hipLaunchKernelGGL(colsum_rows, dim3(cdiv(static_cast<long long>(A1) * H, 256)), dim3(256), 0, s,
-                       w.plan_w.splits, A1 * H, wpart, dWp);
-  }
+  hipLaunchKernelGGL(colsum_rows, dim3(cdiv(static_cast<long long>(A1) * H, 256)), dim3(256), 0, s, w.plan_w.splits,
+                     A1 * H, wpart, dWp);
   hipLaunchKernelGGL(colsum_chunks, dim3(cdiv(A1, 256), w.nchunk), dim3(256), 0, s, N, A1, kRowsPerChunk, dz, dbpart);
   hipLaunchKernelGGL(colsum_rows, dim3(cdiv(A1, 256)), dim3(256), 0, s, w.nchunk, A1, dbpart, dbp);
   hipLaunchKernelGGL(colsum_chunks, dim3(1, w.nchunk), dim3(256), 0, s, N, kStatCols, kRowsPerChunk, rowstats, spart);

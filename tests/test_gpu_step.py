@@ -56,16 +56,19 @@ def test_full_step_matches_oracle(name):
         assert e <= lim or abs(s[i] - r) <= lim, k
     for k in PARAM_ORDER:
         assert_close("grad " + k, host(st.G[k]), ref["grads"][k], tol)
-    # Adam update: compared on the parameter change
+    # Adam update, compared on the parameter change.  At step 1 the update is
+    # lr * g / (|g| + eps), whose derivative lr * eps / (|g| + eps)^2 amplifies
+    # the gradient's own (tolerated) error for elements with |g| near eps, so
+    # the bound adds that first-order term to one fp32 rounding of theta.
+    g_ref = ref["grad_flat"]
     dref = ref["p_new"] - p_before
     err = np.abs(host(st.p32) - ref["p_new"])
     ulp = np.spacing(np.abs(ref["p_new"]).astype(np.float32)).astype(np.float64)
-    frac = err / (tol * np.max(np.abs(dref)) + ulp)
+    dg = tol * np.max(np.abs(g_ref))
+    sens = cfg.lr * cfg.adam_eps * dg / (np.abs(g_ref) + cfg.adam_eps) ** 2
+    frac = err / (tol * np.max(np.abs(dref)) + ulp + sens)
     print(f"    adam: max err/bound = {frac.max():.3f}", flush=True)
-    # a bf16 gradient may flip the sign of elements whose gradient is ~0; Adam's
-    # first step moves them by lr either way, so count those separately
-    bad = frac > 1.0
-    assert bad.mean() <= (2e-3 if cfg.dtype == "bf16" else 0.0), bad.mean()
+    assert frac.max() <= 1.0
 
 
 def test_two_steps_equal_checkpoint_resume():
@@ -83,6 +86,7 @@ def test_two_steps_equal_checkpoint_resume():
     _, _, c = _setup(cfg)
     for k in ("p32", "m", "v"):
         getattr(c, k).copy_(ck[k].cuda())
+    c.sync_bf16()
     c.step_count = n
     c.run()
     for k in ("p32", "m", "v", "g"):
