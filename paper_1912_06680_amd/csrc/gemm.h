@@ -496,11 +496,12 @@ inline void launch_gemm_f32(const AL& al, const BL& bl, const Epi& epi, int M, i
   hipLaunchKernelGGL((gemm_f32_fma<AL, BL, Epi>), grid, dim3(256), 0, s, al, bl, epi, M, N, K, kps);
 }
 
-// Tile configurations of the bf16 engine: block tile, waves (x 64 threads).
+// Tile configurations of the bf16 engines: block tile, waves (x 64 threads).
+//   kDma256    256 x 256, 8 waves, direct-to-LDS 4-stage pipeline (gemm_dma.h)
 //   k256x256   256 x 256, 4 waves of 128 x 128 (one wave per SIMD)
 //   k256x256w8 256 x 256, 8 waves of 128 x 64 (two waves per SIMD)
 //   k128x128   128 x 128, 4 waves of 64 x 64
-enum class BfTile { k256x256, k256x256w8, k128x128 };
+enum class BfTile { kDma256, k256x256, k256x256w8, k128x128 };
 
 template <class AL, class BL, class Epi>
 inline void launch_gemm_bf16(const AL& al, const BL& bl, const Epi& epi, int M, int N, int K, int splits,
@@ -520,72 +521,6 @@ inline void launch_gemm_bf16(const AL& al, const BL& bl, const Epi& epi, int M, 
     hipLaunchKernelGGL((gemm_bf16_mfma<128, 128, 64, 64, AL, BL, Epi>), dim3(tiles, 1, splits), dim3(256), 0, s, al,
                        bl, epi, M, N, K, kps);
   }
-}
-
-// --------------------------------------------------------------- planning
-
-struct GemmPlan {
-  bool bf16;
-  BfTile tile;
-  int splits;
-};
-
-inline int cdiv(long long a, long long b) { return static_cast<int>((a + b - 1) / b); }
-
-// Choose tile shape and split-K so the launch has >= ~256 blocks (one per
-// CU) while every split keeps a reasonable number of K tiles.
-// Tile variant used for 256 x 256 blocks; O5_BF16_TILE=w4|w8|128 overrides
-// the choice (for tuning runs).
-inline int bf16_tile_override() {
-  static const int v = [] {
-    const char* e = std::getenv("O5_BF16_TILE");
-    if (!e) return 0;
-    if (e[0] == 'w' && e[1] == '4') return 1;
-    if (e[0] == 'w' && e[1] == '8') return 2;
-    if (e[0] == '1') return 3;
-    return 0;
-  }();
-  return v;
-}
-
-inline GemmPlan plan_gemm(bool bf16, int M, int N, int K) {
-  GemmPlan p{bf16, BfTile::k256x256w8, 1};
-  if (!bf16) {
-    const int tiles = cdiv(M, 64) * cdiv(N, 64);
-    const int nkt = cdiv(K, 16);
-    int s = cdiv(512, tiles);
-    s = std::min(s, std::max(1, nkt / 8));
-    p.splits = std::max(1, std::min(s, 16));
-    return p;
-  }
-  const int nkt = cdiv(K, 64);
-  const int t256 = cdiv(M, 256) * cdiv(N, 256);
-  const int ov = bf16_tile_override();
-  if (t256 >= 64 && ov != 3) {
-    int s = cdiv(256, t256);
-    s = std::min(s, std::max(1, nkt / 16));
-    p.tile = ov == 1 ? BfTile::k256x256 : BfTile::k256x256w8;
-    p.splits = std::max(1, std::min(s, 8));
-    return p;
-  }
-  const int t128 = cdiv(M, 128) * cdiv(N, 128);
-  int s = cdiv(256, t128);
-  s = std::min(s, std::max(1, nkt / 8));
-  p.tile = BfTile::k128x128;
-  p.splits = std::max(1, std::min(s, 8));
-  return p;
-}
-
-template <class AL, class BL, class Epi>
-inline void run_gemm(const GemmPlan& p, const AL& al, const BL& bl, const Epi& epi, int M, int N, int K,
-                     hipStream_t s) {
-  if constexpr (AL::kBf16 && BL::kBf16) {
-    if (p.bf16) {
-      launch_gemm_bf16(al, bl, epi, M, N, K, p.splits, p.tile, s);
-      return;
-    }
-  }
-  launch_gemm_f32(al, bl, epi, M, N, K, p.splits, s);
 }
 
 }  // namespace o5

@@ -1,0 +1,399 @@
+// bf16 MFMA GEMM fed by direct-to-LDS loads (gfx950):
+//   C[i, j] = sum_k A(i, k) * B(j, k)  (+ epilogue), fp32 accumulate.
+//
+// Pipeline: the K loop runs over tiles of 32 k held in a ring of 4 LDS
+// stages.  Tiles are copied global -> LDS by global_load_lds_dwordx4 (16
+// bytes per lane, written at M0 + 16 * lane), so no registers stage the
+// operands and three tiles are in flight while one is multiplied: each
+// iteration waits (vmcnt) for its own tile only, meets the other waves at one
+// barrier, issues the copy of the tile three steps ahead into the stage that
+// was just freed, and runs its MFMAs.  The four stages are four distinct LDS
+// arrays and the loop is unrolled by four, so the compiler can see that the
+// copies in flight never alias the LDS reads (it would otherwise wait for
+// every copy before each read); the barrier is a bare s_barrier (a fence
+// would also wait for the copies).
+//
+// Operand layouts in LDS (one stage; 256 rows/columns x 32 k):
+//  * K-contiguous operand: [row][32 k] bf16 = 64 bytes per row, 16-byte
+//    chunk c of row r stored at slot c ^ ((r >> 2) & 3).  A fragment read
+//    (16 consecutive rows, one chunk) then touches 16 distinct 16-byte bank
+//    groups.  Fragments are single ds_read_b128.
+//  * I-contiguous operand (the reduction index k is the row): [32 k][256 i]
+//    bf16 = 512 bytes per k row, 16-byte unit u of row k stored at position
+//    u ^ (4 * (k & 3)).  Fragments are two ds_read_b64_tr_b16: within each
+//    16-lane group the 16 lanes' 4-element reads form a 64-element sequence
+//    S and lane i receives S[i], S[16+i], S[32+i], S[48+i]; when lane j reads
+//    row k0 + j/4, columns n0 + 4(j%4) .. +3, lane i receives k0..k0+3 of
+//    column n0 + i -- an MFMA operand slice.  The swizzle keeps the 4 rows x
+//    4 eight-byte pieces of a 32-lane half on distinct banks.
+// MFMA v_mfma_f32_32x32x16_bf16: lane l supplies row/column (l & 31) and the
+// k slice 8*(l >> 5) .. +7 of a 16-wide k step, for both operands alike.
+//
+// Block tile 256 x 256, 8 waves (2 x 4) of 128 x 64, two waves per SIMD.
+// Rows or k beyond the matrix read a static zero row, so every address the
+// copies use is inside a buffer.
+#pragma once
+
+#include "gemm.h"
+
+namespace o5 {
+
+namespace dma {
+
+constexpr int BM = 256, BN = 256, BK = 32, STAGES = 4;
+constexpr int WM = 128, WN = 64, WAVES_M = BM / WM, WAVES_N = BN / WN;
+constexpr int NWAVES = WAVES_M * WAVES_N;  // 8
+constexpr int NT = NWAVES * 64;            // 512
+constexpr int TILE_BYTES = 256 * BK * 2;   // 16 KB per operand per stage
+constexpr int COPIES = TILE_BYTES / 1024 / NWAVES;  // 1 KB copies per wave per operand per tile (2)
+
+// 1 KB of zeros: the source of every copy that falls outside a matrix.
+__device__ __attribute__((aligned(16))) const uint16_t kZeroRow[512] = {};
+
+// One wave-wide copy of 64 x 16 bytes into LDS at lds_wave_base + 16 * lane.
+// Written as inline asm so that the compiler's wait-count pass neither tracks
+// these copies (it would wait for all of them before every LDS read) nor
+// edits the explicit waits below; ordering against the LDS reads is kept by
+// wait_copies + wave_barrier.
+__device__ __forceinline__ void copy16(const void* g, char* lds_wave_base) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(
+      static_cast<uint32_t>(reinterpret_cast<size_t>((__attribute__((address_space(3))) char*)(lds_wave_base))));
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+
+// ------------------------------------------------- K-contiguous operand
+// Rows i of the operand are K-contiguous; two sources along k (split at K0,
+// a multiple of 32): k < K0 -> p0[i*ld0 + k], else p1[i*ld1 + k - K0].
+// mask1[i] != 0 zeroes the second source for row i.
+template <typename E>
+struct KTile {
+  const char* ptr0[COPIES];  // row start in source 0 (bytes), or nullptr = zero row
+  const char* ptr1[COPIES];  // row start in source 1
+  int koff;                  // byte offset of this lane's 16-byte chunk within a tile
+
+  __device__ __forceinline__ void init(const KRows2<E>& l, int row0, int wave, int lane) {
+    const int slot = lane & 3;
+#pragma unroll
+    for (int q = 0; q < COPIES; ++q) {
+      const int r = (wave * COPIES + q) * 16 + (lane >> 2);  // tile row this lane fills
+      const int row = row0 + r;
+      const int chunk = slot ^ ((r >> 2) & 3);
+      koff = chunk * 16;
+      const bool valid = row < l.rows;
+      const bool masked = valid && l.mask1 != nullptr && l.mask1[row] != 0;
+      ptr0[q] = valid ? reinterpret_cast<const char*>(l.p0 + static_cast<size_t>(row) * l.ld0) : nullptr;
+      ptr1[q] = (valid && !masked && l.p1 != nullptr)
+                    ? reinterpret_cast<const char*>(l.p1 + static_cast<size_t>(row) * l.ld1)
+                    : nullptr;
+    }
+  }
+  // copy tile starting at k0 into `stage` (this wave's 1 KB pieces)
+  __device__ __forceinline__ void issue(const KRows2<E>& l, int k0, char* stage, int wave) const {
+    const bool seg0 = k0 < l.K0;
+    const int kb = seg0 ? k0 : k0 - l.K0;  // element offset inside the source row
+    const bool kin = k0 + koff / 2 < l.K;
+#pragma unroll
+    for (int q = 0; q < COPIES; ++q) {
+      const char* p = seg0 ? ptr0[q] : ptr1[q];
+      const void* g = (p != nullptr && kin) ? static_cast<const void*>(p + kb * 2 + koff)
+                                            : static_cast<const void*>(kZeroRow);
+      copy16(g, stage + (wave * COPIES + q) * 1024);
+    }
+  }
+};
+
+// LDS byte offset of chunk c (0..3) of K-contiguous tile row r.
+__device__ __forceinline__ int koffset(int r, int c) { return r * 64 + ((c ^ ((r >> 2) & 3)) << 4); }
+
+template <int NBLK>
+__device__ __forceinline__ void read_k(const char* stage, int row0, int lane, int kk, bf16x8_t (&f)[NBLK]) {
+  const int c = kk * 2 + (lane >> 5);
+#pragma unroll
+  for (int b = 0; b < NBLK; ++b) {
+    const int r = row0 + b * 32 + (lane & 31);
+    f[b] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(stage + koffset(r, c)));
+  }
+}
+
+// ------------------------------------------------- I-contiguous operand
+// Element (i, k) at row k of the source: i < I0 -> p0[k*ld0 + i]; i >= I0 ->
+// (k < kswitch ? p1a + k*ld1 : p1b + (k - kswitch)*ld1)[i - I0].  No mask.
+template <typename E>
+struct ITile {
+  int col[COPIES];   // element column of this lane's 16 bytes inside its source row
+  int kl[COPIES];    // tile k row this copy fills
+  uint32_t second;   // bit q: the lane's columns come from the second source
+  uint32_t ok;       // bit q: the lane's columns are inside the matrix
+
+  __device__ __forceinline__ void init(const ICols2<E>& l, int row0, int wave, int lane) {
+    second = 0;
+    ok = 0;
+#pragma unroll
+    for (int q = 0; q < COPIES; ++q) {
+      const int piece = wave * COPIES + q;  // 1 KB piece = 2 k rows of 512 bytes
+      const int k = piece * 2 + (lane >> 5);
+      const int u = (lane & 31) ^ (4 * (k & 3));
+      const int i = row0 + u * 8;
+      kl[q] = k;
+      const bool in = i < l.I;
+      const bool sec = i >= l.I0;
+      ok |= (in ? 1u : 0u) << q;
+      second |= (sec ? 1u : 0u) << q;
+      col[q] = sec ? i - l.I0 : i;
+    }
+  }
+  __device__ __forceinline__ void issue(const ICols2<E>& l, int k0, char* stage, int wave) const {
+#pragma unroll
+    for (int q = 0; q < COPIES; ++q) {
+      const int k = k0 + kl[q];
+      const bool valid = ((ok >> q) & 1u) && k < l.K;
+      const E* row;
+      if ((second >> q) & 1u)
+        row = k < l.kswitch ? l.p1a + static_cast<size_t>(k) * l.ld1
+                            : l.p1b + static_cast<size_t>(k - l.kswitch) * l.ld1;
+      else
+        row = l.p0 + static_cast<size_t>(k) * l.ld0;
+      const void* g = valid ? static_cast<const void*>(row + col[q]) : static_cast<const void*>(kZeroRow);
+      copy16(g, stage + (wave * COPIES + q) * 1024);
+    }
+  }
+};
+
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+
+// Two transpose reads give lane (l & 31)'s 8 k values (8*(l>>5) .. +7 of k
+// step kk) for 32-wide block b of an I-contiguous stage.
+template <int NBLK>
+__device__ __forceinline__ void read_i(const char* stage, int col0, int lane, int kk, bf16x8_t (&f)[NBLK]) {
+  const int g = lane >> 4, j = lane & 15;
+  const int kg = kk * 16 + 8 * (g >> 1);
+#pragma unroll
+  for (int b = 0; b < NBLK; ++b) {
+    const int nb = col0 + b * 32 + 16 * (g & 1) + 4 * (j & 3);  // first column this lane reads
+    v4s_t h[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int k = kg + 4 * r + (j >> 2);
+      const int u = nb >> 3;
+      const int off = k * 512 + ((u ^ (4 * (k & 3))) << 4) + ((nb & 7) << 1);
+      h[r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s_t*)(stage + off));
+    }
+    struct {
+      v4s_t a, b;
+    } pair{h[0], h[1]};
+    f[b] = __builtin_bit_cast(bf16x8_t, pair);
+  }
+}
+
+// operand traits
+template <class L>
+struct Op;
+template <typename E>
+struct Op<KRows2<E>> {
+  using Tile = KTile<E>;
+  template <int NBLK>
+  __device__ __forceinline__ static void read(const char* s, int r0, int lane, int kk, bf16x8_t (&f)[NBLK]) {
+    read_k<NBLK>(s, r0, lane, kk, f);
+  }
+};
+template <typename E>
+struct Op<ICols2<E>> {
+  using Tile = ITile<E>;
+  template <int NBLK>
+  __device__ __forceinline__ static void read(const char* s, int r0, int lane, int kk, bf16x8_t (&f)[NBLK]) {
+    read_i<NBLK>(s, r0, lane, kk, f);
+  }
+};
+
+__device__ __forceinline__ void wave_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Wait until at most `tiles_after` tiles' copies (2*COPIES each per wave)
+// are still in flight.
+__device__ __forceinline__ void wait_copies(int tiles_after) {
+  static_assert(2 * COPIES == 4, "wait counts below assume 4 copies per tile");
+  __builtin_amdgcn_sched_barrier(0);
+  if (tiles_after >= 2)
+    asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+  else if (tiles_after == 1)
+    asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+  else
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+}  // namespace dma
+
+template <class AL, class BL, class Epi>
+__global__ void __launch_bounds__(dma::NT, 1)
+    gemm_bf16_dma(AL al, BL bl, Epi epi, int M, int N, int K, int ktiles_per_split) {
+  using namespace dma;
+  constexpr int MB = WM / 32, NB = WN / 32;
+  __shared__ __attribute__((aligned(1024))) char a0[TILE_BYTES], a1[TILE_BYTES], a2[TILE_BYTES], a3[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char b0[TILE_BYTES], b1[TILE_BYTES], b2[TILE_BYTES], b3[TILE_BYTES];
+  using ATile = typename Op<AL>::Tile;
+  using BTile = typename Op<BL>::Tile;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm0 = (wave / WAVES_N) * WM, wn0 = (wave % WAVES_N) * WN;
+  int tm, tn;
+  xcd_tile(blockIdx.x, (M + BM - 1) / BM, (N + BN - 1) / BN, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int split = blockIdx.z;
+  const int nkt = (K + BK - 1) / BK;
+  const int kt0 = split * ktiles_per_split;
+  const int kt1 = min(nkt, kt0 + ktiles_per_split);
+
+  f32x16_t acc[MB][NB];
+#pragma unroll
+  for (int a = 0; a < MB; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.0f;
+
+  ATile ta;
+  BTile tb;
+  ta.init(al, m0, wave, lane);
+  tb.init(bl, n0, wave, lane);
+
+  // prologue: tiles kt0, kt0+1, kt0+2 into stages 0, 1, 2
+  if (kt0 + 0 < kt1) { ta.issue(al, (kt0 + 0) * BK, a0, wave); tb.issue(bl, (kt0 + 0) * BK, b0, wave); }
+  if (kt0 + 1 < kt1) { ta.issue(al, (kt0 + 1) * BK, a1, wave); tb.issue(bl, (kt0 + 1) * BK, b1, wave); }
+  if (kt0 + 2 < kt1) { ta.issue(al, (kt0 + 2) * BK, a2, wave); tb.issue(bl, (kt0 + 2) * BK, b2, wave); }
+
+  // one K tile: wait for its copies, barrier, refill the freed stage, multiply
+  auto step = [&](int kt, const char* as, const char* bs, char* an, char* bn) {
+    wait_copies(min(kt + 2, kt1 - 1) - kt);
+    wave_barrier();
+    if (kt + 3 < kt1) {
+      ta.issue(al, (kt + 3) * BK, an, wave);
+      tb.issue(bl, (kt + 3) * BK, bn, wave);
+    }
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      bf16x8_t af[MB], bfr[NB];
+      Op<AL>::template read<MB>(as, wm0, lane, kk, af);
+      Op<BL>::template read<NB>(bs, wn0, lane, kk, bfr);
+#pragma unroll
+      for (int a = 0; a < MB; ++a)
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
+    }
+  };
+  for (int kt = kt0; kt < kt1; kt += 4) {
+    step(kt, a0, b0, a3, b3);
+    if (kt + 1 < kt1) step(kt + 1, a1, b1, a0, b0);
+    if (kt + 2 < kt1) step(kt + 2, a2, b2, a1, b1);
+    if (kt + 3 < kt1) step(kt + 3, a3, b3, a2, b2);
+  }
+
+  // accumulator layout of a 32 x 32 block: lane holds column (lane & 31);
+  // register e holds row 8*(e/4) + 4*(lane/32) + (e%4)
+  const bool full = m0 + BM <= M && n0 + BN <= N;
+#pragma unroll
+  for (int a = 0; a < MB; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int i = m0 + wm0 + a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        const int j = n0 + wn0 + b * 32 + (lane & 31);
+        if (full || (i < M && j < N)) epi(i, j, acc[a][b][e], split);
+      }
+}
+
+template <class AL, class BL, class Epi>
+inline void launch_gemm_bf16_dma(const AL& al, const BL& bl, const Epi& epi, int M, int N, int K, int splits,
+                                 hipStream_t s) {
+  const int nkt = (K + dma::BK - 1) / dma::BK;
+  const int kps = (nkt + splits - 1) / splits;
+  const unsigned tiles = ((M + 255) / 256) * ((N + 255) / 256);
+  hipLaunchKernelGGL((gemm_bf16_dma<AL, BL, Epi>), dim3(tiles, 1, splits), dim3(dma::NT), 0, s, al, bl, epi, M, N,
+                     K, kps);
+}
+
+// --------------------------------------------------------------- planning
+
+struct GemmPlan {
+  bool bf16;
+  BfTile tile;
+  int splits;
+};
+
+inline int cdiv(long long a, long long b) { return static_cast<int>((a + b - 1) / b); }
+
+// Engine used for 256 x 256 blocks; O5_BF16_TILE=w4|w8|128 selects one of the
+// register-staged engines instead (for comparison runs).
+inline int bf16_tile_override() {
+  static const int v = [] {
+    const char* e = std::getenv("O5_BF16_TILE");
+    if (!e) return 0;
+    if (e[0] == 'w' && e[1] == '4') return 1;
+    if (e[0] == 'w' && e[1] == '8') return 2;
+    if (e[0] == '1') return 3;
+    return 0;
+  }();
+  return v;
+}
+
+// Choose engine, tile and split-K so the launch has >= ~256 blocks (one per
+// CU) while every split keeps a reasonable number of K tiles.
+inline GemmPlan plan_gemm(bool bf16, int M, int N, int K) {
+  GemmPlan p{bf16, BfTile::kDma256, 1};
+  if (!bf16) {
+    const int tiles = cdiv(M, 64) * cdiv(N, 64);
+    const int nkt = cdiv(K, 16);
+    int s = cdiv(512, tiles);
+    s = std::min(s, std::max(1, nkt / 8));
+    p.splits = std::max(1, std::min(s, 16));
+    return p;
+  }
+  const int nkt = cdiv(K, 64);
+  const int t256 = cdiv(M, 256) * cdiv(N, 256);
+  const int ov = bf16_tile_override();
+  if (t256 >= 64 && ov != 3) {
+    int s = cdiv(256, t256);
+    s = std::min(s, std::max(1, nkt / 16));
+    p.tile = ov == 1 ? BfTile::k256x256 : ov == 2 ? BfTile::k256x256w8 : BfTile::kDma256;
+    p.splits = std::max(1, std::min(s, 8));
+    return p;
+  }
+  const int t128 = cdiv(M, 128) * cdiv(N, 128);
+  int s = cdiv(256, t128);
+  s = std::min(s, std::max(1, nkt / 8));
+  p.tile = BfTile::k128x128;
+  p.splits = std::max(1, std::min(s, 8));
+  return p;
+}
+
+// The direct-to-LDS engine takes I-contiguous operands without a mask only.
+template <class L>
+inline bool dma_ok(const L&) { return true; }
+template <typename E>
+inline bool dma_ok(const ICols2<E>& l) { return l.mask1 == nullptr; }
+
+template <class AL, class BL, class Epi>
+inline void run_gemm(const GemmPlan& p, const AL& al, const BL& bl, const Epi& epi, int M, int N, int K,
+                     hipStream_t s) {
+  if constexpr (AL::kBf16 && BL::kBf16) {
+    if (p.bf16) {
+      if (p.tile == BfTile::kDma256 && dma_ok(al) && dma_ok(bl)) {
+        launch_gemm_bf16_dma(al, bl, epi, M, N, K, p.splits, s);
+        return;
+      }
+      launch_gemm_bf16(al, bl, epi, M, N, K, p.splits,
+                       p.tile == BfTile::kDma256 ? BfTile::k256x256w8 : p.tile, s);
+      return;
+    }
+  }
+  launch_gemm_f32(al, bl, epi, M, N, K, p.splits, s);
+}
+
+}  // namespace o5

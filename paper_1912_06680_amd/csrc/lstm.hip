@@ -20,7 +20,7 @@
 //
 // fp32 path: the FMA engine; bf16 path: the MFMA engine, with h, the saved
 // gates and dG stored in bf16 and everything else in fp32.
-#include "gemm.h"
+#include "gemm_dma.h"
 #include "reduce.h"
 
 namespace o5 {
@@ -144,6 +144,28 @@ __global__ void __launch_bounds__(256) lstm_bwd_cell(
   }
 }
 
+// hp[r] = (1 - reset[r]) * (r < B ? h0[r] : h[r - B]) over the T*B rows: the
+// hidden state each step multiplied (its input from the previous step), as
+// one contiguous operand for the weight-gradient GEMM.  8 elements per thread.
+template <typename E>
+__global__ void __launch_bounds__(256) build_hprev(int T, int B, int H, const E* __restrict__ h0e,
+                                                   const E* __restrict__ h, const uint8_t* __restrict__ reset,
+                                                   E* __restrict__ hp) {
+  static_assert(sizeof(E) == 2, "bf16 only");
+  const size_t n8 = static_cast<size_t>(T) * B * H / 8;
+  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= n8) return;
+  const size_t e = i * 8;
+  const size_t r = e / H;
+  const size_t col = e - r * H;
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (!(reset && reset[r])) {
+    const E* src = r < static_cast<size_t>(B) ? h0e + r * H + col : h + (r - B) * H + col;
+    v = *reinterpret_cast<const uint4*>(src);
+  }
+  *reinterpret_cast<uint4*>(hp + e) = v;
+}
+
 // ---------------------------------------------------------------- layouts
 
 struct FwdWs {
@@ -165,7 +187,7 @@ static FwdWs fwd_ws(o5_dtype dt, int T, int B, int D, int H) {
 }
 
 struct BwdWs {
-  size_t dG, dc, rec, h0e, dbpart, total;
+  size_t dG, dc, rec, h0e, dbpart, hp, total;
   int nbc;
   GemmPlan plan_dh, plan_dw, plan_dx;
 };
@@ -190,6 +212,8 @@ static BwdWs bwd_ws(o5_dtype dt, int T, int B, int D, int H) {
   o += align_up(static_cast<size_t>(B) * H * dtype_size(dt));
   w.dbpart = o;
   o += align_up(static_cast<size_t>(T) * w.nbc * 4 * H * sizeof(float));
+  w.hp = o;
+  if (bf) o += align_up(static_cast<size_t>(T) * B * H * dtype_size(dt));
   w.total = o;
   return w;
 }
@@ -291,11 +315,23 @@ static int lstm_bptt_impl(int T, int B, int D, int H, const E* x, const E* Wx, c
   {
     const int R = T * B;
     ICols2<E> al{dG, nullptr, nullptr, nullptr, 4 * H, 0, 4 * H, 4 * H, R, 0};
-    ICols2<E> bl{x, h0e, h, reset, D, H, D, D + H, R, B};
     EpiStoreF32Split2 epi{dWx, dWh, D, H, D};
-    ktimer_begin(kSiteLstmDwGemm, s);
-    run_gemm(w.plan_dw, al, bl, epi, 4 * H, D + H, R, s);
-    ktimer_end(kSiteLstmDwGemm, s);
+    if constexpr (sizeof(E) == 2) {
+      // the masked previous hidden state as one contiguous operand
+      E* hp = reinterpret_cast<E*>(ws + w.hp);
+      const size_t n8 = static_cast<size_t>(R) * H / 8;
+      hipLaunchKernelGGL(build_hprev<E>, dim3(static_cast<unsigned>((n8 + 255) / 256)), dim3(256), 0, s, T, B, H, h0e,
+                         h, reset, hp);
+      ICols2<E> bl{x, hp, hp, nullptr, D, H, D, D + H, R, R};
+      ktimer_begin(kSiteLstmDwGemm, s);
+      run_gemm(w.plan_dw, al, bl, epi, 4 * H, D + H, R, s);
+      ktimer_end(kSiteLstmDwGemm, s);
+    } else {
+      ICols2<E> bl{x, h0e, h, reset, D, H, D, D + H, R, B};
+      ktimer_begin(kSiteLstmDwGemm, s);
+      run_gemm(w.plan_dw, al, bl, epi, 4 * H, D + H, R, s);
+      ktimer_end(kSiteLstmDwGemm, s);
+    }
   }
   hipLaunchKernelGGL(colsum_rows, dim3(cdiv(4 * H, 256)), dim3(256), 0, s, T * w.nbc, 4 * H, dbpart, db);
   if (dx) {
