@@ -31,8 +31,8 @@ def _hipcc():
     raise RuntimeError("hipcc not found (ROCm is required to build libo5)")
 
 
-def _compile(hipcc, src, obj):
-    cmd = [hipcc, *HIPCC_FLAGS, "-c", src, "-o", obj]
+def _compile(hipcc, src, obj, defines=()):
+    cmd = [hipcc, *HIPCC_FLAGS, *[f"-D{d}" for d in defines], "-c", src, "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     msgs = "\n".join(l for l in (res.stdout + res.stderr).splitlines()
                      if "is not a recognized feature" not in l)
@@ -41,26 +41,29 @@ def _compile(hipcc, src, obj):
     return msgs
 
 
-def build(verbose=False):
-    """Compile all HIP sources and link libo5.so.  Always rebuilds."""
+def build(verbose=False, out=None, defines=()):
+    """Compile all HIP sources and link libo5.so (or `out`).  Always rebuilds.
+    `defines` are extra -D flags (tuning variants)."""
     hipcc = _hipcc()
-    os.makedirs(BUILD_DIR, exist_ok=True)
+    lib_path = out or LIB_PATH
+    build_dir = BUILD_DIR if out is None else out + ".build"
+    os.makedirs(build_dir, exist_ok=True)
     srcs = sorted(f for f in os.listdir(CSRC) if f.endswith(".hip"))
-    objs = [os.path.join(BUILD_DIR, s[:-4] + ".o") for s in srcs]
+    objs = [os.path.join(build_dir, s[:-4] + ".o") for s in srcs]
     jobs = min(len(srcs), max(1, min(8, os.cpu_count() or 1)))
     with _cf.ThreadPoolExecutor(jobs) as ex:
-        futs = [ex.submit(_compile, hipcc, os.path.join(CSRC, s), o) for s, o in zip(srcs, objs)]
+        futs = [ex.submit(_compile, hipcc, os.path.join(CSRC, s), o, defines) for s, o in zip(srcs, objs)]
         for s, f in zip(srcs, futs):
             msgs = f.result()
             if verbose and msgs.strip():
                 print(f"[{s}]\n{msgs}", file=sys.stderr)
-    tmp = LIB_PATH + ".tmp"
+    tmp = lib_path + ".tmp"
     cmd = [hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed:\n{res.stdout}{res.stderr}")
-    os.replace(tmp, LIB_PATH)
-    return LIB_PATH
+    os.replace(tmp, lib_path)
+    return lib_path
 
 
 if __name__ == "__main__":

@@ -89,6 +89,11 @@ struct KRows2 {
   const E* p1;
   const uint8_t* mask1;
   int ld0, ld1, K0, K, rows;
+  // gate gathering (direct-to-LDS engine only): when gstride > 0, tile row r
+  // of the block starting at row0 is source row (r / 64) * gstride +
+  // row0 / 4 + r % 64, i.e. a 256-row tile holds the four gate blocks
+  // (stride gstride = H) of 64 consecutive hidden units.
+  int gstride = 0;
 
   __device__ __forceinline__ float at(int i, int k) const {
     if (i >= rows || k >= K) return 0.0f;
@@ -269,6 +274,7 @@ struct ICols2 {
 // Plain fp32 store of C (row-major, ldc) into slice `split` of a stack of
 // M x N partial results (slice stride = sstride elements).
 struct EpiStoreF32 {
+  static constexpr int kTileSmem = 0;
   float* c;
   int ldc;
   size_t sstride;
@@ -280,6 +286,7 @@ struct EpiStoreF32 {
 // Store into one of two fp32 matrices split by column: j < J0 -> c0[i*ld0 + j],
 // else c1[i*ld1 + j - J0]  (dW = [dW_x | dW_h]).
 struct EpiStoreF32Split2 {
+  static constexpr int kTileSmem = 0;
   float* c0;
   float* c1;
   int ld0, ld1, J0;
@@ -294,6 +301,7 @@ struct EpiStoreF32Split2 {
 // Store converted to the element type E (dx in the GEMM input type).
 template <typename E>
 struct EpiStoreElem {
+  static constexpr int kTileSmem = 0;
   E* c;
   int ldc;
   __device__ __forceinline__ void operator()(int i, int j, float v, int) const {

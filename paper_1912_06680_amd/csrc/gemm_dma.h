@@ -36,6 +36,10 @@
 
 #include "gemm.h"
 
+#ifndef O5_DMA_READ_AHEAD
+#define O5_DMA_READ_AHEAD 0
+#endif
+
 namespace o5 {
 
 namespace dma {
@@ -76,7 +80,7 @@ struct KTile {
 #pragma unroll
     for (int q = 0; q < COPIES; ++q) {
       const int r = (wave * COPIES + q) * 16 + (lane >> 2);  // tile row this lane fills
-      const int row = row0 + r;
+      const int row = l.gstride > 0 ? (r >> 6) * l.gstride + (row0 >> 2) + (r & 63) : row0 + r;
       const int chunk = slot ^ ((r >> 2) & 3);
       koff = chunk * 16;
       const bool valid = row < l.rows;
@@ -232,8 +236,18 @@ __global__ void __launch_bounds__(dma::NT, 1)
     gemm_bf16_dma(AL al, BL bl, Epi epi, int M, int N, int K, int ktiles_per_split) {
   using namespace dma;
   constexpr int MB = WM / 32, NB = WN / 32;
-  __shared__ __attribute__((aligned(1024))) char a0[TILE_BYTES], a1[TILE_BYTES], a2[TILE_BYTES], a3[TILE_BYTES];
-  __shared__ __attribute__((aligned(1024))) char b0[TILE_BYTES], b1[TILE_BYTES], b2[TILE_BYTES], b3[TILE_BYTES];
+  // stages: A tiles at s * TILE_BYTES, B tiles at (4 + s) * TILE_BYTES; a tile
+  // epilogue may reuse the whole array after the K loop.
+  constexpr int SMEM = Epi::kTileSmem > 8 * TILE_BYTES ? Epi::kTileSmem : 8 * TILE_BYTES;
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+  char* const a0 = smem + 0 * TILE_BYTES;
+  char* const a1 = smem + 1 * TILE_BYTES;
+  char* const a2 = smem + 2 * TILE_BYTES;
+  char* const a3 = smem + 3 * TILE_BYTES;
+  char* const b0 = smem + 4 * TILE_BYTES;
+  char* const b1 = smem + 5 * TILE_BYTES;
+  char* const b2 = smem + 6 * TILE_BYTES;
+  char* const b3 = smem + 7 * TILE_BYTES;
   using ATile = typename Op<AL>::Tile;
   using BTile = typename Op<BL>::Tile;
 
@@ -275,6 +289,25 @@ __global__ void __launch_bounds__(dma::NT, 1)
       ta.issue(al, (kt + 3) * BK, an, wave);
       tb.issue(bl, (kt + 3) * BK, bn, wave);
     }
+#if O5_DMA_READ_AHEAD
+    // both k steps' fragments are requested before the first MFMA, so the
+    // second step's LDS latency hides under the first step's MFMAs
+    bf16x8_t af[2][MB], bfr[2][NB];
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      Op<AL>::template read<MB>(as, wm0, lane, kk, af[kk]);
+      Op<BL>::template read<NB>(bs, wn0, lane, kk, bfr[kk]);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * (MB + NB) * 2, 0);  // all LDS reads first
+    __builtin_amdgcn_sched_group_barrier(0x008, 2 * MB * NB, 0);        // then the MFMAs
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk)
+#pragma unroll
+      for (int a = 0; a < MB; ++a)
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kk][a], bfr[kk][b], acc[a][b], 0, 0, 0);
+#else
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
       bf16x8_t af[MB], bfr[NB];
@@ -286,6 +319,7 @@ __global__ void __launch_bounds__(dma::NT, 1)
         for (int b = 0; b < NB; ++b)
           acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
     }
+#endif
   };
   for (int kt = kt0; kt < kt1; kt += 4) {
     step(kt, a0, b0, a3, b3);
@@ -294,19 +328,24 @@ __global__ void __launch_bounds__(dma::NT, 1)
     if (kt + 3 < kt1) step(kt + 3, a3, b3, a2, b2);
   }
 
-  // accumulator layout of a 32 x 32 block: lane holds column (lane & 31);
-  // register e holds row 8*(e/4) + 4*(lane/32) + (e%4)
-  const bool full = m0 + BM <= M && n0 + BN <= N;
+  if constexpr (Epi::kTileSmem > 0) {
+    wave_barrier();  // every wave is done with the stages
+    epi.template tile<MB, NB>(acc, smem, m0, n0, wave / WAVES_N, wave % WAVES_N, lane, tid, M);
+  } else {
+    // accumulator layout of a 32 x 32 block: lane holds column (lane & 31);
+    // register e holds row 8*(e/4) + 4*(lane/32) + (e%4)
+    const bool full = m0 + BM <= M && n0 + BN <= N;
 #pragma unroll
-  for (int a = 0; a < MB; ++a)
+    for (int a = 0; a < MB; ++a)
 #pragma unroll
-    for (int b = 0; b < NB; ++b)
+      for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int i = m0 + wm0 + a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        const int j = n0 + wn0 + b * 32 + (lane & 31);
-        if (full || (i < M && j < N)) epi(i, j, acc[a][b][e], split);
-      }
+        for (int e = 0; e < 16; ++e) {
+          const int i = m0 + wm0 + a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+          const int j = n0 + wn0 + b * 32 + (lane & 31);
+          if (full || (i < M && j < N)) epi(i, j, acc[a][b][e], split);
+        }
+  }
 }
 
 template <class AL, class BL, class Epi>

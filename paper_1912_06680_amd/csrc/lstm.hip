@@ -73,6 +73,81 @@ __global__ void __launch_bounds__(256) lstm_fwd_cell(int B, int H, int S, const 
   }
 }
 
+// The forward cell fused into the epilogue of the step's GEMM.  The GEMM's B
+// tile is gate-gathered (256 columns = gates i, f, g, o of 64 hidden units),
+// so wave (wm, wn) of the 2 x 4 wave grid holds gate wn of 64 units for 128
+// rows.  In two passes of 128 rows the waves of one row half park their
+// accumulators in LDS ([gate][row][unit], rows padded to 72 floats so the
+// two half-waves of a store hit disjoint banks), then all 512 threads read
+// the four gates of their (row, unit) and finish the cell: c, h and the
+// saved gates go straight to HBM and the pre-activations never do.
+template <typename E>
+struct EpiLstmCell {
+  static constexpr int kPad = 72;
+  static constexpr int kTileSmem = 4 * 128 * kPad * 4;  // 144 KB
+  const float* bias;
+  const float* c_prev;
+  const uint8_t* reset_t;
+  E* h_out;
+  float* c_out;
+  E* gates_out;
+  int H;
+
+  template <int MB, int NB>
+  __device__ __forceinline__ void tile(f32x16_t (&acc)[MB][NB], char* smem, int m0, int n0, int wm, int wn, int lane,
+                                       int tid, int M) const {
+    static_assert(MB * 32 == 128 && NB * 32 == 64, "expects 128 x 64 wave tiles");
+    float* lds = reinterpret_cast<float*>(smem);
+    const int j = (n0 >> 2) + (tid & 63);  // this thread's hidden unit
+    const int rg = tid >> 6;               // row group 0..7
+    const size_t G = 4 * static_cast<size_t>(H);
+    const float bi = bias[j], bf = bias[H + j], bg = bias[2 * H + j], bo = bias[3 * H + j];
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      if (wm == p) {
+#pragma unroll
+        for (int a = 0; a < MB; ++a)
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              const int row = a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+              const int unit = b * 32 + (lane & 31);
+              lds[(wn * 128 + row) * kPad + unit] = acc[a][b][e];
+            }
+      }
+      __syncthreads();
+      for (int i = 0; i < 16; ++i) {
+        const int row = rg + 8 * i;
+        const int bidx = m0 + p * 128 + row;
+        if (bidx < M) {
+          const int u = tid & 63;
+          const float ai = lds[(0 * 128 + row) * kPad + u] + bi;
+          const float af = lds[(1 * 128 + row) * kPad + u] + bf;
+          const float ag = lds[(2 * 128 + row) * kPad + u] + bg;
+          const float ao = lds[(3 * 128 + row) * kPad + u] + bo;
+          const float keep = (reset_t && reset_t[bidx]) ? 0.0f : 1.0f;
+          const size_t hj = static_cast<size_t>(bidx) * H + j;
+          const float cp = keep * c_prev[hj];
+          const float ig = sigmoid_f(ai), fg = sigmoid_f(af), gg = tanh_f(ag), og = sigmoid_f(ao);
+          const float c = fg * cp + ig * gg;
+          c_out[hj] = c;
+          h_out[hj] = elem<E>::from_f32(og * tanh_f(c));
+          if (gates_out) {
+            E* gp = gates_out + static_cast<size_t>(bidx) * G;
+            gp[j] = elem<E>::from_f32(ig);
+            gp[H + j] = elem<E>::from_f32(fg);
+            gp[2 * H + j] = elem<E>::from_f32(gg);
+            gp[3 * H + j] = elem<E>::from_f32(og);
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  __device__ __forceinline__ void operator()(int, int, float, int) const {}
+};
+
 // Backward cell for step t.  rec: [S][B][H] partial sums of dG_{t+1} W_h (or
 // NULL at t = T-1).  dc: in = dc arriving at c_t, out = dc for c_{t-1}.
 template <typename E>
@@ -244,6 +319,25 @@ static int lstm_fwd_impl(int T, int B, int D, int H, const E* x, const E* Wx, co
     h0e = tmp;
   } else {
     h0e = h0;
+  }
+  if constexpr (sizeof(E) == 2) {
+    if (w.plan.tile == BfTile::kDma256 && w.plan.splits == 1) {
+      // one launch per step: GEMM with the cell fused into its epilogue
+      for (int t = 0; t < T; ++t) {
+        const E* hprev = t == 0 ? h0e : h + (t - 1) * BH;
+        const uint8_t* rt = reset ? reset + static_cast<size_t>(t) * B : nullptr;
+        KRows2<E> al{x + static_cast<size_t>(t) * B * D, hprev, rt, D, H, D, D + H, B};
+        KRows2<E> bl{Wx, Wh, nullptr, D, H, D, D + H, 4 * H};
+        bl.gstride = H;
+        const float* cprev = t == 0 ? c0 : c + (t - 1) * BH;
+        E* gt = gates ? gates + static_cast<size_t>(t) * B * 4 * H : nullptr;
+        EpiLstmCell<E> epi{bias, cprev, rt, h + t * BH, c + t * BH, gt, H};
+        ktimer_begin(kSiteLstmFwdGemm, s);
+        launch_gemm_bf16_dma(al, bl, epi, B, 4 * H, D + H, 1, s);
+        ktimer_end(kSiteLstmFwdGemm, s);
+      }
+      return check_launch("o5_lstm_fwd");
+    }
   }
   const dim3 pw_grid(cdiv(H, kPwCols), cdiv(B, kPwRows));
   for (int t = 0; t < T; ++t) {
