@@ -26,29 +26,82 @@ __device__ __forceinline__ void adam_one(const AdamConsts& c, float& p, float& m
   p = p - c.lr * (m * c.inv_bc1) / (sq + c.eps);
 }
 
+typedef float nf4 __attribute__((ext_vector_type(4)));
+typedef uint32_t nu2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float4 ld_nt(const float4* p) {
+  const nf4 v = __builtin_nontemporal_load(reinterpret_cast<const nf4*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void st_nt(float4* p, float4 v) {
+  nf4 w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, reinterpret_cast<nf4*>(p));
+}
+__device__ __forceinline__ void st_nt(uint2* p, uint2 v) {
+  nu2 w = {v.x, v.y};
+  __builtin_nontemporal_store(w, reinterpret_cast<nu2*>(p));
+}
+
+__device__ __forceinline__ void adam4(const AdamConsts& c, size_t i, float* __restrict__ p, float* __restrict__ m,
+                                      float* __restrict__ v, const float* __restrict__ g, float4& pp, float4& mm,
+                                      float4& vv, float4& gg) {
+  (void)p; (void)m; (void)v; (void)g; (void)i;
+  adam_one(c, pp.x, mm.x, vv.x, gg.x);
+  adam_one(c, pp.y, mm.y, vv.y, gg.y);
+  adam_one(c, pp.z, mm.z, vv.z, gg.z);
+  adam_one(c, pp.w, mm.w, vv.w, gg.w);
+}
+
+// Each thread updates two groups of 4 parameters per iteration (indices i and
+// i + stride), so 8 independent 16-byte loads are in flight per thread; the
+// stream is touched once per step, hence the non-temporal hints.
 template <bool kBf16Out>
 __global__ void __launch_bounds__(256) adam_kernel(size_t n, float* __restrict__ p, float* __restrict__ m,
                                                    float* __restrict__ v, const float* __restrict__ g,
                                                    uint16_t* __restrict__ pb, AdamConsts c) {
   const size_t n4 = n / 4;
   const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
-  for (size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n4; i += stride) {
-    float4 pp = reinterpret_cast<float4*>(p)[i];
-    float4 mm = reinterpret_cast<float4*>(m)[i];
-    float4 vv = reinterpret_cast<float4*>(v)[i];
-    const float4 gg = reinterpret_cast<const float4*>(g)[i];
-    adam_one(c, pp.x, mm.x, vv.x, gg.x);
-    adam_one(c, pp.y, mm.y, vv.y, gg.y);
-    adam_one(c, pp.z, mm.z, vv.z, gg.z);
-    adam_one(c, pp.w, mm.w, vv.w, gg.w);
-    reinterpret_cast<float4*>(p)[i] = pp;
-    reinterpret_cast<float4*>(m)[i] = mm;
-    reinterpret_cast<float4*>(v)[i] = vv;
+  float4* p4 = reinterpret_cast<float4*>(p);
+  float4* m4 = reinterpret_cast<float4*>(m);
+  float4* v4 = reinterpret_cast<float4*>(v);
+  const float4* g4 = reinterpret_cast<const float4*>(g);
+  uint2* pb2 = reinterpret_cast<uint2*>(pb);
+  size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  for (; i + stride < n4; i += 2 * stride) {
+    const size_t k = i + stride;
+    float4 pa = ld_nt(p4 + i), pk = ld_nt(p4 + k);
+    float4 ma = ld_nt(m4 + i), mk = ld_nt(m4 + k);
+    float4 va = ld_nt(v4 + i), vk = ld_nt(v4 + k);
+    float4 ga = ld_nt(g4 + i), gk = ld_nt(g4 + k);
+    adam4(c, i, p, m, v, g, pa, ma, va, ga);
+    adam4(c, k, p, m, v, g, pk, mk, vk, gk);
+    st_nt(p4 + i, pa);
+    st_nt(p4 + k, pk);
+    st_nt(m4 + i, ma);
+    st_nt(m4 + k, mk);
+    st_nt(v4 + i, va);
+    st_nt(v4 + k, vk);
     if (kBf16Out) {
-      uint2 o;
-      o.x = f32_to_bf16_bits(pp.x) | (static_cast<uint32_t>(f32_to_bf16_bits(pp.y)) << 16);
-      o.y = f32_to_bf16_bits(pp.z) | (static_cast<uint32_t>(f32_to_bf16_bits(pp.w)) << 16);
-      reinterpret_cast<uint2*>(pb)[i] = o;
+      uint2 oa, ok;
+      oa.x = f32_to_bf16_bits(pa.x) | (static_cast<uint32_t>(f32_to_bf16_bits(pa.y)) << 16);
+      oa.y = f32_to_bf16_bits(pa.z) | (static_cast<uint32_t>(f32_to_bf16_bits(pa.w)) << 16);
+      ok.x = f32_to_bf16_bits(pk.x) | (static_cast<uint32_t>(f32_to_bf16_bits(pk.y)) << 16);
+      ok.y = f32_to_bf16_bits(pk.z) | (static_cast<uint32_t>(f32_to_bf16_bits(pk.w)) << 16);
+      st_nt(pb2 + i, oa);
+      st_nt(pb2 + k, ok);
+    }
+  }
+  for (; i < n4; i += stride) {
+    float4 pa = p4[i], ma = m4[i], va = v4[i], ga = g4[i];
+    adam4(c, i, p, m, v, g, pa, ma, va, ga);
+    p4[i] = pa;
+    m4[i] = ma;
+    v4[i] = va;
+    if (kBf16Out) {
+      uint2 oa;
+      oa.x = f32_to_bf16_bits(pa.x) | (static_cast<uint32_t>(f32_to_bf16_bits(pa.y)) << 16);
+      oa.y = f32_to_bf16_bits(pa.z) | (static_cast<uint32_t>(f32_to_bf16_bits(pa.w)) << 16);
+      pb2[i] = oa;
     }
   }
   if (blockIdx.x == 0) {
@@ -91,8 +144,8 @@ extern "C" int o5_adam_step(size_t n, float* p, float* m, float* v, const float*
   c.inv_bc2 = static_cast<float>(1.0 / (1.0 - std::pow(static_cast<double>(hp.beta2), step)));
   c.eps = hp.eps;
   c.clip_k = hp.clip_k;
-  size_t blocks = (n / 4 + 255) / 256;
-  const size_t cap = 256 * 16;  // 16 blocks per CU of MI355X: enough waves in flight to saturate HBM
+  size_t blocks = (n / 8 + 255) / 256;
+  const size_t cap = 256 * 8;  // 8 blocks of 256 threads per CU of MI355X, 8 loads in flight each
   if (blocks > cap) blocks = cap;
   if (blocks < 1) blocks = 1;
   ktimer_begin(kSiteAdam, as_stream(stream));

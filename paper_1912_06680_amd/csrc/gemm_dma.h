@@ -39,17 +39,27 @@
 #ifndef O5_DMA_READ_AHEAD
 #define O5_DMA_READ_AHEAD 0
 #endif
+#ifndef O5_DMA_WAVES
+#define O5_DMA_WAVES 8
+#endif
 
 namespace o5 {
 
 namespace dma {
 
 constexpr int BM = 256, BN = 256, BK = 32, STAGES = 4;
-constexpr int WM = 128, WN = 64, WAVES_M = BM / WM, WAVES_N = BN / WN;
-constexpr int NWAVES = WAVES_M * WAVES_N;  // 8
-constexpr int NT = NWAVES * 64;            // 512
+#if O5_DMA_WAVES == 4
+// 4 waves (2 x 2) of 128 x 128, one wave per SIMD
+constexpr int WM = 128, WN = 128;
+#else
+// 8 waves (2 x 4) of 128 x 64, two waves per SIMD
+constexpr int WM = 128, WN = 64;
+#endif
+constexpr int WAVES_M = BM / WM, WAVES_N = BN / WN;
+constexpr int NWAVES = WAVES_M * WAVES_N;
+constexpr int NT = NWAVES * 64;
 constexpr int TILE_BYTES = 256 * BK * 2;   // 16 KB per operand per stage
-constexpr int COPIES = TILE_BYTES / 1024 / NWAVES;  // 1 KB copies per wave per operand per tile (2)
+constexpr int COPIES = TILE_BYTES / 1024 / NWAVES;  // 1 KB copies per wave per operand per tile
 
 // 1 KB of zeros: the source of every copy that falls outside a matrix.
 __device__ __attribute__((aligned(16))) const uint16_t kZeroRow[512] = {};
@@ -218,12 +228,12 @@ __device__ __forceinline__ void wave_barrier() {
 // Wait until at most `tiles_after` tiles' copies (2*COPIES each per wave)
 // are still in flight.
 __device__ __forceinline__ void wait_copies(int tiles_after) {
-  static_assert(2 * COPIES == 4, "wait counts below assume 4 copies per tile");
+  constexpr int L = 2 * COPIES;
   __builtin_amdgcn_sched_barrier(0);
   if (tiles_after >= 2)
-    asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * L) : "memory");
   else if (tiles_after == 1)
-    asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(L) : "memory");
   else
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __builtin_amdgcn_sched_barrier(0);
@@ -330,7 +340,7 @@ __global__ void __launch_bounds__(dma::NT, 1)
 
   if constexpr (Epi::kTileSmem > 0) {
     wave_barrier();  // every wave is done with the stages
-    epi.template tile<MB, NB>(acc, smem, m0, n0, wave / WAVES_N, wave % WAVES_N, lane, tid, M);
+    epi.template tile<MB, NB>(acc, smem, m0, n0, wave / WAVES_N, wn0, lane, tid, M);
   } else {
     // accumulator layout of a 32 x 32 block: lane holds column (lane & 31);
     // register e holds row 8*(e/4) + 4*(lane/32) + (e%4)

@@ -75,8 +75,9 @@ __global__ void __launch_bounds__(256) lstm_fwd_cell(int B, int H, int S, const 
 
 // The forward cell fused into the epilogue of the step's GEMM.  The GEMM's B
 // tile is gate-gathered (256 columns = gates i, f, g, o of 64 hidden units),
-// so wave (wm, wn) of the 2 x 4 wave grid holds gate wn of 64 units for 128
-// rows.  In two passes of 128 rows the waves of one row half park their
+// so a wave whose tile starts at column wn0 holds gate (column / 64) of unit
+// (column % 64) for 128 rows.  In two passes of 128 rows the waves of one row
+// half park their
 // accumulators in LDS ([gate][row][unit], rows padded to 72 floats so the
 // two half-waves of a store hit disjoint banks), then all 512 threads read
 // the four gates of their (row, unit) and finish the cell: c, h and the
@@ -94,12 +95,13 @@ struct EpiLstmCell {
   int H;
 
   template <int MB, int NB>
-  __device__ __forceinline__ void tile(f32x16_t (&acc)[MB][NB], char* smem, int m0, int n0, int wm, int wn, int lane,
+  __device__ __forceinline__ void tile(f32x16_t (&acc)[MB][NB], char* smem, int m0, int n0, int wm, int wn0, int lane,
                                        int tid, int M) const {
-    static_assert(MB * 32 == 128 && NB * 32 == 64, "expects 128 x 64 wave tiles");
+    static_assert(MB * 32 == 128, "expects 128-row wave tiles");
     float* lds = reinterpret_cast<float*>(smem);
     const int j = (n0 >> 2) + (tid & 63);  // this thread's hidden unit
-    const int rg = tid >> 6;               // row group 0..7
+    const int rg = tid >> 6;               // row group
+    const int rstep = blockDim.x >> 6;     // row groups in the block
     const size_t G = 4 * static_cast<size_t>(H);
     const float bi = bias[j], bf = bias[H + j], bg = bias[2 * H + j], bo = bias[3 * H + j];
 #pragma unroll
@@ -112,13 +114,12 @@ struct EpiLstmCell {
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
               const int row = a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-              const int unit = b * 32 + (lane & 31);
-              lds[(wn * 128 + row) * kPad + unit] = acc[a][b][e];
+              const int col = wn0 + b * 32 + (lane & 31);  // gate col / 64, unit col % 64
+              lds[((col >> 6) * 128 + row) * kPad + (col & 63)] = acc[a][b][e];
             }
       }
       __syncthreads();
-      for (int i = 0; i < 16; ++i) {
-        const int row = rg + 8 * i;
+      for (int row = rg; row < 128; row += rstep) {
         const int bidx = m0 + p * 128 + row;
         if (bidx < M) {
           const int u = tid & 63;
@@ -148,8 +149,33 @@ struct EpiLstmCell {
   __device__ __forceinline__ void operator()(int, int, float, int) const {}
 };
 
+// Four consecutive elements as float4 (fp32 or bf16 storage).
+template <typename E> struct Vec4;
+template <> struct Vec4<float> {
+  __device__ __forceinline__ static float4 load(const float* p) { return *reinterpret_cast<const float4*>(p); }
+  __device__ __forceinline__ static void store(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+};
+template <> struct Vec4<uint16_t> {
+  __device__ __forceinline__ static float4 load(const uint16_t* p) {
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                       __uint_as_float(u.y & 0xffff0000u));
+  }
+  __device__ __forceinline__ static void store(uint16_t* p, float4 v) {
+    uint2 u;
+    u.x = f32_to_bf16_bits(v.x) | (static_cast<uint32_t>(f32_to_bf16_bits(v.y)) << 16);
+    u.y = f32_to_bf16_bits(v.z) | (static_cast<uint32_t>(f32_to_bf16_bits(v.w)) << 16);
+    *reinterpret_cast<uint2*>(p) = u;
+  }
+};
+
+__device__ __forceinline__ float4 f4(float a) { return make_float4(a, a, a, a); }
+
 // Backward cell for step t.  rec: [S][B][H] partial sums of dG_{t+1} W_h (or
 // NULL at t = T-1).  dc: in = dc arriving at c_t, out = dc for c_{t-1}.
+// Block: 64 hidden units x 32 rows; each thread owns 4 consecutive units of
+// 2 rows (16-byte fp32 and 8-byte bf16 accesses) and the block writes one
+// partial column sum of dG per gate and unit for the bias gradient.
 template <typename E>
 __global__ void __launch_bounds__(256) lstm_bwd_cell(
     int B, int H, int S, const float* __restrict__ rec, const uint8_t* __restrict__ reset_next,
@@ -157,65 +183,90 @@ __global__ void __launch_bounds__(256) lstm_bwd_cell(
     float* dc_out, const E* __restrict__ gates_t, const float* __restrict__ c_t,
     const float* __restrict__ c_prev, const uint8_t* __restrict__ reset_t, E* __restrict__ dG_t,
     float* __restrict__ db_part) {
-  __shared__ float red[kPwRowGroups][4][kPwCols];
-  const int jl = threadIdx.x & 63;
-  const int j = blockIdx.x * kPwCols + jl;
-  const int rg = threadIdx.x >> 6;
+  constexpr int kRowGroups = 16;
+  __shared__ float red[kRowGroups][4][kPwCols];
+  const int jq = threadIdx.x & 15;
+  const int rg = threadIdx.x >> 4;
+  const int j = blockIdx.x * kPwCols + jq * 4;
   const size_t G = 4 * static_cast<size_t>(H);
   const size_t sstride = static_cast<size_t>(B) * H;
-  float sdi = 0.f, sdf = 0.f, sdg = 0.f, sdo = 0.f;
-  if (j < H) {
-    for (int r = rg; r < kPwRows; r += kPwRowGroups) {
-      const int b = blockIdx.y * kPwRows + r;
-      if (b >= B) break;
-      const size_t hj = static_cast<size_t>(b) * H + j;
-      const size_t row = static_cast<size_t>(b) * G;
-      float dh = dh_t[hj];
-      if (dh_extra) dh += dh_extra[hj];
-      if (rec) {
-        float acc = 0.0f;
-        for (int s = 0; s < S; ++s) acc += rec[s * sstride + hj];
-        const float keep_n = (reset_next && reset_next[b]) ? 0.0f : 1.0f;
-        dh += keep_n * acc;
+  float4 sd[4] = {f4(0.f), f4(0.f), f4(0.f), f4(0.f)};
+  for (int r = rg; r < kPwRows; r += kRowGroups) {
+    const int b = blockIdx.y * kPwRows + r;
+    if (b >= B) break;
+    const size_t hj = static_cast<size_t>(b) * H + j;
+    const size_t row = static_cast<size_t>(b) * G;
+    float4 dh = Vec4<float>::load(dh_t + hj);
+    if (dh_extra) {
+      const float4 e = Vec4<float>::load(dh_extra + hj);
+      dh = make_float4(dh.x + e.x, dh.y + e.y, dh.z + e.z, dh.w + e.w);
+    }
+    if (rec) {
+      float4 acc = f4(0.f);
+      for (int s = 0; s < S; ++s) {
+        const float4 v = Vec4<float>::load(rec + s * sstride + hj);
+        acc = make_float4(acc.x + v.x, acc.y + v.y, acc.z + v.z, acc.w + v.w);
       }
-      const float dcin = dc_in ? dc_in[hj] : 0.0f;
-      const float ig = elem<E>::to_f32(gates_t[row + j]);
-      const float fg = elem<E>::to_f32(gates_t[row + H + j]);
-      const float gg = elem<E>::to_f32(gates_t[row + 2 * H + j]);
-      const float og = elem<E>::to_f32(gates_t[row + 3 * H + j]);
-      const float tc = tanh_f(c_t[hj]);
-      const float keep = (reset_t && reset_t[b]) ? 0.0f : 1.0f;
-      const float cp = keep * c_prev[hj];
-      const float dc = dcin + dh * og * (1.0f - tc * tc);
-      const float dai = dc * gg * ig * (1.0f - ig);
-      const float daf = dc * cp * fg * (1.0f - fg);
-      const float dag = dc * ig * (1.0f - gg * gg);
-      const float dao = dh * tc * og * (1.0f - og);
-      dc_out[hj] = keep * dc * fg;
-      dG_t[row + j] = elem<E>::from_f32(dai);
-      dG_t[row + H + j] = elem<E>::from_f32(daf);
-      dG_t[row + 2 * H + j] = elem<E>::from_f32(dag);
-      dG_t[row + 3 * H + j] = elem<E>::from_f32(dao);
-      sdi += dai;
-      sdf += daf;
-      sdg += dag;
-      sdo += dao;
+      const float kn = (reset_next && reset_next[b]) ? 0.0f : 1.0f;
+      dh = make_float4(dh.x + kn * acc.x, dh.y + kn * acc.y, dh.z + kn * acc.z, dh.w + kn * acc.w);
     }
+    const float4 dcin = dc_in ? Vec4<float>::load(dc_in + hj) : f4(0.f);
+    const float4 ig = Vec4<E>::load(gates_t + row + j);
+    const float4 fg = Vec4<E>::load(gates_t + row + H + j);
+    const float4 gg = Vec4<E>::load(gates_t + row + 2 * H + j);
+    const float4 og = Vec4<E>::load(gates_t + row + 3 * H + j);
+    const float4 ct = Vec4<float>::load(c_t + hj);
+    const float4 cpr = Vec4<float>::load(c_prev + hj);
+    const float keep = (reset_t && reset_t[b]) ? 0.0f : 1.0f;
+    const float* dhp = &dh.x;
+    const float* dcp = &dcin.x;
+    const float* ip = &ig.x;
+    const float* fp = &fg.x;
+    const float* gp = &gg.x;
+    const float* op = &og.x;
+    const float* cp_ = &ct.x;
+    const float* pp = &cpr.x;
+    float4 dco, dai, daf, dag, dao;
+    float* dcop = &dco.x;
+    float* aip = &dai.x;
+    float* afp = &daf.x;
+    float* agp = &dag.x;
+    float* aop = &dao.x;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float tc = tanh_f(cp_[q]);
+      const float cprev = keep * pp[q];
+      const float dc = dcp[q] + dhp[q] * op[q] * (1.0f - tc * tc);
+      aip[q] = dc * gp[q] * ip[q] * (1.0f - ip[q]);
+      afp[q] = dc * cprev * fp[q] * (1.0f - fp[q]);
+      agp[q] = dc * ip[q] * (1.0f - gp[q] * gp[q]);
+      aop[q] = dhp[q] * tc * op[q] * (1.0f - op[q]);
+      dcop[q] = keep * dc * fp[q];
+    }
+    Vec4<float>::store(dc_out + hj, dco);
+    Vec4<E>::store(dG_t + row + j, dai);
+    Vec4<E>::store(dG_t + row + H + j, daf);
+    Vec4<E>::store(dG_t + row + 2 * H + j, dag);
+    Vec4<E>::store(dG_t + row + 3 * H + j, dao);
+    sd[0] = make_float4(sd[0].x + dai.x, sd[0].y + dai.y, sd[0].z + dai.z, sd[0].w + dai.w);
+    sd[1] = make_float4(sd[1].x + daf.x, sd[1].y + daf.y, sd[1].z + daf.z, sd[1].w + daf.w);
+    sd[2] = make_float4(sd[2].x + dag.x, sd[2].y + dag.y, sd[2].z + dag.z, sd[2].w + dag.w);
+    sd[3] = make_float4(sd[3].x + dao.x, sd[3].y + dao.y, sd[3].z + dao.z, sd[3].w + dao.w);
   }
-  red[rg][0][jl] = sdi;
-  red[rg][1][jl] = sdf;
-  red[rg][2][jl] = sdg;
-  red[rg][3][jl] = sdo;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    red[rg][g][jq * 4 + 0] = sd[g].x;
+    red[rg][g][jq * 4 + 1] = sd[g].y;
+    red[rg][g][jq * 4 + 2] = sd[g].z;
+    red[rg][g][jq * 4 + 3] = sd[g].w;
+  }
   __syncthreads();
-  if (rg == 0 && j < H) {
-    float* out = db_part + static_cast<size_t>(blockIdx.y) * G;
+  {
+    const int g = threadIdx.x >> 6, jl = threadIdx.x & 63;
+    float sum = 0.0f;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      float s = 0.0f;
-#pragma unroll
-      for (int q = 0; q < kPwRowGroups; ++q) s += red[q][g][jl];
-      out[g * H + j] = s;
-    }
+    for (int q = 0; q < kRowGroups; ++q) sum += red[q][g][jl];
+    db_part[static_cast<size_t>(blockIdx.y) * G + g * H + blockIdx.x * kPwCols + jl] = sum;
   }
 }
 
