@@ -37,6 +37,99 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def source_digest():
+    """sha256 over the library's kernel sources (csrc/*), in name order."""
+    import hashlib
+    d = os.path.join(ROOT, "paper_1912_06680_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(d)):
+        h.update(f.encode())
+        with open(os.path.join(d, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the counter runs summarised in
+    profiles/traffic.json, or None when absent or taken on other sources."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_digest") != source_digest():
+        return None
+    k = t.get("kernels", {}).get(kernel)
+    if not k:
+        return None
+    return k["fetch_bytes_per_launch"] + k["write_bytes_per_launch"]
+
+
+# Kernel (symbol substring) behind each timed site, for the counter summary.
+# Where one symbol serves several sites the most frequent (symbol, grid)
+# group is taken: the recurrent GEMM runs T times per step.
+SITE_SYMBOLS = {
+    "lstm_fwd_gemm": "EpiLstmCell",
+    "lstm_dh_gemm": "gemm_bf16_dma<o5::KRows2<unsigned short>, o5::ICols2<unsigned short>, o5::EpiStoreF32>",
+    "lstm_dw_gemm": "EpiStoreF32Split2",
+    "lstm_bwd_cell": "lstm_bwd_cell",
+    "adam_step": "adam_kernel",
+    "gae": "gae_",
+}
+COPY_REF_N = 1 << 26   # fp32 elements of the reference conversion (256 MiB read, 128 MiB written)
+
+
+def summarize_counters(fetch_dir, write_dir):
+    """Turn two `rocprofv3 --pmc FETCH_SIZE` / `--pmc WRITE_SIZE` runs of
+    `bench.py --copy-ref` into profiles/traffic.json.  Both counters read KiB
+    per dispatch; each is scaled by bytes/counter of the reference conversion
+    (COPY_REF_N fp32 elements read, as many bf16 written), which is the only
+    o5_f32_to_bf16 dispatch with COPY_REF_N / 8 threads."""
+    import csv
+    import glob
+
+    def load(d, counter):
+        groups = {}
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(f) as fh:
+                for r in csv.DictReader(fh):
+                    if r["Counter_Name"] != counter:
+                        continue
+                    key = (r["Kernel_Name"], int(r["Grid_Size"]))
+                    groups.setdefault(key, []).append(float(r["Counter_Value"]) * 1024.0)
+        if not groups:
+            raise SystemExit(f"no {counter} rows under {d}")
+        return groups
+
+    out = {"source_digest": source_digest(), "kernels": {}}
+    scale = {}
+    for name, d, ref_bytes in (("FETCH_SIZE", fetch_dir, 4.0 * COPY_REF_N), ("WRITE_SIZE", write_dir, 2.0 * COPY_REF_N)):
+        g = load(d, name)
+        ref = [v for (k, grid), v in g.items() if "f32_to_bf16_kernel" in k and grid == COPY_REF_N // 8]
+        if len(ref) != 1:
+            raise SystemExit(f"{name}: reference conversion not found exactly once")
+        counted = sum(ref[0]) / len(ref[0])
+        scale[name] = ref_bytes / counted
+        out[name] = {"copy_ref_counted_bytes": counted, "copy_ref_bytes": ref_bytes, "scale": scale[name]}
+        for site, sym in SITE_SYMBOLS.items():
+            cand = [(len(v), k, v) for k, v in g.items() if sym in k[0]]
+            if not cand:
+                continue
+            _, (kname, grid), v = max(cand, key=lambda c: c[0])
+            e = out["kernels"].setdefault(site, {"symbol": kname[:160], "grid_threads": grid})
+            key = "fetch_bytes_per_launch" if name == "FETCH_SIZE" else "write_bytes_per_launch"
+            e[key] = round(scale[name] * sum(v) / len(v))
+            e["dispatches_" + name.lower()] = len(v)
+    out["kernels"] = {k: v for k, v in out["kernels"].items()
+                      if "fetch_bytes_per_launch" in v and "write_bytes_per_launch" in v}
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    with open(path, "w") as fh:
+        json.dump(out, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(out, indent=1))
+
+
 def gpu_behaviour(st, inp):
     """Untimed: actions, log-probabilities and values of a perturbed policy,
     produced by the library itself (forward pass + sampler)."""
@@ -133,7 +226,14 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="full4096")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-ref", action="store_true",
+                    help="after timing, run one conversion of 2^26 fp32 elements (counter scale reference)")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write profiles/traffic.json from two rocprofv3 --pmc runs and exit (no GPU)")
     args = ap.parse_args()
+    if args.summarize_counters:
+        summarize_counters(*args.summarize_counters)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU path "
               "(gradient all-reduce before Adam) is not built", file=sys.stderr)
@@ -170,6 +270,12 @@ def main():
     ms_step = elapsed * 1e3 / args.steps
     value = B * T * args.steps / elapsed
     stats = st.stats.cpu().numpy().tolist()
+    if args.copy_ref:
+        src = torch.ones(COPY_REF_N, dtype=torch.float32, device="cuda")
+        dst = torch.empty(COPY_REF_N, dtype=torch.bfloat16, device="cuda")
+        o5.o5_f32_to_bf16(COPY_REF_N, src, dst)
+        torch.cuda.synchronize()
+        del src, dst
     log(f"{ms_step:.3f} ms/step, {value:.0f} timesteps/s, loss {stats[0]:.5f}")
 
     # per-site device time and algorithmic work per launch
@@ -208,7 +314,7 @@ def main():
     dom = max(flops, key=lambda s: kernels.get(s, {}).get("ms_per_step", 0.0))
     dk = kernels[dom]
     roofline = {"bound": "mfma", "achieved": dk["tflops"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(dk["tflops"] / PEAK_BF16_TFLOPS, 4), "traffic": None, "kernel": dom,
+                "frac": round(dk["tflops"] / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic(dom), "kernel": dom,
                 "flop_per_launch": flops[dom], "ms_per_launch": dk["ms_per_launch"]}
     step_flop = 2.0 * T * B * 4 * H * (D + H) + 2.0 * 4 * H * ((T - 1) * B * H + T * B * H + T * B * D) + \
         3 * 2.0 * T * B * A1 * H

@@ -34,6 +34,8 @@
 // copies use is inside a buffer.
 #pragma once
 
+#include <type_traits>
+
 #include "gemm.h"
 
 #ifndef O5_DMA_READ_AHEAD
@@ -42,12 +44,16 @@
 #ifndef O5_DMA_WAVES
 #define O5_DMA_WAVES 8
 #endif
+#ifndef O5_DMA_STAGES
+#define O5_DMA_STAGES 4
+#endif
 
 namespace o5 {
 
 namespace dma {
 
-constexpr int BM = 256, BN = 256, BK = 32, STAGES = 4;
+constexpr int BM = 256, BN = 256, BK = 32, STAGES = O5_DMA_STAGES;
+static_assert(STAGES >= 3 && STAGES <= 5, "3..5 stages fit in 160 KB of LDS");
 #if O5_DMA_WAVES == 4
 // 4 waves (2 x 2) of 128 x 128, one wave per SIMD
 constexpr int WM = 128, WN = 128;
@@ -230,13 +236,24 @@ __device__ __forceinline__ void wave_barrier() {
 __device__ __forceinline__ void wait_copies(int tiles_after) {
   constexpr int L = 2 * COPIES;
   __builtin_amdgcn_sched_barrier(0);
-  if (tiles_after >= 2)
+  if (tiles_after >= 3)
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * L) : "memory");
+  else if (tiles_after == 2)
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * L) : "memory");
   else if (tiles_after == 1)
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(L) : "memory");
   else
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __builtin_amdgcn_sched_barrier(0);
+}
+
+// Calls f(integral_constant<int, I>) for I = 0 .. N-1 (compile-time unroll).
+template <int I, int N, class F>
+__device__ __forceinline__ void unroll(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    unroll<I + 1, N>(f);
+  }
 }
 
 }  // namespace dma
@@ -246,18 +263,10 @@ __global__ void __launch_bounds__(dma::NT, 1)
     gemm_bf16_dma(AL al, BL bl, Epi epi, int M, int N, int K, int ktiles_per_split) {
   using namespace dma;
   constexpr int MB = WM / 32, NB = WN / 32;
-  // stages: A tiles at s * TILE_BYTES, B tiles at (4 + s) * TILE_BYTES; a tile
-  // epilogue may reuse the whole array after the K loop.
-  constexpr int SMEM = Epi::kTileSmem > 8 * TILE_BYTES ? Epi::kTileSmem : 8 * TILE_BYTES;
+  // stage s: A tile at s * TILE_BYTES, B tile at (STAGES + s) * TILE_BYTES;
+  // a tile epilogue may reuse the whole array after the K loop.
+  constexpr int SMEM = Epi::kTileSmem > 2 * STAGES * TILE_BYTES ? Epi::kTileSmem : 2 * STAGES * TILE_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
-  char* const a0 = smem + 0 * TILE_BYTES;
-  char* const a1 = smem + 1 * TILE_BYTES;
-  char* const a2 = smem + 2 * TILE_BYTES;
-  char* const a3 = smem + 3 * TILE_BYTES;
-  char* const b0 = smem + 4 * TILE_BYTES;
-  char* const b1 = smem + 5 * TILE_BYTES;
-  char* const b2 = smem + 6 * TILE_BYTES;
-  char* const b3 = smem + 7 * TILE_BYTES;
   using ATile = typename Op<AL>::Tile;
   using BTile = typename Op<BL>::Tile;
 
@@ -286,18 +295,22 @@ __global__ void __launch_bounds__(dma::NT, 1)
   ta.init(al, m0, wave, lane);
   tb.init(bl, n0, wave, lane);
 
-  // prologue: tiles kt0, kt0+1, kt0+2 into stages 0, 1, 2
-  if (kt0 + 0 < kt1) { ta.issue(al, (kt0 + 0) * BK, a0, wave); tb.issue(bl, (kt0 + 0) * BK, b0, wave); }
-  if (kt0 + 1 < kt1) { ta.issue(al, (kt0 + 1) * BK, a1, wave); tb.issue(bl, (kt0 + 1) * BK, b1, wave); }
-  if (kt0 + 2 < kt1) { ta.issue(al, (kt0 + 2) * BK, a2, wave); tb.issue(bl, (kt0 + 2) * BK, b2, wave); }
+  // prologue: tiles kt0 .. kt0 + STAGES - 2 into stages 0 .. STAGES - 2
+  unroll<0, STAGES - 1>([&](auto I) {
+    constexpr int st = decltype(I)::value;
+    if (kt0 + st < kt1) {
+      ta.issue(al, (kt0 + st) * BK, smem + st * TILE_BYTES, wave);
+      tb.issue(bl, (kt0 + st) * BK, smem + (STAGES + st) * TILE_BYTES, wave);
+    }
+  });
 
   // one K tile: wait for its copies, barrier, refill the freed stage, multiply
   auto step = [&](int kt, const char* as, const char* bs, char* an, char* bn) {
-    wait_copies(min(kt + 2, kt1 - 1) - kt);
+    wait_copies(min(kt + STAGES - 2, kt1 - 1) - kt);
     wave_barrier();
-    if (kt + 3 < kt1) {
-      ta.issue(al, (kt + 3) * BK, an, wave);
-      tb.issue(bl, (kt + 3) * BK, bn, wave);
+    if (kt + STAGES - 1 < kt1) {
+      ta.issue(al, (kt + STAGES - 1) * BK, an, wave);
+      tb.issue(bl, (kt + STAGES - 1) * BK, bn, wave);
     }
 #if O5_DMA_READ_AHEAD
     // both k steps' fragments are requested before the first MFMA, so the
@@ -331,11 +344,16 @@ __global__ void __launch_bounds__(dma::NT, 1)
     }
 #endif
   };
-  for (int kt = kt0; kt < kt1; kt += 4) {
-    step(kt, a0, b0, a3, b3);
-    if (kt + 1 < kt1) step(kt + 1, a1, b1, a0, b0);
-    if (kt + 2 < kt1) step(kt + 2, a2, b2, a1, b1);
-    if (kt + 3 < kt1) step(kt + 3, a3, b3, a2, b2);
+  // the stage of tile kt is (kt - kt0) % STAGES; unrolling by STAGES keeps
+  // every stage address a compile-time constant
+  for (int kt = kt0; kt < kt1; kt += STAGES) {
+    unroll<0, STAGES>([&](auto I) {
+      constexpr int st = decltype(I)::value;
+      constexpr int nx = (st + STAGES - 1) % STAGES;  // stage refilled during this step
+      if (kt + st < kt1)
+        step(kt + st, smem + st * TILE_BYTES, smem + (STAGES + st) * TILE_BYTES, smem + nx * TILE_BYTES,
+             smem + (STAGES + nx) * TILE_BYTES);
+    });
   }
 
   if constexpr (Epi::kTileSmem > 0) {

@@ -159,3 +159,48 @@ def test_lstm_paper_scale_sampled_rows():
     assert_close("c[rows]", host(got["c"])[:, rows], ref["c"], TOL_BF16)
     for k in ("dWx", "dWh", "db"):
         assert_close(k, host(got[k]), ref[k], TOL_BF16)
+
+
+def test_lstm_dma_engine_ragged_sampled_rows():
+    """Shapes that select the direct-to-LDS engine with partial tiles in every
+    dimension: B = 2000 rows (last M tile partial), H = 1984 (4H and D+H not
+    multiples of 256, dh's N = H ragged), D = 1088, T*B = 4000 (K of the
+    weight-gradient GEMM not a multiple of 32), with state resets.  Checked
+    on sampled rows as in the paper-scale test."""
+    need_gpu()
+    T, B, D, H = 2, 2000, 1088, 1984
+    banner(f"lstm dma ragged T={T} B={B} D={D} H={H}")
+    rng = np.random.Generator(np.random.PCG64(7))
+    bound = 1.0 / np.sqrt(H)
+    inp = dict(
+        Wx=((rng.random((4 * H, D), dtype=np.float32) * 2 - 1) * bound).astype(np.float32),
+        Wh=((rng.random((4 * H, H), dtype=np.float32) * 2 - 1) * bound).astype(np.float32),
+        b=((rng.random(4 * H, dtype=np.float32) * 2 - 1) * bound).astype(np.float32),
+        x=rng.standard_normal((T, B, D), dtype=np.float32),
+        h0=(rng.standard_normal((B, H), dtype=np.float32) * 0.1).astype(np.float32),
+        c0=(rng.standard_normal((B, H), dtype=np.float32) * 0.1).astype(np.float32),
+    )
+    reset = np.zeros((T, B), np.uint8)
+    rows = np.array([3, 1790, 1999])
+    reset[1, 1790] = 1          # reset inside a sampled row
+    reset[0, 3] = 1
+    reset[1, 500] = 1
+    inp["reset"] = reset
+    dh = np.zeros((T, B, H), np.float32)
+    dh[:, rows] = rng.standard_normal((T, len(rows), H), dtype=np.float32)
+    inp["dh"] = dh
+    inp["dhT"] = None
+    inp["dcT"] = None
+    got = _run_gpu(inp, T, B, D, H, True, with_final=False, want_dx=False)
+    sub = dict(inp)
+    sub["x"] = inp["x"][:, rows]
+    sub["h0"] = inp["h0"][rows]
+    sub["c0"] = inp["c0"][rows]
+    sub["reset"] = reset[:, rows]
+    sub["dh"] = dh[:, rows]
+    ref = _oracle(sub, True, with_final=False)
+    assert_close("h[rows]", host(got["h"])[:, rows], ref["h"], TOL_BF16)
+    assert_close("c[rows]", host(got["c"])[:, rows], ref["c"], TOL_BF16)
+    assert_close("gates[rows]", host(got["gates"])[:, rows], ref["gates"], TOL_BF16)
+    for k in ("dWx", "dWh", "db"):
+        assert_close(k, host(got[k]), ref[k], TOL_BF16)
