@@ -85,17 +85,17 @@ __device__ __forceinline__ void copy16(const void* g, char* lds_wave_base) {
 // Rows i of the operand are K-contiguous; two sources along k (split at K0,
 // a multiple of 32): k < K0 -> p0[i*ld0 + k], else p1[i*ld1 + k - K0].
 // mask1[i] != 0 zeroes the second source for row i.
-template <typename E>
+template <typename E, int NC = COPIES>
 struct KTile {
-  const char* ptr0[COPIES];  // row start in source 0 (bytes), or nullptr = zero row
-  const char* ptr1[COPIES];  // row start in source 1
+  const char* ptr0[NC];  // row start in source 0 (bytes), or nullptr = zero row
+  const char* ptr1[NC];  // row start in source 1
   int koff;                  // byte offset of this lane's 16-byte chunk within a tile
 
   __device__ __forceinline__ void init(const KRows2<E>& l, int row0, int wave, int lane) {
     const int slot = lane & 3;
 #pragma unroll
-    for (int q = 0; q < COPIES; ++q) {
-      const int r = (wave * COPIES + q) * 16 + (lane >> 2);  // tile row this lane fills
+    for (int q = 0; q < NC; ++q) {
+      const int r = (wave * NC + q) * 16 + (lane >> 2);  // tile row this lane fills
       const int row = l.gstride > 0 ? (r >> 6) * l.gstride + (row0 >> 2) + (r & 63) : row0 + r;
       const int chunk = slot ^ ((r >> 2) & 3);
       koff = chunk * 16;
@@ -107,18 +107,20 @@ struct KTile {
                     : nullptr;
     }
   }
-  // copy tile starting at k0 into `stage` (this wave's 1 KB pieces)
-  __device__ __forceinline__ void issue(const KRows2<E>& l, int k0, char* stage, int wave) const {
+  // copy piece q of the tile starting at k0 into `stage`
+  __device__ __forceinline__ void issue_one(const KRows2<E>& l, int k0, char* stage, int wave, int q) const {
     const bool seg0 = k0 < l.K0;
     const int kb = seg0 ? k0 : k0 - l.K0;  // element offset inside the source row
     const bool kin = k0 + koff / 2 < l.K;
+    const char* p = seg0 ? ptr0[q] : ptr1[q];
+    const void* g = (p != nullptr && kin) ? static_cast<const void*>(p + kb * 2 + koff)
+                                          : static_cast<const void*>(kZeroRow);
+    copy16(g, stage + (wave * NC + q) * 1024);
+  }
+  // copy tile starting at k0 into `stage` (this wave's 1 KB pieces)
+  __device__ __forceinline__ void issue(const KRows2<E>& l, int k0, char* stage, int wave) const {
 #pragma unroll
-    for (int q = 0; q < COPIES; ++q) {
-      const char* p = seg0 ? ptr0[q] : ptr1[q];
-      const void* g = (p != nullptr && kin) ? static_cast<const void*>(p + kb * 2 + koff)
-                                            : static_cast<const void*>(kZeroRow);
-      copy16(g, stage + (wave * COPIES + q) * 1024);
-    }
+    for (int q = 0; q < NC; ++q) issue_one(l, k0, stage, wave, q);
   }
 };
 
@@ -231,21 +233,22 @@ __device__ __forceinline__ void wave_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-// Wait until at most `tiles_after` tiles' copies (2*COPIES each per wave)
+// Wait until at most `tiles_after` tiles' copies (PER_TILE per wave each)
 // are still in flight.
-__device__ __forceinline__ void wait_copies(int tiles_after) {
-  constexpr int L = 2 * COPIES;
+template <int PER_TILE>
+__device__ __forceinline__ void wait_copies_n(int tiles_after) {
   __builtin_amdgcn_sched_barrier(0);
   if (tiles_after >= 3)
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * L) : "memory");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * PER_TILE) : "memory");
   else if (tiles_after == 2)
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * L) : "memory");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * PER_TILE) : "memory");
   else if (tiles_after == 1)
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(L) : "memory");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(PER_TILE) : "memory");
   else
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __builtin_amdgcn_sched_barrier(0);
 }
+__device__ __forceinline__ void wait_copies(int tiles_after) { wait_copies_n<2 * COPIES>(tiles_after); }
 
 // Calls f(integral_constant<int, I>) for I = 0 .. N-1 (compile-time unroll).
 template <int I, int N, class F>
@@ -384,83 +387,6 @@ inline void launch_gemm_bf16_dma(const AL& al, const BL& bl, const Epi& epi, int
   const unsigned tiles = ((M + 255) / 256) * ((N + 255) / 256);
   hipLaunchKernelGGL((gemm_bf16_dma<AL, BL, Epi>), dim3(tiles, 1, splits), dim3(dma::NT), 0, s, al, bl, epi, M, N,
                      K, kps);
-}
-
-// --------------------------------------------------------------- planning
-
-struct GemmPlan {
-  bool bf16;
-  BfTile tile;
-  int splits;
-};
-
-inline int cdiv(long long a, long long b) { return static_cast<int>((a + b - 1) / b); }
-
-// Engine used for 256 x 256 blocks; O5_BF16_TILE=w4|w8|128 selects one of the
-// register-staged engines instead (for comparison runs).
-inline int bf16_tile_override() {
-  static const int v = [] {
-    const char* e = std::getenv("O5_BF16_TILE");
-    if (!e) return 0;
-    if (e[0] == 'w' && e[1] == '4') return 1;
-    if (e[0] == 'w' && e[1] == '8') return 2;
-    if (e[0] == '1') return 3;
-    return 0;
-  }();
-  return v;
-}
-
-// Choose engine, tile and split-K so the launch has >= ~256 blocks (one per
-// CU) while every split keeps a reasonable number of K tiles.
-inline GemmPlan plan_gemm(bool bf16, int M, int N, int K) {
-  GemmPlan p{bf16, BfTile::kDma256, 1};
-  if (!bf16) {
-    const int tiles = cdiv(M, 64) * cdiv(N, 64);
-    const int nkt = cdiv(K, 16);
-    int s = cdiv(512, tiles);
-    s = std::min(s, std::max(1, nkt / 8));
-    p.splits = std::max(1, std::min(s, 16));
-    return p;
-  }
-  const int nkt = cdiv(K, 64);
-  const int t256 = cdiv(M, 256) * cdiv(N, 256);
-  const int ov = bf16_tile_override();
-  if (t256 >= 64 && ov != 3) {
-    int s = cdiv(256, t256);
-    s = std::min(s, std::max(1, nkt / 16));
-    p.tile = ov == 1 ? BfTile::k256x256 : ov == 2 ? BfTile::k256x256w8 : BfTile::kDma256;
-    p.splits = std::max(1, std::min(s, 8));
-    return p;
-  }
-  const int t128 = cdiv(M, 128) * cdiv(N, 128);
-  int s = cdiv(256, t128);
-  s = std::min(s, std::max(1, nkt / 8));
-  p.tile = BfTile::k128x128;
-  p.splits = std::max(1, std::min(s, 8));
-  return p;
-}
-
-// The direct-to-LDS engine takes I-contiguous operands without a mask only.
-template <class L>
-inline bool dma_ok(const L&) { return true; }
-template <typename E>
-inline bool dma_ok(const ICols2<E>& l) { return l.mask1 == nullptr; }
-
-template <class AL, class BL, class Epi>
-inline void run_gemm(const GemmPlan& p, const AL& al, const BL& bl, const Epi& epi, int M, int N, int K,
-                     hipStream_t s) {
-  if constexpr (AL::kBf16 && BL::kBf16) {
-    if (p.bf16) {
-      if (p.tile == BfTile::kDma256 && dma_ok(al) && dma_ok(bl)) {
-        launch_gemm_bf16_dma(al, bl, epi, M, N, K, p.splits, s);
-        return;
-      }
-      launch_gemm_bf16(al, bl, epi, M, N, K, p.splits,
-                       p.tile == BfTile::kDma256 ? BfTile::k256x256w8 : p.tile, s);
-      return;
-    }
-  }
-  launch_gemm_f32(al, bl, epi, M, N, K, p.splits, s);
 }
 
 }  // namespace o5

@@ -1,0 +1,287 @@
+// bf16 MFMA GEMM for two K-contiguous operands (gfx950):
+//   C[i, j] = sum_k A(i, k) * B(j, k)  (+ epilogue), fp32 accumulate.
+//
+// Block tile 256 x 256 by 4 waves (2 x 2) of 128 x 128, one wave per SIMD:
+// each fragment read from LDS feeds four MFMAs, so a K tile's b128 fragment
+// reads (about one per 5 clocks per CU) cost a third of its MFMA time.
+//
+// Operands go global -> LDS by direct-to-LDS copies (16 bytes per lane,
+// written at M0 + 16 * lane) through a ring of STAGES stages of BK k.  With
+// BK = 64 a copy instruction fetches 8 rows x 128 bytes, i.e. whole cache
+// lines; with BK = 32 it fetches 16 half lines, which halves the rate at
+// which the L2 feeds the CU.  BK = 64 leaves room for two stages only.
+//
+// With one wave per SIMD nothing else hides LDS latency, so the wave
+// software-pipelines its fragments: those of k step s + 1 are read while the
+// MFMAs of step s run.  Before the last k step of tile r the wave waits for
+// its own copies of tile r + 1, meets the other waves at the barrier (after
+// which the stage of tile r is free: every wave has finished reading it),
+// reads the first fragments of tile r + 1 and then interleaves the copies
+// that refill stage r with the MFMAs of that last step.  The copies are
+// inline asm, so the compiler neither waits for them before LDS reads nor
+// edits the explicit waits; each wave issues copies for tiles 0 .. n +
+// STAGES - 2 (those past the K range read zeros or data no one uses, into
+// stages no one reads again), so the wait counts are constants.
+//
+// LDS layout of one operand stage: [256 rows][BK k] bf16, the 16-byte chunk
+// c of row r stored at slot c ^ ((r / R) % C) with C = BK / 8 chunks per row
+// and R = 128 / BK rows per 256 bytes, so the 16 rows of a fragment read
+// fall on 16 distinct 16-byte bank groups.
+#pragma once
+
+#include "gemm_dma.h"
+
+#ifndef O5_KK_BK
+#define O5_KK_BK 64
+#endif
+
+namespace o5 {
+
+namespace kk {
+
+constexpr int BM = 256, BN = 256;
+constexpr int WM = 128, WN = 128, WAVES_N = 2, NWAVES = 4, NT = NWAVES * 64;
+constexpr int MB = WM / 32, NB = WN / 32;
+
+template <int BK>
+struct Cfg {
+  static_assert(BK == 32 || BK == 64, "BK is 32 or 64");
+  static constexpr int STAGES = BK == 64 ? 2 : 4;
+  static constexpr int ROW_BYTES = BK * 2;
+  static constexpr int CPR = BK / 8;                     // 16-byte chunks per row
+  static constexpr int RPI = 1024 / ROW_BYTES;           // rows per 1 KB copy
+  static constexpr int R256 = 256 / ROW_BYTES;           // rows per 256 bytes
+  static constexpr int TILE_BYTES = 256 * ROW_BYTES;     // one operand, one stage
+  static constexpr int NC = TILE_BYTES / 1024 / NWAVES;  // copies per wave per operand per tile
+  static constexpr int KSTEPS = BK / 16;
+  static constexpr int SMEM = 2 * STAGES * TILE_BYTES;
+};
+
+template <int BK>
+__device__ __forceinline__ int slot(int r, int c) {
+  using C = Cfg<BK>;
+  return c ^ ((r / C::R256) % C::CPR);
+}
+
+// Per-lane state for copying one operand's 256-row tiles: copy q of wave w
+// fills tile rows (w * NC + q) * RPI .. + RPI - 1; the lane fetches the chunk
+// that belongs at slot (lane % CPR) of row (lane / CPR).
+template <typename E, int BK>
+struct Tile {
+  using C = Cfg<BK>;
+  const char* ptr0[C::NC];  // row start in source 0 (bytes), or nullptr = zero row
+  const char* ptr1[C::NC];  // row start in source 1
+  int koff[C::NC];          // byte offset of the lane's chunk inside the tile's k range
+
+  __device__ __forceinline__ void init(const KRows2<E>& l, int row0, int wave, int lane) {
+#pragma unroll
+    for (int q = 0; q < C::NC; ++q) {
+      const int r = (wave * C::NC + q) * C::RPI + lane / C::CPR;  // tile row this lane fills
+      const int row = l.gstride > 0 ? (r >> 6) * l.gstride + (row0 >> 2) + (r & 63) : row0 + r;
+      koff[q] = slot<BK>(r, lane % C::CPR) * 16;
+      const bool valid = row < l.rows;
+      const bool masked = valid && l.mask1 != nullptr && l.mask1[row] != 0;
+      ptr0[q] = valid ? reinterpret_cast<const char*>(l.p0 + static_cast<size_t>(row) * l.ld0) : nullptr;
+      ptr1[q] = (valid && !masked && l.p1 != nullptr)
+                    ? reinterpret_cast<const char*>(l.p1 + static_cast<size_t>(row) * l.ld1)
+                    : nullptr;
+    }
+  }
+  // copy q of the tile starting at k0 into `stage`
+  __device__ __forceinline__ void issue_one(const KRows2<E>& l, int k0, char* stage, int wave, int q) const {
+    const bool seg0 = k0 < l.K0;
+    const int kb = seg0 ? k0 : k0 - l.K0;  // element offset inside the source row
+    const bool kin = k0 + koff[q] / 2 < l.K;
+    const char* p = seg0 ? ptr0[q] : ptr1[q];
+    const void* g = (p != nullptr && kin) ? static_cast<const void*>(p + kb * 2 + koff[q])
+                                          : static_cast<const void*>(dma::kZeroRow);
+    dma::copy16(g, stage + (wave * C::NC + q) * 1024);
+  }
+  __device__ __forceinline__ void issue(const KRows2<E>& l, int k0, char* stage, int wave) const {
+#pragma unroll
+    for (int q = 0; q < C::NC; ++q) issue_one(l, k0, stage, wave, q);
+  }
+};
+
+struct Frags {
+  bf16x8_t a[MB], b[NB];
+};
+
+// Fragments of k step s (16 k) for the wave's 128 x 128 tile: lane l holds row
+// (l & 31) of each 32-row block and the 8 k values 8 * (l >> 5) .. + 7.
+template <int BK, int NBLK>
+__device__ __forceinline__ void read_rows(const char* stage, int row0, int lane, int s, bf16x8_t (&f)[NBLK]) {
+  const int c = s * 2 + (lane >> 5);
+#pragma unroll
+  for (int b = 0; b < NBLK; ++b) {
+    const int r = row0 + b * 32 + (lane & 31);
+    f[b] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(stage + r * (BK * 2) + slot<BK>(r, c) * 16));
+  }
+}
+
+template <int BK>
+__device__ __forceinline__ void read(const char* as, const char* bs, int wm0, int wn0, int lane, int s, Frags& f) {
+  read_rows<BK, MB>(as, wm0, lane, s, f.a);
+  read_rows<BK, NB>(bs, wn0, lane, s, f.b);
+}
+
+__device__ __forceinline__ void mfma_all(const Frags& f, f32x16_t (&acc)[MB][NB]) {
+#pragma unroll
+  for (int a = 0; a < MB; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[a], f.b[b], acc[a][b], 0, 0, 0);
+}
+
+// The same MFMAs with the wave's 2 * NC copies of the tile at k0 spread
+// evenly among them (the order is pinned by scheduling barriers).
+template <typename E, int BK>
+__device__ __forceinline__ void mfma_all_refill(const Frags& f, f32x16_t (&acc)[MB][NB], const Tile<E, BK>& ta,
+                                                const Tile<E, BK>& tb, const KRows2<E>& al, const KRows2<E>& bl,
+                                                int k0, char* as, char* bs, int wave) {
+  constexpr int NC = Cfg<BK>::NC;
+  constexpr int PER = (2 * NC + MB * NB - 1) / (MB * NB);  // copies after each MFMA
+  dma::unroll<0, MB * NB>([&](auto I) {
+    constexpr int m = decltype(I)::value;
+    constexpr int a = m / NB, b = m % NB;
+    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[a], f.b[b], acc[a][b], 0, 0, 0);
+    dma::unroll<0, PER>([&](auto J) {
+      constexpr int q = m * PER + decltype(J)::value;
+      if constexpr (q < NC)
+        ta.issue_one(al, k0, as, wave, q);
+      else if constexpr (q < 2 * NC)
+        tb.issue_one(bl, k0, bs, wave, q - NC);
+    });
+    __builtin_amdgcn_sched_barrier(0);
+  });
+}
+
+}  // namespace kk
+
+template <int BK, class Epi, typename E>
+__global__ void __launch_bounds__(kk::NT, 1)
+    gemm_kk(KRows2<E> al, KRows2<E> bl, Epi epi, int M, int N, int K, int ktiles_per_split) {
+  using namespace kk;
+  using C = Cfg<BK>;
+  constexpr int STAGES = C::STAGES, TB = C::TILE_BYTES, KS = C::KSTEPS;
+  constexpr int PER_TILE = 2 * C::NC;  // copies per wave per tile
+  static_assert(sizeof(E) == 2, "bf16 operands only");
+  static_assert(KS % 2 == 0, "the fragment double buffer assumes an even number of k steps");
+  constexpr int SMEM = Epi::kTileSmem > C::SMEM ? Epi::kTileSmem : C::SMEM;
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm0 = (wave / WAVES_N) * WM, wn0 = (wave % WAVES_N) * WN;
+  int tm, tn;
+  xcd_tile(blockIdx.x, (M + BM - 1) / BM, (N + BN - 1) / BN, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int split = blockIdx.z;
+  const int nkt = (K + BK - 1) / BK;
+  const int kt0 = split * ktiles_per_split;
+  const int n = min(nkt, kt0 + ktiles_per_split) - kt0;  // K tiles of this split
+
+  f32x16_t acc[MB][NB];
+#pragma unroll
+  for (int a = 0; a < MB; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.0f;
+
+  if (n > 0) {
+    Tile<E, BK> ta, tb;
+    ta.init(al, m0, wave, lane);
+    tb.init(bl, n0, wave, lane);
+    char* const sA = smem;
+    char* const sB = smem + STAGES * TB;
+
+    // prologue: tiles 0 .. STAGES-2 in flight; wait for tile 0; the last
+    // stage's tile; the first fragments
+#pragma unroll
+    for (int st = 0; st < STAGES - 1; ++st) {
+      ta.issue(al, (kt0 + st) * BK, sA + st * TB, wave);
+      tb.issue(bl, (kt0 + st) * BK, sB + st * TB, wave);
+    }
+    dma::wait_copies_n<PER_TILE>(STAGES - 2);
+    dma::wave_barrier();
+    ta.issue(al, (kt0 + STAGES - 1) * BK, sA + (STAGES - 1) * TB, wave);
+    tb.issue(bl, (kt0 + STAGES - 1) * BK, sB + (STAGES - 1) * TB, wave);
+    Frags f[2];
+    read<BK>(sA, sB, wm0, wn0, lane, 0, f[0]);
+
+    // tile r lives in stage r % STAGES
+    for (int r = 0; r < n - 1; ++r) {
+      const int st = (r % STAGES) * TB;
+      const int nx = ((r + 1) % STAGES) * TB;
+      // k steps 0 .. KS-2 of tile r, each with the next step's fragments in flight
+      dma::unroll<0, KS - 1>([&](auto S) {
+        constexpr int s = decltype(S)::value;
+        read<BK>(sA + st, sB + st, wm0, wn0, lane, s + 1, f[(s + 1) & 1]);
+        __builtin_amdgcn_sched_group_barrier(0x100, MB + NB, 0);  // the LDS reads first
+        __builtin_amdgcn_sched_group_barrier(0x008, MB * NB, 0);  // then the MFMAs
+        mfma_all(f[s & 1], acc);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      // every wave done reading stage st; tile r + 1 landed
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      dma::wait_copies_n<PER_TILE>(STAGES - 2);
+      dma::wave_barrier();
+      read<BK>(sA + nx, sB + nx, wm0, wn0, lane, 0, f[0]);
+      __builtin_amdgcn_sched_barrier(0);
+      // last k step of tile r; stage st refilled with tile r + STAGES
+      mfma_all_refill<E, BK>(f[1], acc, ta, tb, al, bl, (kt0 + r + STAGES) * BK, sA + st, sB + st, wave);
+    }
+    {
+      // the last tile; its first fragments are in f[0]
+      const int st = ((n - 1) % STAGES) * TB;
+      dma::unroll<0, KS>([&](auto S) {
+        constexpr int s = decltype(S)::value;
+        if constexpr (s + 1 < KS) read<BK>(sA + st, sB + st, wm0, wn0, lane, s + 1, f[(s + 1) & 1]);
+        mfma_all(f[s & 1], acc);
+      });
+    }
+    dma::wait_copies_n<PER_TILE>(0);  // no copy outlives the loop
+  }
+
+  if constexpr (Epi::kTileSmem > 0) {
+    dma::wave_barrier();  // every wave is done with the stages
+    epi.template tile<MB, NB>(acc, smem, m0, n0, wave / WAVES_N, wn0, lane, tid, M);
+  } else {
+    // accumulator layout of a 32 x 32 block: lane holds column (lane & 31);
+    // register e holds row 8*(e/4) + 4*(lane/32) + (e%4)
+    const bool full = m0 + BM <= M && n0 + BN <= N;
+#pragma unroll
+    for (int a = 0; a < MB; ++a)
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int i = m0 + wm0 + a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+          const int j = n0 + wn0 + b * 32 + (lane & 31);
+          if (full || (i < M && j < N)) epi(i, j, acc[a][b][e], split);
+        }
+  }
+}
+
+template <class Epi, typename E>
+inline void launch_gemm_kk(const KRows2<E>& al, const KRows2<E>& bl, const Epi& epi, int M, int N, int K, int splits,
+                           hipStream_t s) {
+  constexpr int BK = O5_KK_BK;
+  const int nkt = (K + BK - 1) / BK;
+  const int kps = (nkt + splits - 1) / splits;
+  const unsigned tiles = ((M + kk::BM - 1) / kk::BM) * ((N + kk::BN - 1) / kk::BN);
+  hipLaunchKernelGGL((gemm_kk<BK, Epi, E>), dim3(tiles, 1, splits), dim3(kk::NT), 0, s, al, bl, epi, M, N, K, kps);
+}
+
+// The K-contiguous engine is the default for two K-contiguous bf16 operands;
+// O5_GEMM_ENGINE=dma selects the 8-wave direct-to-LDS engine instead.
+inline bool kk_engine_enabled() {
+  static const bool v = [] {
+    const char* e = std::getenv("O5_GEMM_ENGINE");
+    return !(e && e[0] == 'd');
+  }();
+  return v;
+}
+
+}  // namespace o5

@@ -1,0 +1,93 @@
+// GEMM planning and dispatch: engine, tile and split-K for a problem shape.
+#pragma once
+
+#include <type_traits>
+
+#include "gemm_kk.h"
+
+namespace o5 {
+
+// --------------------------------------------------------------- planning
+
+struct GemmPlan {
+  bool bf16;
+  BfTile tile;
+  int splits;
+};
+
+inline int cdiv(long long a, long long b) { return static_cast<int>((a + b - 1) / b); }
+
+// Engine used for 256 x 256 blocks; O5_BF16_TILE=w4|w8|128 selects one of the
+// register-staged engines instead (for comparison runs).
+inline int bf16_tile_override() {
+  static const int v = [] {
+    const char* e = std::getenv("O5_BF16_TILE");
+    if (!e) return 0;
+    if (e[0] == 'w' && e[1] == '4') return 1;
+    if (e[0] == 'w' && e[1] == '8') return 2;
+    if (e[0] == '1') return 3;
+    return 0;
+  }();
+  return v;
+}
+
+// Choose engine, tile and split-K so the launch has >= ~256 blocks (one per
+// CU) while every split keeps a reasonable number of K tiles.
+inline GemmPlan plan_gemm(bool bf16, int M, int N, int K) {
+  GemmPlan p{bf16, BfTile::kDma256, 1};
+  if (!bf16) {
+    const int tiles = cdiv(M, 64) * cdiv(N, 64);
+    const int nkt = cdiv(K, 16);
+    int s = cdiv(512, tiles);
+    s = std::min(s, std::max(1, nkt / 8));
+    p.splits = std::max(1, std::min(s, 16));
+    return p;
+  }
+  const int nkt = cdiv(K, 64);
+  const int t256 = cdiv(M, 256) * cdiv(N, 256);
+  const int ov = bf16_tile_override();
+  if (t256 >= 64 && ov != 3) {
+    int s = cdiv(256, t256);
+    s = std::min(s, std::max(1, nkt / 16));
+    p.tile = ov == 1 ? BfTile::k256x256 : ov == 2 ? BfTile::k256x256w8 : BfTile::kDma256;
+    p.splits = std::max(1, std::min(s, 8));
+    return p;
+  }
+  const int t128 = cdiv(M, 128) * cdiv(N, 128);
+  int s = cdiv(256, t128);
+  s = std::min(s, std::max(1, nkt / 8));
+  p.tile = BfTile::k128x128;
+  p.splits = std::max(1, std::min(s, 8));
+  return p;
+}
+
+// The direct-to-LDS engine takes I-contiguous operands without a mask only.
+template <class L>
+inline bool dma_ok(const L&) { return true; }
+template <typename E>
+inline bool dma_ok(const ICols2<E>& l) { return l.mask1 == nullptr; }
+
+template <class AL, class BL, class Epi>
+inline void run_gemm(const GemmPlan& p, const AL& al, const BL& bl, const Epi& epi, int M, int N, int K,
+                     hipStream_t s) {
+  if constexpr (AL::kBf16 && BL::kBf16) {
+    if (p.bf16) {
+      if constexpr (std::is_same_v<AL, KRows2<uint16_t>> && std::is_same_v<BL, KRows2<uint16_t>>) {
+        if (p.tile == BfTile::kDma256 && kk_engine_enabled()) {
+          launch_gemm_kk(al, bl, epi, M, N, K, p.splits, s);
+          return;
+        }
+      }
+      if (p.tile == BfTile::kDma256 && dma_ok(al) && dma_ok(bl)) {
+        launch_gemm_bf16_dma(al, bl, epi, M, N, K, p.splits, s);
+        return;
+      }
+      launch_gemm_bf16(al, bl, epi, M, N, K, p.splits,
+                       p.tile == BfTile::kDma256 ? BfTile::k256x256w8 : p.tile, s);
+      return;
+    }
+  }
+  launch_gemm_f32(al, bl, epi, M, N, K, p.splits, s);
+}
+
+}  // namespace o5

@@ -20,7 +20,7 @@
 //
 // fp32 path: the FMA engine; bf16 path: the MFMA engine, with h, the saved
 // gates and dG stored in bf16 and everything else in fp32.
-#include "gemm_dma.h"
+#include "gemm_plan.h"
 #include "reduce.h"
 
 namespace o5 {
@@ -73,82 +73,6 @@ __global__ void __launch_bounds__(256) lstm_fwd_cell(int B, int H, int S, const 
   }
 }
 
-// The forward cell fused into the epilogue of the step's GEMM.  The GEMM's B
-// tile is gate-gathered (256 columns = gates i, f, g, o of 64 hidden units),
-// so a wave whose tile starts at column wn0 holds gate (column / 64) of unit
-// (column % 64) for 128 rows.  In two passes of 128 rows the waves of one row
-// half park their
-// accumulators in LDS ([gate][row][unit], rows padded to 72 floats so the
-// two half-waves of a store hit disjoint banks), then all 512 threads read
-// the four gates of their (row, unit) and finish the cell: c, h and the
-// saved gates go straight to HBM and the pre-activations never do.
-template <typename E>
-struct EpiLstmCell {
-  static constexpr int kPad = 72;
-  static constexpr int kTileSmem = 4 * 128 * kPad * 4;  // 144 KB
-  const float* bias;
-  const float* c_prev;
-  const uint8_t* reset_t;
-  E* h_out;
-  float* c_out;
-  E* gates_out;
-  int H;
-
-  template <int MB, int NB>
-  __device__ __forceinline__ void tile(f32x16_t (&acc)[MB][NB], char* smem, int m0, int n0, int wm, int wn0, int lane,
-                                       int tid, int M) const {
-    static_assert(MB * 32 == 128, "expects 128-row wave tiles");
-    float* lds = reinterpret_cast<float*>(smem);
-    const int j = (n0 >> 2) + (tid & 63);  // this thread's hidden unit
-    const int rg = tid >> 6;               // row group
-    const int rstep = blockDim.x >> 6;     // row groups in the block
-    const size_t G = 4 * static_cast<size_t>(H);
-    const float bi = bias[j], bf = bias[H + j], bg = bias[2 * H + j], bo = bias[3 * H + j];
-#pragma unroll
-    for (int p = 0; p < 2; ++p) {
-      if (wm == p) {
-#pragma unroll
-        for (int a = 0; a < MB; ++a)
-#pragma unroll
-          for (int b = 0; b < NB; ++b)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              const int row = a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-              const int col = wn0 + b * 32 + (lane & 31);  // gate col / 64, unit col % 64
-              lds[((col >> 6) * 128 + row) * kPad + (col & 63)] = acc[a][b][e];
-            }
-      }
-      __syncthreads();
-      for (int row = rg; row < 128; row += rstep) {
-        const int bidx = m0 + p * 128 + row;
-        if (bidx < M) {
-          const int u = tid & 63;
-          const float ai = lds[(0 * 128 + row) * kPad + u] + bi;
-          const float af = lds[(1 * 128 + row) * kPad + u] + bf;
-          const float ag = lds[(2 * 128 + row) * kPad + u] + bg;
-          const float ao = lds[(3 * 128 + row) * kPad + u] + bo;
-          const float keep = (reset_t && reset_t[bidx]) ? 0.0f : 1.0f;
-          const size_t hj = static_cast<size_t>(bidx) * H + j;
-          const float cp = keep * c_prev[hj];
-          const float ig = sigmoid_f(ai), fg = sigmoid_f(af), gg = tanh_f(ag), og = sigmoid_f(ao);
-          const float c = fg * cp + ig * gg;
-          c_out[hj] = c;
-          h_out[hj] = elem<E>::from_f32(og * tanh_f(c));
-          if (gates_out) {
-            E* gp = gates_out + static_cast<size_t>(bidx) * G;
-            gp[j] = elem<E>::from_f32(ig);
-            gp[H + j] = elem<E>::from_f32(fg);
-            gp[2 * H + j] = elem<E>::from_f32(gg);
-            gp[3 * H + j] = elem<E>::from_f32(og);
-          }
-        }
-      }
-      __syncthreads();
-    }
-  }
-  __device__ __forceinline__ void operator()(int, int, float, int) const {}
-};
-
 // Four consecutive elements as float4 (fp32 or bf16 storage).
 template <typename E> struct Vec4;
 template <> struct Vec4<float> {
@@ -171,6 +95,115 @@ template <> struct Vec4<uint16_t> {
 
 __device__ __forceinline__ float4 f4(float a) { return make_float4(a, a, a, a); }
 
+// The forward cell fused into the epilogue of the step's GEMM.  The GEMM's B
+// tile is gate-gathered (256 columns = gates i, f, g, o of 64 hidden units),
+// so a wave whose tile starts at column wn0 holds gate (column / 64) of unit
+// (column % 64) for 128 rows.  In two passes of 128 rows the waves of one row
+// half park their
+// accumulators in LDS ([gate][row][unit], rows padded to 72 floats so the
+// two half-waves of a store hit disjoint banks), then every thread reads the
+// four gates of 4 consecutive units in each of its rows and finishes the
+// cell: c, h and the saved gates go straight to HBM in 16- and 8-byte
+// pieces and the pre-activations never do.  The previous cell state of a
+// pass is requested before the accumulators are parked, so its latency is
+// paid once per pass rather than once per row.
+template <typename E>
+struct EpiLstmCell {
+  static constexpr int kPad = 72;
+  static constexpr int kTileSmem = 4 * 128 * kPad * 4;  // 144 KB
+  const float* bias;
+  const float* c_prev;
+  const uint8_t* reset_t;
+  E* h_out;
+  float* c_out;
+  E* gates_out;
+  int H;
+
+  template <int MB, int NB>
+  __device__ __forceinline__ void tile(f32x16_t (&acc)[MB][NB], char* smem, int m0, int n0, int wm, int wn0, int lane,
+                                       int tid, int M) const {
+    static_assert(MB * 32 == 128, "expects 128-row wave tiles");
+    float* lds = reinterpret_cast<float*>(smem);
+    // thread -> 4 consecutive hidden units (quad uq) of rows rr, rr + RS, ...
+    const int uq = tid & 15;
+    const int rr = tid >> 4;
+    const int RS = blockDim.x >> 4;   // rows covered per sweep
+    const int NR = 128 / RS;          // sweeps per 128-row pass (8 with 256 threads)
+    const int j = (n0 >> 2) + 4 * uq;  // first hidden unit of the quad
+    const size_t G = 4 * static_cast<size_t>(H);
+    const float4 bi = *reinterpret_cast<const float4*>(bias + j);
+    const float4 bf = *reinterpret_cast<const float4*>(bias + H + j);
+    const float4 bg = *reinterpret_cast<const float4*>(bias + 2 * H + j);
+    const float4 bo = *reinterpret_cast<const float4*>(bias + 3 * H + j);
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      // the previous cell state of this pass, all requests in flight at once
+      float4 cp[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int bidx = m0 + p * 128 + rr + i * RS;
+        cp[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (i < NR && bidx < M) {
+          const bool keep = !(reset_t && reset_t[bidx]);
+          if (keep) cp[i] = *reinterpret_cast<const float4*>(c_prev + static_cast<size_t>(bidx) * H + j);
+        }
+      }
+      if (wm == p) {
+#pragma unroll
+        for (int a = 0; a < MB; ++a)
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              const int row = a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+              const int col = wn0 + b * 32 + (lane & 31);  // gate col / 64, unit col % 64
+              lds[((col >> 6) * 128 + row) * kPad + (col & 63)] = acc[a][b][e];
+            }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int row = rr + i * RS;
+        const int bidx = m0 + p * 128 + row;
+        if (i < NR && bidx < M) {
+          const float4 ai = *reinterpret_cast<const float4*>(lds + (0 * 128 + row) * kPad + 4 * uq);
+          const float4 af = *reinterpret_cast<const float4*>(lds + (1 * 128 + row) * kPad + 4 * uq);
+          const float4 ag = *reinterpret_cast<const float4*>(lds + (2 * 128 + row) * kPad + 4 * uq);
+          const float4 ao = *reinterpret_cast<const float4*>(lds + (3 * 128 + row) * kPad + 4 * uq);
+          float4 ig, fg, gg, og, c, h;
+          const float* pai = &ai.x; const float* paf = &af.x; const float* pag = &ag.x; const float* pao = &ao.x;
+          const float* pbi = &bi.x; const float* pbf = &bf.x; const float* pbg = &bg.x; const float* pbo = &bo.x;
+          const float* pcp = &cp[i].x;
+          float* pig = &ig.x; float* pfg = &fg.x; float* pgg = &gg.x; float* pog = &og.x;
+          float* pc = &c.x; float* ph = &h.x;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            pig[q] = sigmoid_f(pai[q] + pbi[q]);
+            pfg[q] = sigmoid_f(paf[q] + pbf[q]);
+            pgg[q] = tanh_f(pag[q] + pbg[q]);
+            pog[q] = sigmoid_f(pao[q] + pbo[q]);
+            pc[q] = pfg[q] * pcp[q] + pig[q] * pgg[q];
+            ph[q] = pog[q] * tanh_f(pc[q]);
+          }
+          const size_t hj = static_cast<size_t>(bidx) * H + j;
+          *reinterpret_cast<float4*>(c_out + hj) = c;
+          Vec4<E>::store(h_out + hj, h);
+          if (gates_out) {
+            E* gp = gates_out + static_cast<size_t>(bidx) * G + j;
+            Vec4<E>::store(gp, ig);
+            Vec4<E>::store(gp + H, fg);
+            Vec4<E>::store(gp + 2 * H, gg);
+            Vec4<E>::store(gp + 3 * H, og);
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  __device__ __forceinline__ void operator()(int, int, float, int) const {}
+};
+
+
 // Backward cell for step t.  rec: [S][B][H] partial sums of dG_{t+1} W_h (or
 // NULL at t = T-1).  dc: in = dc arriving at c_t, out = dc for c_{t-1}.
 // Block: 64 hidden units x 32 rows; each thread owns 4 consecutive units of
@@ -182,9 +215,11 @@ __global__ void __launch_bounds__(256) lstm_bwd_cell(
     const float* __restrict__ dh_t, const float* __restrict__ dh_extra, const float* dc_in,
     float* dc_out, const E* __restrict__ gates_t, const float* __restrict__ c_t,
     const float* __restrict__ c_prev, const uint8_t* __restrict__ reset_t, E* __restrict__ dG_t,
-    float* __restrict__ db_part) {
+    float* __restrict__ db_part, int db_accumulate, E* __restrict__ dGT, size_t ldt, int col0) {
   constexpr int kRowGroups = 16;
   __shared__ float red[kRowGroups][4][kPwCols];
+  // dG of the block transposed, [gate * 64 + unit][row] (bf16 path only)
+  __shared__ __attribute__((aligned(16))) uint16_t tq[sizeof(E) == 2 ? 4 * kPwCols : 1][kPwRows + 8];
   const int jq = threadIdx.x & 15;
   const int rg = threadIdx.x >> 4;
   const int j = blockIdx.x * kPwCols + jq * 4;
@@ -193,7 +228,16 @@ __global__ void __launch_bounds__(256) lstm_bwd_cell(
   float4 sd[4] = {f4(0.f), f4(0.f), f4(0.f), f4(0.f)};
   for (int r = rg; r < kPwRows; r += kRowGroups) {
     const int b = blockIdx.y * kPwRows + r;
-    if (b >= B) break;
+    if (b >= B) {
+      if constexpr (sizeof(E) == 2) {
+        // rows past B are zero columns of the transposed copy
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) tq[g * kPwCols + jq * 4 + q][r] = 0;
+      }
+      continue;
+    }
     const size_t hj = static_cast<size_t>(b) * H + j;
     const size_t row = static_cast<size_t>(b) * G;
     float4 dh = Vec4<float>::load(dh_t + hj);
@@ -248,6 +292,13 @@ __global__ void __launch_bounds__(256) lstm_bwd_cell(
     Vec4<E>::store(dG_t + row + H + j, daf);
     Vec4<E>::store(dG_t + row + 2 * H + j, dag);
     Vec4<E>::store(dG_t + row + 3 * H + j, dao);
+    if constexpr (sizeof(E) == 2) {
+      const float* gv[4] = {&dai.x, &daf.x, &dag.x, &dao.x};
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) tq[g * kPwCols + jq * 4 + q][r] = f32_to_bf16_bits(gv[g][q]);
+    }
     sd[0] = make_float4(sd[0].x + dai.x, sd[0].y + dai.y, sd[0].z + dai.z, sd[0].w + dai.w);
     sd[1] = make_float4(sd[1].x + daf.x, sd[1].y + daf.y, sd[1].z + daf.z, sd[1].w + daf.w);
     sd[2] = make_float4(sd[2].x + dag.x, sd[2].y + dag.y, sd[2].z + dag.z, sd[2].w + dag.w);
@@ -266,30 +317,68 @@ __global__ void __launch_bounds__(256) lstm_bwd_cell(
     float sum = 0.0f;
 #pragma unroll
     for (int q = 0; q < kRowGroups; ++q) sum += red[q][g][jl];
-    db_part[static_cast<size_t>(blockIdx.y) * G + g * H + blockIdx.x * kPwCols + jl] = sum;
+    float* d = db_part + static_cast<size_t>(blockIdx.y) * G + g * H + blockIdx.x * kPwCols + jl;
+    *d = db_accumulate ? *d + sum : sum;  // the same block owns this entry at every step
+  }
+  if constexpr (sizeof(E) == 2) {
+    if (dGT) {
+      // 256 rows (gate, unit) x kPwRows columns: 4 chunks of 8 rows each
+      const int c = threadIdx.x & 3;
+      for (int u = threadIdx.x >> 2; u < 4 * kPwCols; u += 64) {
+        const int g = u / kPwCols, jl = u % kPwCols;
+        const uint4 v = *reinterpret_cast<const uint4*>(&tq[u][8 * c]);
+        *reinterpret_cast<uint4*>(dGT + (static_cast<size_t>(g) * H + blockIdx.x * kPwCols + jl) * ldt + col0 +
+                                  blockIdx.y * kPwRows + 8 * c) = v;
+      }
+    }
   }
 }
 
-// hp[r] = (1 - reset[r]) * (r < B ? h0[r] : h[r - B]) over the T*B rows: the
-// hidden state each step multiplied (its input from the previous step), as
-// one contiguous operand for the weight-gradient GEMM.  8 elements per thread.
+// Transposed, time-padded operand for the weight-gradient GEMM.  Column
+// k = t * Bp + b of dst (Bp = B rounded up to the cell's row block) holds
+// source row t * B + b; columns with b >= B are zero.  Source row r is
+// s0[r] for r < split, else s1[r - split], and zero where mask[r] is set.
+// So dst row c is column c of [x] (split = T*B) or of the masked previous
+// hidden state h~ (s0 = h0, s1 = h, split = B, mask = reset).  Tiles of 64
+// columns x 64 source rows pass through LDS; 256 threads, 16-byte accesses.
 template <typename E>
-__global__ void __launch_bounds__(256) build_hprev(int T, int B, int H, const E* __restrict__ h0e,
-                                                   const E* __restrict__ h, const uint8_t* __restrict__ reset,
-                                                   E* __restrict__ hp) {
+__global__ void __launch_bounds__(256) transpose_rows(int T, int B, int Bp, int C, const E* __restrict__ s0,
+                                                      const E* __restrict__ s1, int split, int lds,
+                                                      const uint8_t* __restrict__ mask, E* __restrict__ dst,
+                                                      size_t ldd) {
   static_assert(sizeof(E) == 2, "bf16 only");
-  const size_t n8 = static_cast<size_t>(T) * B * H / 8;
-  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= n8) return;
-  const size_t e = i * 8;
-  const size_t r = e / H;
-  const size_t col = e - r * H;
-  uint4 v = make_uint4(0, 0, 0, 0);
-  if (!(reset && reset[r])) {
-    const E* src = r < static_cast<size_t>(B) ? h0e + r * H + col : h + (r - B) * H + col;
-    v = *reinterpret_cast<const uint4*>(src);
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64][72];
+  const int k0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const int kl = (tid >> 3) + 32 * hh, ch = tid & 7;
+    const int k = k0 + kl, c = c0 + ch * 8;
+    const int t = k / Bp, b = k - t * Bp;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (t < T && b < B && c < C) {
+      const int r = t * B + b;
+      if (!(mask && mask[r])) {
+        const E* src = r < split ? s0 + static_cast<size_t>(r) * lds : s1 + static_cast<size_t>(r - split) * lds;
+        v = *reinterpret_cast<const uint4*>(src + c);
+      }
+    }
+    *reinterpret_cast<uint4*>(&tile[kl][ch * 8]) = v;
   }
-  *reinterpret_cast<uint4*>(hp + e) = v;
+  __syncthreads();
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const int cl = (tid >> 3) + 32 * hh, ch = tid & 7;
+    const int c = c0 + cl;
+    if (c < C) {
+      uint4 v;
+      v.x = tile[ch * 8 + 0][cl] | (static_cast<uint32_t>(tile[ch * 8 + 1][cl]) << 16);
+      v.y = tile[ch * 8 + 2][cl] | (static_cast<uint32_t>(tile[ch * 8 + 3][cl]) << 16);
+      v.z = tile[ch * 8 + 4][cl] | (static_cast<uint32_t>(tile[ch * 8 + 5][cl]) << 16);
+      v.w = tile[ch * 8 + 6][cl] | (static_cast<uint32_t>(tile[ch * 8 + 7][cl]) << 16);
+      *reinterpret_cast<uint4*>(dst + static_cast<size_t>(c) * ldd + k0 + ch * 8) = v;
+    }
+  }
 }
 
 // ---------------------------------------------------------------- layouts
@@ -313,20 +402,24 @@ static FwdWs fwd_ws(o5_dtype dt, int T, int B, int D, int H) {
 }
 
 struct BwdWs {
-  size_t dG, dc, rec, h0e, dbpart, hp, total;
+  size_t dG, dc, rec, h0e, dbpart, dGT, XHT, WhT, total;
   int nbc;
+  int Bp;       // B rounded up to the cell's row block (bf16 path: time-padded K of dW)
+  size_t ldt;   // T * Bp, the leading dimension of dGT and XHT
   GemmPlan plan_dh, plan_dw, plan_dx;
 };
 
 static BwdWs bwd_ws(o5_dtype dt, int T, int B, int D, int H) {
   BwdWs w;
   const bool bf = dt == O5_BF16;
+  w.Bp = cdiv(B, 64) * 64;
+  w.nbc = w.Bp / kPwRows;  // cell row blocks; those past B only write zeros
+  w.ldt = static_cast<size_t>(T) * w.Bp;
   w.plan_dh = plan_gemm(bf, B, H, 4 * H);
-  w.plan_dw = plan_gemm(bf, 4 * H, D + H, T * B);
+  w.plan_dw = plan_gemm(bf, 4 * H, D + H, bf ? static_cast<int>(w.ldt) : T * B);
   w.plan_dw.splits = 1;  // dW is written directly (M x N tiles are plentiful)
   w.plan_dx = plan_gemm(bf, T * B, D, 4 * H);
   w.plan_dx.splits = 1;
-  w.nbc = cdiv(B, kPwRows);
   size_t o = 0;
   w.dG = o;
   o += align_up(static_cast<size_t>(T) * B * 4 * H * dtype_size(dt));
@@ -337,9 +430,17 @@ static BwdWs bwd_ws(o5_dtype dt, int T, int B, int D, int H) {
   w.h0e = o;
   o += align_up(static_cast<size_t>(B) * H * dtype_size(dt));
   w.dbpart = o;
-  o += align_up(static_cast<size_t>(T) * w.nbc * 4 * H * sizeof(float));
-  w.hp = o;
-  if (bf) o += align_up(static_cast<size_t>(T) * B * H * dtype_size(dt));
+  o += align_up(static_cast<size_t>(w.nbc) * 4 * H * sizeof(float));
+  w.dGT = w.XHT = w.WhT = o;
+  if (bf) {
+    // K-contiguous operands for the MFMA engine: dG^T, [x | h~]^T, W_h^T
+    w.dGT = o;
+    o += align_up(static_cast<size_t>(4) * H * w.ldt * sizeof(uint16_t));
+    w.XHT = o;
+    o += align_up(static_cast<size_t>(D + H) * w.ldt * sizeof(uint16_t));
+    w.WhT = o;
+    o += align_up(static_cast<size_t>(H) * 4 * H * sizeof(uint16_t));
+  }
   w.total = o;
   return w;
 }
@@ -384,7 +485,10 @@ static int lstm_fwd_impl(int T, int B, int D, int H, const E* x, const E* Wx, co
         E* gt = gates ? gates + static_cast<size_t>(t) * B * 4 * H : nullptr;
         EpiLstmCell<E> epi{bias, cprev, rt, h + t * BH, c + t * BH, gt, H};
         ktimer_begin(kSiteLstmFwdGemm, s);
-        launch_gemm_bf16_dma(al, bl, epi, B, 4 * H, D + H, 1, s);
+        if (kk_engine_enabled())
+          launch_gemm_kk(al, bl, epi, B, 4 * H, D + H, 1, s);
+        else
+          launch_gemm_bf16_dma(al, bl, epi, B, 4 * H, D + H, 1, s);
         ktimer_end(kSiteLstmFwdGemm, s);
       }
       return check_launch("o5_lstm_fwd");
@@ -417,18 +521,25 @@ static int lstm_bptt_impl(int T, int B, int D, int H, const E* x, const E* Wx, c
                           const float* c0, const uint8_t* reset, const E* h, const float* c, const E* gates,
                           const float* dh, const float* dhT, const float* dcT, float* dWx, float* dWh, float* db,
                           E* dx, char* ws, const BwdWs& w, hipStream_t s) {
+  constexpr bool kBf = sizeof(E) == 2;
   const size_t BH = static_cast<size_t>(B) * H;
   const size_t BG = static_cast<size_t>(B) * 4 * H;
   E* dG = reinterpret_cast<E*>(ws + w.dG);
   float* dc = reinterpret_cast<float*>(ws + w.dc);
   float* rec = reinterpret_cast<float*>(ws + w.rec);
   float* dbpart = reinterpret_cast<float*>(ws + w.dbpart);
+  E* dGT = kBf ? reinterpret_cast<E*>(ws + w.dGT) : nullptr;
+  E* XHT = kBf ? reinterpret_cast<E*>(ws + w.XHT) : nullptr;
+  E* WhT = kBf ? reinterpret_cast<E*>(ws + w.WhT) : nullptr;
   const E* h0e;
-  if constexpr (sizeof(E) == 2) {
+  if constexpr (kBf) {
     E* tmp = reinterpret_cast<E*>(ws + w.h0e);
     const int st = o5_f32_to_bf16(BH, h0, reinterpret_cast<uint16_t*>(tmp), s);
     if (st != O5_OK) return st;
     h0e = tmp;
+    // W_h^T [H][4H]: the recurrent GEMM's second operand, K-contiguous
+    hipLaunchKernelGGL(transpose_rows<E>, dim3(cdiv(H, 64), cdiv(4 * H, 64)), dim3(256), 0, s, 1, 4 * H, 4 * H, H, Wh,
+                       Wh, 4 * H, H, nullptr, WhT, static_cast<size_t>(4 * H));
   } else {
     h0e = h0;
   }
@@ -438,10 +549,15 @@ static int lstm_bptt_impl(int T, int B, int D, int H, const E* x, const E* Wx, c
     if (t < T - 1) {
       // R = dG_{t+1} . W_h :  A(i=b, k=n) = dG_{t+1}[b, n];  B(j, k=n) = W_h[n, j]
       KRows2<E> al{dG + (t + 1) * BG, nullptr, nullptr, 4 * H, 0, 4 * H, 4 * H, B};
-      ICols2<E> bl{Wh, nullptr, nullptr, nullptr, H, 0, H, H, 4 * H, 0};
       EpiStoreF32 epi{rec, H, BH};
       ktimer_begin(kSiteLstmDhGemm, s);
-      run_gemm(w.plan_dh, al, bl, epi, B, H, 4 * H, s);
+      if constexpr (kBf) {
+        KRows2<E> bl{WhT, nullptr, nullptr, 4 * H, 0, 4 * H, 4 * H, H};
+        run_gemm(w.plan_dh, al, bl, epi, B, H, 4 * H, s);
+      } else {
+        ICols2<E> bl{Wh, nullptr, nullptr, nullptr, H, 0, H, H, 4 * H, 0};
+        run_gemm(w.plan_dh, al, bl, epi, B, H, 4 * H, s);
+      }
       ktimer_end(kSiteLstmDhGemm, s);
       recp = rec;
     }
@@ -452,33 +568,36 @@ static int lstm_bptt_impl(int T, int B, int D, int H, const E* x, const E* Wx, c
     const float* cprev = t == 0 ? c0 : c + (t - 1) * BH;
     ktimer_begin(kSiteLstmBwdCell, s);
     hipLaunchKernelGGL(lstm_bwd_cell<E>, pw_grid, dim3(256), 0, s, B, H, w.plan_dh.splits, recp, rn, dh + t * BH, dhx,
-                       dcin, dc, gates + t * BG, c + t * BH, cprev, rt, dG + t * BG,
-                       dbpart + static_cast<size_t>(t) * w.nbc * 4 * H);
+                       dcin, dc, gates + t * BG, c + t * BH, cprev, rt, dG + t * BG, dbpart, t < T - 1 ? 1 : 0, dGT,
+                       w.ldt, t * w.Bp);
     ktimer_end(kSiteLstmBwdCell, s);
   }
   // [dW_x | dW_h] = dG^T . [x | h~_prev] over the T*B rows r = t*B + b
   {
-    const int R = T * B;
-    ICols2<E> al{dG, nullptr, nullptr, nullptr, 4 * H, 0, 4 * H, 4 * H, R, 0};
     EpiStoreF32Split2 epi{dWx, dWh, D, H, D};
-    if constexpr (sizeof(E) == 2) {
-      // the masked previous hidden state as one contiguous operand
-      E* hp = reinterpret_cast<E*>(ws + w.hp);
-      const size_t n8 = static_cast<size_t>(R) * H / 8;
-      hipLaunchKernelGGL(build_hprev<E>, dim3(static_cast<unsigned>((n8 + 255) / 256)), dim3(256), 0, s, T, B, H, h0e,
-                         h, reset, hp);
-      ICols2<E> bl{x, hp, hp, nullptr, D, H, D, D + H, R, R};
+    if constexpr (kBf) {
+      // both operands K-contiguous over the time-padded K = T * Bp
+      const int K = static_cast<int>(w.ldt);
+      const int ldt = static_cast<int>(w.ldt);
+      hipLaunchKernelGGL(transpose_rows<E>, dim3(cdiv(D, 64), K / 64), dim3(256), 0, s, T, B, w.Bp, D, x, x, T * B, D,
+                         nullptr, XHT, w.ldt);
+      hipLaunchKernelGGL(transpose_rows<E>, dim3(cdiv(H, 64), K / 64), dim3(256), 0, s, T, B, w.Bp, H, h0e, h, B, H,
+                         reset, XHT + static_cast<size_t>(D) * w.ldt, w.ldt);
+      KRows2<E> al{dGT, nullptr, nullptr, ldt, 0, K, K, 4 * H};
+      KRows2<E> bl{XHT, nullptr, nullptr, ldt, 0, K, K, D + H};
       ktimer_begin(kSiteLstmDwGemm, s);
-      run_gemm(w.plan_dw, al, bl, epi, 4 * H, D + H, R, s);
+      run_gemm(w.plan_dw, al, bl, epi, 4 * H, D + H, K, s);
       ktimer_end(kSiteLstmDwGemm, s);
     } else {
+      const int R = T * B;
+      ICols2<E> al{dG, nullptr, nullptr, nullptr, 4 * H, 0, 4 * H, 4 * H, R, 0};
       ICols2<E> bl{x, h0e, h, reset, D, H, D, D + H, R, B};
       ktimer_begin(kSiteLstmDwGemm, s);
       run_gemm(w.plan_dw, al, bl, epi, 4 * H, D + H, R, s);
       ktimer_end(kSiteLstmDwGemm, s);
     }
   }
-  hipLaunchKernelGGL(colsum_rows, dim3(cdiv(4 * H, 256)), dim3(256), 0, s, T * w.nbc, 4 * H, dbpart, db);
+  hipLaunchKernelGGL(colsum_rows, dim3(cdiv(4 * H, 256)), dim3(256), 0, s, w.nbc, 4 * H, dbpart, db);
   if (dx) {
     // dx = dG . W_x :  A(i=r, k=n) = dG[r, n];  B(j=d, k=n) = W_x[n, d]
     const int R = T * B;

@@ -17,7 +17,7 @@
 // error ~2^-16) laid side by side along K, against the bf16 operand repeated
 // twice, so the product keeps nearly fp32 accuracy.
 // Every reduction has a fixed order, so results are bitwise reproducible.
-#include "gemm_dma.h"
+#include "gemm_plan.h"
 #include "heads.h"
 #include "reduce.h"
 

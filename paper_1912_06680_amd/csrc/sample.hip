@@ -12,7 +12,7 @@
 // logit's noise is a pure function of (seed, counter, row, head, logit) and
 // needs no generator state on the device.  One Philox block yields the noise
 // for 4 consecutive logits of one head.
-#include "gemm_dma.h"
+#include "gemm_plan.h"
 #include "heads.h"
 
 namespace o5 {
