@@ -34,6 +34,9 @@
 #ifndef O5_KK_BK
 #define O5_KK_BK 64
 #endif
+#ifndef O5_KK_SPREAD
+#define O5_KK_SPREAD 2  // k steps over which a tile's copies are issued
+#endif
 
 namespace o5 {
 
@@ -132,24 +135,28 @@ __device__ __forceinline__ void mfma_all(const Frags& f, f32x16_t (&acc)[MB][NB]
     for (int b = 0; b < NB; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[a], f.b[b], acc[a][b], 0, 0, 0);
 }
 
-// The same MFMAs with the wave's 2 * NC copies of the tile at k0 spread
-// evenly among them (the order is pinned by scheduling barriers).
-template <typename E, int BK>
-__device__ __forceinline__ void mfma_all_refill(const Frags& f, f32x16_t (&acc)[MB][NB], const Tile<E, BK>& ta,
-                                                const Tile<E, BK>& tb, const KRows2<E>& al, const KRows2<E>& bl,
-                                                int k0, char* as, char* bs, int wave) {
+// The same MFMAs with copies [Q0, Q1) of the wave's 2 * NC copies of the
+// tile at k0 spread evenly among them (the order is pinned by scheduling
+// barriers).
+template <typename E, int BK, int Q0, int Q1>
+__device__ __forceinline__ void mfma_copies(const Frags& f, f32x16_t (&acc)[MB][NB], const Tile<E, BK>& ta,
+                                            const Tile<E, BK>& tb, const KRows2<E>& al, const KRows2<E>& bl, int k0,
+                                            char* as, char* bs, int wave) {
   constexpr int NC = Cfg<BK>::NC;
-  constexpr int PER = (2 * NC + MB * NB - 1) / (MB * NB);  // copies after each MFMA
+  constexpr int NQ = Q1 - Q0;
   dma::unroll<0, MB * NB>([&](auto I) {
     constexpr int m = decltype(I)::value;
     constexpr int a = m / NB, b = m % NB;
     acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[a], f.b[b], acc[a][b], 0, 0, 0);
-    dma::unroll<0, PER>([&](auto J) {
-      constexpr int q = m * PER + decltype(J)::value;
-      if constexpr (q < NC)
-        ta.issue_one(al, k0, as, wave, q);
-      else if constexpr (q < 2 * NC)
-        tb.issue_one(bl, k0, bs, wave, q - NC);
+    // copies after MFMA m: those q with floor(q * 16 / NQ) == m
+    dma::unroll<Q0, Q1>([&](auto J) {
+      constexpr int q = decltype(J)::value;
+      if constexpr ((q - Q0) * MB * NB / NQ == m) {
+        if constexpr (q < NC)
+          ta.issue_one(al, k0, as, wave, q);
+        else
+          tb.issue_one(bl, k0, bs, wave, q - NC);
+      }
     });
     __builtin_amdgcn_sched_barrier(0);
   });
@@ -157,7 +164,7 @@ __device__ __forceinline__ void mfma_all_refill(const Frags& f, f32x16_t (&acc)[
 
 }  // namespace kk
 
-template <int BK, class Epi, typename E>
+template <int BK, int SPREAD, class Epi, typename E>
 __global__ void __launch_bounds__(kk::NT, 1)
     gemm_kk(KRows2<E> al, KRows2<E> bl, Epi epi, int M, int N, int K, int ktiles_per_split) {
   using namespace kk;
@@ -166,6 +173,7 @@ __global__ void __launch_bounds__(kk::NT, 1)
   constexpr int PER_TILE = 2 * C::NC;  // copies per wave per tile
   static_assert(sizeof(E) == 2, "bf16 operands only");
   static_assert(KS % 2 == 0, "the fragment double buffer assumes an even number of k steps");
+  static_assert(SPREAD >= 1 && SPREAD < KS, "copies must land before the next barrier");
   constexpr int SMEM = Epi::kTileSmem > C::SMEM ? Epi::kTileSmem : C::SMEM;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
@@ -210,27 +218,41 @@ __global__ void __launch_bounds__(kk::NT, 1)
     Frags f[2];
     read<BK>(sA, sB, wm0, wn0, lane, 0, f[0]);
 
-    // tile r lives in stage r % STAGES
+    // tile r lives in stage r % STAGES.  The copies of tile r + STAGES into
+    // the stage freed at the barrier of iteration r are spread over the last
+    // k step of tile r and the first SPREAD - 1 k steps of tile r + 1, so the
+    // vector memory queue never holds a whole tile's copies at once.
+    constexpr int NQ = 2 * C::NC;
     for (int r = 0; r < n - 1; ++r) {
       const int st = (r % STAGES) * TB;
       const int nx = ((r + 1) % STAGES) * TB;
+      const int pst = ((r + STAGES - 1) % STAGES) * TB;   // stage being refilled since iteration r - 1
+      const int pk0 = (kt0 + r + STAGES - 1) * BK;        // and its tile
       // k steps 0 .. KS-2 of tile r, each with the next step's fragments in flight
       dma::unroll<0, KS - 1>([&](auto S) {
         constexpr int s = decltype(S)::value;
         read<BK>(sA + st, sB + st, wm0, wn0, lane, s + 1, f[(s + 1) & 1]);
         __builtin_amdgcn_sched_group_barrier(0x100, MB + NB, 0);  // the LDS reads first
         __builtin_amdgcn_sched_group_barrier(0x008, MB * NB, 0);  // then the MFMAs
-        mfma_all(f[s & 1], acc);
+        if constexpr (s + 1 < SPREAD) {
+          constexpr int q0 = (s + 1) * NQ / SPREAD, q1 = (s + 2) * NQ / SPREAD;
+          if (r > 0)
+            mfma_copies<E, BK, q0, q1>(f[s & 1], acc, ta, tb, al, bl, pk0, sA + pst, sB + pst, wave);
+          else
+            mfma_all(f[s & 1], acc);
+        } else {
+          mfma_all(f[s & 1], acc);
+        }
         __builtin_amdgcn_sched_barrier(0);
       });
       // every wave done reading stage st; tile r + 1 landed
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      dma::wait_copies_n<PER_TILE>(STAGES - 2);
+      dma::wait_copies_n<2 * C::NC>(STAGES - 2);
       dma::wave_barrier();
       read<BK>(sA + nx, sB + nx, wm0, wn0, lane, 0, f[0]);
       __builtin_amdgcn_sched_barrier(0);
-      // last k step of tile r; stage st refilled with tile r + STAGES
-      mfma_all_refill<E, BK>(f[1], acc, ta, tb, al, bl, (kt0 + r + STAGES) * BK, sA + st, sB + st, wave);
+      // last k step of tile r; stage st starts refilling with tile r + STAGES
+      mfma_copies<E, BK, 0, NQ / SPREAD>(f[1], acc, ta, tb, al, bl, (kt0 + r + STAGES) * BK, sA + st, sB + st, wave);
     }
     {
       // the last tile; its first fragments are in f[0]
@@ -271,7 +293,8 @@ inline void launch_gemm_kk(const KRows2<E>& al, const KRows2<E>& bl, const Epi& 
   const int nkt = (K + BK - 1) / BK;
   const int kps = (nkt + splits - 1) / splits;
   const unsigned tiles = ((M + kk::BM - 1) / kk::BM) * ((N + kk::BN - 1) / kk::BN);
-  hipLaunchKernelGGL((gemm_kk<BK, Epi, E>), dim3(tiles, 1, splits), dim3(kk::NT), 0, s, al, bl, epi, M, N, K, kps);
+  hipLaunchKernelGGL((gemm_kk<BK, O5_KK_SPREAD, Epi, E>), dim3(tiles, 1, splits), dim3(kk::NT), 0, s, al, bl, epi, M,
+                     N, K, kps);
 }
 
 // The K-contiguous engine is the default for two K-contiguous bf16 operands;

@@ -217,6 +217,7 @@ __global__ void __launch_bounds__(256) lstm_bwd_cell(
     const float* __restrict__ c_prev, const uint8_t* __restrict__ reset_t, E* __restrict__ dG_t,
     float* __restrict__ db_part, int db_accumulate, E* __restrict__ dGT, size_t ldt, int col0) {
   constexpr int kRowGroups = 16;
+  static_assert(kPwRows == 2 * kRowGroups, "two adjacent rows per thread");
   __shared__ float red[kRowGroups][4][kPwCols];
   // dG of the block transposed, [gate * 64 + unit][row] (bf16 path only)
   __shared__ __attribute__((aligned(16))) uint16_t tq[sizeof(E) == 2 ? 4 * kPwCols : 1][kPwRows + 8];
@@ -226,18 +227,14 @@ __global__ void __launch_bounds__(256) lstm_bwd_cell(
   const size_t G = 4 * static_cast<size_t>(H);
   const size_t sstride = static_cast<size_t>(B) * H;
   float4 sd[4] = {f4(0.f), f4(0.f), f4(0.f), f4(0.f)};
-  for (int r = rg; r < kPwRows; r += kRowGroups) {
+  // this thread's dG values (bf16 bits) of its two adjacent rows, for the
+  // transposed copy; rows past B stay zero
+  uint32_t tbits[2][16] = {};
+#pragma unroll
+  for (int i = 0; i < kPwRows / kRowGroups; ++i) {
+    const int r = rg * (kPwRows / kRowGroups) + i;
     const int b = blockIdx.y * kPwRows + r;
-    if (b >= B) {
-      if constexpr (sizeof(E) == 2) {
-        // rows past B are zero columns of the transposed copy
-#pragma unroll
-        for (int g = 0; g < 4; ++g)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) tq[g * kPwCols + jq * 4 + q][r] = 0;
-      }
-      continue;
-    }
+    if (b >= B) continue;
     const size_t hj = static_cast<size_t>(b) * H + j;
     const size_t row = static_cast<size_t>(b) * G;
     float4 dh = Vec4<float>::load(dh_t + hj);
@@ -297,12 +294,20 @@ __global__ void __launch_bounds__(256) lstm_bwd_cell(
 #pragma unroll
       for (int g = 0; g < 4; ++g)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) tq[g * kPwCols + jq * 4 + q][r] = f32_to_bf16_bits(gv[g][q]);
+        for (int q = 0; q < 4; ++q) tbits[i][g * 4 + q] = f32_to_bf16_bits(gv[g][q]);
     }
     sd[0] = make_float4(sd[0].x + dai.x, sd[0].y + dai.y, sd[0].z + dai.z, sd[0].w + dai.w);
     sd[1] = make_float4(sd[1].x + daf.x, sd[1].y + daf.y, sd[1].z + daf.z, sd[1].w + daf.w);
     sd[2] = make_float4(sd[2].x + dag.x, sd[2].y + dag.y, sd[2].z + dag.z, sd[2].w + dag.w);
     sd[3] = make_float4(sd[3].x + dao.x, sd[3].y + dao.y, sd[3].z + dao.z, sd[3].w + dao.w);
+  }
+  if constexpr (sizeof(E) == 2) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<uint32_t*>(&tq[g * kPwCols + jq * 4 + q][2 * rg]) =
+            tbits[0][g * 4 + q] | (tbits[1][g * 4 + q] << 16);
   }
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
