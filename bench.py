@@ -71,7 +71,7 @@ def measured_traffic(kernel):
 # group is taken: the recurrent GEMM runs T times per step.
 SITE_SYMBOLS = {
     "lstm_fwd_gemm": "EpiLstmCell",
-    "lstm_dh_gemm": "gemm_bf16_dma<o5::KRows2<unsigned short>, o5::ICols2<unsigned short>, o5::EpiStoreF32>",
+    "lstm_dh_gemm": "o5::EpiStoreF32, unsigned short>(o5::KRows2",
     "lstm_dw_gemm": "EpiStoreF32Split2",
     "lstm_bwd_cell": "lstm_bwd_cell",
     "adam_step": "adam_kernel",
