@@ -43,7 +43,13 @@ namespace o5 {
 namespace kk {
 
 constexpr int BM = 256, BN = 256;
-constexpr int WM = 128, WN = 128, WAVES_N = 2, NWAVES = 4, NT = NWAVES * 64;
+#ifndef O5_KK_WAVES
+#define O5_KK_WAVES 4
+#endif
+// 4 waves (2 x 2) of 128 x 128, one per SIMD; or 8 waves (2 x 4) of 128 x 64,
+// two per SIMD
+constexpr int NWAVES = O5_KK_WAVES;
+constexpr int WM = 128, WN = NWAVES == 4 ? 128 : 64, WAVES_N = BN / WN, NT = NWAVES * 64;
 constexpr int MB = WM / 32, NB = WN / 32;
 
 template <int BK>
