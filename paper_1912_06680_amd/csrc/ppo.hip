@@ -7,15 +7,18 @@
 // value loss weight 1.0; appendix "Exploration": entropy bonus 0.01).
 //
 //   z   = h Wp^T                        GEMM  (M = N rows, N = A+1, K = H)
-//   row kernel: + bp, per-head log-softmax, joint log-ratio, clipped
-//        surrogate, value error, entropy -> dz [N, A+1] and per-row stats
+//   row kernel (one wave per row): + bp, per-head log-softmax, joint
+//        log-ratio, clipped surrogate, value error, entropy -> dz [N, A+1],
+//        and per-block partial sums of dz (for dbp) and of the row stats
 //   dh  = dz Wp                         GEMM  (M = N, N = H, K = A+1)
 //   dWp = dz^T h                        GEMM  (M = A+1, N = H, K = N), split-K
-//   dbp, stats: fixed-order column sums.
+//   dbp, stats: fixed-order sums of the block partials.
 // On the bf16 path the two gradient products run on the MFMA engine: dz is
 // written as a pair of bf16 terms hi = bf16(dz), lo = bf16(dz - hi) (relative
 // error ~2^-16) laid side by side along K, against the bf16 operand repeated
-// twice, so the product keeps nearly fp32 accuracy.
+// twice, so the product keeps nearly fp32 accuracy.  For dWp the row kernel
+// also writes the pair transposed ([hi rows; lo rows] x N, K-contiguous), so h
+// is read once: dWp = sum of the hi and lo halves of [hi; lo] h.
 // Every reduction has a fixed order, so results are bitwise reproducible.
 #include "gemm_plan.h"
 #include "heads.h"
@@ -28,88 +31,207 @@ constexpr int kStatCols = 8;
 // The logits store: an EpiStoreF32 under its own type name, so the heads
 // GEMM is a kernel symbol of its own in profiles.
 struct EpiLogits : EpiStoreF32 {};
-constexpr int kRowsPerChunk = 256;
 
-// One thread per row.  zpart: [S][N][A1] partial logits (bias not added).
-// dz doubles as the row's logit scratch: it first receives z, then dL/dz.
-__global__ void __launch_bounds__(256) ppo_rows(int N, int A1, int S, const float* __restrict__ zpart,
-                                                const float* __restrict__ bp, const int32_t* __restrict__ act,
-                                                const float* __restrict__ logp_old, const float* __restrict__ adv,
-                                                const float* __restrict__ ret, const uint8_t* __restrict__ mask,
-                                                HeadsMeta hm, float clip_eps, float vf_coef, float ent_coef,
-                                                float invN, float* __restrict__ dz, float* __restrict__ rowstats,
-                                                uint16_t* __restrict__ dz_hi, uint16_t* __restrict__ dz_lo,
-                                                int ld_hilo) {
-  const int n = blockIdx.x * blockDim.x + threadIdx.x;
-  if (n >= N) return;
-  float* zr = dz + static_cast<size_t>(n) * A1;
+constexpr int kRowsPerWave = 4;
+constexpr int kWavesPerBlock = 8;
+constexpr int kRowsPerBlock = kRowsPerWave * kWavesPerBlock;
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v = fmaxf(v, __shfl_xor(v, d, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+  return v;
+}
+
+// Column c of the row, held by lane c % 64 as its element c / 64.
+template <int CPL>
+__device__ __forceinline__ float column(const float (&z)[CPL], int c) {
+  float v = z[0];
+#pragma unroll
+  for (int i = 1; i < CPL; ++i)
+    if (c >> 6 == i) v = z[i];
+  return __shfl(v, c & 63, 64);
+}
+
+// One wave per row, kRowsPerWave consecutive rows per wave; lane l holds
+// logit columns l + 64 i (i < CPL).  zpart: [S][N][A1] partial logits (bias
+// not added).  Writes dz [N][A1]; on the bf16 path the (hi, lo) pair in row
+// layout [N][ld_hilo] and, when dzT is set, transposed as [2 ld_hilo][ldT]
+// (hi rows, then lo rows; columns n >= N zero).  Each block writes one row
+// of part: the column sums of its dz (A1 values), then the sums of its rows'
+// surrogate, squared value error, entropy, clip indicator, approx-KL term,
+// ratio and non-finite indicator (kStatCols values); all sums in a fixed
+// order.
+template <int CPL>
+__global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
+    int N, int A1, int S, const float* __restrict__ zpart, const float* __restrict__ bp,
+    const int32_t* __restrict__ act, const float* __restrict__ logp_old, const float* __restrict__ adv,
+    const float* __restrict__ ret, const uint8_t* __restrict__ mask, HeadsMeta hm, float clip_eps, float vf_coef,
+    float ent_coef, float invN, float* __restrict__ dz, float* __restrict__ part, uint16_t* __restrict__ dz_hi,
+    uint16_t* __restrict__ dz_lo, int ld_hilo, uint16_t* __restrict__ dzT, int ldT) {
+  __shared__ float red[kWavesPerBlock][CPL * 64 + kStatCols];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int K = hm.K, A = hm.A;
+  int head[CPL];  // head of each column held, -1 for the value column and beyond
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) {
+    const int a = lane + 64 * i;
+    head[i] = -1;
+    for (int k = 0; k < K; ++k)
+      if (a >= hm.off[k] && a < hm.off[k + 1]) head[i] = k;
+  }
+  float csum[CPL] = {};
+  float st[kStatCols] = {};
+  // the transposed pair is kept in registers (16 rows x 2 bytes per column)
+  // only for up to 128 logit columns; beyond that dzT must be null
+  constexpr bool kT = CPL <= 2;
+  constexpr int TC = kT ? CPL : 1;
+  uint32_t thi[TC][kRowsPerWave / 2] = {}, tlo[TC][kRowsPerWave / 2] = {};
   const size_t sstride = static_cast<size_t>(N) * A1;
-  for (int a = 0; a < A1; ++a) {
-    float v = bp[a];
-    for (int s = 0; s < S; ++s) v += zpart[s * sstride + static_cast<size_t>(n) * A1 + a];
-    zr[a] = v;
-  }
-  float lse[kMaxHeads], zbar[kMaxHeads], mk[kMaxHeads];
-  int ak[kMaxHeads];
-  float logpi = 0.0f, ent = 0.0f;
-  for (int k = 0; k < hm.K; ++k) {
-    const int o = hm.off[k], nk = hm.off[k + 1] - o;
-    float zmax = -INFINITY;
-    for (int a = 0; a < nk; ++a) zmax = fmaxf(zmax, zr[o + a]);
-    float se = 0.0f, sez = 0.0f;
-    for (int a = 0; a < nk; ++a) {
-      const float e = expf(zr[o + a] - zmax);
-      se += e;
-      sez += e * zr[o + a];
+  const int n0 = (blockIdx.x * kWavesPerBlock + wave) * kRowsPerWave;
+  for (int rr = 0; rr < kRowsPerWave; ++rr) {
+    const int n = n0 + rr;
+    if (n >= N) break;
+    float z[CPL];
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      const int a = lane + 64 * i;
+      float v = 0.0f;
+      if (a < A1) {
+        v = bp[a];
+        for (int s2 = 0; s2 < S; ++s2) v += zpart[s2 * sstride + static_cast<size_t>(n) * A1 + a];
+      }
+      z[i] = v;
     }
-    lse[k] = zmax + logf(se);
-    zbar[k] = sez / se;
-    ak[k] = act[static_cast<size_t>(n) * hm.K + k];
-    mk[k] = mask ? (mask[static_cast<size_t>(n) * hm.K + k] ? 1.0f : 0.0f) : 1.0f;
-    const int a_sel = min(max(ak[k], 0), nk - 1);
-    logpi += mk[k] * (zr[o + a_sel] - lse[k]);
-    ent += mk[k] * (lse[k] - zbar[k]);
+    float lse[kMaxHeads], zbar[kMaxHeads], mk[kMaxHeads];
+    int ak[kMaxHeads];
+    float logpi = 0.0f, ent = 0.0f;
+#pragma unroll
+    for (int k = 0; k < kMaxHeads; ++k) {
+      if (k < K) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < CPL; ++i)
+          if (head[i] == k) mx = fmaxf(mx, z[i]);
+        mx = wave_max(mx);
+        float se = 0.0f, sez = 0.0f;
+#pragma unroll
+        for (int i = 0; i < CPL; ++i)
+          if (head[i] == k) {
+            const float e = expf(z[i] - mx);
+            se += e;
+            sez += e * z[i];
+          }
+        se = wave_sum(se);
+        sez = wave_sum(sez);
+        lse[k] = mx + logf(se);
+        zbar[k] = sez / se;
+        ak[k] = act[static_cast<size_t>(n) * K + k];
+        mk[k] = mask ? (mask[static_cast<size_t>(n) * K + k] ? 1.0f : 0.0f) : 1.0f;
+        const int nk = hm.off[k + 1] - hm.off[k];
+        const int a_sel = min(max(ak[k], 0), nk - 1);
+        logpi += mk[k] * (column(z, hm.off[k] + a_sel) - lse[k]);
+        ent += mk[k] * (lse[k] - zbar[k]);
+      }
+    }
+    const float Ad = adv[n], R = ret[n];
+    const float dlog = logpi - logp_old[n];
+    const float ratio = expf(dlog);
+    const float rc = fminf(fmaxf(ratio, 1.0f - clip_eps), 1.0f + clip_eps);
+    const float surr = fminf(ratio * Ad, rc * Ad);
+    const float V = column(z, A);
+    const float verr = V - R;
+    const bool flow = (Ad >= 0.0f && ratio <= 1.0f + clip_eps) || (Ad < 0.0f && ratio >= 1.0f - clip_eps);
+    const float g_logpi = flow ? -ratio * Ad * invN : 0.0f;
+    const float ent_scale = ent_coef * invN;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      const int a = lane + 64 * i;
+      float d = 0.0f;
+      if (a == A) d = 2.0f * vf_coef * verr * invN;
+#pragma unroll
+      for (int k = 0; k < kMaxHeads; ++k)
+        if (k < K && head[i] == k) {
+          const float p = expf(z[i] - lse[k]);
+          const float onehot = (a - hm.off[k] == ak[k]) ? 1.0f : 0.0f;
+          d = mk[k] * (g_logpi * (onehot - p) + ent_scale * p * (z[i] - zbar[k]));
+        }
+      if (a < A1) dz[static_cast<size_t>(n) * A1 + a] = d;
+      csum[i] += d;
+      if (dz_hi != nullptr && a < ld_hilo) {
+        const uint16_t hb = f32_to_bf16_bits(d);
+        const uint16_t lb = f32_to_bf16_bits(d - bf16_bits_to_f32(hb));
+        dz_hi[static_cast<size_t>(n) * ld_hilo + a] = hb;
+        dz_lo[static_cast<size_t>(n) * ld_hilo + a] = lb;
+        if constexpr (kT) {
+          const int sh = (rr & 1) * 16;
+#pragma unroll
+          for (int q = 0; q < kRowsPerWave / 2; ++q)
+            if (q == rr >> 1) {
+              thi[i][q] |= static_cast<uint32_t>(hb) << sh;
+              tlo[i][q] |= static_cast<uint32_t>(lb) << sh;
+            }
+        }
+      }
+    }
+    const float row_loss = -surr + vf_coef * verr * verr - ent_coef * ent;
+    st[0] += surr;
+    st[1] += verr * verr;
+    st[2] += ent;
+    st[3] += fabsf(ratio - 1.0f) > clip_eps ? 1.0f : 0.0f;
+    st[4] += (ratio - 1.0f) - dlog;
+    st[5] += ratio;
+    st[6] += isfinite(row_loss) ? 0.0f : 1.0f;
   }
-  const float A = adv[n], R = ret[n];
-  const float dlog = logpi - logp_old[n];
-  const float ratio = expf(dlog);
-  const float rc = fminf(fmaxf(ratio, 1.0f - clip_eps), 1.0f + clip_eps);
-  const float surr = fminf(ratio * A, rc * A);
-  const float V = zr[hm.A];
-  const float verr = V - R;
-  const bool flow = (A >= 0.0f && ratio <= 1.0f + clip_eps) || (A < 0.0f && ratio >= 1.0f - clip_eps);
-  const float g_logpi = flow ? -ratio * A * invN : 0.0f;
-  const float ent_scale = ent_coef * invN;
-  for (int k = 0; k < hm.K; ++k) {
-    const int o = hm.off[k], nk = hm.off[k + 1] - o;
-    for (int a = 0; a < nk; ++a) {
-      const float z = zr[o + a];
-      const float p = expf(z - lse[k]);
-      const float onehot = (a == ak[k]) ? 1.0f : 0.0f;
-      zr[o + a] = mk[k] * (g_logpi * (onehot - p) + ent_scale * p * (z - zbar[k]));
+  if (kT && dzT != nullptr) {
+    // kRowsPerWave consecutive rows of each column held: 8 bytes of a dz^T row
+    static_assert(kRowsPerWave == 4, "one 8-byte store per column and half");
+#pragma unroll
+    for (int i = 0; i < TC; ++i) {
+      const int a = lane + 64 * i;
+      if (a < ld_hilo) {
+        *reinterpret_cast<uint2*>(dzT + static_cast<size_t>(a) * ldT + n0) = make_uint2(thi[i][0], thi[i][1]);
+        *reinterpret_cast<uint2*>(dzT + static_cast<size_t>(ld_hilo + a) * ldT + n0) = make_uint2(tlo[i][0], tlo[i][1]);
+      }
     }
   }
-  zr[hm.A] = 2.0f * vf_coef * verr * invN;
-  if (dz_hi != nullptr) {  // bf16 pair (hi, lo) of the row, zero-padded to ld_hilo
-    uint16_t* hr = dz_hi + static_cast<size_t>(n) * ld_hilo;
-    uint16_t* lr = dz_lo + static_cast<size_t>(n) * ld_hilo;
-    for (int a = 0; a < ld_hilo; ++a) {
-      const float v = a < A1 ? zr[a] : 0.0f;
-      const uint16_t hb = f32_to_bf16_bits(v);
-      hr[a] = hb;
-      lr[a] = f32_to_bf16_bits(v - bf16_bits_to_f32(hb));
-    }
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) red[wave][64 * i + lane] = csum[i];
+  if (lane < kStatCols) {
+    float v = 0.0f;
+#pragma unroll
+    for (int q = 0; q < kStatCols; ++q)
+      if (q == lane) v = st[q];
+    red[wave][CPL * 64 + lane] = v;
   }
-  const float row_loss = -surr + vf_coef * verr * verr - ent_coef * ent;
-  float* st = rowstats + static_cast<size_t>(n) * kStatCols;
-  st[0] = surr;
-  st[1] = verr * verr;
-  st[2] = ent;
-  st[3] = fabsf(ratio - 1.0f) > clip_eps ? 1.0f : 0.0f;
-  st[4] = (ratio - 1.0f) - dlog;
-  st[5] = ratio;
-  st[6] = isfinite(row_loss) ? 0.0f : 1.0f;
-  st[7] = 0.0f;
+  __syncthreads();
+  const int W = A1 + kStatCols;
+  for (int t = threadIdx.x; t < W; t += blockDim.x) {
+    const int c = t < A1 ? t : CPL * 64 + (t - A1);
+    float v = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) v += red[w][c];
+    part[static_cast<size_t>(blockIdx.x) * W + t] = v;
+  }
+}
+
+// dWp[a, j] = sum over splits s of part[s, a, j] + part[s, A1p + a, j]
+// (the hi and lo halves), fixed order.
+__global__ void __launch_bounds__(256) sum_hilo_splits(int S, int A1, int A1p, int H, const float* __restrict__ part,
+                                                       float* __restrict__ out) {
+  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= static_cast<size_t>(A1) * H) return;
+  const size_t hs = static_cast<size_t>(A1p) * H;  // offset of the lo half
+  float v = 0.0f;
+  for (int s2 = 0; s2 < S; ++s2) {
+    const float* p = part + static_cast<size_t>(s2) * 2 * hs;
+    v += p[i] + p[hs + i];
+  }
+  out[i] = v;
 }
 
 // dst [R, H] bf16 = src [A1, H] with rows A1..R-1 zero.
@@ -122,24 +244,29 @@ __global__ void __launch_bounds__(256) pad_rows_bf16(int A1, int R, int H, const
   dst[i] = r < A1 ? src[i] : static_cast<uint16_t>(0);
 }
 
-__global__ void ppo_finalize(const float* __restrict__ sums, float invN, float vf_coef, float ent_coef,
-                             float* __restrict__ stats) {
+// stats from the summed block partials (sums = [dz column sums (A1) | row
+// stat sums (kStatCols)]); also copies the bias gradient out.
+__global__ void ppo_finalize(int A1, const float* __restrict__ sums, float invN, float vf_coef, float ent_coef,
+                             float* __restrict__ stats, float* __restrict__ dbp) {
+  for (int a = threadIdx.x; a < A1; a += blockDim.x) dbp[a] = sums[a];
   if (threadIdx.x != 0) return;
-  const float pg = -sums[0] * invN, vf = sums[1] * invN, ent = sums[2] * invN;
+  const float* ss = sums + A1;
+  const float pg = -ss[0] * invN, vf = ss[1] * invN, ent = ss[2] * invN;
   stats[0] = pg + vf_coef * vf - ent_coef * ent;
   stats[1] = pg;
   stats[2] = vf;
   stats[3] = ent;
-  stats[4] = sums[3] * invN;
-  stats[5] = sums[4] * invN;
-  stats[6] = sums[5] * invN;
-  stats[7] = sums[6];
+  stats[4] = ss[3] * invN;
+  stats[5] = ss[4] * invN;
+  stats[6] = ss[5] * invN;
+  stats[7] = ss[6];
 }
 
 struct PpoWs {
-  size_t zpart, dz, rowstats, wpart, dbpart, spart, ssum, dzhi, dzlo, wpad, total;
+  size_t zpart, dz, part, sums, wpart, dzhi, dzlo, dzT, wpad, total;
   GemmPlan plan_z, plan_w, plan_h;
-  int nchunk, A1, A1p;
+  int nblk, A1, A1p, ldT, wsplits;
+  bool dwp_t;  // dWp from the transposed (hi; lo) pair, h read once
 };
 
 static PpoWs ppo_ws(o5_dtype dt, int N, int H, int A1) {
@@ -147,27 +274,33 @@ static PpoWs ppo_ws(o5_dtype dt, int N, int H, int A1) {
   const bool bf = dt == O5_BF16;
   w.A1 = A1;
   w.A1p = cdiv(A1, 64) * 64;  // padded logit count: a multiple of the K tile
+  w.nblk = cdiv(N, kRowsPerBlock);
+  w.ldT = w.nblk * kRowsPerBlock;
+  w.dwp_t = bf && w.A1p <= 128;
   w.plan_z = plan_gemm(bf, N, A1, H);
   w.plan_w = bf ? plan_gemm(true, A1, H, 2 * N) : plan_gemm(false, A1, H, N);
   w.plan_h = bf ? plan_gemm(true, N, H, 2 * w.A1p) : GemmPlan{false, BfTile::k128x128, 1};
   w.plan_h.splits = 1;
-  w.nchunk = cdiv(N, kRowsPerChunk);
+  w.wsplits = 1;
+  if (w.dwp_t) {
+    // M = 2 A1p (one 256-row tile), N = H, K = N: split K so the grid has
+    // about 256 blocks, each with at least 8 K tiles of 32
+    const int tiles = cdiv(H, 256);
+    w.wsplits = std::max(1, std::min(cdiv(256, tiles), cdiv(N, 32) / 8));
+  }
   size_t o = 0;
   w.zpart = o;
   o += align_up(static_cast<size_t>(w.plan_z.splits) * N * A1 * 4);
   w.dz = o;
   o += align_up(static_cast<size_t>(N) * A1 * 4);
-  w.rowstats = o;
-  o += align_up(static_cast<size_t>(N) * kStatCols * 4);
+  w.part = o;
+  o += align_up(static_cast<size_t>(w.nblk) * (A1 + kStatCols) * 4);
+  w.sums = o;
+  o += align_up(static_cast<size_t>(A1 + kStatCols) * 4);
   w.wpart = o;
-  o += align_up(static_cast<size_t>(w.plan_w.splits) * A1 * H * 4);
-  w.dbpart = o;
-  o += align_up(static_cast<size_t>(w.nchunk) * A1 * 4);
-  w.spart = o;
-  o += align_up(static_cast<size_t>(w.nchunk) * kStatCols * 4);
-  w.ssum = o;
-  o += align_up(kStatCols * 4);
-  w.dzhi = w.dzlo = w.wpad = 0;
+  o += align_up(w.dwp_t ? static_cast<size_t>(w.wsplits) * 2 * w.A1p * H * 4
+                        : static_cast<size_t>(w.plan_w.splits) * A1 * H * 4);
+  w.dzhi = w.dzlo = w.dzT = w.wpad = 0;
   if (bf) {
     w.dzhi = o;
     o += align_up(static_cast<size_t>(N) * w.A1p * 2);
@@ -175,6 +308,10 @@ static PpoWs ppo_ws(o5_dtype dt, int N, int H, int A1) {
     o += align_up(static_cast<size_t>(N) * w.A1p * 2);
     w.wpad = o;
     o += align_up(static_cast<size_t>(w.A1p) * H * 2);
+    if (w.dwp_t) {
+      w.dzT = o;
+      o += align_up(static_cast<size_t>(2) * w.A1p * w.ldT * 2);
+    }
   }
   w.total = o;
   return w;
@@ -199,6 +336,16 @@ int check_heads(const char* fn, o5_dtype dt, int N, int H, int K, const int* hea
   return O5_OK;
 }
 
+template <int CPL>
+static void launch_rows(const PpoWs& w, int N, int A1, int S, const float* zpart, const float* bp, const int32_t* act,
+                        const float* logp_old, const float* adv, const float* ret, const uint8_t* mask,
+                        const HeadsMeta& hm, o5_ppo_hp hp, float invN, float* dz, float* part, uint16_t* dzhi,
+                        uint16_t* dzlo, uint16_t* dzT, hipStream_t s) {
+  hipLaunchKernelGGL(ppo_rows<CPL>, dim3(w.nblk), dim3(kWavesPerBlock * 64), 0, s, N, A1, S, zpart, bp, act, logp_old,
+                     adv, ret, mask, hm, hp.clip_eps, hp.vf_coef, hp.ent_coef, invN, dz, part, dzhi, dzlo, w.A1p, dzT,
+                     w.ldT);
+}
+
 template <typename E>
 static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, const float* bp, const int32_t* act,
                     const float* logp_old, const float* adv, const float* ret, const uint8_t* mask, o5_ppo_hp hp,
@@ -206,11 +353,9 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
   const int A1 = hm.A + 1;
   float* zpart = reinterpret_cast<float*>(ws + w.zpart);
   float* dz = reinterpret_cast<float*>(ws + w.dz);
-  float* rowstats = reinterpret_cast<float*>(ws + w.rowstats);
+  float* part = reinterpret_cast<float*>(ws + w.part);
+  float* sums = reinterpret_cast<float*>(ws + w.sums);
   float* wpart = reinterpret_cast<float*>(ws + w.wpart);
-  float* dbpart = reinterpret_cast<float*>(ws + w.dbpart);
-  float* spart = reinterpret_cast<float*>(ws + w.spart);
-  float* ssum = reinterpret_cast<float*>(ws + w.ssum);
   const float invN = 1.0f / static_cast<float>(N);
   {  // z = h Wp^T
     KRows2<E> al{h, nullptr, nullptr, H, 0, H, H, N};
@@ -220,12 +365,24 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
   }
   uint16_t* dzhi = nullptr;
   uint16_t* dzlo = nullptr;
+  uint16_t* dzT = nullptr;
   if constexpr (sizeof(E) == 2) {
     dzhi = reinterpret_cast<uint16_t*>(ws + w.dzhi);
     dzlo = reinterpret_cast<uint16_t*>(ws + w.dzlo);
+    if (w.dwp_t) dzT = reinterpret_cast<uint16_t*>(ws + w.dzT);
   }
-  hipLaunchKernelGGL(ppo_rows, dim3(cdiv(N, 256)), dim3(256), 0, s, N, A1, w.plan_z.splits, zpart, bp, act, logp_old,
-                     adv, ret, mask, hm, hp.clip_eps, hp.vf_coef, hp.ent_coef, invN, dz, rowstats, dzhi, dzlo, w.A1p);
+  const int S = w.plan_z.splits;
+  const int cpl = cdiv(A1, 64);
+  if (cpl <= 1)
+    launch_rows<1>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, hm, hp, invN, dz, part, dzhi, dzlo, dzT, s);
+  else if (cpl <= 2)
+    launch_rows<2>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, hm, hp, invN, dz, part, dzhi, dzlo, dzT, s);
+  else if (cpl <= 4)
+    launch_rows<4>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, hm, hp, invN, dz, part, dzhi, dzlo, dzT, s);
+  else if (cpl <= 8)
+    launch_rows<8>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, hm, hp, invN, dz, part, dzhi, dzlo, dzT, s);
+  else
+    launch_rows<16>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, hm, hp, invN, dz, part, dzhi, dzlo, dzT, s);
   if constexpr (sizeof(E) == 2) {
     const int A1p = w.A1p;
     uint16_t* wpad = reinterpret_cast<uint16_t*>(ws + w.wpad);
@@ -237,11 +394,22 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
       EpiStoreF32 epi{dh, H, 0};
       run_gemm(w.plan_h, al, bl, epi, N, H, 2 * A1p, s);
     }
-    {  // dWp = [dz_hi ; dz_lo]^T . [h ; h]  (K = 2N), split over K, fixed-order sum
+    if (w.dwp_t) {
+      // [dWp_hi ; dWp_lo] = [hi ; lo]^T-rows . h  (M = 2 A1p, N = H, K = N), split over K
+      KRows2<uint16_t> al{dzT, nullptr, nullptr, w.ldT, 0, N, N, 2 * A1p};
+      ICols2<uint16_t> bl{h, nullptr, nullptr, nullptr, H, 0, H, H, N, 0};
+      EpiStoreF32 epi{wpart, H, static_cast<size_t>(2) * A1p * H};
+      launch_gemm_bf16_dma(al, bl, epi, 2 * A1p, H, N, w.wsplits, s);
+      hipLaunchKernelGGL(sum_hilo_splits, dim3(cdiv(static_cast<long long>(A1) * H, 256)), dim3(256), 0, s,
+                         w.wsplits, A1, A1p, H, wpart, dWp);
+    } else {
+      // dWp = [dz_hi ; dz_lo]^T . [h ; h]  (K = 2N), split over K, fixed-order sum
       ICols2<uint16_t> al{dzhi, dzhi, dzlo, nullptr, A1p, A1p, 0, A1p, 2 * N, N};
       ICols2<uint16_t> bl{h, h, h, nullptr, H, H, 0, H, 2 * N, N};
       EpiStoreF32 epi{wpart, H, static_cast<size_t>(A1) * H};
       run_gemm(w.plan_w, al, bl, epi, A1, H, 2 * N, s);
+      hipLaunchKernelGGL(colsum_rows, dim3(cdiv(static_cast<long long>(A1) * H, 256)), dim3(256), 0, s,
+                         w.plan_w.splits, A1 * H, wpart, dWp);
     }
   } else {
     {  // dh = dz Wp  (fp32 FMA engine)
@@ -256,14 +424,11 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
       EpiStoreF32 epi{wpart, H, static_cast<size_t>(A1) * H};
       launch_gemm_f32(al, bl, epi, A1, H, N, w.plan_w.splits, s);
     }
+    hipLaunchKernelGGL(colsum_rows, dim3(cdiv(static_cast<long long>(A1) * H, 256)), dim3(256), 0, s, w.plan_w.splits,
+                       A1 * H, wpart, dWp);
   }
-  hipLaunchKernelGGL(colsum_rows, dim3(cdiv(static_cast<long long>(A1) * H, 256)), dim3(256), 0, s, w.plan_w.splits,
-                     A1 * H, wpart, dWp);
-  hipLaunchKernelGGL(colsum_chunks, dim3(cdiv(A1, 256), w.nchunk), dim3(256), 0, s, N, A1, kRowsPerChunk, dz, dbpart);
-  hipLaunchKernelGGL(colsum_rows, dim3(cdiv(A1, 256)), dim3(256), 0, s, w.nchunk, A1, dbpart, dbp);
-  hipLaunchKernelGGL(colsum_chunks, dim3(1, w.nchunk), dim3(256), 0, s, N, kStatCols, kRowsPerChunk, rowstats, spart);
-  hipLaunchKernelGGL(colsum_rows, dim3(1), dim3(256), 0, s, w.nchunk, kStatCols, spart, ssum);
-  hipLaunchKernelGGL(ppo_finalize, dim3(1), dim3(64), 0, s, ssum, invN, hp.vf_coef, hp.ent_coef, stats);
+  hipLaunchKernelGGL(colsum_tree, dim3(A1 + kStatCols), dim3(256), 0, s, w.nblk, A1 + kStatCols, part, sums);
+  hipLaunchKernelGGL(ppo_finalize, dim3(1), dim3(256), 0, s, A1, sums, invN, hp.vf_coef, hp.ent_coef, stats, dbp);
   return check_launch("o5_ppo_loss_grad");
 }
 

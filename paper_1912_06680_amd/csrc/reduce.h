@@ -26,4 +26,23 @@ static __global__ void __launch_bounds__(256) colsum_rows(int P, int N, const fl
   out[n] = s;
 }
 
+// out[n] = sum over the P rows of part, one block of 256 threads per column:
+// thread t sums rows t, t + 256, ... in order, then a fixed-shape tree in LDS.
+// For short columns of many rows (where one thread per column would walk all
+// P rows alone).
+static __global__ void __launch_bounds__(256) colsum_tree(int P, int N, const float* __restrict__ part,
+                                                        float* __restrict__ out) {
+  __shared__ float red[256];
+  const int n = blockIdx.x;
+  float s = 0.0f;
+  for (int p = threadIdx.x; p < P; p += 256) s += part[static_cast<size_t>(p) * N + n];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[n] = red[0];
+}
+
 }  // namespace o5

@@ -48,6 +48,9 @@ PPO_CASES = [
     ("f32-mask-ragged", 1001, 128, (5, 3, 7), False, True),
     ("bf16-mid", 4096, 1024, HEADS, True, True),
     ("bf16-one-head", 333, 192, (8,), True, False),
+    # 191 logit columns: three per lane, heads crossing the 64-column lane
+    # blocks, and the dWp product without the transposed pair
+    ("bf16-wide-heads", 500, 128, (100, 60, 30), True, True),
 ]
 
 
