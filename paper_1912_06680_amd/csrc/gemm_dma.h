@@ -78,7 +78,9 @@ __device__ __attribute__((aligned(16))) const uint16_t kZeroRow[512] = {};
 __device__ __forceinline__ void copy16(const void* g, char* lds_wave_base) {
   const uint32_t lds = __builtin_amdgcn_readfirstlane(
       static_cast<uint32_t>(reinterpret_cast<size_t>((__attribute__((address_space(3))) char*)(lds_wave_base))));
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+  // one wait state between the M0 write and the LDS DMA that reads it (a
+  // hazard the compiler would handle for instructions it can see)
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
 }
 
 // ------------------------------------------------- K-contiguous operand

@@ -72,43 +72,73 @@ __device__ __forceinline__ int slot(int r, int c) {
   return c ^ ((r / C::R256) % C::CPR);
 }
 
-// Per-lane state for copying one operand's 256-row tiles: copy q of wave w
-// fills tile rows (w * NC + q) * RPI .. + RPI - 1; the lane fetches the chunk
-// that belongs at slot (lane % CPR) of row (lane / CPR).
+typedef int rsrc_t __attribute__((ext_vector_type(4)));
+
+// Buffer resource for bytes [base, base + bytes): raw (stride 0), 32-bit
+// words, out-of-range reads return zero.
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  rsrc_t r;
+  r.x = static_cast<int>(static_cast<uint32_t>(b));
+  r.y = static_cast<int>(static_cast<uint32_t>(b >> 32) & 0xffffu);
+  r.z = static_cast<int>(bytes);
+  r.w = 0x00020000;
+  return r;
+}
+
+constexpr uint32_t kOutOfRange = 0xfffffff0u;  // a byte offset past every operand buffer
+
+// Per-lane state for copying one operand's 256-row tiles with buffer loads to
+// LDS: copy q of wave w fills tile rows (w * NC + q) * RPI .. + RPI - 1; the
+// lane fetches the chunk that belongs at slot (lane % CPR) of row (lane /
+// CPR).  The lane's byte offset into each source is fixed; the tile's k moves
+// in the scalar offset, so a copy is one s_mov and one buffer load.  Rows past
+// the operand, and masked rows of the second source, get an offset past the
+// buffer and so read zeros.  Requires K0 and K multiples of BK (no tile
+// straddles a source boundary or the end) and sources below 2^31 bytes.
 template <typename E, int BK>
 struct Tile {
   using C = Cfg<BK>;
-  const char* ptr0[C::NC];  // row start in source 0 (bytes), or nullptr = zero row
-  const char* ptr1[C::NC];  // row start in source 1
-  int koff[C::NC];          // byte offset of the lane's chunk inside the tile's k range
+  rsrc_t rs0, rs1;
+  uint32_t voff0[C::NC], voff1[C::NC];
+  int K0, kmax;
 
   __device__ __forceinline__ void init(const KRows2<E>& l, int row0, int wave, int lane) {
+    K0 = l.K0;
+    kmax = l.K - BK;
+    rs0 = make_rsrc(l.p0, static_cast<uint32_t>(static_cast<size_t>(l.rows) * l.ld0 * sizeof(E)));
+    rs1 = make_rsrc(l.p1 != nullptr ? l.p1 : l.p0,
+                    l.p1 != nullptr ? static_cast<uint32_t>(static_cast<size_t>(l.rows) * l.ld1 * sizeof(E)) : 0u);
 #pragma unroll
     for (int q = 0; q < C::NC; ++q) {
       const int r = (wave * C::NC + q) * C::RPI + lane / C::CPR;  // tile row this lane fills
       const int row = l.gstride > 0 ? (r >> 6) * l.gstride + (row0 >> 2) + (r & 63) : row0 + r;
-      koff[q] = slot<BK>(r, lane % C::CPR) * 16;
+      const uint32_t koff = slot<BK>(r, lane % C::CPR) * 16;
       const bool valid = row < l.rows;
       const bool masked = valid && l.mask1 != nullptr && l.mask1[row] != 0;
-      ptr0[q] = valid ? reinterpret_cast<const char*>(l.p0 + static_cast<size_t>(row) * l.ld0) : nullptr;
-      ptr1[q] = (valid && !masked && l.p1 != nullptr)
-                    ? reinterpret_cast<const char*>(l.p1 + static_cast<size_t>(row) * l.ld1)
-                    : nullptr;
+      voff0[q] = valid ? static_cast<uint32_t>(row) * l.ld0 * sizeof(E) + koff : kOutOfRange;
+      voff1[q] = (valid && !masked && l.p1 != nullptr) ? static_cast<uint32_t>(row) * l.ld1 * sizeof(E) + koff
+                                                        : kOutOfRange;
     }
   }
-  // copy q of the tile starting at k0 into `stage`
-  __device__ __forceinline__ void issue_one(const KRows2<E>& l, int k0, char* stage, int wave, int q) const {
-    const bool seg0 = k0 < l.K0;
-    const int kb = seg0 ? k0 : k0 - l.K0;  // element offset inside the source row
-    const bool kin = k0 + koff[q] / 2 < l.K;
-    const char* p = seg0 ? ptr0[q] : ptr1[q];
-    const void* g = (p != nullptr && kin) ? static_cast<const void*>(p + kb * 2 + koff[q])
-                                          : static_cast<const void*>(dma::kZeroRow);
-    dma::copy16(g, stage + (wave * C::NC + q) * 1024);
+  // copy q of the tile starting at k0 into the stage at LDS address `stage`;
+  // tiles past the end (the ring's trailing copies) re-read the last tile into
+  // a stage no one reads
+  __device__ __forceinline__ void issue_one(int k0, uint32_t stage, int wave, int q) const {
+    k0 = min(k0, kmax);
+    const bool seg0 = k0 < K0;
+    const uint32_t soff = static_cast<uint32_t>(seg0 ? k0 : k0 - K0) * sizeof(E);
+    const uint32_t voff = seg0 ? voff0[q] : voff1[q];
+    const rsrc_t rs = seg0 ? rs0 : rs1;
+    const uint32_t lds = stage + (wave * C::NC + q) * 1024;
+    // (s_nop: one wait state between the M0 write and the LDS DMA reading it)
+    asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(voff), "s"(rs), "s"(soff),
+                 "s"(lds)
+                 : "memory", "m0");
   }
-  __device__ __forceinline__ void issue(const KRows2<E>& l, int k0, char* stage, int wave) const {
+  __device__ __forceinline__ void issue(int k0, uint32_t stage, int wave) const {
 #pragma unroll
-    for (int q = 0; q < C::NC; ++q) issue_one(l, k0, stage, wave, q);
+    for (int q = 0; q < C::NC; ++q) issue_one(k0, stage, wave, q);
   }
 };
 
@@ -146,8 +176,7 @@ __device__ __forceinline__ void mfma_all(const Frags& f, f32x16_t (&acc)[MB][NB]
 // barriers).
 template <typename E, int BK, int Q0, int Q1>
 __device__ __forceinline__ void mfma_copies(const Frags& f, f32x16_t (&acc)[MB][NB], const Tile<E, BK>& ta,
-                                            const Tile<E, BK>& tb, const KRows2<E>& al, const KRows2<E>& bl, int k0,
-                                            char* as, char* bs, int wave) {
+                                            const Tile<E, BK>& tb, int k0, uint32_t as, uint32_t bs, int wave) {
   constexpr int NC = Cfg<BK>::NC;
   constexpr int NQ = Q1 - Q0;
   dma::unroll<0, MB * NB>([&](auto I) {
@@ -159,9 +188,9 @@ __device__ __forceinline__ void mfma_copies(const Frags& f, f32x16_t (&acc)[MB][
       constexpr int q = decltype(J)::value;
       if constexpr ((q - Q0) * MB * NB / NQ == m) {
         if constexpr (q < NC)
-          ta.issue_one(al, k0, as, wave, q);
+          ta.issue_one(k0, as, wave, q);
         else
-          tb.issue_one(bl, k0, bs, wave, q - NC);
+          tb.issue_one(k0, bs, wave, q - NC);
       }
     });
     __builtin_amdgcn_sched_barrier(0);
@@ -209,18 +238,21 @@ __global__ void __launch_bounds__(kk::NT, 1)
     tb.init(bl, n0, wave, lane);
     char* const sA = smem;
     char* const sB = smem + STAGES * TB;
+    // the same stages as LDS byte addresses, for the copies' M0
+    const uint32_t lA = static_cast<uint32_t>(reinterpret_cast<size_t>((__attribute__((address_space(3))) char*)smem));
+    const uint32_t lB = lA + STAGES * TB;
 
     // prologue: tiles 0 .. STAGES-2 in flight; wait for tile 0; the last
     // stage's tile; the first fragments
 #pragma unroll
     for (int st = 0; st < STAGES - 1; ++st) {
-      ta.issue(al, (kt0 + st) * BK, sA + st * TB, wave);
-      tb.issue(bl, (kt0 + st) * BK, sB + st * TB, wave);
+      ta.issue((kt0 + st) * BK, lA + st * TB, wave);
+      tb.issue((kt0 + st) * BK, lB + st * TB, wave);
     }
     dma::wait_copies_n<PER_TILE>(STAGES - 2);
     dma::wave_barrier();
-    ta.issue(al, (kt0 + STAGES - 1) * BK, sA + (STAGES - 1) * TB, wave);
-    tb.issue(bl, (kt0 + STAGES - 1) * BK, sB + (STAGES - 1) * TB, wave);
+    ta.issue((kt0 + STAGES - 1) * BK, lA + (STAGES - 1) * TB, wave);
+    tb.issue((kt0 + STAGES - 1) * BK, lB + (STAGES - 1) * TB, wave);
     Frags f[2];
     read<BK>(sA, sB, wm0, wn0, lane, 0, f[0]);
 
@@ -243,7 +275,7 @@ __global__ void __launch_bounds__(kk::NT, 1)
         if constexpr (s + 1 < SPREAD) {
           constexpr int q0 = (s + 1) * NQ / SPREAD, q1 = (s + 2) * NQ / SPREAD;
           if (r > 0)
-            mfma_copies<E, BK, q0, q1>(f[s & 1], acc, ta, tb, al, bl, pk0, sA + pst, sB + pst, wave);
+            mfma_copies<E, BK, q0, q1>(f[s & 1], acc, ta, tb, pk0, lA + pst, lB + pst, wave);
           else
             mfma_all(f[s & 1], acc);
         } else {
@@ -258,7 +290,7 @@ __global__ void __launch_bounds__(kk::NT, 1)
       read<BK>(sA + nx, sB + nx, wm0, wn0, lane, 0, f[0]);
       __builtin_amdgcn_sched_barrier(0);
       // last k step of tile r; stage st starts refilling with tile r + STAGES
-      mfma_copies<E, BK, 0, NQ / SPREAD>(f[1], acc, ta, tb, al, bl, (kt0 + r + STAGES) * BK, sA + st, sB + st, wave);
+      mfma_copies<E, BK, 0, NQ / SPREAD>(f[1], acc, ta, tb, (kt0 + r + STAGES) * BK, lA + st, lB + st, wave);
     }
     {
       // the last tile; its first fragments are in f[0]
@@ -301,6 +333,16 @@ inline void launch_gemm_kk(const KRows2<E>& al, const KRows2<E>& bl, const Epi& 
   const unsigned tiles = ((M + kk::BM - 1) / kk::BM) * ((N + kk::BN - 1) / kk::BN);
   hipLaunchKernelGGL((gemm_kk<BK, O5_KK_SPREAD, Epi, E>), dim3(tiles, 1, splits), dim3(kk::NT), 0, s, al, bl, epi, M,
                      N, K, kps);
+}
+
+// Operands the buffer-load copies can take: K and the source split K0 whole
+// tiles, every source below 2^31 bytes.
+template <typename E>
+inline bool kk_fits(const KRows2<E>& l) {
+  constexpr int BK = O5_KK_BK;
+  const size_t b0 = static_cast<size_t>(l.rows) * l.ld0 * sizeof(E);
+  const size_t b1 = l.p1 != nullptr ? static_cast<size_t>(l.rows) * l.ld1 * sizeof(E) : 0;
+  return l.K >= BK && l.K % BK == 0 && l.K0 % BK == 0 && b0 < (size_t{1} << 31) && b1 < (size_t{1} << 31);
 }
 
 // The K-contiguous engine is the default for two K-contiguous bf16 operands;

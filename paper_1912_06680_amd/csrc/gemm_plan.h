@@ -73,7 +73,7 @@ inline void run_gemm(const GemmPlan& p, const AL& al, const BL& bl, const Epi& e
   if constexpr (AL::kBf16 && BL::kBf16) {
     if (p.bf16) {
       if constexpr (std::is_same_v<AL, KRows2<uint16_t>> && std::is_same_v<BL, KRows2<uint16_t>>) {
-        if (p.tile == BfTile::kDma256 && kk_engine_enabled()) {
+        if (p.tile == BfTile::kDma256 && kk_engine_enabled() && kk_fits(al) && kk_fits(bl)) {
           launch_gemm_kk(al, bl, epi, M, N, K, p.splits, s);
           return;
         }
