@@ -1,27 +1,32 @@
 // bf16 MFMA GEMM for two K-contiguous operands (gfx950):
 //   C[i, j] = sum_k A(i, k) * B(j, k)  (+ epilogue), fp32 accumulate.
 //
-// Block tile 256 x 256 by 4 waves (2 x 2) of 128 x 128, one wave per SIMD:
-// each fragment read from LDS feeds four MFMAs, so a K tile's b128 fragment
-// reads (about one per 5 clocks per CU) cost a third of its MFMA time.
+// Block tile 256 x 256, one block per CU.  By default 8 waves (2 x 4) of
+// 128 x 64, two per SIMD, so one wave's MFMAs run while the other issues
+// copies or waits at a barrier; the alternative of 4 waves of 128 x 128 (one
+// per SIMD, each fragment read from LDS feeding four MFMAs) measured a few
+// percent slower overall.
 //
-// Operands go global -> LDS by direct-to-LDS copies (16 bytes per lane,
-// written at M0 + 16 * lane) through a ring of STAGES stages of BK k.  With
-// BK = 64 a copy instruction fetches 8 rows x 128 bytes, i.e. whole cache
-// lines; with BK = 32 it fetches 16 half lines, which halves the rate at
-// which the L2 feeds the CU.  BK = 64 leaves room for two stages only.
+// Operands go global -> LDS by buffer loads with the LDS flag (16 bytes per
+// lane, written at M0 + 16 * lane) through a ring of STAGES stages of BK k.
+// With BK = 64 a copy instruction moves 8 rows x 128 bytes, i.e. whole cache
+// lines; with BK = 32 it moves 16 half lines, which halves the rate at which
+// the L2 feeds the CU.  BK = 64 leaves room for two stages only.  Each lane's
+// byte offset into its operand is fixed for the whole K loop and the tile's
+// k travels in the scalar offset, so a copy is one s_mov to M0 and one load;
+// rows outside the operand get an offset past the buffer and read zeros.
 //
-// With one wave per SIMD nothing else hides LDS latency, so the wave
-// software-pipelines its fragments: those of k step s + 1 are read while the
-// MFMAs of step s run.  Before the last k step of tile r the wave waits for
-// its own copies of tile r + 1, meets the other waves at the barrier (after
-// which the stage of tile r is free: every wave has finished reading it),
-// reads the first fragments of tile r + 1 and then interleaves the copies
-// that refill stage r with the MFMAs of that last step.  The copies are
-// inline asm, so the compiler neither waits for them before LDS reads nor
-// edits the explicit waits; each wave issues copies for tiles 0 .. n +
-// STAGES - 2 (those past the K range read zeros or data no one uses, into
-// stages no one reads again), so the wait counts are constants.
+// The wave software-pipelines its fragments: those of k step s + 1 are read
+// while the MFMAs of step s run.  Before the last k step of tile r the wave
+// waits for its own copies of tile r + 1, meets the other waves at the
+// barrier (after which the stage of tile r is free: every wave has finished
+// reading it), reads the first fragments of tile r + 1, and then issues the
+// copies that refill stage r interleaved with its MFMAs, spread over that k
+// step and the first k step of the next tile.  The copies are inline asm, so
+// the compiler neither waits for them before LDS reads nor edits the explicit
+// waits; each wave issues copies for tiles 0 .. n + STAGES - 2 (those past
+// the K range re-read the last tile into a stage no one reads again), so the
+// wait counts are constants.
 //
 // LDS layout of one operand stage: [256 rows][BK k] bf16, the 16-byte chunk
 // c of row r stored at slot c ^ ((r / R) % C) with C = BK / 8 chunks per row
@@ -44,10 +49,10 @@ namespace kk {
 
 constexpr int BM = 256, BN = 256;
 #ifndef O5_KK_WAVES
-#define O5_KK_WAVES 4
+#define O5_KK_WAVES 8
 #endif
-// 4 waves (2 x 2) of 128 x 128, one per SIMD; or 8 waves (2 x 4) of 128 x 64,
-// two per SIMD
+// 8 waves (2 x 4) of 128 x 64, two per SIMD (default); or 4 waves (2 x 2) of
+// 128 x 128, one per SIMD
 constexpr int NWAVES = O5_KK_WAVES;
 constexpr int WM = 128, WN = NWAVES == 4 ? 128 : 64, WAVES_N = BN / WN, NT = NWAVES * 64;
 constexpr int MB = WM / 32, NB = WN / 32;
