@@ -25,9 +25,10 @@
 //    and the fragments of k-step kk+1 are read from LDS while the MFMAs of
 //    k-step kk run;
 //  * blocks are dealt round-robin to the 8 XCDs; each XCD gets a contiguous
-//    run of tiles ordered in groups of 8 M-tiles (M-tile fastest), so the
-//    ~32 blocks an XCD runs at once cover 8 M-tiles x 4 N-tiles and share
-//    both operands in that XCD's L2;
+//    run of tiles ordered in groups of kGroupM = 4 M-tiles (M-tile fastest),
+//    so the ~32 blocks an XCD runs at once cover 4 M-tiles x 8 N-tiles and
+//    share both operands in that XCD's L2 (4 measured faster than 8 or 16
+//    on the weight-gradient GEMM);
 //  * optional split-K over gridDim.z; split z writes its partial sums to
 //    its own slice (the caller reduces the slices in a fixed order).
 #pragma once
@@ -363,7 +364,10 @@ __global__ void __launch_bounds__(256) gemm_f32_fma(AL al, BL bl, Epi epi, int M
 
 // ------------------------------------------------------ bf16 MFMA engine
 
-constexpr int kGroupM = 8;
+#ifndef O5_GROUP_M
+#define O5_GROUP_M 4
+#endif
+constexpr int kGroupM = O5_GROUP_M;
 
 // Map the linear block id to a (tile_m, tile_n) pair.  Blocks are dealt
 // round-robin to the 8 XCDs, so each XCD first gets a contiguous run of

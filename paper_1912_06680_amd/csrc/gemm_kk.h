@@ -21,8 +21,9 @@
 // waits for its own copies of tile r + 1, meets the other waves at the
 // barrier (after which the stage of tile r is free: every wave has finished
 // reading it), reads the first fragments of tile r + 1, and then issues the
-// copies that refill stage r interleaved with its MFMAs, spread over that k
-// step and the first k step of the next tile.  The copies are inline asm, so
+// copies that refill stage r interleaved with its MFMAs (with SPREAD > 1
+// also over the first SPREAD - 1 k steps of the next tile; one step measured
+// best with two waves per SIMD, two steps with one).  The copies are inline asm, so
 // the compiler neither waits for them before LDS reads nor edits the explicit
 // waits; each wave issues copies for tiles 0 .. n + STAGES - 2 (those past
 // the K range re-read the last tile into a stage no one reads again), so the
@@ -40,7 +41,7 @@
 #define O5_KK_BK 64
 #endif
 #ifndef O5_KK_SPREAD
-#define O5_KK_SPREAD 2  // k steps over which a tile's copies are issued
+#define O5_KK_SPREAD 1  // k steps over which a tile's copies are issued
 #endif
 
 namespace o5 {
