@@ -252,6 +252,15 @@ __device__ __forceinline__ void wait_copies_n(int tiles_after) {
 }
 __device__ __forceinline__ void wait_copies(int tiles_after) { wait_copies_n<2 * COPIES>(tiles_after); }
 
+// s_waitcnt vmcnt(N) between scheduling barriers.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
 // Calls f(integral_constant<int, I>) for I = 0 .. N-1 (compile-time unroll).
 template <int I, int N, class F>
 __device__ __forceinline__ void unroll(F&& f) {

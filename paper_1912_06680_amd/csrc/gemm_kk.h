@@ -40,8 +40,8 @@
 #ifndef O5_KK_BK
 #define O5_KK_BK 64
 #endif
-#ifndef O5_KK_SPREAD
-#define O5_KK_SPREAD 1  // k steps over which a tile's copies are issued
+#ifndef O5_KK_RING
+#define O5_KK_RING 1
 #endif
 
 namespace o5 {
@@ -62,6 +62,12 @@ template <int BK>
 struct Cfg {
   static_assert(BK == 32 || BK == 64, "BK is 32 or 64");
   static constexpr int STAGES = BK == 64 ? 2 : 4;
+  // BK = 64 with O5_KK_RING: the operand tiles A_t, B_t take turns in one
+  // ring of 5 slots of 32 KB (A_t in slot 2t % 5, B_t in slot (2t + 1) % 5):
+  // the barrier of tile t frees the slots of A_t and B_t, which receive
+  // B_{t+2} and A_{t+3}, so about one and a half tiles are in flight
+  // instead of one, in all 160 KB of LDS
+  static constexpr bool RING = BK == 64 && O5_KK_RING;
   static constexpr int ROW_BYTES = BK * 2;
   static constexpr int CPR = BK / 8;                     // 16-byte chunks per row
   static constexpr int RPI = 1024 / ROW_BYTES;           // rows per 1 KB copy
@@ -69,7 +75,7 @@ struct Cfg {
   static constexpr int TILE_BYTES = 256 * ROW_BYTES;     // one operand, one stage
   static constexpr int NC = TILE_BYTES / 1024 / NWAVES;  // copies per wave per operand per tile
   static constexpr int KSTEPS = BK / 16;
-  static constexpr int SMEM = 2 * STAGES * TILE_BYTES;
+  static constexpr int SMEM = RING ? 5 * TILE_BYTES : 2 * STAGES * TILE_BYTES;
 };
 
 template <int BK>
@@ -177,26 +183,27 @@ __device__ __forceinline__ void mfma_all(const Frags& f, f32x16_t (&acc)[MB][NB]
     for (int b = 0; b < NB; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[a], f.b[b], acc[a][b], 0, 0, 0);
 }
 
-// The same MFMAs with copies [Q0, Q1) of the wave's 2 * NC copies of the
-// tile at k0 spread evenly among them (the order is pinned by scheduling
-// barriers).
-template <typename E, int BK, int Q0, int Q1>
+// The same MFMAs with the wave's copies of a B tile (k kb, LDS address bs)
+// and then an A tile (ka, as) spread evenly among them (the order is pinned
+// by scheduling barriers; the waits count on B's copies being older).
+template <typename E, int BK>
 __device__ __forceinline__ void mfma_copies(const Frags& f, f32x16_t (&acc)[MB][NB], const Tile<E, BK>& ta,
-                                            const Tile<E, BK>& tb, int k0, uint32_t as, uint32_t bs, int wave) {
+                                            const Tile<E, BK>& tb, int ka, uint32_t as, int kb, uint32_t bs,
+                                            int wave) {
   constexpr int NC = Cfg<BK>::NC;
-  constexpr int NQ = Q1 - Q0;
+  constexpr int NQ = 2 * NC;
   dma::unroll<0, MB * NB>([&](auto I) {
     constexpr int m = decltype(I)::value;
     constexpr int a = m / NB, b = m % NB;
     acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[a], f.b[b], acc[a][b], 0, 0, 0);
-    // copies after MFMA m: those q with floor(q * 16 / NQ) == m
-    dma::unroll<Q0, Q1>([&](auto J) {
+    // copies after MFMA m: those q with floor(q * MB * NB / NQ) == m
+    dma::unroll<0, NQ>([&](auto J) {
       constexpr int q = decltype(J)::value;
-      if constexpr ((q - Q0) * MB * NB / NQ == m) {
+      if constexpr (q * MB * NB / NQ == m) {
         if constexpr (q < NC)
-          ta.issue_one(k0, as, wave, q);
+          tb.issue_one(kb, bs, wave, q);
         else
-          tb.issue_one(k0, bs, wave, q - NC);
+          ta.issue_one(ka, as, wave, q - NC);
       }
     });
     __builtin_amdgcn_sched_barrier(0);
@@ -205,16 +212,15 @@ __device__ __forceinline__ void mfma_copies(const Frags& f, f32x16_t (&acc)[MB][
 
 }  // namespace kk
 
-template <int BK, int SPREAD, class Epi, typename E>
+template <int BK, class Epi, typename E>
 __global__ void __launch_bounds__(kk::NT, 1)
     gemm_kk(KRows2<E> al, KRows2<E> bl, Epi epi, int M, int N, int K, int ktiles_per_split) {
   using namespace kk;
   using C = Cfg<BK>;
-  constexpr int STAGES = C::STAGES, TB = C::TILE_BYTES, KS = C::KSTEPS;
-  constexpr int PER_TILE = 2 * C::NC;  // copies per wave per tile
+  constexpr int STAGES = C::STAGES, TB = C::TILE_BYTES, KS = C::KSTEPS, NC = C::NC;
+  constexpr bool RING = C::RING;
   static_assert(sizeof(E) == 2, "bf16 operands only");
   static_assert(KS % 2 == 0, "the fragment double buffer assumes an even number of k steps");
-  static_assert(SPREAD >= 1 && SPREAD < KS, "copies must land before the next barrier");
   constexpr int SMEM = Epi::kTileSmem > C::SMEM ? Epi::kTileSmem : C::SMEM;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
@@ -242,72 +248,76 @@ __global__ void __launch_bounds__(kk::NT, 1)
     Tile<E, BK> ta, tb;
     ta.init(al, m0, wave, lane);
     tb.init(bl, n0, wave, lane);
-    char* const sA = smem;
-    char* const sB = smem + STAGES * TB;
-    // the same stages as LDS byte addresses, for the copies' M0
-    const uint32_t lA = static_cast<uint32_t>(reinterpret_cast<size_t>((__attribute__((address_space(3))) char*)smem));
-    const uint32_t lB = lA + STAGES * TB;
+    // LDS byte offset of A_t and B_t (t relative to the split's first tile)
+    auto aoff = [&](int t) { return RING ? ((2 * t) % 5) * TB : (t % STAGES) * TB; };
+    auto boff = [&](int t) { return RING ? ((2 * t + 1) % 5) * TB : (STAGES + t % STAGES) * TB; };
+    // the same memory as an LDS address, for the copies' M0
+    const uint32_t l0 = static_cast<uint32_t>(reinterpret_cast<size_t>((__attribute__((address_space(3))) char*)smem));
+    auto copy_a = [&](int t) { ta.issue((kt0 + t) * BK, l0 + aoff(t), wave); };
+    auto copy_b = [&](int t) { tb.issue((kt0 + t) * BK, l0 + boff(t), wave); };
 
-    // prologue: tiles 0 .. STAGES-2 in flight; wait for tile 0; the last
-    // stage's tile; the first fragments
+    // Prologue.  Stages: tiles 0 .. STAGES-2, wait for tile 0, tile
+    // STAGES-1.  Ring: A0 B0 A1 B1 A2, wait for B0.  In both cases the copies
+    // still allowed in flight at every later wait are a fixed count: WAIT.
+    constexpr int WAIT = RING ? NC : (STAGES - 2) * 2 * NC;
+    if constexpr (RING) {
+      copy_a(0);
+      copy_b(0);
+      copy_a(1);
+      copy_b(1);
+      copy_a(2);
+      dma::wait_copies_n<NC>(3);
+      dma::wave_barrier();
+    } else {
 #pragma unroll
-    for (int st = 0; st < STAGES - 1; ++st) {
-      ta.issue((kt0 + st) * BK, lA + st * TB, wave);
-      tb.issue((kt0 + st) * BK, lB + st * TB, wave);
+      for (int t = 0; t < STAGES - 1; ++t) {
+        copy_a(t);
+        copy_b(t);
+      }
+      dma::wait_copies_n<2 * NC>(STAGES - 2);
+      dma::wave_barrier();
+      copy_a(STAGES - 1);
+      copy_b(STAGES - 1);
     }
-    dma::wait_copies_n<PER_TILE>(STAGES - 2);
-    dma::wave_barrier();
-    ta.issue((kt0 + STAGES - 1) * BK, lA + (STAGES - 1) * TB, wave);
-    tb.issue((kt0 + STAGES - 1) * BK, lB + (STAGES - 1) * TB, wave);
     Frags f[2];
-    read<BK>(sA, sB, wm0, wn0, lane, 0, f[0]);
+    read<BK>(smem + aoff(0), smem + boff(0), wm0, wn0, lane, 0, f[0]);
 
-    // tile r lives in stage r % STAGES.  The copies of tile r + STAGES into
-    // the stage freed at the barrier of iteration r are spread over the last
-    // k step of tile r and the first SPREAD - 1 k steps of tile r + 1, so the
-    // vector memory queue never holds a whole tile's copies at once.
-    constexpr int NQ = 2 * C::NC;
     for (int r = 0; r < n - 1; ++r) {
-      const int st = (r % STAGES) * TB;
-      const int nx = ((r + 1) % STAGES) * TB;
-      const int pst = ((r + STAGES - 1) % STAGES) * TB;   // stage being refilled since iteration r - 1
-      const int pk0 = (kt0 + r + STAGES - 1) * BK;        // and its tile
+      const int ao = aoff(r), bo = boff(r);
       // k steps 0 .. KS-2 of tile r, each with the next step's fragments in flight
       dma::unroll<0, KS - 1>([&](auto S) {
         constexpr int s = decltype(S)::value;
-        read<BK>(sA + st, sB + st, wm0, wn0, lane, s + 1, f[(s + 1) & 1]);
+        read<BK>(smem + ao, smem + bo, wm0, wn0, lane, s + 1, f[(s + 1) & 1]);
         __builtin_amdgcn_sched_group_barrier(0x100, MB + NB, 0);  // the LDS reads first
         __builtin_amdgcn_sched_group_barrier(0x008, MB * NB, 0);  // then the MFMAs
-        if constexpr (s + 1 < SPREAD) {
-          constexpr int q0 = (s + 1) * NQ / SPREAD, q1 = (s + 2) * NQ / SPREAD;
-          if (r > 0)
-            mfma_copies<E, BK, q0, q1>(f[s & 1], acc, ta, tb, pk0, lA + pst, lB + pst, wave);
-          else
-            mfma_all(f[s & 1], acc);
-        } else {
-          mfma_all(f[s & 1], acc);
-        }
+        mfma_all(f[s & 1], acc);
         __builtin_amdgcn_sched_barrier(0);
       });
-      // every wave done reading stage st; tile r + 1 landed
+      // every wave done reading tile r; tile r + 1 landed
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      dma::wait_copies_n<2 * C::NC>(STAGES - 2);
+      dma::vm_wait<WAIT>();
       dma::wave_barrier();
-      read<BK>(sA + nx, sB + nx, wm0, wn0, lane, 0, f[0]);
+      read<BK>(smem + aoff(r + 1), smem + boff(r + 1), wm0, wn0, lane, 0, f[0]);
       __builtin_amdgcn_sched_barrier(0);
-      // last k step of tile r; stage st starts refilling with tile r + STAGES
-      mfma_copies<E, BK, 0, NQ / SPREAD>(f[1], acc, ta, tb, (kt0 + r + STAGES) * BK, lA + st, lB + st, wave);
+      // last k step of tile r; the slots of tile r refill (stages: with tile
+      // r + STAGES; ring: with B_{r+2} and A_{r+3})
+      if constexpr (RING)
+        mfma_copies<E, BK>(f[1], acc, ta, tb, (kt0 + r + 3) * BK, l0 + aoff(r + 3), (kt0 + r + 2) * BK,
+                           l0 + boff(r + 2), wave);
+      else
+        mfma_copies<E, BK>(f[1], acc, ta, tb, (kt0 + r + STAGES) * BK, l0 + aoff(r + STAGES),
+                           (kt0 + r + STAGES) * BK, l0 + boff(r + STAGES), wave);
     }
     {
       // the last tile; its first fragments are in f[0]
-      const int st = ((n - 1) % STAGES) * TB;
+      const int ao = aoff(n - 1), bo = boff(n - 1);
       dma::unroll<0, KS>([&](auto S) {
         constexpr int s = decltype(S)::value;
-        if constexpr (s + 1 < KS) read<BK>(sA + st, sB + st, wm0, wn0, lane, s + 1, f[(s + 1) & 1]);
+        if constexpr (s + 1 < KS) read<BK>(smem + ao, smem + bo, wm0, wn0, lane, s + 1, f[(s + 1) & 1]);
         mfma_all(f[s & 1], acc);
       });
     }
-    dma::wait_copies_n<PER_TILE>(0);  // no copy outlives the loop
+    dma::vm_wait<0>();  // no copy outlives the loop
   }
 
   if constexpr (Epi::kTileSmem > 0) {
@@ -337,8 +347,7 @@ inline void launch_gemm_kk(const KRows2<E>& al, const KRows2<E>& bl, const Epi& 
   const int nkt = (K + BK - 1) / BK;
   const int kps = (nkt + splits - 1) / splits;
   const unsigned tiles = ((M + kk::BM - 1) / kk::BM) * ((N + kk::BN - 1) / kk::BN);
-  hipLaunchKernelGGL((gemm_kk<BK, O5_KK_SPREAD, Epi, E>), dim3(tiles, 1, splits), dim3(kk::NT), 0, s, al, bl, epi, M,
-                     N, K, kps);
+  hipLaunchKernelGGL((gemm_kk<BK, Epi, E>), dim3(tiles, 1, splits), dim3(kk::NT), 0, s, al, bl, epi, M, N, K, kps);
 }
 
 // Operands the buffer-load copies can take: K and the source split K0 whole
