@@ -17,6 +17,13 @@ Readings where the paper is silent:
 
 Layouts are time-major: x [T, B, D], h and c [T, B, H], gates [T, B, 4H].
 W_x is [4H, D] and W_h is [4H, H]: row g*H + j holds gate g of unit j.
+
+Optional ``store``: a rounding function (e.g. to bf16) applied where a
+reduced-precision implementation stores a tensor that a later product reads:
+the hidden state (fed back, returned, and used by the weight gradient), the
+saved gates, and the gate-gradient dG as an operand of the recurrent and
+weight-gradient products.  The cell state, the bias gradient and all
+arithmetic stay fp64.  Without it every value is fp64.
 """
 import numpy as np
 
@@ -38,12 +45,19 @@ def _keep(reset, t, B):
     return 1.0 - np.asarray(reset[t], dtype=np.float64).reshape(B, 1)
 
 
-def lstm_forward(x, Wx, Wh, b, h0, c0, reset=None):
+def _identity(a):
+    return a
+
+
+def lstm_forward(x, Wx, Wh, b, h0, c0, reset=None, store=None):
     """Run T steps of the LSTM.
 
     Returns (h [T,B,H], c [T,B,H], gates [T,B,4H]) where ``gates`` holds the
-    post-activation values (i, f, g, o) that backpropagation needs.
+    post-activation values (i, f, g, o) that backpropagation needs.  With
+    ``store``, h and the saved gates are stored through it (the cell state is
+    computed from the exact gates) and the recurrent input is the stored h.
     """
+    store = store or _identity
     x = np.asarray(x, np.float64)
     Wx = np.asarray(Wx, np.float64)
     Wh = np.asarray(Wh, np.float64)
@@ -53,7 +67,7 @@ def lstm_forward(x, Wx, Wh, b, h0, c0, reset=None):
     h = np.empty((T, B, H))
     c = np.empty((T, B, H))
     gates = np.empty((T, B, 4 * H))
-    h_prev = np.asarray(h0, np.float64)
+    h_prev = store(np.asarray(h0, np.float64))
     c_prev = np.asarray(c0, np.float64)
     for t in range(T):
         keep = _keep(reset, t, B)
@@ -65,14 +79,14 @@ def lstm_forward(x, Wx, Wh, b, h0, c0, reset=None):
         g = np.tanh(a[:, 2 * H:3 * H])
         o = sigmoid(a[:, 3 * H:4 * H])
         c[t] = f * c_tilde + i * g
-        h[t] = o * np.tanh(c[t])
-        gates[t] = np.concatenate([i, f, g, o], axis=1)
+        h[t] = store(o * np.tanh(c[t]))
+        gates[t] = store(np.concatenate([i, f, g, o], axis=1))
         h_prev, c_prev = h[t], c[t]
     return h, c, gates
 
 
 def lstm_bptt(x, Wx, Wh, h0, c0, reset, h, c, gates, dh, dhT=None, dcT=None,
-              want_dx=False):
+              want_dx=False, store=None):
     """Truncated BPTT through the T steps of ``lstm_forward``.
 
     The objective differentiated is
@@ -81,8 +95,13 @@ def lstm_bptt(x, Wx, Wh, h0, c0, reset, h, c, gates, dh, dhT=None, dcT=None,
     heads and ``dhT``/``dcT`` the gradient arriving at the final state.
     Nothing flows into h0 or c0.
 
+    With ``store``, h0 enters the weight gradient through it and the gate
+    gradient enters every product (dW, dx and the recurrent term) through it;
+    the bias gradient sums the exact gate gradient.
+
     Returns (dWx [4H,D], dWh [4H,H], db [4H], dx [T,B,D] or None).
     """
+    store = store or _identity
     x = np.asarray(x, np.float64)
     Wx = np.asarray(Wx, np.float64)
     Wh = np.asarray(Wh, np.float64)
@@ -97,7 +116,7 @@ def lstm_bptt(x, Wx, Wh, h0, c0, reset, h, c, gates, dh, dhT=None, dcT=None,
     dc_next = np.zeros((B, H)) if dcT is None else np.array(dcT, np.float64)
     for t in reversed(range(T)):
         keep = _keep(reset, t, B)
-        h_prev = np.asarray(h0, np.float64) if t == 0 else h[t - 1]
+        h_prev = store(np.asarray(h0, np.float64)) if t == 0 else h[t - 1]
         c_prev = np.asarray(c0, np.float64) if t == 0 else c[t - 1]
         h_tilde = keep * h_prev
         c_tilde = keep * c_prev
@@ -120,13 +139,14 @@ def lstm_bptt(x, Wx, Wh, h0, c0, reset, h, c, gates, dh, dhT=None, dcT=None,
                              dg * (1.0 - g * g),
                              do * o * (1.0 - o)], axis=1)      # [B, 4H]
 
-        dWx += da.T @ x[t]
-        dWh += da.T @ h_tilde
+        dab = store(da)
+        dWx += dab.T @ x[t]
+        dWh += dab.T @ h_tilde
         db += da.sum(axis=0)
         if want_dx:
-            dx[t] = da @ Wx
+            dx[t] = dab @ Wx
 
         # gradient into the carried state of step t-1; truncated at t = 0
-        dh_next = keep * (da @ Wh)
+        dh_next = keep * (dab @ Wh)
         dc_next = keep * dc_tilde
     return dWx, dWh, db, dx

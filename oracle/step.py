@@ -58,13 +58,14 @@ def ppo_step(params, x, h0, c0, rewards, dones, values, act, logp_old,
     Tn, B, _ = xx.shape
     H = Wh.shape[1]
 
-    h, c, gates = _lstm.lstm_forward(xx, Wx, Wh, b, h0, c0, reset)
+    store = round_to_bf16 if bf16 else None
+    h, c, gates = _lstm.lstm_forward(xx, Wx, Wh, b, h0, c0, reset, store=store)
     N = Tn * B
     stats, dh_rows, dWp, dbp, _ = _ppo.ppo_loss_grad(
         h.reshape(N, H), Wp, bp, act, logp_old, adv_s.reshape(N), ret_s.reshape(N),
         head_sizes, clip_eps, vf_coef, ent_coef, head_mask)
     dWx, dWh, db, _ = _lstm.lstm_bptt(xx, Wx, Wh, h0, c0, reset, h, c, gates,
-                                      dh_rows.reshape(Tn, B, H))
+                                      dh_rows.reshape(Tn, B, H), store=store)
     grads = {"Wx": dWx, "Wh": dWh, "b": db, "Wp": dWp, "bp": dbp}
 
     p = flatten(params)

@@ -57,6 +57,12 @@ CONFIGS = {
     "mid_bf16": Config("mid_bf16", B=256, T=16, D=1024, H=1024,
                        head_sizes=(30, 8, 32, 4), L=256, S=16, done_p=0.005,
                        state_std=0.1, dtype="bf16"),
+    # Large bf16 step, small enough for the fp64 oracle in seconds, large
+    # enough that the forward, recurrent and weight-gradient GEMMs all run on
+    # the 256 x 256 MFMA engine: 2048 samples of 2 steps = 64 segments of 64.
+    "big_bf16": Config("big_bf16", B=2048, T=2, D=2048, H=2048,
+                       head_sizes=(30, 8, 32, 4), L=64, S=64, done_p=0.01,
+                       state_std=0.1, dtype="bf16"),
     # Paper-scale LSTM forward + BPTT only.
     "lstm4096": Config("lstm4096", B=1024, T=16, D=4096, H=4096, state_std=0.1,
                        dtype="bf16"),

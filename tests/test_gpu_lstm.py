@@ -1,8 +1,9 @@
 """GPU parity: o5_lstm_fwd and o5_lstm_bptt against the fp64 oracle.
 
 fp32 path: every input fp32, tolerance 1e-4.  bf16 path: the oracle takes
-the bf16-rounded x, W_x, W_h; the GPU keeps h, the saved gates and dG in bf16
-and accumulates in fp32; tolerance 3e-2.  Shapes span several tiles with
+the bf16-rounded x, W_x, W_h and rounds h, the saved gates and dG where the
+GPU stores them in bf16 (the oracle's ``store``); both accumulate exactly or
+in fp32; tolerance 3e-2.  Shapes span several tiles with
 ragged edges in B and in the 4H / D+H dimensions, resets inside samples, and
 the paper-scale shape (B=1024, T=16, D=H=4096) on sampled rows.
 """
@@ -59,11 +60,12 @@ def _run_gpu(inp, T, B, D, H, bf16, with_final=True, want_dx=True):
 
 def _oracle(inp, bf16, with_final=True):
     rnd = round_to_bf16 if bf16 else (lambda a: np.asarray(a, np.float64))
+    store = round_to_bf16 if bf16 else None  # h, saved gates, dG as stored on the bf16 path
     x, Wx, Wh = rnd(inp["x"]), rnd(inp["Wx"]), rnd(inp["Wh"])
-    h, c, gates = lstm_forward(x, Wx, Wh, inp["b"], inp["h0"], inp["c0"], inp["reset"])
+    h, c, gates = lstm_forward(x, Wx, Wh, inp["b"], inp["h0"], inp["c0"], inp["reset"], store=store)
     dWx, dWh, db, dx = lstm_bptt(x, Wx, Wh, inp["h0"], inp["c0"], inp["reset"], h, c, gates, inp["dh"],
                                  inp["dhT"] if with_final else None, inp["dcT"] if with_final else None,
-                                 want_dx=True)
+                                 want_dx=True, store=store)
     return dict(h=h, c=c, gates=gates, dWx=dWx, dWh=dWh, db=db, dx=dx)
 
 

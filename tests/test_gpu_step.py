@@ -32,7 +32,7 @@ def _oracle_step(cfg, inp, beh, adam_state=None, step=1, params=None):
                     cfg.clip_k, step, bf16=cfg.dtype == "bf16")
 
 
-@pytest.mark.parametrize("name", ["tiny", "mid", "mid_bf16"])
+@pytest.mark.parametrize("name", ["tiny", "mid", "mid_bf16", "big_bf16"])
 def test_full_step_matches_oracle(name):
     need_gpu()
     cfg = synth.CONFIGS[name]

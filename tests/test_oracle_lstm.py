@@ -171,3 +171,30 @@ def test_bptt_truncation_no_gradient_into_start_state():
         outs.append(lstm_bptt(x, Wx, Wh, hh, c0, reset, h, c, gates, dh)[:3])
     for a, bb in zip(*outs):
         assert np.array_equal(a, bb)
+
+
+def test_store_rounds_at_the_storage_points():
+    """With store = bf16 rounding, h and the saved gates are bf16 values, the
+    recurrence reads the rounded h, and the cell state is built from the exact
+    gates."""
+    from oracle.bf16 import round_to_bf16
+    rng = np.random.default_rng(11)
+    T, B, D, H = 2, 3, 5, 4
+    x = rng.standard_normal((T, B, D))
+    Wx = rng.standard_normal((4 * H, D)) * 0.5
+    Wh = rng.standard_normal((4 * H, H)) * 0.5
+    b = rng.standard_normal(4 * H) * 0.1
+    h0 = rng.standard_normal((B, H)) * 0.3
+    c0 = rng.standard_normal((B, H)) * 0.3
+    h, c, gates = lstm_forward(x, Wx, Wh, b, h0, c0, store=round_to_bf16)
+    assert np.array_equal(round_to_bf16(h), h)
+    assert np.array_equal(round_to_bf16(gates), gates)
+    # step 1 by hand from the rounded h_0 and the exact c_0
+    a = x[1] @ Wx.T + h[0] @ Wh.T + b
+    sig = lambda v: 1.0 / (1.0 + np.exp(-v))
+    i, f, g, o = sig(a[:, :H]), sig(a[:, H:2 * H]), np.tanh(a[:, 2 * H:3 * H]), sig(a[:, 3 * H:])
+    np.testing.assert_allclose(c[1], f * c[0] + i * g, rtol=1e-14, atol=1e-15)
+    np.testing.assert_array_equal(h[1], round_to_bf16(o * np.tanh(c[1])))
+    # the first step reads the rounded h0
+    a0 = x[0] @ Wx.T + round_to_bf16(h0) @ Wh.T + b
+    np.testing.assert_array_equal(gates[0][:, :H], round_to_bf16(sig(a0[:, :H])))
