@@ -279,7 +279,7 @@ static PpoWs ppo_ws(o5_dtype dt, int N, int H, int A1) {
   w.dwp_t = bf && w.A1p <= 128;
   w.plan_z = plan_gemm(bf, N, A1, H);
   w.plan_w = bf ? plan_gemm(true, A1, H, 2 * N) : plan_gemm(false, A1, H, N);
-  w.plan_h = bf ? plan_gemm(true, N, H, 2 * w.A1p) : GemmPlan{false, BfTile::k128x128, 1};
+  w.plan_h = bf ? plan_gemm(true, N, H, 2 * w.A1p) : GemmPlan{false, BfTile::k128x128, 1, 256};
   w.plan_h.splits = 1;
   w.wsplits = 1;
   if (w.dwp_t) {
