@@ -216,7 +216,80 @@ def cpu_baseline(cfg, target_s=15.0):
     return {"value": sub.B * sub.T / dt, "unit": "timesteps/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{sub.B} samples x T={sub.T} (D=H={sub.H}, heads {tuple(sub.head_sizes)}, each sample "
                       f"its own GAE segment), one full step of the fp64 NumPy oracle incl. Adam over all "
-                      f"{synth.n_params(sub)} params, {dt:.2f} s"}
+                      f"{synth.n_params(sub)} params, {dt:.2f} s on {cpu_model()}"}
+
+
+def hbm_kernels(cfg, reps=20, warm=3):
+    """The HBM-bound kernels on their own, at the sizes their bandwidth is
+    judged on: GAE over L=256-step segments at S = 128 (the step's size,
+    latency-bound), 11,520 (the paper's 2.9M-timestep batch) and 131,072
+    (33.5M timesteps, beyond the 256 MB infinity cache); Adam at the step's
+    parameter count and at 158,502,815.  Each is timed with events on the
+    launch stream, median of `reps` after `warm` untimed calls, cold (a
+    512 MB buffer written before every call) and warm."""
+    import torch
+    from paper_1912_06680_amd import o5, synth
+    dev = "cuda"
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(0)
+    flush = torch.empty(128 << 20, dtype=torch.float32, device=dev)
+
+    def timed(fn, cold):
+        ts = []
+        for i in range(warm + reps):
+            if cold:
+                flush.fill_(float(i))
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            if i >= warm:
+                ts.append(e0.elapsed_time(e1) * 1e3)
+        return float(np.median(ts))
+
+    def entry(kernel, size, nbytes, fn):
+        cold, hot = timed(fn, True), timed(fn, False)
+        return {"kernel": kernel, "size": size, "bytes": int(nbytes), "cold_us": round(cold, 2),
+                "warm_us": round(hot, 2), "cold_gbs": round(nbytes / cold * 1e-3, 1),
+                "frac_hbm_peak_cold": round(nbytes / cold * 1e-3 / PEAK_HBM_GBS, 4)}
+
+    out = []
+    L = 256
+    for S in (cfg.S, 11520, 131072):
+        r = torch.randn((L, S), generator=gen, device=dev)
+        v = torch.randn((L + 1, S), generator=gen, device=dev)
+        done = (torch.rand((L, S), generator=gen, device=dev) < 0.002).to(torch.uint8)
+        adv = torch.empty((L, S), device=dev)
+        ret = torch.empty((L, S), device=dev)
+        out.append(entry("gae", f"L={L} S={S}", 17 * L * S + 4 * S,
+                         lambda: o5.o5_gae(L, S, r, v, done, cfg.gamma, cfg.lam, adv, ret)))
+        del r, v, done, adv, ret
+    for n in (synth.n_params(cfg), 158502815):
+        p = torch.randn(n, generator=gen, device=dev) * 0.02
+        g = torch.randn(n, generator=gen, device=dev) * 1e-3
+        m = g * 0.1
+        v = g * g
+        pb = torch.empty(n, dtype=torch.bfloat16, device=dev)
+        out.append(entry("adam_step", f"n={n}", 30 * n,
+                         lambda: o5.o5_adam_step(n, p, m, v, g, pb, cfg.lr, cfg.beta1, cfg.beta2, cfg.adam_eps,
+                                                 cfg.clip_k, 10)))
+        del p, g, m, v, pb
+    del flush
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown CPU"
 
 
 def main():
@@ -226,6 +299,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="full4096")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-hbm-kernels", action="store_true",
+                    help="skip the standalone GAE / Adam bandwidth measurements")
     ap.add_argument("--copy-ref", action="store_true",
                     help="after timing, run one conversion of 2^26 fp32 elements (counter scale reference)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -319,6 +394,11 @@ def main():
     step_flop = 2.0 * T * B * 4 * H * (D + H) + 2.0 * 4 * H * ((T - 1) * B * H + T * B * H + T * B * D) + \
         3 * 2.0 * T * B * A1 * H
 
+    hbm = None
+    if not args.no_hbm_kernels:
+        log("standalone HBM-bound kernels (GAE, Adam), cold and warm")
+        hbm = hbm_kernels(cfg)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
@@ -339,6 +419,7 @@ def main():
         "lstm_gemm_tflops": round(lstm_gemm_tflops, 2),
         "step_tflops": round(step_flop / (ms_step * 1e-3) / 1e12, 2),
         "kernels": kernels,
+        "hbm_kernels": hbm,
         "loss_stats": [round(s, 6) for s in stats],
     }
     print(json.dumps(out), flush=True)

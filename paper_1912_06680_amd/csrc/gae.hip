@@ -3,15 +3,22 @@
 // "Timescales and Staleness").
 //
 // GAE is the reverse linear recurrence  A_t = delta_t + c_t A_{t+1}  with
-// c_t = gamma lambda (1 - done_t) and A_L = 0.  Two kernels:
-//  * lane per segment (large S): each lane walks its segment backwards;
-//    at every step a wave reads 64 consecutive segments, so every load and
-//    store is coalesced and the kernel streams at HBM rate.
-//  * wave per segment (small S): the 64 lanes of a wave split the segment
-//    into 64 chunks, reduce each chunk to an affine map A_in -> alpha + beta
-//    A_in, combine the maps with a wavefront suffix scan (shuffles), then
-//    replay their chunk from the correct carry-in.  This cuts the serial
-//    dependency from L to L/64 + log2(64) steps.
+// c_t = gamma lambda (1 - done_t) and A_L = 0.  A stretch of steps reduces
+// to an affine map A_in -> alpha + beta A_in of the advantage arriving from
+// its end, and maps compose, so a segment can be cut into chunks that are
+// reduced in parallel, combined, and replayed from their carry-in.  Three
+// kernels:
+//  * wave per segment (S <= 4096): the 64 lanes of a wave take 64 chunks of
+//    one segment and combine their maps with a wavefront suffix scan
+//    (shuffles): L/64 + log2(64) dependent steps;
+//  * chunked lanes (S > 4096, L <= 256): lane = segment, wave = one of 8
+//    chunks of at most 32 steps, kept in registers between the reduce and
+//    the replay; the 8 maps of a segment combine through LDS.  A wave reads
+//    64 consecutive segments at each step (coalesced), every input is read
+//    once, and a block of 8 waves covers 64 segments, so 11,520 segments
+//    (the paper's batch) already give 1,440 waves;
+//  * lane per segment (longer segments): each lane walks its whole segment
+//    backwards, coalesced as above.
 #include "common.h"
 
 namespace o5 {
@@ -40,6 +47,7 @@ __global__ void __launch_bounds__(256) gae_lane_per_segment(int L, int S, const 
       vv[u] = v[idx];
       dd[u] = done[idx];
     }
+    __builtin_amdgcn_sched_barrier(0);  // keep every load of the chunk ahead of the recurrence
 #pragma unroll
     for (int u = 0; u < kGaeLaneUnroll; ++u) {
       const float nd = dd[u] ? 0.0f : 1.0f;
@@ -61,6 +69,131 @@ __global__ void __launch_bounds__(256) gae_lane_per_segment(int L, int S, const 
     adv[idx] = carry;
     ret[idx] = carry + vt;
     vnext = vt;
+  }
+}
+
+constexpr int kGaeChunks = 8;      // waves per block = chunks per segment
+constexpr int kGaeChunkMax = 32;   // steps per chunk (so L <= 256)
+
+// Lane = segment (64 per block), wave c = chunk c of ceil(L / 8) steps.
+__global__ void __launch_bounds__(kGaeChunks * 64) gae_chunked(int L, int S, const float* __restrict__ r,
+                                                               const float* __restrict__ v,
+                                                               const uint8_t* __restrict__ done, float gamma,
+                                                               float gl, float* __restrict__ adv,
+                                                               float* __restrict__ ret) {
+  __shared__ float map_a[kGaeChunks][64], map_b[kGaeChunks][64];
+  const int lane = threadIdx.x & 63;
+  const int c = threadIdx.x >> 6;
+  const int s = blockIdx.x * 64 + lane;
+  const bool live = s < S;
+  const size_t S_ = static_cast<size_t>(S);
+  const int q = (L + kGaeChunks - 1) / kGaeChunks;  // <= kGaeChunkMax (checked on the host)
+  const int t0 = c * q;
+  const int t1 = min(t0 + q, L);
+  // the chunk's inputs, all requests in flight at once
+  float rr[kGaeChunkMax], vv[kGaeChunkMax], nd[kGaeChunkMax];
+#pragma unroll
+  for (int u = 0; u < kGaeChunkMax; ++u) {
+    rr[u] = 0.0f;
+    vv[u] = 0.0f;
+    nd[u] = 1.0f;
+    if (live && t0 + u < t1) {
+      const size_t idx = static_cast<size_t>(t0 + u) * S_ + s;
+      rr[u] = r[idx];
+      vv[u] = v[idx];
+      nd[u] = done[idx] ? 0.0f : 1.0f;
+    }
+  }
+  const float v_end = (live && t0 < t1) ? v[static_cast<size_t>(t1) * S_ + s] : 0.0f;  // V(t1); row L bootstraps
+  // reduce: A(t0) = alpha + beta A(t1)
+  float alpha = 0.0f, beta = 1.0f, vn = v_end;
+#pragma unroll
+  for (int u = kGaeChunkMax - 1; u >= 0; --u) {
+    if (t0 + u < t1) {
+      const float delta = rr[u] + gamma * nd[u] * vn - vv[u];
+      const float k = gl * nd[u];
+      alpha = delta + k * alpha;
+      beta = k * beta;
+      vn = vv[u];
+    }
+  }
+  map_a[c][lane] = alpha;
+  map_b[c][lane] = beta;
+  __syncthreads();
+  // carry-in A(t1): the maps of the later chunks applied to A_L = 0
+  float carry = 0.0f;
+  for (int k = kGaeChunks - 1; k > c; --k) carry = map_a[k][lane] + map_b[k][lane] * carry;
+  // replay from the carry-in
+  vn = v_end;
+#pragma unroll
+  for (int u = kGaeChunkMax - 1; u >= 0; --u) {
+    if (t0 + u < t1) {
+      const float delta = rr[u] + gamma * nd[u] * vn - vv[u];
+      carry = delta + gl * nd[u] * carry;
+      if (live) {
+        const size_t idx = static_cast<size_t>(t0 + u) * S_ + s;
+        adv[idx] = carry;
+        ret[idx] = carry + vv[u];
+      }
+      vn = vv[u];
+    }
+  }
+}
+
+// Lane = 4 consecutive segments (16-byte loads and stores: a wave moves 1 KB
+// of a row per instruction), walking backwards in chunks of kGaeLaneUnroll
+// steps whose loads are all issued before the recurrence runs.  S % 4 == 0.
+__global__ void __launch_bounds__(64) gae_lane4(int L, int S, const float* __restrict__ r,
+                                                const float* __restrict__ v, const uint8_t* __restrict__ done,
+                                                float gamma, float gl, float* __restrict__ adv,
+                                                float* __restrict__ ret) {
+  const int g = blockIdx.x * blockDim.x + threadIdx.x;  // segments 4g .. 4g + 3
+  const size_t S4 = static_cast<size_t>(S) / 4;
+  if (static_cast<size_t>(g) >= S4) return;
+  const float4* r4 = reinterpret_cast<const float4*>(r);
+  const float4* v4 = reinterpret_cast<const float4*>(v);
+  const uchar4* d4 = reinterpret_cast<const uchar4*>(done);
+  float4* a4 = reinterpret_cast<float4*>(adv);
+  float4* q4 = reinterpret_cast<float4*>(ret);
+  float cy[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  const float4 vl = v4[static_cast<size_t>(L) * S4 + g];
+  float vn[4] = {vl.x, vl.y, vl.z, vl.w};
+  auto step = [&](size_t idx, const float4& rq, const float4& vq, const uchar4& dq) {
+    const float rs[4] = {rq.x, rq.y, rq.z, rq.w};
+    const float vs[4] = {vq.x, vq.y, vq.z, vq.w};
+    const uint8_t ds[4] = {dq.x, dq.y, dq.z, dq.w};
+    float ao[4], ro[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float nd = ds[k] ? 0.0f : 1.0f;
+      const float delta = rs[k] + gamma * nd * vn[k] - vs[k];
+      cy[k] = delta + gl * nd * cy[k];
+      ao[k] = cy[k];
+      ro[k] = cy[k] + vs[k];
+      vn[k] = vs[k];
+    }
+    a4[idx] = make_float4(ao[0], ao[1], ao[2], ao[3]);
+    q4[idx] = make_float4(ro[0], ro[1], ro[2], ro[3]);
+  };
+  int t_hi = L - 1;
+  while (t_hi + 1 >= kGaeLaneUnroll) {
+    float4 rr[kGaeLaneUnroll], vv[kGaeLaneUnroll];
+    uchar4 dd[kGaeLaneUnroll];
+#pragma unroll
+    for (int u = 0; u < kGaeLaneUnroll; ++u) {
+      const size_t idx = static_cast<size_t>(t_hi - u) * S4 + g;
+      rr[u] = r4[idx];
+      vv[u] = v4[idx];
+      dd[u] = d4[idx];
+    }
+    __builtin_amdgcn_sched_barrier(0);  // keep every load of the chunk ahead of the recurrence
+#pragma unroll
+    for (int u = 0; u < kGaeLaneUnroll; ++u) step(static_cast<size_t>(t_hi - u) * S4 + g, rr[u], vv[u], dd[u]);
+    t_hi -= kGaeLaneUnroll;
+  }
+  for (; t_hi >= 0; --t_hi) {
+    const size_t idx = static_cast<size_t>(t_hi) * S4 + g;
+    step(idx, r4[idx], v4[idx], d4[idx]);
   }
 }
 
@@ -139,8 +272,11 @@ __global__ void __launch_bounds__(256) segments_to_samples_kernel(int L, int S, 
 
 using namespace o5;
 
-// Segments per launch below which the wave-per-segment scan is used.
+// Segments per launch up to which the wave-per-segment scan is used, and
+// below which the chunked-lane kernel is (above it there are enough lanes
+// for one per segment, and 16-byte accesses stream better).
 static constexpr int kGaeWaveScanMaxS = 4096;
+static constexpr int kGaeChunkedMaxS = 32768;
 
 extern "C" int o5_gae(int L, int S, const float* r, const float* v, const uint8_t* done, float gamma,
                       float lambda, float* adv, float* ret, void* stream) {
@@ -158,6 +294,13 @@ extern "C" int o5_gae(int L, int S, const float* r, const float* v, const uint8_
   if (S <= kGaeWaveScanMaxS) {
     hipLaunchKernelGGL(gae_wave_per_segment, dim3((S + 3) / 4), dim3(256), 0, as_stream(stream), L, S,
                        r, v, done, gamma, gl, adv, ret);
+  } else if (S < kGaeChunkedMaxS && L <= kGaeChunks * kGaeChunkMax) {
+    hipLaunchKernelGGL(gae_chunked, dim3((S + 63) / 64), dim3(kGaeChunks * 64), 0, as_stream(stream), L, S, r, v,
+                       done, gamma, gl, adv, ret);
+  } else if (S % 4 == 0 && aligned16(r) && aligned16(v) && aligned16(adv) && aligned16(ret) &&
+             reinterpret_cast<uintptr_t>(done) % 4 == 0) {
+    hipLaunchKernelGGL(gae_lane4, dim3((S / 4 + 63) / 64), dim3(64), 0, as_stream(stream), L, S, r, v, done,
+                       gamma, gl, adv, ret);
   } else {
     hipLaunchKernelGGL(gae_lane_per_segment, dim3((S + 255) / 256), dim3(256), 0, as_stream(stream), L,
                        S, r, v, done, gamma, gl, adv, ret);
