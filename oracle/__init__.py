@@ -17,6 +17,9 @@ method computes, written so that it can be checked against the paper by eye:
                 and entropy bonus, with gradients (subsection "Optimizing the
                 Policy"; appendix "Exploration", subsection "Loss function";
                 appendix "Neural Network Architecture").
+* ``reward`` -- reward post-processing ahead of GAE: game time weighting,
+                team spirit, zero sum, normalisation by a running standard
+                deviation (appendix "Reward Weights"; Table "Hyperparameters").
 * ``adam``   -- Adam with the per-parameter gradient clip to +-5 sqrt(v)
                 (subsection "Optimizing the Policy"; Table "Hyperparameters").
 * ``philox`` -- Philox4x64-10 counter-based generator and Gumbel-max action
