@@ -223,8 +223,9 @@ def hbm_kernels(cfg, reps=20, warm=3):
     """The HBM-bound kernels on their own, at the sizes their bandwidth is
     judged on: GAE over L=256-step segments at S = 128 (the step's size,
     latency-bound), 11,520 (the paper's 2.9M-timestep batch) and 131,072
-    (33.5M timesteps, beyond the 256 MB infinity cache); Adam at the step's
-    parameter count and at 158,502,815.  Each is timed with events on the
+    (33.5M timesteps, beyond the 256 MB infinity cache); the reward
+    post-processing ahead of GAE at 1,152 and 13,107 games of ten heroes;
+    Adam at the step's parameter count and at 158,502,815.  Each is timed with events on the
     launch stream, median of `reps` after `warm` untimed calls, cold (a
     512 MB buffer written before every call) and warm."""
     import torch
@@ -266,6 +267,15 @@ def hbm_kernels(cfg, reps=20, warm=3):
         out.append(entry("gae", f"L={L} S={S}", 17 * L * S + 4 * S,
                          lambda: o5.o5_gae(L, S, r, v, done, cfg.gamma, cfg.lam, adv, ret)))
         del r, v, done, adv, ret
+    for G in (1152, 13107):   # 11,520 and 131,070 segments: 5v5 games
+        ri = synth.reward_inputs(L, G, seed=G)
+        sh, oc, gt = (torch.from_numpy(ri[k]).to(dev) for k in ("shaped", "outcome", "game_time"))
+        stats = torch.zeros(3, dtype=torch.float64, device=dev)
+        rr = torch.empty((L, 10 * G), device=dev)
+        rws = torch.empty(max(o5.o5_reward_process_workspace_bytes(L, G), 256), dtype=torch.uint8, device=dev)
+        out.append(entry("reward_process", f"L={L} G={G} (S={10 * G})", 12 * L * 10 * G + 4 * L * G,
+                         lambda: o5.o5_reward_process(L, G, sh, oc, gt, 0.3, 0.6, 10.0, 1e-8, stats, rr, rws)))
+        del sh, oc, gt, stats, rr, rws
     for n in (synth.n_params(cfg), 158502815):
         p = torch.randn(n, generator=gen, device=dev) * 0.02
         g = torch.randn(n, generator=gen, device=dev) * 1e-3

@@ -147,6 +147,48 @@ int o5_gae(int L, int S, const float* r, const float* v, const uint8_t* done,
            float gamma, float lambda, float* adv, float* ret, void* stream);
 
 /* ------------------------------------------------------------------------
+ * o5_reward_process -- the reward post-processing ahead of GAE (appendix
+ * "Reward Weights": zero sum, game time weighting, team spirit; Table
+ * "Hyperparameters": rewards are normalised by a running estimate of their
+ * standard deviation).  G games of two teams of five heroes; hero h of team
+ * k in game g is segment s = 10 g + 5 k + h of the [L, S] layout that
+ * o5_gae reads (S = 10 G).  For step t of game g and hero i of team A
+ * (enemy team B):
+ *
+ *   rho_i = shaped_i * decay_base^(game_time / decay_minutes) + outcome_i
+ *   z_i   = (1 - tau) rho_i + tau mean_{j in A} rho_j - mean_{j in B} rho_j
+ *   r_i   = z_i / sqrt(var + eps)
+ *
+ * (team spirit mixes each hero's reward with its team's mean; the zero-sum
+ * step subtracts the enemies' mean, which team spirit leaves unchanged).
+ * var is the variance of every z seen so far: the running summary `stats`
+ * = (count, mean, M2), M2 the sum of squared deviations from the mean, is
+ * merged with this call's values (fp64, fixed order) and written back
+ * before r is formed.  Start from stats = (0, 0, 0).
+ *
+ * L, G      >= 1, 10 L G < 2^31.
+ * shaped    [L, S] fp32 raw shaped rewards.   outcome: [L, S] fp32 win/loss
+ *           reward, not time-weighted, or NULL (= 0).   game_time: [L, G]
+ *           fp32, minutes since the game began.
+ * hp        tau in [0, 1] (0.3 in the paper's baseline); 0 < decay_base <= 1
+ *           (0.6); decay_minutes > 0 (10); eps > 0 (1e-8).
+ * stats     [3] fp64, updated in place.
+ * r         out [L, S] fp32 (no overlap with the inputs).
+ * ws        scratch of o5_reward_process_workspace_bytes(L, G) bytes.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  float tau;           /* team spirit */
+  float decay_base;    /* 0.6 */
+  float decay_minutes; /* 10 */
+  float eps;           /* 1e-8 */
+} o5_reward_hp;
+
+size_t o5_reward_process_workspace_bytes(int L, int G);
+int o5_reward_process(int L, int G, const float* shaped, const float* outcome,
+                      const float* game_time, o5_reward_hp hp, double* stats,
+                      float* r, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * o5_segments_to_samples -- cut each of S segments of L steps into L/T
  * samples of T steps, the unit truncated BPTT runs on (Figure "Timescales
  * and Staleness": a segment is subdivided into samples of 16 policy
@@ -272,7 +314,8 @@ int o5_f32_to_bf16(size_t n, const float* src, uint16_t* dst, void* stream);
  * and returns the summed device time in milliseconds and the number of
  * launches.  Sites: 0 lstm_fwd_gemm, 1 lstm_fwd_cell, 2 lstm_dh_gemm,
  * 3 lstm_bwd_cell, 4 lstm_dw_gemm, 5 lstm_dx_gemm, 6 ppo_loss_grad (whole
- * call), 7 adam_step, 8 gae, 9 policy_sample (whole call).
+ * call), 7 adam_step, 8 gae, 9 policy_sample (whole call), 10
+ * reward_process (whole call).
  * o5_ktimer_site_name returns the site's name ("" if out of range).
  * ------------------------------------------------------------------------ */
 int o5_ktimer_enable(int on);

@@ -60,6 +60,7 @@ enum KSite {
   kSiteAdam,
   kSiteGae,
   kSiteSample,
+  kSiteReward,
   kSiteCount
 };
 // When timing is on, record an event on `s` before / after a launch site.

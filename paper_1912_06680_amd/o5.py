@@ -24,6 +24,7 @@ EXPORTED = (
     "o5_lstm_fwd_workspace_bytes", "o5_lstm_fwd",
     "o5_lstm_bptt_workspace_bytes", "o5_lstm_bptt",
     "o5_gae", "o5_segments_to_samples",
+    "o5_reward_process_workspace_bytes", "o5_reward_process",
     "o5_ppo_loss_grad_workspace_bytes", "o5_ppo_loss_grad",
     "o5_adam_step",
     "o5_policy_sample_workspace_bytes", "o5_policy_sample",
@@ -32,7 +33,7 @@ EXPORTED = (
 )
 
 KTIMER_SITES = ("lstm_fwd_gemm", "lstm_fwd_cell", "lstm_dh_gemm", "lstm_bwd_cell", "lstm_dw_gemm",
-                "lstm_dx_gemm", "ppo_loss_grad", "adam_step", "gae", "policy_sample")
+                "lstm_dx_gemm", "ppo_loss_grad", "adam_step", "gae", "policy_sample", "reward_process")
 
 
 class O5Error(RuntimeError):
@@ -48,6 +49,11 @@ class PpoHp(ctypes.Structure):
 class AdamHp(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
                 ("eps", ctypes.c_float), ("clip_k", ctypes.c_float)]
+
+
+class RewardHp(ctypes.Structure):
+    _fields_ = [("tau", ctypes.c_float), ("decay_base", ctypes.c_float), ("decay_minutes", ctypes.c_float),
+                ("eps", ctypes.c_float)]
 
 
 _vp = ctypes.c_void_p
@@ -66,6 +72,8 @@ _SIGS = {
     "o5_lstm_bptt": (_i, [_i, _i, _i, _i, _i] + [_vp] * 17 + [_sz, _vp]),
     "o5_gae": (_i, [_i, _i, _vp, _vp, _vp, _f, _f, _vp, _vp, _vp]),
     "o5_segments_to_samples": (_i, [_i, _i, _i] + [_vp] * 6 + [_vp]),
+    "o5_reward_process_workspace_bytes": (_sz, [_i, _i]),
+    "o5_reward_process": (_i, [_i, _i, _vp, _vp, _vp, RewardHp, _vp, _vp, _vp, _sz, _vp]),
     "o5_ppo_loss_grad_workspace_bytes": (_sz, [_i, _i, _i, _i, _vp]),
     "o5_ppo_loss_grad": (_i, [_i, _i, _i, _i, _vp] + [_vp] * 8 + [PpoHp] + [_vp] * 5 + [_sz, _vp]),
     "o5_adam_step": (_i, [_sz, _vp, _vp, _vp, _vp, _vp, AdamHp, _i, _vp]),
@@ -174,6 +182,18 @@ def o5_gae(L, S, r, v, done, gamma, lam, adv, ret, stream=None):
 def o5_segments_to_samples(L, S, T, adv, ret, done, adv_s, ret_s, reset, stream=None):
     _check("o5_segments_to_samples", lib().o5_segments_to_samples(
         L, S, T, _p(adv), _p(ret), _p(done), _p(adv_s), _p(ret_s), _p(reset), _stream(stream)))
+
+
+def o5_reward_process_workspace_bytes(L, G):
+    return lib().o5_reward_process_workspace_bytes(L, G)
+
+
+def o5_reward_process(L, G, shaped, outcome, game_time, tau, decay_base, decay_minutes, eps, stats, r, ws,
+                      stream=None):
+    wp, wn = _ws(ws)
+    hp = RewardHp(tau, decay_base, decay_minutes, eps)
+    _check("o5_reward_process", lib().o5_reward_process(L, G, _p(shaped), _p(outcome), _p(game_time), hp,
+                                                        _p(stats), _p(r), wp, wn, _stream(stream)))
 
 
 def o5_ppo_loss_grad_workspace_bytes(dt, N, H, head_sizes):

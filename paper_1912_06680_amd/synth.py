@@ -142,3 +142,24 @@ def uniform_ints(rng, shape, highs):
     """Integers in [0, highs[k]) along the last axis (e.g. actions per head)."""
     cols = [rng.integers(0, int(h), size=shape) for h in highs]
     return np.stack(cols, axis=-1).astype(np.int32)
+
+
+# Minutes of game time per policy step: the game runs at 30 frames per
+# second and the agent acts on every fourth frame (section "Dota 2"; section
+# "Training System", subsection "Playing Dota using AI").
+STEP_MINUTES = 4.0 / 30.0 / 60.0
+
+
+def reward_inputs(L: int, G: int, seed: int = 0, outcome_p: float = 0.01) -> dict:
+    """Raw rewards of G games of two teams of five over L steps, drawn in this
+    order: shaped [L, 10G] ~ N(0, 1); outcome [L, 10G], +-1 with probability
+    outcome_p each (else 0); the game minute at which each segment starts,
+    U(0, 60) per game, from which game_time [L, G] advances STEP_MINUTES per
+    step.  float32."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    shaped = _normal(rng, (L, 10 * G))
+    u = rng.random((L, 10 * G))
+    outcome = np.where(u < outcome_p, 1.0, np.where(u < 2 * outcome_p, -1.0, 0.0)).astype(np.float32)
+    start = rng.random(G) * 60.0
+    game_time = (start[None, :] + STEP_MINUTES * np.arange(L)[:, None]).astype(np.float32)
+    return {"shaped": shaped, "outcome": outcome, "game_time": game_time}

@@ -59,6 +59,18 @@ def test_host_validation_errors(lib):
     need = L.o5_lstm_fwd_workspace_bytes(1, 16, 8, 64, 128)
     assert need > 0
     assert L.o5_lstm_fwd(1, 16, 8, 64, 128, *([16] * 11), need - 1, None) == 5
+    # reward post-processing: shapes, argument ranges, workspace
+    rhp = o5.RewardHp(0.3, 0.6, 10.0, 1e-8)
+    assert L.o5_reward_process(0, 4, 16, None, 16, rhp, 16, 16, 16, 1 << 20, None) == 2
+    assert L.o5_reward_process(4, 4, 16, None, None, rhp, 16, 16, 16, 1 << 20, None) == 1
+    assert L.o5_reward_process(4, 4, 16, 0x1008, 16, rhp, 16, 16, 16, 1 << 20, None) == 4
+    assert L.o5_reward_process(4, 4, 16, None, 16, o5.RewardHp(1.5, 0.6, 10.0, 1e-8), 16, 16, 16, 1 << 20,
+                               None) == 7
+    assert L.o5_reward_process(4, 4, 16, None, 16, o5.RewardHp(0.3, 0.6, 0.0, 1e-8), 16, 16, 16, 1 << 20,
+                               None) == 7
+    need = L.o5_reward_process_workspace_bytes(4, 4)
+    assert need > 0
+    assert L.o5_reward_process(4, 4, 16, None, 16, rhp, 16, 16, 16, need - 1, None) == 5
     # heads
     heads = (ctypes.c_int * 2)(3, 0)
     assert L.o5_ppo_loss_grad_workspace_bytes(0, 8, 64, 2, heads) == 0
@@ -71,6 +83,8 @@ def test_workspace_queries_are_positive(lib):
         assert o5.o5_lstm_bptt_workspace_bytes(dt, 16, 2048, 4096, 4096) > 0
         assert o5.o5_ppo_loss_grad_workspace_bytes(dt, 32768, 4096, (30, 8, 32, 4)) > 0
         assert o5.o5_policy_sample_workspace_bytes(dt, 4096, 4096, (30, 8, 32, 4)) > 0
+    assert o5.o5_reward_process_workspace_bytes(256, 13107) > 0
+    assert o5.o5_reward_process_workspace_bytes(0, 1) == 0
 
 
 def test_binding_arity_matches_header():
