@@ -207,12 +207,15 @@ def cpu_baseline(cfg, target_s=15.0):
                  sub.beta1, sub.beta2, sub.adam_eps, sub.clip_k, 1, bf16=sub.dtype == "bf16")
         return time.perf_counter() - t0, sub
 
-    nb = 4
-    dt, sub = run(nb)
-    if dt < target_s / 3:
-        nb = int(max(nb, min(cfg.B, round(nb * target_s / dt))))
-        if nb > 4:
-            dt, sub = run(nb)
+    # the step has a fixed part (Adam over every parameter) and a part linear
+    # in the samples: two small runs give both, the third is sized to target_s
+    dt1, _ = run(2)
+    dt2, sub = run(6)
+    dt = dt2
+    per = max((dt2 - dt1) / 4, 0.02 * dt2 / 6)   # floor against timing noise
+    nb = int(min(cfg.B, 256, max(6, round(6 + (target_s - dt2) / per))))
+    if nb > 6:
+        dt, sub = run(nb)
     return {"value": sub.B * sub.T / dt, "unit": "timesteps/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{sub.B} samples x T={sub.T} (D=H={sub.H}, heads {tuple(sub.head_sizes)}, each sample "
                       f"its own GAE segment), one full step of the fp64 NumPy oracle incl. Adam over all "
