@@ -92,16 +92,21 @@ def uniform_for_logits(B, head_sizes, seed, counter):
     return out
 
 
-def gumbel_max_sample(z, head_sizes, seed, counter):
-    """Sample one action per head by argmax(z + Gumbel noise).
+def gumbel_max_sample(z, head_sizes, seed, counter, avail=None):
+    """Sample one action per head by argmax(z + Gumbel noise) over the
+    head's available logits (avail [B, A], 1 = available, or None).
 
     z is [B, A+1] (last column = value).  Returns (act [B,K] int32,
-    logp [B] = sum_k log softmax(z_k)[a_k], value [B], scores list of
-    [B, n_k] = z_k + G for near-tie inspection).
+    logp [B] = sum_k log softmax(z_k)[a_k] over the available logits,
+    value [B], scores list of [B, n_k] = z_k + G for near-tie inspection,
+    -inf where unavailable).  A head with no available logit gets action -1
+    and adds nothing to logp.
     """
     z = np.asarray(z, np.float64)
     B = z.shape[0]
     us = uniform_for_logits(B, head_sizes, seed, counter)
+    A = int(sum(head_sizes))
+    av_all = np.ones((B, A), bool) if avail is None else np.asarray(avail) != 0
     act = np.empty((B, len(head_sizes)), dtype=np.int32)
     logp = np.zeros(B)
     scores = []
@@ -109,12 +114,16 @@ def gumbel_max_sample(z, head_sizes, seed, counter):
     rows = np.arange(B)
     for k, n in enumerate(head_sizes):
         zk = z[:, off:off + n]
-        s = zk - np.log(-np.log(us[k]))
+        av = av_all[:, off:off + n]
+        some = av.any(axis=1)
+        s = np.where(av, zk - np.log(-np.log(us[k])), -np.inf)
         a = np.argmax(s, axis=1)          # first maximum wins ties
-        act[:, k] = a
-        zmax = zk.max(axis=1, keepdims=True)
-        lse = zmax[:, 0] + np.log(np.exp(zk - zmax).sum(axis=1))
-        logp += zk[rows, a] - lse
+        act[:, k] = np.where(some, a, -1)
+        zmax = np.where(av, zk, -np.inf).max(axis=1, keepdims=True)
+        zmax = np.where(some[:, None], zmax, 0.0)
+        se = np.where(av, np.exp(zk - zmax), 0.0).sum(axis=1)
+        lse = zmax[:, 0] + np.log(np.where(some, se, 1.0))
+        logp += np.where(some, zk[rows, a] - lse, 0.0)
         scores.append(s)
         off += n
     return act, logp, z[:, off], scores

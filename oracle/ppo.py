@@ -8,7 +8,8 @@ What the paper fixes:
   (appendix "Neural Network Architecture");
 * the action is factorised into a primary action and parameter actions, one
   categorical distribution per head; heads that the primary action ignores
-  are masked out of the optimisation (appendix "Action Space");
+  are masked out of the optimisation, and at each timestep action filters
+  restrict the choice to the available actions (appendix "Action Space");
 * PPO clipped surrogate with clip 0.2, value loss weight 1.0 (Table
   "Hyperparameters"); entropy bonus c * S[pi](s_t) with c = 0.01 (appendix
   "Exploration", subsection "Loss function").
@@ -18,11 +19,17 @@ factorised action (per-head log-probabilities summed under the head mask);
 no advantage normalisation; value loss (V - R)^2 without a 1/2 factor and
 without clipping; natural-log entropy; means over the N timesteps; the
 gradient of the surrogate flows when (A >= 0 and r <= 1+eps) or
-(A < 0 and r >= 1-eps), inclusive at the kinks.
+(A < 0 and r >= 1-eps), inclusive at the kinks.  Availability: an
+unavailable logit is left out of its head's softmax (its probability is 0,
+it carries no gradient and it does not enter the entropy); a head with no
+available logit in a row contributes log-probability 0, entropy 0 and no
+gradient; a taken action that is unavailable has log-probability -inf.  A
+head whose mask is 0 contributes nothing whatever its log-probability.
 
 Shapes: h [N, H]; Wp [A+1, H] with the last row the value head; bp [A+1];
 act [N, K] (integer index within each head); logp_old, adv, ret [N];
-head_mask [N, K] or None (all ones).
+head_mask [N, K] or None (all ones); avail [N, A] (1 = available) or None
+(all available).
 """
 import numpy as np
 
@@ -43,31 +50,40 @@ def heads_forward(h, Wp, bp):
         np.asarray(bp, np.float64)
 
 
-def head_logprob_entropy(z, act, head_sizes):
-    """Per-head log-probability of the taken action, entropy and softmax.
+def head_logprob_entropy(z, act, head_sizes, avail=None):
+    """Per-head log-probability of the taken action, entropy and softmax,
+    each head's softmax taken over its available logits only.
 
     Returns (logp [N,K], ent [N,K], probs list of [N, n_k]).
     """
     N = z.shape[0]
     off = head_offsets(head_sizes)
     K = len(head_sizes)
+    av_all = np.ones((N, off[-1]), bool) if avail is None else np.asarray(avail) != 0
     logp = np.empty((N, K))
     ent = np.empty((N, K))
     probs = []
     rows = np.arange(N)
     for k in range(K):
         zk = z[:, off[k]:off[k + 1]]
-        zmax = zk.max(axis=1, keepdims=True)
-        lse = (zmax + np.log(np.exp(zk - zmax).sum(axis=1, keepdims=True)))[:, 0]
-        p = np.exp(zk - lse[:, None])
-        logp[:, k] = zk[rows, act[:, k]] - lse
-        ent[:, k] = lse - (p * zk).sum(axis=1)
+        av = av_all[:, off[k]:off[k + 1]]
+        some = av.any(axis=1)
+        zmax = np.where(av, zk, -np.inf).max(axis=1, keepdims=True)
+        zmax = np.where(some[:, None], zmax, 0.0)
+        e = np.where(av, np.exp(zk - zmax), 0.0)
+        se = e.sum(axis=1, keepdims=True)
+        lse = np.where(some, (zmax + np.log(np.where(some[:, None], se, 1.0)))[:, 0], 0.0)
+        p = np.where(some[:, None], e / np.where(some[:, None], se, 1.0), 0.0)
+        taken = av[rows, act[:, k]]
+        logp[:, k] = np.where(some, np.where(taken, zk[rows, act[:, k]] - lse, -np.inf), 0.0)
+        ent[:, k] = np.where(some, lse - (p * np.where(av, zk, 0.0)).sum(axis=1), 0.0)
         probs.append(p)
     return logp, ent, probs
 
 
 def ppo_loss_grad(h, Wp, bp, act, logp_old, adv, ret, head_sizes,
-                  clip_eps=0.2, vf_coef=1.0, ent_coef=0.01, head_mask=None):
+                  clip_eps=0.2, vf_coef=1.0, ent_coef=0.01, head_mask=None,
+                  avail=None):
     """Loss statistics and gradients with respect to h, Wp and bp.
 
     Returns (stats dict, dh [N,H], dWp [A+1,H], dbp [A+1], z [N,A+1]).
@@ -87,12 +103,13 @@ def ppo_loss_grad(h, Wp, bp, act, logp_old, adv, ret, head_sizes,
 
     z = heads_forward(h, Wp, bp)
     V = z[:, A]
-    logp, ent_k, probs = head_logprob_entropy(z, act, head_sizes)
-    logpi = (mask * logp).sum(axis=1)
+    logp, ent_k, probs = head_logprob_entropy(z, act, head_sizes, avail)
+    on = mask != 0
+    logpi = np.where(on, logp, 0.0).sum(axis=1)
     ratio = np.exp(logpi - logp_old)
     clipped = np.clip(ratio, 1.0 - clip_eps, 1.0 + clip_eps)
     surr = np.minimum(ratio * A_, clipped * A_)
-    ent = (mask * ent_k).sum(axis=1)
+    ent = np.where(on, ent_k, 0.0).sum(axis=1)
     verr = V - R_
 
     pg = -surr.mean()
@@ -117,15 +134,19 @@ def ppo_loss_grad(h, Wp, bp, act, logp_old, adv, ret, head_sizes,
     g_logpi = -np.where(flow, ratio * A_, 0.0) / N          # dL_pg / d logpi
     dz = np.zeros_like(z)
     rows = np.arange(N)
+    av_all = np.ones((N, A), bool) if avail is None else np.asarray(avail) != 0
     for k in range(K):
         zk = z[:, off[k]:off[k + 1]]
+        av = av_all[:, off[k]:off[k + 1]]
         p = probs[k]
         onehot = np.zeros_like(p)
         onehot[rows, act[:, k]] = 1.0
-        dpg = (g_logpi * mask[:, k])[:, None] * (onehot - p)
-        zbar = (p * zk).sum(axis=1, keepdims=True)
-        dent = -p * (zk - zbar)                                # dS_k / dz_k
-        dz[:, off[k]:off[k + 1]] = dpg - (ent_coef / N) * mask[:, k:k + 1] * dent
+        onehot *= av                                           # an unavailable taken action has no gradient
+        use = (on[:, k] & av.any(axis=1))[:, None]
+        dpg = g_logpi[:, None] * (onehot - p)
+        zbar = (p * np.where(av, zk, 0.0)).sum(axis=1, keepdims=True)
+        dent = -p * np.where(av, zk - zbar, 0.0)               # dS_k / dz_k
+        dz[:, off[k]:off[k + 1]] = np.where(use & av, dpg - (ent_coef / N) * dent, 0.0)
     dz[:, A] = 2.0 * vf_coef * verr / N
 
     dh = dz @ Wp
