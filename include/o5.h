@@ -209,7 +209,8 @@ int o5_segments_to_samples(int L, int S, int T, const float* adv, const float* r
  * (appendix "Neural Network Architecture": the action logits and the value
  * are linear projections of the LSTM state, sharing the network and its
  * gradients; appendix "Action Space": a factorised action with masking of
- * ignored parameter heads; subsection "Optimizing the Policy" and Table
+ * ignored parameter heads, each timestep's choice restricted by action
+ * filters to the available actions; subsection "Optimizing the Policy" and Table
  * "Hyperparameters": PPO clipping 0.2, value loss weight 1.0; appendix
  * "Exploration", "Loss function": entropy bonus c S[pi], c = 0.01).
  *
@@ -227,6 +228,12 @@ int o5_segments_to_samples(int L, int S, int T, const float* adv, const float* r
  * logp_old, adv, ret [N] fp32 (behaviour log-probability of the joint
  *          action, advantage, value target).
  * head_mask [N, K] uint8 or NULL (all heads count).
+ * avail    [N, A] uint8 or NULL (all available): nonzero marks an available
+ *          logit.  Each head's softmax runs over its available logits only;
+ *          an unavailable logit gets probability 0 and no gradient; a head
+ *          with no available logit in a row adds nothing; an unavailable
+ *          taken action has log-probability -inf (ratio 0).  A head with
+ *          head_mask 0 adds nothing in every case.
  * hp       {clip_eps, vf_coef, ent_coef}.
  * stats    out [8] fp32: total, pg, vf, ent, clipfrac (mean |r-1| > eps),
  *          approx_kl (mean (r - 1) - log r), mean_ratio, nonfinite (rows
@@ -246,7 +253,8 @@ size_t o5_ppo_loss_grad_workspace_bytes(o5_dtype dt, int N, int H, int K,
 int o5_ppo_loss_grad(o5_dtype dt, int N, int H, int K, const int* head_sizes,
                      const void* h, const void* Wp, const float* bp,
                      const int32_t* act, const float* logp_old, const float* adv,
-                     const float* ret, const uint8_t* head_mask, o5_ppo_hp hp,
+                     const float* ret, const uint8_t* head_mask,
+                     const uint8_t* avail, o5_ppo_hp hp,
                      float* stats, float* dh, float* dWp, float* dbp,
                      void* ws, size_t ws_bytes, void* stream);
 
@@ -284,18 +292,23 @@ int o5_adam_step(size_t n, float* p, float* m, float* v, const float* g,
  * from Philox4x64-10 (Salmon et al., SC'11): the noise for logit a of head
  * k in row b is word (a mod 4) of the block with counter
  * (a div 4, k, b, counter) and key (seed, 0); U = ((word >> 40) + 0.5)/2^24.
- * Ties go to the lowest index.
+ * Ties go to the lowest index.  Only available logits are drawn (appendix
+ * "Action Space": action filters): the argmax and the log-sum-exp of the
+ * log-probability run over them; the noise of a logit does not depend on
+ * the mask.
  *
  * dt, B, H, K, head_sizes, h [B, H], Wp, bp: as for o5_ppo_loss_grad.
- * act      out [B, K] int32.   logp: out [B] fp32, joint log-probability
- *          of the sampled action.   value: out [B] fp32.
+ * avail    [B, A] uint8 or NULL (all available), as for o5_ppo_loss_grad.
+ * act      out [B, K] int32; -1 for a head with no available logit.
+ * logp     out [B] fp32, joint log-probability of the sampled action (heads
+ *          with no available logit add nothing).   value: out [B] fp32.
  * ws       scratch of o5_policy_sample_workspace_bytes(...) bytes.
  * ------------------------------------------------------------------------ */
 size_t o5_policy_sample_workspace_bytes(o5_dtype dt, int B, int H, int K,
                                         const int* head_sizes);
 int o5_policy_sample(o5_dtype dt, int B, int H, int K, const int* head_sizes,
                      const void* h, const void* Wp, const float* bp,
-                     uint64_t seed, uint64_t counter,
+                     const uint8_t* avail, uint64_t seed, uint64_t counter,
                      int32_t* act, float* logp, float* value,
                      void* ws, size_t ws_bytes, void* stream);
 

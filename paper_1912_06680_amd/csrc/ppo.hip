@@ -7,8 +7,9 @@
 // value loss weight 1.0; appendix "Exploration": entropy bonus 0.01).
 //
 //   z   = h Wp^T                        GEMM  (M = N rows, N = A+1, K = H)
-//   row kernel (one wave per row): + bp, per-head log-softmax, joint
-//        log-ratio, clipped surrogate, value error, entropy -> dz [N, A+1],
+//   row kernel (one wave per row): + bp, per-head log-softmax over the
+//        available logits, joint log-ratio, clipped surrogate, value error,
+//        entropy -> dz [N, A+1],
 //        and per-block partial sums of dz (for dbp) and of the row stats
 //   dh  = dz Wp                         GEMM  (M = N, N = H, K = A+1)
 //   dWp = dz^T h                        GEMM  (M = A+1, N = H, K = N), split-K
@@ -59,7 +60,10 @@ __device__ __forceinline__ float column(const float (&z)[CPL], int c) {
 
 // One wave per row, kRowsPerWave consecutive rows per wave; lane l holds
 // logit columns l + 64 i (i < CPL).  zpart: [S][N][A1] partial logits (bias
-// not added).  Writes dz [N][A1]; on the bf16 path the (hi, lo) pair in row
+// not added).  avail [N][A] (or null = all available): an unavailable logit
+// is left out of its head's softmax and gets no gradient; a head with no
+// available logit adds nothing; an unavailable taken action has
+// log-probability -inf.  Writes dz [N][A1]; on the bf16 path the (hi, lo) pair in row
 // layout [N][ld_hilo] and, when dzT is set, transposed as [2 ld_hilo][ldT]
 // (hi rows, then lo rows; columns n >= N zero).  Each block writes one row
 // of part: the column sums of its dz (A1 values), then the sums of its rows'
@@ -70,7 +74,8 @@ template <int CPL>
 __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
     int N, int A1, int S, const float* __restrict__ zpart, const float* __restrict__ bp,
     const int32_t* __restrict__ act, const float* __restrict__ logp_old, const float* __restrict__ adv,
-    const float* __restrict__ ret, const uint8_t* __restrict__ mask, HeadsMeta hm, float clip_eps, float vf_coef,
+    const float* __restrict__ ret, const uint8_t* __restrict__ mask, const uint8_t* __restrict__ avail, HeadsMeta hm,
+    float clip_eps, float vf_coef,
     float ent_coef, float invN, float* __restrict__ dz, float* __restrict__ part, uint16_t* __restrict__ dz_hi,
     uint16_t* __restrict__ dz_lo, int ld_hilo, uint16_t* __restrict__ dzT, int ldT) {
   __shared__ float red[kWavesPerBlock][CPL * 64 + kStatCols];
@@ -107,7 +112,14 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
       }
       z[i] = v;
     }
-    float lse[kMaxHeads], zbar[kMaxHeads], mk[kMaxHeads];
+    bool av[CPL];
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      const int a = lane + 64 * i;
+      av[i] = avail == nullptr || a >= A || avail[static_cast<size_t>(n) * A + a] != 0;
+    }
+    float lse[kMaxHeads], zbar[kMaxHeads];
+    bool mk[kMaxHeads], some[kMaxHeads];
     int ak[kMaxHeads];
     float logpi = 0.0f, ent = 0.0f;
 #pragma unroll
@@ -116,26 +128,32 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
         float mx = -INFINITY;
 #pragma unroll
         for (int i = 0; i < CPL; ++i)
-          if (head[i] == k) mx = fmaxf(mx, z[i]);
+          if (head[i] == k && av[i]) mx = fmaxf(mx, z[i]);
         mx = wave_max(mx);
         float se = 0.0f, sez = 0.0f;
 #pragma unroll
         for (int i = 0; i < CPL; ++i)
-          if (head[i] == k) {
+          if (head[i] == k && av[i]) {
             const float e = expf(z[i] - mx);
             se += e;
             sez += e * z[i];
           }
         se = wave_sum(se);
         sez = wave_sum(sez);
-        lse[k] = mx + logf(se);
-        zbar[k] = sez / se;
+        some[k] = se > 0.0f;  // the maximum contributes e = 1
+        lse[k] = some[k] ? mx + logf(se) : 0.0f;
+        zbar[k] = some[k] ? sez / se : 0.0f;
         ak[k] = act[static_cast<size_t>(n) * K + k];
-        mk[k] = mask ? (mask[static_cast<size_t>(n) * K + k] ? 1.0f : 0.0f) : 1.0f;
+        mk[k] = mask == nullptr || mask[static_cast<size_t>(n) * K + k] != 0;
         const int nk = hm.off[k + 1] - hm.off[k];
         const int a_sel = min(max(ak[k], 0), nk - 1);
-        logpi += mk[k] * (column(z, hm.off[k] + a_sel) - lse[k]);
-        ent += mk[k] * (lse[k] - zbar[k]);
+        const float z_sel = column(z, hm.off[k] + a_sel);
+        bool taken = true;
+        if (avail != nullptr) taken = avail[static_cast<size_t>(n) * A + hm.off[k] + a_sel] != 0;
+        if (mk[k] && some[k]) {
+          logpi += taken ? z_sel - lse[k] : -INFINITY;
+          ent += lse[k] - zbar[k];
+        }
       }
     }
     const float Ad = adv[n], R = ret[n];
@@ -155,10 +173,10 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
       if (a == A) d = 2.0f * vf_coef * verr * invN;
 #pragma unroll
       for (int k = 0; k < kMaxHeads; ++k)
-        if (k < K && head[i] == k) {
+        if (k < K && head[i] == k && mk[k] && some[k] && av[i]) {
           const float p = expf(z[i] - lse[k]);
           const float onehot = (a - hm.off[k] == ak[k]) ? 1.0f : 0.0f;
-          d = mk[k] * (g_logpi * (onehot - p) + ent_scale * p * (z[i] - zbar[k]));
+          d = g_logpi * (onehot - p) + ent_scale * p * (z[i] - zbar[k]);
         }
       if (a < A1) dz[static_cast<size_t>(n) * A1 + a] = d;
       csum[i] += d;
@@ -339,16 +357,17 @@ int check_heads(const char* fn, o5_dtype dt, int N, int H, int K, const int* hea
 template <int CPL>
 static void launch_rows(const PpoWs& w, int N, int A1, int S, const float* zpart, const float* bp, const int32_t* act,
                         const float* logp_old, const float* adv, const float* ret, const uint8_t* mask,
-                        const HeadsMeta& hm, o5_ppo_hp hp, float invN, float* dz, float* part, uint16_t* dzhi,
-                        uint16_t* dzlo, uint16_t* dzT, hipStream_t s) {
+                        const uint8_t* avail, const HeadsMeta& hm, o5_ppo_hp hp, float invN, float* dz, float* part,
+                        uint16_t* dzhi, uint16_t* dzlo, uint16_t* dzT, hipStream_t s) {
   hipLaunchKernelGGL(ppo_rows<CPL>, dim3(w.nblk), dim3(kWavesPerBlock * 64), 0, s, N, A1, S, zpart, bp, act, logp_old,
-                     adv, ret, mask, hm, hp.clip_eps, hp.vf_coef, hp.ent_coef, invN, dz, part, dzhi, dzlo, w.A1p, dzT,
+                     adv, ret, mask, avail, hm, hp.clip_eps, hp.vf_coef, hp.ent_coef, invN, dz, part, dzhi, dzlo, w.A1p, dzT,
                      w.ldT);
 }
 
 template <typename E>
 static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, const float* bp, const int32_t* act,
-                    const float* logp_old, const float* adv, const float* ret, const uint8_t* mask, o5_ppo_hp hp,
+                    const float* logp_old, const float* adv, const float* ret, const uint8_t* mask,
+                    const uint8_t* avail, o5_ppo_hp hp,
                     float* stats, float* dh, float* dWp, float* dbp, char* ws, const PpoWs& w, hipStream_t s) {
   const int A1 = hm.A + 1;
   float* zpart = reinterpret_cast<float*>(ws + w.zpart);
@@ -374,15 +393,20 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
   const int S = w.plan_z.splits;
   const int cpl = cdiv(A1, 64);
   if (cpl <= 1)
-    launch_rows<1>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, hm, hp, invN, dz, part, dzhi, dzlo, dzT, s);
+    launch_rows<1>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, hp, invN, dz, part, dzhi, dzlo,
+                   dzT, s);
   else if (cpl <= 2)
-    launch_rows<2>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, hm, hp, invN, dz, part, dzhi, dzlo, dzT, s);
+    launch_rows<2>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, hp, invN, dz, part, dzhi, dzlo,
+                   dzT, s);
   else if (cpl <= 4)
-    launch_rows<4>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, hm, hp, invN, dz, part, dzhi, dzlo, dzT, s);
+    launch_rows<4>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, hp, invN, dz, part, dzhi, dzlo,
+                   dzT, s);
   else if (cpl <= 8)
-    launch_rows<8>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, hm, hp, invN, dz, part, dzhi, dzlo, dzT, s);
+    launch_rows<8>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, hp, invN, dz, part, dzhi, dzlo,
+                   dzT, s);
   else
-    launch_rows<16>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, hm, hp, invN, dz, part, dzhi, dzlo, dzT, s);
+    launch_rows<16>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, hp, invN, dz, part, dzhi, dzlo,
+                   dzT, s);
   if constexpr (sizeof(E) == 2) {
     const int A1p = w.A1p;
     uint16_t* wpad = reinterpret_cast<uint16_t*>(ws + w.wpad);
@@ -444,7 +468,8 @@ extern "C" size_t o5_ppo_loss_grad_workspace_bytes(o5_dtype dt, int N, int H, in
 
 extern "C" int o5_ppo_loss_grad(o5_dtype dt, int N, int H, int K, const int* head_sizes, const void* h, const void* Wp,
                                 const float* bp, const int32_t* act, const float* logp_old, const float* adv,
-                                const float* ret, const uint8_t* head_mask, o5_ppo_hp hp, float* stats, float* dh,
+                                const float* ret, const uint8_t* head_mask, const uint8_t* avail, o5_ppo_hp hp,
+                                float* stats, float* dh,
                                 float* dWp, float* dbp, void* ws, size_t ws_bytes, void* stream) {
   HeadsMeta hm;
   int st = check_heads("o5_ppo_loss_grad", dt, N, H, K, head_sizes, &hm);
@@ -459,6 +484,7 @@ extern "C" int o5_ppo_loss_grad(o5_dtype dt, int N, int H, int K, const int* hea
   O5_PTR(adv, "adv");
   O5_PTR(ret, "ret");
   O5_OPT_PTR(head_mask, "head_mask");
+  O5_OPT_PTR(avail, "avail");
   O5_PTR(stats, "stats");
   O5_PTR(dh, "dh");
   O5_PTR(dWp, "dWp");
@@ -472,10 +498,10 @@ extern "C" int o5_ppo_loss_grad(o5_dtype dt, int N, int H, int K, const int* hea
   ktimer_begin(kSitePpo, s);
   if (dt == O5_BF16)
     st = ppo_impl<uint16_t>(N, H, hm, static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(Wp), bp, act,
-                              logp_old, adv, ret, head_mask, hp, stats, dh, dWp, dbp, wsp, w, s);
+                              logp_old, adv, ret, head_mask, avail, hp, stats, dh, dWp, dbp, wsp, w, s);
   else
     st = ppo_impl<float>(N, H, hm, static_cast<const float*>(h), static_cast<const float*>(Wp), bp, act, logp_old, adv,
-                         ret, head_mask, hp, stats, dh, dWp, dbp, wsp, w, s);
+                         ret, head_mask, avail, hp, stats, dh, dWp, dbp, wsp, w, s);
   ktimer_end(kSitePpo, s);
   return st;
 }

@@ -43,8 +43,12 @@ __device__ __forceinline__ void philox4x64_10(uint64_t& c0, uint64_t& c1, uint64
 }
 
 // One thread per row b.  zpart: [S][B][A1] partial logits without bias.
+// avail [B][A] or null: unavailable logits are never drawn and leave the
+// log-sum-exp; a head with no available logit gets action -1 and adds
+// nothing to logp.  The noise of a logit does not depend on the mask.
 __global__ void __launch_bounds__(256) gumbel_sample_rows(int B, int A1, int S, const float* __restrict__ zpart,
-                                                          const float* __restrict__ bp, HeadsMeta hm, uint64_t seed,
+                                                          const float* __restrict__ bp,
+                                                          const uint8_t* __restrict__ avail, HeadsMeta hm, uint64_t seed,
                                                           uint64_t counter, int32_t* __restrict__ act,
                                                           float* __restrict__ logp, float* __restrict__ value) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
@@ -55,7 +59,7 @@ __global__ void __launch_bounds__(256) gumbel_sample_rows(int B, int A1, int S, 
   for (int k = 0; k < hm.K; ++k) {
     const int o = hm.off[k], nk = hm.off[k + 1] - o;
     float best = -INFINITY, zbest = 0.0f, zmax = -INFINITY, se = 0.0f;
-    int besta = 0;
+    int besta = -1;
     uint64_t w[4] = {0, 0, 0, 0};
     for (int a = 0; a < nk; ++a) {
       if ((a & 3) == 0) {
@@ -67,12 +71,13 @@ __global__ void __launch_bounds__(256) gumbel_sample_rows(int B, int A1, int S, 
         w[2] = c2;
         w[3] = c3;
       }
+      if (avail != nullptr && avail[static_cast<size_t>(b) * hm.A + o + a] == 0) continue;
       float z = bp[o + a];
       for (int s = 0; s < S; ++s) z += zrow[s * sstride + o + a];
       const uint64_t word = (a & 3) == 0 ? w[0] : (a & 3) == 1 ? w[1] : (a & 3) == 2 ? w[2] : w[3];
       const float u = (static_cast<float>(word >> 40) + 0.5f) * 5.9604644775390625e-08f;  // 2^-24
       const float score = z - logf(-logf(u));
-      if (score > best) {
+      if (besta < 0 || score > best) {
         best = score;
         besta = a;
         zbest = z;
@@ -86,7 +91,7 @@ __global__ void __launch_bounds__(256) gumbel_sample_rows(int B, int A1, int S, 
       }
     }
     act[static_cast<size_t>(b) * hm.K + k] = besta;
-    lp += zbest - (zmax + logf(se));
+    if (besta >= 0) lp += zbest - (zmax + logf(se));
   }
   float v = bp[hm.A];
   for (int s = 0; s < S; ++s) v += zrow[s * sstride + hm.A];
@@ -111,7 +116,8 @@ extern "C" size_t o5_policy_sample_workspace_bytes(o5_dtype dt, int B, int H, in
 }
 
 extern "C" int o5_policy_sample(o5_dtype dt, int B, int H, int K, const int* head_sizes, const void* h, const void* Wp,
-                                const float* bp, uint64_t seed, uint64_t counter, int32_t* act, float* logp,
+                                const float* bp, const uint8_t* avail, uint64_t seed, uint64_t counter, int32_t* act,
+                                float* logp,
                                 float* value, void* ws, size_t ws_bytes, void* stream) {
   HeadsMeta hm;
   int st = check_heads("o5_policy_sample", dt, B, H, K, head_sizes, &hm);
@@ -119,6 +125,7 @@ extern "C" int o5_policy_sample(o5_dtype dt, int B, int H, int K, const int* hea
   O5_PTR(h, "h");
   O5_PTR(Wp, "Wp");
   O5_PTR(bp, "bp");
+  O5_OPT_PTR(avail, "avail");
   O5_PTR(act, "act");
   O5_PTR(logp, "logp");
   O5_PTR(value, "value");
@@ -140,8 +147,8 @@ extern "C" int o5_policy_sample(o5_dtype dt, int B, int H, int K, const int* hea
     KRows2<float> bl{static_cast<const float*>(Wp), nullptr, nullptr, H, 0, H, H, A1};
     run_gemm(plan, al, bl, EpiStoreF32{zpart, A1, static_cast<size_t>(B) * A1}, B, A1, H, s);
   }
-  hipLaunchKernelGGL(gumbel_sample_rows, dim3(cdiv(B, 256)), dim3(256), 0, s, B, A1, plan.splits, zpart, bp, hm, seed,
-                     counter, act, logp, value);
+  hipLaunchKernelGGL(gumbel_sample_rows, dim3(cdiv(B, 256)), dim3(256), 0, s, B, A1, plan.splits, zpart, bp, avail, hm,
+                     seed, counter, act, logp, value);
   ktimer_end(kSiteSample, s);
   return check_launch("o5_policy_sample");
 }

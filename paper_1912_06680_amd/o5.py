@@ -75,10 +75,10 @@ _SIGS = {
     "o5_reward_process_workspace_bytes": (_sz, [_i, _i]),
     "o5_reward_process": (_i, [_i, _i, _vp, _vp, _vp, RewardHp, _vp, _vp, _vp, _sz, _vp]),
     "o5_ppo_loss_grad_workspace_bytes": (_sz, [_i, _i, _i, _i, _vp]),
-    "o5_ppo_loss_grad": (_i, [_i, _i, _i, _i, _vp] + [_vp] * 8 + [PpoHp] + [_vp] * 5 + [_sz, _vp]),
+    "o5_ppo_loss_grad": (_i, [_i, _i, _i, _i, _vp] + [_vp] * 9 + [PpoHp] + [_vp] * 5 + [_sz, _vp]),
     "o5_adam_step": (_i, [_sz, _vp, _vp, _vp, _vp, _vp, AdamHp, _i, _vp]),
     "o5_policy_sample_workspace_bytes": (_sz, [_i, _i, _i, _i, _vp]),
-    "o5_policy_sample": (_i, [_i, _i, _i, _i, _vp, _vp, _vp, _vp, _u64, _u64, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "o5_policy_sample": (_i, [_i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _u64, _u64, _vp, _vp, _vp, _vp, _sz, _vp]),
     "o5_f32_to_bf16": (_i, [_sz, _vp, _vp, _vp]),
     "o5_ktimer_enable": (_i, [_i]),
     "o5_ktimer_read": (_i, [_i, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int)]),
@@ -201,12 +201,12 @@ def o5_ppo_loss_grad_workspace_bytes(dt, N, H, head_sizes):
 
 
 def o5_ppo_loss_grad(dt, N, H, head_sizes, h, Wp, bp, act, logp_old, adv, ret, head_mask,
-                     clip_eps, vf_coef, ent_coef, stats, dh, dWp, dbp, ws, stream=None):
+                     clip_eps, vf_coef, ent_coef, stats, dh, dWp, dbp, ws, stream=None, avail=None):
     wp, wn = _ws(ws)
     hp = PpoHp(clip_eps, vf_coef, ent_coef)
     _check("o5_ppo_loss_grad", lib().o5_ppo_loss_grad(
         dt, N, H, len(head_sizes), _heads(head_sizes), _p(h), _p(Wp), _p(bp), _p(act),
-        _p(logp_old), _p(adv), _p(ret), _p(head_mask), hp, _p(stats), _p(dh), _p(dWp),
+        _p(logp_old), _p(adv), _p(ret), _p(head_mask), _p(avail), hp, _p(stats), _p(dh), _p(dWp),
         _p(dbp), wp, wn, _stream(stream)))
 
 
@@ -221,10 +221,10 @@ def o5_policy_sample_workspace_bytes(dt, B, H, head_sizes):
 
 
 def o5_policy_sample(dt, B, H, head_sizes, h, Wp, bp, seed, counter, act, logp, value, ws,
-                     stream=None):
+                     stream=None, avail=None):
     wp, wn = _ws(ws)
     _check("o5_policy_sample", lib().o5_policy_sample(
-        dt, B, H, len(head_sizes), _heads(head_sizes), _p(h), _p(Wp), _p(bp), int(seed),
+        dt, B, H, len(head_sizes), _heads(head_sizes), _p(h), _p(Wp), _p(bp), _p(avail), int(seed),
         int(counter), _p(act), _p(logp), _p(value), wp, wn, _stream(stream)))
 
 

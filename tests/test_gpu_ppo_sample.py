@@ -16,7 +16,26 @@ HEADS = (30, 8, 32, 4)
 KINKS = (np.log(1.2), np.log(0.8))
 
 
-def _inputs(N, H, heads, seed, bf16, with_mask):
+def _avail(rng, N, heads, mask):
+    """Availability [N, A]: each logit available with probability 0.7, at
+    least one per head, the taken action among them; where a head's mask is
+    0, one row in three has no available logit at all (an empty head)."""
+    off = np.concatenate([[0], np.cumsum(heads)])
+    av = rng.random((N, off[-1])) < 0.7
+    act = np.zeros((N, len(heads)), np.int32)
+    for k, n in enumerate(heads):
+        blk = av[:, off[k]:off[k + 1]]
+        none = ~blk.any(axis=1)
+        blk[none, rng.integers(0, n, none.sum())] = True
+        for i in range(N):
+            act[i, k] = rng.choice(np.flatnonzero(blk[i]))
+        if mask is not None:
+            empty = (mask[:, k] == 0) & (rng.random(N) < 1 / 3)
+            blk[empty] = False
+    return av.astype(np.uint8), act
+
+
+def _inputs(N, H, heads, seed, bf16, with_mask, with_avail=False):
     rng = np.random.Generator(np.random.PCG64(seed))
     A1 = sum(heads) + 1
     bound = 1.0 / np.sqrt(H)
@@ -27,41 +46,49 @@ def _inputs(N, H, heads, seed, bf16, with_mask):
     adv = rng.standard_normal(N, dtype=np.float32)
     ret = rng.standard_normal(N, dtype=np.float32)
     mask = (rng.random((N, len(heads))) < 0.8).astype(np.uint8) if with_mask else None
+    avail = None
+    if with_avail:
+        avail, act = _avail(rng, N, heads, mask)
     # behaviour log-probabilities: the oracle's current log-probability shifted
     # by U(-0.4, 0.4), kept >= 0.01 away from the clip kinks log(1.2), log(0.8)
     hh = round_to_bf16(h) if bf16 else h.astype(np.float64)
     ww = round_to_bf16(Wp) if bf16 else Wp.astype(np.float64)
     z = heads_forward(hh, ww, bp)
-    logp, _, _ = head_logprob_entropy(z, act, heads)
+    logp, _, _ = head_logprob_entropy(z, act, heads, avail)
     m = np.ones_like(logp) if mask is None else mask.astype(np.float64)
-    logpi = (m * logp).sum(axis=1)
+    logpi = np.where(m != 0, logp, 0.0).sum(axis=1)
     shift = rng.uniform(-0.4, 0.4, N)
     for kk in KINKS:   # r = exp(-shift); keep -shift away from the kinks
         near = np.abs(-shift - kk) < 0.01
         shift[near] += 0.03
     logp_old = (logpi + shift).astype(np.float32)
-    return dict(h=h, Wp=Wp, bp=bp, act=act, adv=adv, ret=ret, mask=mask, logp_old=logp_old, hh=hh, ww=ww)
+    return dict(h=h, Wp=Wp, bp=bp, act=act, adv=adv, ret=ret, mask=mask, avail=avail, logp_old=logp_old, hh=hh,
+                ww=ww)
 
 
 PPO_CASES = [
-    ("f32-small", 64, 64, HEADS, False, False),
-    ("f32-mask-ragged", 1001, 128, (5, 3, 7), False, True),
-    ("bf16-mid", 4096, 1024, HEADS, True, True),
-    ("bf16-one-head", 333, 192, (8,), True, False),
+    ("f32-small", 64, 64, HEADS, False, False, False),
+    ("f32-mask-ragged", 1001, 128, (5, 3, 7), False, True, False),
+    ("bf16-mid", 4096, 1024, HEADS, True, True, False),
+    ("bf16-one-head", 333, 192, (8,), True, False, False),
     # 191 logit columns: three per lane, heads crossing the 64-column lane
     # blocks, and the dWp product without the transposed pair
-    ("bf16-wide-heads", 500, 128, (100, 60, 30), True, True),
+    ("bf16-wide-heads", 500, 128, (100, 60, 30), True, True, False),
+    # availability masks, with empty heads under a zero head mask
+    ("f32-avail", 777, 128, HEADS, False, True, True),
+    ("bf16-avail-wide", 500, 128, (100, 60, 30), True, True, True),
+    ("f32-avail-no-head-mask", 300, 64, (5, 3, 7), False, False, True),
 ]
 
 
-@pytest.mark.parametrize("name,N,H,heads,bf16,with_mask", PPO_CASES, ids=[c[0] for c in PPO_CASES])
-def test_ppo_loss_grad_matches_oracle(name, N, H, heads, bf16, with_mask):
+@pytest.mark.parametrize("name,N,H,heads,bf16,with_mask,with_avail", PPO_CASES, ids=[c[0] for c in PPO_CASES])
+def test_ppo_loss_grad_matches_oracle(name, N, H, heads, bf16, with_mask, with_avail):
     need_gpu()
-    banner(f"ppo {name} N={N} H={H} heads={heads} bf16={bf16}")
-    inp = _inputs(N, H, heads, seed=N + H, bf16=bf16, with_mask=with_mask)
+    banner(f"ppo {name} N={N} H={H} heads={heads} bf16={bf16} avail={with_avail}")
+    inp = _inputs(N, H, heads, seed=N + H, bf16=bf16, with_mask=with_mask, with_avail=with_avail)
     stats_ref, dh_ref, dWp_ref, dbp_ref, _ = ppo_loss_grad(
         inp["hh"], inp["ww"], inp["bp"], inp["act"], inp["logp_old"], inp["adv"], inp["ret"], heads,
-        0.2, 1.0, 0.01, inp["mask"])
+        0.2, 1.0, 0.01, inp["mask"], inp["avail"])
     dt = o5.O5_BF16 if bf16 else o5.O5_F32
     A1 = sum(heads) + 1
     stats = torch.empty(8, dtype=torch.float32, device="cuda")
@@ -70,9 +97,10 @@ def test_ppo_loss_grad_matches_oracle(name, N, H, heads, bf16, with_mask):
     dbp = torch.empty(A1, dtype=torch.float32, device="cuda")
     ws = workspace(o5.o5_ppo_loss_grad_workspace_bytes(dt, N, H, heads))
     mask = dev(inp["mask"]) if inp["mask"] is not None else None
+    avail = dev(inp["avail"]) if inp["avail"] is not None else None
     o5.o5_ppo_loss_grad(dt, N, H, heads, dev_dt(inp["h"], bf16), dev_dt(inp["Wp"], bf16), dev_f32(inp["bp"]),
                         dev(inp["act"]), dev_f32(inp["logp_old"]), dev_f32(inp["adv"]), dev_f32(inp["ret"]),
-                        mask, 0.2, 1.0, 0.01, stats, dh, dWp, dbp, ws)
+                        mask, 0.2, 1.0, 0.01, stats, dh, dWp, dbp, ws, avail=avail)
     tol = TOL_BF16 if bf16 else TOL_F32
     st = host(stats)
     for i, name_ in enumerate(STAT_NAMES):
@@ -107,30 +135,41 @@ def test_ppo_ratio_one_invariant_on_gpu():
     assert st[4] == 0.0 and abs(st[6] - 1.0) < 1e-5
 
 
-SAMPLE_CASES = [("f32", 512, 256, False), ("bf16", 1000, 512, True)]
+SAMPLE_CASES = [("f32", 512, 256, False, False), ("bf16", 1000, 512, True, False),
+                ("f32-avail", 600, 128, False, True), ("bf16-avail", 700, 256, True, True)]
 
 
-@pytest.mark.parametrize("name,B,H,bf16", SAMPLE_CASES, ids=[c[0] for c in SAMPLE_CASES])
-def test_policy_sample_matches_oracle(name, B, H, bf16):
+@pytest.mark.parametrize("name,B,H,bf16,with_avail", SAMPLE_CASES, ids=[c[0] for c in SAMPLE_CASES])
+def test_policy_sample_matches_oracle(name, B, H, bf16, with_avail):
     need_gpu()
-    banner(f"policy_sample {name} B={B} H={H}")
-    inp = _inputs(B, H, HEADS, seed=B, bf16=bf16, with_mask=False)
+    banner(f"policy_sample {name} B={B} H={H} avail={with_avail}")
+    inp = _inputs(B, H, HEADS, seed=B, bf16=bf16, with_mask=with_avail, with_avail=with_avail)
     seed, counter = 12345, 7
     act_ref, logp_ref, v_ref, scores = gumbel_max_sample(heads_forward(inp["hh"], inp["ww"], inp["bp"]), HEADS,
-                                                          seed, counter)
+                                                          seed, counter, inp["avail"])
     dt = o5.O5_BF16 if bf16 else o5.O5_F32
     act = torch.empty((B, len(HEADS)), dtype=torch.int32, device="cuda")
     logp = torch.empty(B, dtype=torch.float32, device="cuda")
     value = torch.empty(B, dtype=torch.float32, device="cuda")
     ws = workspace(o5.o5_policy_sample_workspace_bytes(dt, B, H, HEADS))
     o5.o5_policy_sample(dt, B, H, HEADS, dev_dt(inp["h"], bf16), dev_dt(inp["Wp"], bf16), dev_f32(inp["bp"]), seed,
-                        counter, act, logp, value, ws)
+                        counter, act, logp, value, ws,
+                        avail=dev(inp["avail"]) if inp["avail"] is not None else None)
     a = act.cpu().numpy()
+    if inp["avail"] is not None:
+        off = np.concatenate([[0], np.cumsum(HEADS)])
+        for k in range(len(HEADS)):
+            blk = inp["avail"][:, off[k]:off[k + 1]]
+            empty = ~blk.any(axis=1)
+            assert np.all(a[empty, k] == -1) and np.all(act_ref[empty, k] == -1)
+            taken = a[~empty, k]
+            assert np.all(blk[~empty][np.arange(taken.size), taken] == 1), "an unavailable action was drawn"
     # unique where the oracle's best score leads the runner-up by > 1e-4
     agree = np.ones(B, bool)
     for k in range(len(HEADS)):
         s = np.sort(scores[k], axis=1)
-        clear = (s[:, -1] - s[:, -2]) > 1e-4
+        with np.errstate(invalid="ignore"):       # empty heads: -inf - -inf
+            clear = ~(s[:, -1] - s[:, -2] <= 1e-4)  # (a single available logit leads by +inf)
         mism = (a[:, k] != act_ref[:, k])
         assert not np.any(mism & clear), f"head {k}: {np.sum(mism & clear)} clear-cut mismatches"
         # near ties: the GPU's choice must be one of the near-maximal logits
