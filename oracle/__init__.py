@@ -17,6 +17,10 @@ method computes, written so that it can be checked against the paper by eye:
                 and entropy bonus, with gradients (subsection "Optimizing the
                 Policy"; appendix "Exploration", subsection "Loss function";
                 appendix "Neural Network Architecture").
+* ``prelstm`` -- the LSTM's input side: running observation normalisation,
+                the pre-LSTM fully-connected layer and the cross-hero
+                max-pool, forward and backward (appendices "Observation
+                Space" and "Neural Network Architecture").
 * ``reward`` -- reward post-processing ahead of GAE: game time weighting,
                 team spirit, zero sum, normalisation by a running standard
                 deviation (appendix "Reward Weights"; Table "Hyperparameters").
