@@ -228,7 +228,11 @@ def hbm_kernels(cfg, reps=20, warm=3):
     latency-bound), 11,520 (the paper's 2.9M-timestep batch) and 131,072
     (33.5M timesteps, beyond the 256 MB infinity cache); the reward
     post-processing ahead of GAE at 1,152 and 13,107 games of ten heroes;
-    Adam at the step's parameter count and at 158,502,815.  Each is timed with events on the
+    the LSTM's input side (observation normalisation, pre-LSTM layer with
+    the cross-hero pool, and its backward) at the step's shape with teams of
+    five (B = 2040); Adam at the step's parameter count and at 158,502,815.
+    The input-side layer entries also give the warm TFLOP/s of their GEMM
+    work (2 N D Do each way) over the whole call.  Each is timed with events on the
     launch stream, median of `reps` after `warm` untimed calls, cold (a
     512 MB buffer written before every call) and warm."""
     import torch
@@ -279,6 +283,37 @@ def hbm_kernels(cfg, reps=20, warm=3):
         out.append(entry("reward_process", f"L={L} G={G} (S={10 * G})", 12 * L * 10 * G + 4 * L * G,
                          lambda: o5.o5_reward_process(L, G, sh, oc, gt, 0.3, 0.6, 10.0, 1e-8, stats, rr, rws)))
         del sh, oc, gt, stats, rr, rws
+    # the LSTM's input side at the step's shape: 408 teams x 5 replicas x 16
+    # steps of a 4096-wide observation into the 4096-wide LSTM input
+    Tq, Bq, Do, D = cfg.T, 2040, cfg.D, cfg.D
+    Nq = Tq * Bq
+    dtq = o5.O5_BF16 if cfg.dtype == "bf16" else o5.O5_F32
+    et = torch.bfloat16 if dtq == o5.O5_BF16 else torch.float32
+    obs = torch.randn((Nq, Do), generator=gen, device=dev) * 2.0 + 1.0
+    ostats = torch.zeros((3, Do), dtype=torch.float64, device=dev)
+    oq = torch.empty((Nq, Do), dtype=et, device=dev)
+    ows = torch.empty(o5.o5_obs_normalize_workspace_bytes(Nq, Do), dtype=torch.uint8, device=dev)
+    out.append(entry("obs_normalize", f"N={Nq} Do={Do}", Nq * Do * (4 + oq.element_size()),
+                     lambda: o5.o5_obs_normalize(dtq, Nq, Do, obs, ostats, 5.0, 1e-8, oq, ows)))
+    del obs
+    Wq = (torch.randn((D, Do), generator=gen, device=dev) / Do ** 0.5).to(et)
+    bq = torch.zeros(D, device=dev)
+    yq = torch.empty((Nq, D), device=dev)
+    xq = torch.empty((Nq, D), dtype=et, device=dev)
+    fl = 2.0 * Nq * D * Do
+    e = entry("prelstm_fwd", f"T={Tq} B={Bq} Do={Do} D={D}", Nq * Do * 2 + D * Do * 2 + Nq * D * (4 + 4 + 2),
+              lambda: o5.o5_prelstm_fwd(dtq, Tq, Bq, Do, D, oq, Wq, bq, yq, xq))
+    e["tflops_warm"] = round(fl / e["warm_us"] * 1e-6, 1)
+    out.append(e)
+    dxq = torch.randn((Nq, D), generator=gen, device=dev).to(et)
+    dWq = torch.empty((D, Do), device=dev)
+    dbq = torch.empty(D, device=dev)
+    pws = torch.empty(o5.o5_prelstm_bwd_workspace_bytes(dtq, Tq, Bq, Do, D), dtype=torch.uint8, device=dev)
+    e = entry("prelstm_bwd", f"T={Tq} B={Bq} Do={Do} D={D}", Nq * D * (4 + 2 + 2 + 2) + Nq * Do * 2 + D * Do * 4,
+              lambda: o5.o5_prelstm_bwd(dtq, Tq, Bq, Do, D, oq, yq, dxq, dWq, dbq, pws))
+    e["tflops_warm"] = round(fl / e["warm_us"] * 1e-6, 1)
+    out.append(e)
+    del oq, Wq, bq, yq, xq, dxq, dWq, dbq, pws, ows, ostats
     for n in (synth.n_params(cfg), 158502815):
         p = torch.randn(n, generator=gen, device=dev) * 0.02
         g = torch.randn(n, generator=gen, device=dev) * 1e-3

@@ -189,6 +189,63 @@ int o5_reward_process(int L, int G, const float* shaped, const float* outcome,
                       float* r, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * o5_obs_normalize -- observation normalisation (appendix "Observation
+ * Space": every float observation has a running mean and standard
+ * deviation of all data ever observed subtracted and divided out, the
+ * result clipped to (-5, 5)).  Per feature j the running summary (count,
+ * mean, M2 = sum of squared deviations) is merged with this call's N rows
+ * (fp64, fixed order) and written back; then
+ *
+ *   o[n, j] = clamp((obs[n, j] - mean_j) / sqrt(M2_j / count_j + eps), -clip, clip)
+ *
+ * dt       type of o (bf16: the operand of the pre-LSTM layer).
+ * N >= 1 rows; Do features, a positive multiple of 4.
+ * obs      [N, Do] fp32.   stats: [3, Do] fp64 (counts, means, M2),
+ *          updated in place; start from zeros.
+ * clip     5 in the paper; eps > 0 (1e-8) keeps a constant feature at 0.
+ * o        out [N, Do] dt.   ws: o5_obs_normalize_workspace_bytes(N, Do).
+ * ------------------------------------------------------------------------ */
+size_t o5_obs_normalize_workspace_bytes(int N, int Do);
+int o5_obs_normalize(o5_dtype dt, int N, int Do, const float* obs, double* stats,
+                     float clip, float eps, void* o, void* ws, size_t ws_bytes,
+                     void* stream);
+
+/* ------------------------------------------------------------------------
+ * o5_prelstm_fwd / o5_prelstm_bwd -- the layer between the flattened
+ * observation and the LSTM (appendix "Neural Network Architecture": a
+ * fully-connected layer, then a cross-hero pool that max-pools the first
+ * 25% of the vector across the five replica networks of a team):
+ *
+ *   y = relu(o W^T + b)                                  [N, D] fp32
+ *   x[n, j] = max over the 5 replicas of y[., j]  (j < D/4),  y[n, j] else
+ *
+ * The five replicas of a team are five consecutive samples b = 5 q + r of
+ * the time-major [T, B, .] layout (B a multiple of 5), pooled at every
+ * timestep.  The backward takes dx = dL/dx (from o5_lstm_bptt), sends the
+ * pooled features' summed gradient to the first replica attaining the
+ * maximum, applies the ReLU mask and returns
+ *
+ *   dW = dpre^T o  [D, Do] fp32,   db = sum_n dpre [D] fp32
+ *
+ * (bf16 path: dpre is rounded to bf16 as the operand of dW; db sums the
+ * unrounded values).  No gradient reaches the observation.
+ *
+ * dt       type of o, W, x and dx.   T >= 1; B a positive multiple of 5 with
+ *          T B / 5 <= 65535; Do and D positive multiples of 64.
+ * o        [T B, Do] dt (from o5_obs_normalize).   W: [D, Do] dt.   b: [D].
+ * y        out (fwd) / in (bwd) [T B, D] fp32: the layer's output before the
+ *          pool, kept for the backward.   x: out [T B, D] dt, the LSTM input.
+ * dx       [T B, D] dt.   dW, db: out.
+ * ws       (bwd) o5_prelstm_bwd_workspace_bytes(dt, T, B, Do, D) bytes.
+ * ------------------------------------------------------------------------ */
+int o5_prelstm_fwd(o5_dtype dt, int T, int B, int Do, int D, const void* o,
+                   const void* W, const float* b, float* y, void* x, void* stream);
+size_t o5_prelstm_bwd_workspace_bytes(o5_dtype dt, int T, int B, int Do, int D);
+int o5_prelstm_bwd(o5_dtype dt, int T, int B, int Do, int D, const void* o,
+                   const float* y, const void* dx, float* dW, float* db,
+                   void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * o5_segments_to_samples -- cut each of S segments of L steps into L/T
  * samples of T steps, the unit truncated BPTT runs on (Figure "Timescales
  * and Staleness": a segment is subdivided into samples of 16 policy
@@ -328,7 +385,8 @@ int o5_f32_to_bf16(size_t n, const float* src, uint16_t* dst, void* stream);
  * launches.  Sites: 0 lstm_fwd_gemm, 1 lstm_fwd_cell, 2 lstm_dh_gemm,
  * 3 lstm_bwd_cell, 4 lstm_dw_gemm, 5 lstm_dx_gemm, 6 ppo_loss_grad (whole
  * call), 7 adam_step, 8 gae, 9 policy_sample (whole call), 10
- * reward_process (whole call).
+ * reward_process, 11 obs_normalize, 12 prelstm_fwd, 13 prelstm_bwd (whole
+ * calls).
  * o5_ktimer_site_name returns the site's name ("" if out of range).
  * ------------------------------------------------------------------------ */
 int o5_ktimer_enable(int on);

@@ -51,7 +51,8 @@ struct KTimer {
 KTimer g_kt;
 const char* kSiteNames[kSiteCount] = {"lstm_fwd_gemm", "lstm_fwd_cell", "lstm_dh_gemm", "lstm_bwd_cell",
                                       "lstm_dw_gemm",  "lstm_dx_gemm",  "ppo_loss_grad", "adam_step",
-                                      "gae",           "policy_sample", "reward_process"};
+                                      "gae",           "policy_sample", "reward_process",
+                                      "obs_normalize", "prelstm_fwd",   "prelstm_bwd"};
 }  // namespace
 
 void ktimer_begin(int site, hipStream_t s) {

@@ -61,6 +61,9 @@ enum KSite {
   kSiteGae,
   kSiteSample,
   kSiteReward,
+  kSiteObsNorm,
+  kSitePreFwd,
+  kSitePreBwd,
   kSiteCount
 };
 // When timing is on, record an event on `s` before / after a launch site.

@@ -25,6 +25,8 @@ EXPORTED = (
     "o5_lstm_bptt_workspace_bytes", "o5_lstm_bptt",
     "o5_gae", "o5_segments_to_samples",
     "o5_reward_process_workspace_bytes", "o5_reward_process",
+    "o5_obs_normalize_workspace_bytes", "o5_obs_normalize", "o5_prelstm_fwd",
+    "o5_prelstm_bwd_workspace_bytes", "o5_prelstm_bwd",
     "o5_ppo_loss_grad_workspace_bytes", "o5_ppo_loss_grad",
     "o5_adam_step",
     "o5_policy_sample_workspace_bytes", "o5_policy_sample",
@@ -33,7 +35,8 @@ EXPORTED = (
 )
 
 KTIMER_SITES = ("lstm_fwd_gemm", "lstm_fwd_cell", "lstm_dh_gemm", "lstm_bwd_cell", "lstm_dw_gemm",
-                "lstm_dx_gemm", "ppo_loss_grad", "adam_step", "gae", "policy_sample", "reward_process")
+                "lstm_dx_gemm", "ppo_loss_grad", "adam_step", "gae", "policy_sample", "reward_process",
+                "obs_normalize", "prelstm_fwd", "prelstm_bwd")
 
 
 class O5Error(RuntimeError):
@@ -74,6 +77,11 @@ _SIGS = {
     "o5_segments_to_samples": (_i, [_i, _i, _i] + [_vp] * 6 + [_vp]),
     "o5_reward_process_workspace_bytes": (_sz, [_i, _i]),
     "o5_reward_process": (_i, [_i, _i, _vp, _vp, _vp, RewardHp, _vp, _vp, _vp, _sz, _vp]),
+    "o5_obs_normalize_workspace_bytes": (_sz, [_i, _i]),
+    "o5_obs_normalize": (_i, [_i, _i, _i, _vp, _vp, _f, _f, _vp, _vp, _sz, _vp]),
+    "o5_prelstm_fwd": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "o5_prelstm_bwd_workspace_bytes": (_sz, [_i, _i, _i, _i, _i]),
+    "o5_prelstm_bwd": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "o5_ppo_loss_grad_workspace_bytes": (_sz, [_i, _i, _i, _i, _vp]),
     "o5_ppo_loss_grad": (_i, [_i, _i, _i, _i, _vp] + [_vp] * 9 + [PpoHp] + [_vp] * 5 + [_sz, _vp]),
     "o5_adam_step": (_i, [_sz, _vp, _vp, _vp, _vp, _vp, AdamHp, _i, _vp]),
@@ -194,6 +202,31 @@ def o5_reward_process(L, G, shaped, outcome, game_time, tau, decay_base, decay_m
     hp = RewardHp(tau, decay_base, decay_minutes, eps)
     _check("o5_reward_process", lib().o5_reward_process(L, G, _p(shaped), _p(outcome), _p(game_time), hp,
                                                         _p(stats), _p(r), wp, wn, _stream(stream)))
+
+
+def o5_obs_normalize_workspace_bytes(N, Do):
+    return lib().o5_obs_normalize_workspace_bytes(N, Do)
+
+
+def o5_obs_normalize(dt, N, Do, obs, stats, clip, eps, o, ws, stream=None):
+    wp, wn = _ws(ws)
+    _check("o5_obs_normalize", lib().o5_obs_normalize(dt, N, Do, _p(obs), _p(stats), float(clip), float(eps), _p(o),
+                                                      wp, wn, _stream(stream)))
+
+
+def o5_prelstm_fwd(dt, T, B, Do, D, o, W, b, y, x, stream=None):
+    _check("o5_prelstm_fwd", lib().o5_prelstm_fwd(dt, T, B, Do, D, _p(o), _p(W), _p(b), _p(y), _p(x),
+                                                  _stream(stream)))
+
+
+def o5_prelstm_bwd_workspace_bytes(dt, T, B, Do, D):
+    return lib().o5_prelstm_bwd_workspace_bytes(dt, T, B, Do, D)
+
+
+def o5_prelstm_bwd(dt, T, B, Do, D, o, y, dx, dW, db, ws, stream=None):
+    wp, wn = _ws(ws)
+    _check("o5_prelstm_bwd", lib().o5_prelstm_bwd(dt, T, B, Do, D, _p(o), _p(y), _p(dx), _p(dW), _p(db), wp, wn,
+                                                  _stream(stream)))
 
 
 def o5_ppo_loss_grad_workspace_bytes(dt, N, H, head_sizes):
