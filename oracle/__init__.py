@@ -21,6 +21,8 @@ method computes, written so that it can be checked against the paper by eye:
                 the pre-LSTM fully-connected layer and the cross-hero
                 max-pool, forward and backward (appendices "Observation
                 Space" and "Neural Network Architecture").
+* ``surgery`` -- widening the LSTM and extending its input on the flat
+                parameter vector, with Adam's moments (appendix "Surgery").
 * ``reward`` -- reward post-processing ahead of GAE: game time weighting,
                 team spirit, zero sum, normalisation by a running standard
                 deviation (appendix "Reward Weights"; Table "Hyperparameters").
