@@ -91,3 +91,21 @@ def widen(p, m, v, D, H, A1, D2, H2, scale, seed):
     new_p["Wp"][:, H:] = 0.0
     cat = lambda d: np.concatenate([d[k].ravel() for k in ("Wx", "Wh", "b", "Wp", "bp")])
     return cat(new_p), cat(new_m), cat(new_v)
+
+
+def fold_input(p, m, v, D, H, A1, Dk, E):
+    """Fold the last D - Dk LSTM inputs, a constant vector E, into the bias
+    (appendix "Bloopers", subsection "Zero Team Spirit Embedding": a constant
+    part of the input of a fully-connected layer is the same as a modified
+    bias, B' = W [0, E] + B):
+    b' = b + Wx[:, Dk:] E and Wx' = Wx[:, :Dk].  The moments of the dropped
+    columns are discarded; every other parameter keeps its moments."""
+    parts = [split(a, D, H, A1) for a in (p, m, v)]
+    outs = []
+    for i, P in enumerate(parts):
+        Q = {k: np.array(a, copy=True) for k, a in P.items()}
+        Q["Wx"] = np.ascontiguousarray(P["Wx"][:, :Dk])
+        if i == 0:
+            Q["b"] = (P["b"].astype(np.float64) + P["Wx"][:, Dk:].astype(np.float64) @ np.asarray(E, np.float64))
+        outs.append(np.concatenate([np.asarray(Q[k], np.float64).ravel() for k in ("Wx", "Wh", "b", "Wp", "bp")]))
+    return tuple(outs)

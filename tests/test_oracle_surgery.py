@@ -105,3 +105,24 @@ def test_noise_is_uniform_and_seeded():
     assert np.array_equal(u, noise(200_000, 3, 0.25)) and not np.array_equal(u, noise(200_000, 4, 0.25))
     # the value is fp32(scale * (2U - 1)) with both factors fp32: sign symmetry of the construction
     assert abs(float(np.mean(u))) < 2e-3
+
+
+def test_folding_a_constant_input_into_the_bias_preserves_the_function():
+    from oracle.surgery import fold_input
+    p, m, v = _old(9)
+    Dk = 4
+    E = np.random.default_rng(10).standard_normal(D - Dk)
+    p2, m2, v2 = fold_input(p, m, v, D, H, A1, Dk, E)
+    assert p2.size == n_params(Dk, H, A1)
+    x2, h0, c0, _, _, reset = _inputs(11)
+    xk = x2[..., :Dk]
+    xfull = np.concatenate([xk, np.broadcast_to(E, xk.shape[:2] + (D - Dk,))], axis=-1)
+    hs, cs, z = _run(p, D, H, xfull, h0, c0, reset)
+    hs2, cs2, z2 = _run(p2, Dk, H, xk, h0, c0, reset)
+    np.testing.assert_allclose(hs2, hs, rtol=0, atol=1e-13)
+    np.testing.assert_allclose(cs2, cs, rtol=0, atol=1e-13)
+    np.testing.assert_allclose(z2, z, rtol=0, atol=1e-13)
+    # moments: the kept parameters keep theirs, the dropped columns' are gone
+    Po, Pn = split(m, D, H, A1), split(m2, Dk, H, A1)
+    assert np.array_equal(Pn["Wx"], Po["Wx"][:, :Dk]) and np.array_equal(Pn["b"], Po["b"])
+    assert np.array_equal(Pn["Wh"], Po["Wh"]) and np.array_equal(Pn["Wp"], Po["Wp"])
