@@ -230,7 +230,8 @@ def hbm_kernels(cfg, reps=20, warm=3):
     post-processing ahead of GAE at 1,152 and 13,107 games of ten heroes;
     the LSTM's input side (observation normalisation, pre-LSTM layer with
     the cross-hero pool, and its backward) at the step's shape with teams of
-    five (B = 2040); Adam at the step's parameter count and at 158,502,815.
+    five (B = 2040); the surgery that widens the LSTM from 2048 to 4096
+    units; Adam at the step's parameter count and at 158,502,815.
     The input-side layer entries also give the warm TFLOP/s of their GEMM
     work (2 N D Do each way) over the whole call.  Each is timed with events on the
     launch stream, median of `reps` after `warm` untimed calls, cold (a
@@ -314,6 +315,15 @@ def hbm_kernels(cfg, reps=20, warm=3):
     e["tflops_warm"] = round(fl / e["warm_us"] * 1e-6, 1)
     out.append(e)
     del oq, Wq, bq, yq, xq, dxq, dWq, dbq, pws, ows, ostats
+    # surgery: the paper's LSTM widening 2048 -> 4096 units (input 4096,
+    # heads 75), parameters and both moments
+    A1q = sum(cfg.head_sizes) + 1
+    n_old, n_new = o5.o5_param_count(D, 2048, A1q), o5.o5_param_count(D, 4096, A1q)
+    olds = [torch.randn(n_old, generator=gen, device=dev) * 0.02 for _ in range(3)]
+    news = [torch.empty(n_new, device=dev) for _ in range(3)]
+    out.append(entry("surgery_widen", f"D={D} H=2048->4096 A1={A1q}", 12 * (n_old + n_new),
+                     lambda: o5.o5_surgery_widen(D, 2048, A1q, D, 4096, *olds, *news, 1e-3, 7)))
+    del olds, news
     for n in (synth.n_params(cfg), 158502815):
         p = torch.randn(n, generator=gen, device=dev) * 0.02
         g = torch.randn(n, generator=gen, device=dev) * 1e-3

@@ -370,6 +370,44 @@ int o5_policy_sample(o5_dtype dt, int B, int H, int K, const int* head_sizes,
                      void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Surgery on the flat parameter vector (appendix "Surgery"; subsection
+ * "Continual Transfer via Surgery").  Layout of a vector for (D, H, A1):
+ * Wx [4H, D], Wh [4H, H], b [4H], Wp [A1, H], bp [A1], fp32, gate blocks
+ * (i, f, g, o) along 4H; o5_param_count(D, H, A1) gives its length (0 for
+ * sizes < 1).  m and v are Adam's moments in the same layout.
+ *
+ * o5_surgery_widen -- widen the LSTM from H to H2 >= H units and extend its
+ * input from D to D2 >= D features.  Old weights keep their places; the
+ * LSTM's new weights (rows of new units, columns of Wh reading new units,
+ * new biases) are scale * (2U - 1), U from Philox4x64-10 with counter
+ * (e div 4, 0, 0, 0) and key (seed, 1), word e mod 4, for element e of the
+ * new vector, U = ((word >> 40) + 1/2) / 2^24 (the paper used values much
+ * smaller than the existing weights); columns of Wx reading new inputs and
+ * columns of Wp reading new units are 0, so with scale = 0 the widened
+ * network computes the old function exactly on the old units.  Old
+ * parameters keep their moments, new ones start at 0 (the paper restarts
+ * with learning rate 0 for a while: o5_adam_step with lr = 0 leaves p
+ * bitwise unchanged while the moments adapt).
+ * m_old, v_old may be NULL (zeros).  The new buffers must not overlap the
+ * old ones.
+ *
+ * o5_surgery_fold_input -- the last D - Dk inputs of the LSTM are a constant
+ * vector E [D - Dk] (appendix "Bloopers", subsection "Zero Team Spirit
+ * Embedding": a constant input is a modified bias): b' = b + Wx[:, Dk:] E,
+ * Wx' = Wx[:, :Dk], the rest copied; the dropped columns' moments are
+ * discarded, every other parameter keeps its moments.  1 <= Dk < D.
+ * ------------------------------------------------------------------------ */
+size_t o5_param_count(int D, int H, int A1);
+int o5_surgery_widen(int D, int H, int A1, int D2, int H2, const float* p_old,
+                     const float* m_old, const float* v_old, float* p_new,
+                     float* m_new, float* v_new, float scale, uint64_t seed,
+                     void* stream);
+int o5_surgery_fold_input(int D, int H, int A1, int Dk, const float* E,
+                          const float* p_old, const float* m_old,
+                          const float* v_old, float* p_new, float* m_new,
+                          float* v_new, void* stream);
+
+/* ------------------------------------------------------------------------
  * o5_f32_to_bf16 -- round n fp32 values to bfloat16 (nearest, ties to
  * even; NaN stays NaN).  Used to build the bf16 GEMM operands.
  * ------------------------------------------------------------------------ */

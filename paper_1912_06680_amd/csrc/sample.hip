@@ -14,33 +14,9 @@
 // for 4 consecutive logits of one head.
 #include "gemm_plan.h"
 #include "heads.h"
+#include "philox.h"
 
 namespace o5 {
-
-constexpr uint64_t kPhiloxM0 = 0xD2E7470EE14C6C93ull;
-constexpr uint64_t kPhiloxM1 = 0xCA5A826395121157ull;
-constexpr uint64_t kPhiloxW0 = 0x9E3779B97F4A7C15ull;  // golden ratio
-constexpr uint64_t kPhiloxW1 = 0xBB67AE8584CAA73Bull;  // sqrt(3) - 1
-
-// Philox4x64 with 10 rounds; the key is bumped by the Weyl increments
-// between rounds.
-__device__ __forceinline__ void philox4x64_10(uint64_t& c0, uint64_t& c1, uint64_t& c2, uint64_t& c3, uint64_t k0,
-                                              uint64_t k1) {
-#pragma unroll
-  for (int r = 0; r < 10; ++r) {
-    if (r > 0) {
-      k0 += kPhiloxW0;
-      k1 += kPhiloxW1;
-    }
-    const uint64_t hi0 = __umul64hi(kPhiloxM0, c0), lo0 = kPhiloxM0 * c0;
-    const uint64_t hi1 = __umul64hi(kPhiloxM1, c2), lo1 = kPhiloxM1 * c2;
-    const uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
-    c0 = n0;
-    c1 = lo1;
-    c2 = n2;
-    c3 = lo0;
-  }
-}
 
 // One thread per row b.  zpart: [S][B][A1] partial logits without bias.
 // avail [B][A] or null: unavailable logits are never drawn and leave the
@@ -75,7 +51,7 @@ __global__ void __launch_bounds__(256) gumbel_sample_rows(int B, int A1, int S, 
       float z = bp[o + a];
       for (int s = 0; s < S; ++s) z += zrow[s * sstride + o + a];
       const uint64_t word = (a & 3) == 0 ? w[0] : (a & 3) == 1 ? w[1] : (a & 3) == 2 ? w[2] : w[3];
-      const float u = (static_cast<float>(word >> 40) + 0.5f) * 5.9604644775390625e-08f;  // 2^-24
+      const float u = philox_uniform24(word);
       const float score = z - logf(-logf(u));
       if (besta < 0 || score > best) {
         best = score;

@@ -31,6 +31,7 @@ EXPORTED = (
     "o5_adam_step",
     "o5_policy_sample_workspace_bytes", "o5_policy_sample",
     "o5_f32_to_bf16",
+    "o5_param_count", "o5_surgery_widen", "o5_surgery_fold_input",
     "o5_ktimer_enable", "o5_ktimer_read", "o5_ktimer_site_name",
 )
 
@@ -88,6 +89,9 @@ _SIGS = {
     "o5_policy_sample_workspace_bytes": (_sz, [_i, _i, _i, _i, _vp]),
     "o5_policy_sample": (_i, [_i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _u64, _u64, _vp, _vp, _vp, _vp, _sz, _vp]),
     "o5_f32_to_bf16": (_i, [_sz, _vp, _vp, _vp]),
+    "o5_param_count": (_sz, [_i, _i, _i]),
+    "o5_surgery_widen": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _f, _u64, _vp]),
+    "o5_surgery_fold_input": (_i, [_i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "o5_ktimer_enable": (_i, [_i]),
     "o5_ktimer_read": (_i, [_i, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int)]),
     "o5_ktimer_site_name": (ctypes.c_char_p, [_i]),
@@ -259,6 +263,22 @@ def o5_policy_sample(dt, B, H, head_sizes, h, Wp, bp, seed, counter, act, logp, 
     _check("o5_policy_sample", lib().o5_policy_sample(
         dt, B, H, len(head_sizes), _heads(head_sizes), _p(h), _p(Wp), _p(bp), _p(avail), int(seed),
         int(counter), _p(act), _p(logp), _p(value), wp, wn, _stream(stream)))
+
+
+def o5_param_count(D, H, A1):
+    return lib().o5_param_count(D, H, A1)
+
+
+def o5_surgery_widen(D, H, A1, D2, H2, p_old, m_old, v_old, p_new, m_new, v_new, scale, seed, stream=None):
+    _check("o5_surgery_widen", lib().o5_surgery_widen(D, H, A1, D2, H2, _p(p_old), _p(m_old), _p(v_old), _p(p_new),
+                                                      _p(m_new), _p(v_new), float(scale), int(seed),
+                                                      _stream(stream)))
+
+
+def o5_surgery_fold_input(D, H, A1, Dk, E, p_old, m_old, v_old, p_new, m_new, v_new, stream=None):
+    _check("o5_surgery_fold_input", lib().o5_surgery_fold_input(D, H, A1, Dk, _p(E), _p(p_old), _p(m_old),
+                                                                _p(v_old), _p(p_new), _p(m_new), _p(v_new),
+                                                                _stream(stream)))
 
 
 def o5_f32_to_bf16(n, src, dst, stream=None):

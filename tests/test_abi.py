@@ -71,6 +71,18 @@ def test_host_validation_errors(lib):
     need = L.o5_reward_process_workspace_bytes(4, 4)
     assert need > 0
     assert L.o5_reward_process(4, 4, 16, None, 16, rhp, 16, 16, 16, need - 1, None) == 5
+    # input side: teams of five, widths multiple of 64
+    assert L.o5_prelstm_fwd(1, 2, 7, 64, 64, 16, 16, 16, 16, 16, None) == 2
+    assert L.o5_prelstm_fwd(1, 2, 10, 64, 96, 16, 16, 16, 16, 16, None) == 2
+    assert L.o5_prelstm_fwd(5, 2, 10, 64, 64, 16, 16, 16, 16, 16, None) == 3
+    assert L.o5_obs_normalize(0, 10, 6, 16, 16, 5.0, 1e-8, 16, 16, 1 << 20, None) == 2
+    assert L.o5_obs_normalize(0, 10, 8, 16, 16, 0.0, 1e-8, 16, 16, 1 << 20, None) == 7
+    # surgery: shrinking is not a widening; folding keeps at least one input
+    assert L.o5_surgery_widen(64, 64, 9, 32, 64, 16, None, None, 16, 16, 16, 0.01, 1, None) == 2
+    assert L.o5_surgery_widen(64, 64, 9, 64, 128, 16, None, None, 16, 16, 16, -1.0, 1, None) == 7
+    assert L.o5_surgery_widen(64, 64, 9, 64, 128, None, None, None, 16, 16, 16, 0.01, 1, None) == 1
+    assert L.o5_surgery_fold_input(64, 64, 9, 64, 16, 16, None, None, 16, 16, 16, None) == 2
+    assert L.o5_param_count(4096, 4096, 75) == 134541387
     # heads
     heads = (ctypes.c_int * 2)(3, 0)
     assert L.o5_ppo_loss_grad_workspace_bytes(0, 8, 64, 2, heads) == 0
