@@ -235,19 +235,23 @@ def hbm_kernels(cfg, reps=20, warm=3):
     The input-side layer entries also give the warm TFLOP/s of their GEMM
     work (2 N D Do each way) over the whole call.  Each is timed with events on the
     launch stream, median of `reps` after `warm` untimed calls, cold (a
-    512 MB buffer written before every call) and warm."""
+    512 MB buffer read before every call) and warm."""
     import torch
     from paper_1912_06680_amd import o5, synth
     dev = "cuda"
     gen = torch.Generator(device=dev)
     gen.manual_seed(0)
-    flush = torch.empty(128 << 20, dtype=torch.float32, device=dev)
+    flush = torch.ones(128 << 20, dtype=torch.float32, device=dev)
+    flush_sum = torch.zeros((), dtype=torch.float32, device=dev)
 
     def timed(fn, cold):
         ts = []
         for i in range(warm + reps):
             if cold:
-                flush.fill_(float(i))
+                # read 512 MB: evicts the inputs from the L2s and the infinity
+                # cache without leaving dirty lines to be written back during
+                # the timed call
+                flush_sum.copy_(flush.sum())
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record()

@@ -17,8 +17,9 @@
 //    64 consecutive segments at each step (coalesced), every input is read
 //    once, and a block of 8 waves covers 64 segments, so 11,520 segments
 //    (the paper's batch) already give 1,440 waves;
-//  * lane per segment (longer segments): each lane walks its whole segment
-//    backwards, coalesced as above.
+//  * otherwise (S >= 32768, or L > 256): a lane per 4 segments with 16-byte
+//    accesses when S is a multiple of 4, else a lane per segment; each lane
+//    walks its segments backwards, coalesced as above.
 #include "common.h"
 
 namespace o5 {
@@ -140,60 +141,82 @@ __global__ void __launch_bounds__(kGaeChunks * 64) gae_chunked(int L, int S, con
   }
 }
 
-// Lane = 4 consecutive segments (16-byte loads and stores: a wave moves 1 KB
-// of a row per instruction), walking backwards in chunks of kGaeLaneUnroll
-// steps whose loads are all issued before the recurrence runs.  S % 4 == 0.
-__global__ void __launch_bounds__(64) gae_lane4(int L, int S, const float* __restrict__ r,
-                                                const float* __restrict__ v, const uint8_t* __restrict__ done,
-                                                float gamma, float gl, float* __restrict__ adv,
-                                                float* __restrict__ ret) {
-  const int g = blockIdx.x * blockDim.x + threadIdx.x;  // segments 4g .. 4g + 3
-  const size_t S4 = static_cast<size_t>(S) / 4;
-  if (static_cast<size_t>(g) >= S4) return;
-  const float4* r4 = reinterpret_cast<const float4*>(r);
-  const float4* v4 = reinterpret_cast<const float4*>(v);
-  const uchar4* d4 = reinterpret_cast<const uchar4*>(done);
-  float4* a4 = reinterpret_cast<float4*>(adv);
-  float4* q4 = reinterpret_cast<float4*>(ret);
-  float cy[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  const float4 vl = v4[static_cast<size_t>(L) * S4 + g];
-  float vn[4] = {vl.x, vl.y, vl.z, vl.w};
-  auto step = [&](size_t idx, const float4& rq, const float4& vq, const uchar4& dq) {
-    const float rs[4] = {rq.x, rq.y, rq.z, rq.w};
-    const float vs[4] = {vq.x, vq.y, vq.z, vq.w};
-    const uint8_t ds[4] = {dq.x, dq.y, dq.z, dq.w};
-    float ao[4], ro[4];
+// V consecutive segments per lane (V = 4: 16-byte loads and stores, a wave
+// moves 1 KB of a row per instruction), walking backwards in chunks of
+// kGaeLaneUnroll steps whose loads are all issued before the recurrence
+// runs.  S % V == 0.
+template <int V> struct GaeVec;
+template <> struct GaeVec<2> {
+  typedef float2 F;
+  typedef uchar2 U;
+  __device__ static float get(const F& v, int k) { return k == 0 ? v.x : v.y; }
+  __device__ static uint8_t get(const U& v, int k) { return k == 0 ? v.x : v.y; }
+  __device__ static F make(const float* a) { return make_float2(a[0], a[1]); }
+};
+template <> struct GaeVec<4> {
+  typedef float4 F;
+  typedef uchar4 U;
+  __device__ static float get(const F& v, int k) { return k == 0 ? v.x : k == 1 ? v.y : k == 2 ? v.z : v.w; }
+  __device__ static uint8_t get(const U& v, int k) { return k == 0 ? v.x : k == 1 ? v.y : k == 2 ? v.z : v.w; }
+  __device__ static F make(const float* a) { return make_float4(a[0], a[1], a[2], a[3]); }
+};
+
+template <int V>
+__global__ void __launch_bounds__(64) gae_laneV(int L, int S, const float* __restrict__ r, const float* __restrict__ v,
+                                                const uint8_t* __restrict__ done, float gamma, float gl,
+                                                float* __restrict__ adv, float* __restrict__ ret) {
+  typedef GaeVec<V> G;
+  typedef typename G::F F;
+  typedef typename G::U U;
+  const int g = blockIdx.x * blockDim.x + threadIdx.x;  // segments V g .. V g + V - 1
+  const size_t SV = static_cast<size_t>(S) / V;
+  if (static_cast<size_t>(g) >= SV) return;
+  const F* rv = reinterpret_cast<const F*>(r);
+  const F* vv4 = reinterpret_cast<const F*>(v);
+  const U* dv = reinterpret_cast<const U*>(done);
+  F* av = reinterpret_cast<F*>(adv);
+  F* qv = reinterpret_cast<F*>(ret);
+  float cy[V], vn[V];
+  const F vl = vv4[static_cast<size_t>(L) * SV + g];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const float nd = ds[k] ? 0.0f : 1.0f;
-      const float delta = rs[k] + gamma * nd * vn[k] - vs[k];
+  for (int k = 0; k < V; ++k) {
+    cy[k] = 0.0f;
+    vn[k] = G::get(vl, k);
+  }
+  auto step = [&](size_t idx, const F& rq, const F& vq, const U& dq) {
+    float ao[V], ro[V];
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+      const float nd = G::get(dq, k) ? 0.0f : 1.0f;
+      const float vs = G::get(vq, k);
+      const float delta = G::get(rq, k) + gamma * nd * vn[k] - vs;
       cy[k] = delta + gl * nd * cy[k];
       ao[k] = cy[k];
-      ro[k] = cy[k] + vs[k];
-      vn[k] = vs[k];
+      ro[k] = cy[k] + vs;
+      vn[k] = vs;
     }
-    a4[idx] = make_float4(ao[0], ao[1], ao[2], ao[3]);
-    q4[idx] = make_float4(ro[0], ro[1], ro[2], ro[3]);
+    av[idx] = G::make(ao);
+    qv[idx] = G::make(ro);
   };
   int t_hi = L - 1;
   while (t_hi + 1 >= kGaeLaneUnroll) {
-    float4 rr[kGaeLaneUnroll], vv[kGaeLaneUnroll];
-    uchar4 dd[kGaeLaneUnroll];
+    F rr[kGaeLaneUnroll], vq[kGaeLaneUnroll];
+    U dd[kGaeLaneUnroll];
 #pragma unroll
     for (int u = 0; u < kGaeLaneUnroll; ++u) {
-      const size_t idx = static_cast<size_t>(t_hi - u) * S4 + g;
-      rr[u] = r4[idx];
-      vv[u] = v4[idx];
-      dd[u] = d4[idx];
+      const size_t idx = static_cast<size_t>(t_hi - u) * SV + g;
+      rr[u] = rv[idx];
+      vq[u] = vv4[idx];
+      dd[u] = dv[idx];
     }
     __builtin_amdgcn_sched_barrier(0);  // keep every load of the chunk ahead of the recurrence
 #pragma unroll
-    for (int u = 0; u < kGaeLaneUnroll; ++u) step(static_cast<size_t>(t_hi - u) * S4 + g, rr[u], vv[u], dd[u]);
+    for (int u = 0; u < kGaeLaneUnroll; ++u) step(static_cast<size_t>(t_hi - u) * SV + g, rr[u], vq[u], dd[u]);
     t_hi -= kGaeLaneUnroll;
   }
   for (; t_hi >= 0; --t_hi) {
-    const size_t idx = static_cast<size_t>(t_hi) * S4 + g;
-    step(idx, r4[idx], v4[idx], d4[idx]);
+    const size_t idx = static_cast<size_t>(t_hi) * SV + g;
+    step(idx, rv[idx], vv4[idx], dv[idx]);
   }
 }
 
@@ -277,6 +300,7 @@ using namespace o5;
 // for one per segment, and 16-byte accesses stream better).
 static constexpr int kGaeWaveScanMaxS = 4096;
 static constexpr int kGaeChunkedMaxS = 32768;
+static constexpr int kGaeLaneV = 4;  // segments per lane of the large-S kernel
 
 extern "C" int o5_gae(int L, int S, const float* r, const float* v, const uint8_t* done, float gamma,
                       float lambda, float* adv, float* ret, void* stream) {
@@ -297,10 +321,10 @@ extern "C" int o5_gae(int L, int S, const float* r, const float* v, const uint8_
   } else if (S < kGaeChunkedMaxS && L <= kGaeChunks * kGaeChunkMax) {
     hipLaunchKernelGGL(gae_chunked, dim3((S + 63) / 64), dim3(kGaeChunks * 64), 0, as_stream(stream), L, S, r, v,
                        done, gamma, gl, adv, ret);
-  } else if (S % 4 == 0 && aligned16(r) && aligned16(v) && aligned16(adv) && aligned16(ret) &&
-             reinterpret_cast<uintptr_t>(done) % 4 == 0) {
-    hipLaunchKernelGGL(gae_lane4, dim3((S / 4 + 63) / 64), dim3(64), 0, as_stream(stream), L, S, r, v, done,
-                       gamma, gl, adv, ret);
+  } else if (S % kGaeLaneV == 0 && aligned16(r) && aligned16(v) && aligned16(adv) && aligned16(ret) &&
+             reinterpret_cast<uintptr_t>(done) % kGaeLaneV == 0) {
+    hipLaunchKernelGGL(gae_laneV<kGaeLaneV>, dim3((S / kGaeLaneV + 63) / 64), dim3(64), 0, as_stream(stream), L, S,
+                       r, v, done, gamma, gl, adv, ret);
   } else {
     hipLaunchKernelGGL(gae_lane_per_segment, dim3((S + 255) / 256), dim3(256), 0, as_stream(stream), L,
                        S, r, v, done, gamma, gl, adv, ret);
