@@ -201,7 +201,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
     st[1] += verr * verr;
     st[2] += ent;
     st[3] += fabsf(ratio - 1.0f) > clip_eps ? 1.0f : 0.0f;
-    st[4] += (ratio - 1.0f) - dlog;
+    st[4] += expm1f(dlog) - dlog;  // (r - 1) - log r without the cancellation in r - 1
     st[5] += ratio;
     st[6] += isfinite(row_loss) ? 0.0f : 1.0f;
   }

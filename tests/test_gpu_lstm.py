@@ -77,6 +77,11 @@ CASES = [
     ("bf16-ragged-reset", 3, 300, 128, 192, True, 0.2),
     ("bf16-mid", 16, 256, 1024, 1024, True, 0.005),
     ("bf16-tall", 4, 520, 256, 320, True, 0.05),
+    # one step (no recurrent-gradient GEMM at all), a single sequence, an
+    # input wider than the state
+    ("f32-T1-B1", 1, 1, 64, 64, False, 0.0),
+    ("bf16-T1", 1, 130, 128, 64, True, 0.0),
+    ("bf16-wide-input", 2, 96, 320, 128, True, 0.1),
 ]
 
 

@@ -78,6 +78,9 @@ PPO_CASES = [
     ("f32-avail", 777, 128, HEADS, False, True, True),
     ("bf16-avail-wide", 500, 128, (100, 60, 30), True, True, True),
     ("f32-avail-no-head-mask", 300, 64, (5, 3, 7), False, False, True),
+    # a single row; single-logit heads (certain actions)
+    ("f32-one-row", 1, 64, HEADS, False, False, False),
+    ("bf16-single-logit-heads", 100, 64, (1, 4, 1), True, True, False),
 ]
 
 
