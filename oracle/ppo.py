@@ -30,6 +30,16 @@ Shapes: h [N, H]; Wp [A+1, H] with the last row the value head; bp [A+1];
 act [N, K] (integer index within each head); logp_old, adv, ret [N];
 head_mask [N, K] or None (all ones); avail [N, A] (1 = available) or None
 (all available).
+
+Unit-selection head (appendix "Neural Network Architecture": the unit
+embeddings from the observation processing are carried beside the LSTM and
+used by the action heads to choose a unit to target).  Optionally head k
+scores its n_k units against per-row embeddings E [N, n_k, d]: a query
+q = h Wq^T + bq [N, d], logits z_k[n, u] = <q[n], E[n, u]>.  Reading: the
+query is a linear projection of the LSTM state, the score a plain dot
+product; the rows of Wp and bp that belong to head k are then unused (zero
+gradient).  The gradient reaches Wq, bq and h through q; none is taken into
+E (the observation encoder is not part of this build).
 """
 import numpy as np
 
@@ -81,12 +91,20 @@ def head_logprob_entropy(z, act, head_sizes, avail=None):
     return logp, ent, probs
 
 
+def unit_logits(h, Wq, bq, E):
+    """Query q = h Wq^T + bq and logits z[n, u] = <q[n], E[n, u]>."""
+    q = np.asarray(h, np.float64) @ np.asarray(Wq, np.float64).T + np.asarray(bq, np.float64)
+    return q, np.einsum("nj,nuj->nu", q, np.asarray(E, np.float64))
+
+
 def ppo_loss_grad(h, Wp, bp, act, logp_old, adv, ret, head_sizes,
                   clip_eps=0.2, vf_coef=1.0, ent_coef=0.01, head_mask=None,
-                  avail=None):
+                  avail=None, unit=None):
     """Loss statistics and gradients with respect to h, Wp and bp.
 
-    Returns (stats dict, dh [N,H], dWp [A+1,H], dbp [A+1], z [N,A+1]).
+    Returns (stats dict, dh [N,H], dWp [A+1,H], dbp [A+1], z [N,A+1]); with
+    ``unit`` = dict(head=k, Wq=[d,H], bq=[d], E=[N,n_k,d]) also
+    (dWq [d,H], dbq [d]) as a sixth element.
     """
     h = np.asarray(h, np.float64)
     Wp = np.asarray(Wp, np.float64)
@@ -102,6 +120,9 @@ def ppo_loss_grad(h, Wp, bp, act, logp_old, adv, ret, head_sizes,
         np.asarray(head_mask, np.float64)
 
     z = heads_forward(h, Wp, bp)
+    if unit is not None:
+        ku = unit["head"]
+        _, z[:, off[ku]:off[ku + 1]] = unit_logits(h, unit["Wq"], unit["bq"], unit["E"])
     V = z[:, A]
     logp, ent_k, probs = head_logprob_entropy(z, act, head_sizes, avail)
     on = mask != 0
@@ -149,7 +170,18 @@ def ppo_loss_grad(h, Wp, bp, act, logp_old, adv, ret, head_sizes,
         dz[:, off[k]:off[k + 1]] = np.where(use & av, dpg - (ent_coef / N) * dent, 0.0)
     dz[:, A] = 2.0 * vf_coef * verr / N
 
-    dh = dz @ Wp
+    if unit is None:
+        dh = dz @ Wp
+        dWp = dz.T @ h
+        dbp = dz.sum(axis=0)
+        return stats, dh, dWp, dbp, z
+    # head k's logits come from the query: its gradient goes to q, not to Wp
+    ku = unit["head"]
+    dz_u = dz[:, off[ku]:off[ku + 1]].copy()
+    dz[:, off[ku]:off[ku + 1]] = 0.0
+    Wq = np.asarray(unit["Wq"], np.float64)
+    dq = np.einsum("nu,nuj->nj", dz_u, np.asarray(unit["E"], np.float64))
+    dh = dz @ Wp + dq @ Wq
     dWp = dz.T @ h
     dbp = dz.sum(axis=0)
-    return stats, dh, dWp, dbp, z
+    return stats, dh, dWp, dbp, z, (dq.T @ h, dq.sum(axis=0))
