@@ -228,7 +228,10 @@ def hbm_kernels(cfg, reps=20, warm=3):
     latency-bound), 11,520 (the paper's 2.9M-timestep batch) and 131,072
     (33.5M timesteps, beyond the 256 MB infinity cache); the reward
     post-processing ahead of GAE at 1,152 and 13,107 games of ten heroes;
-    the LSTM's input side (observation normalisation, pre-LSTM layer with
+    the PPO loss with a unit-selection head scoring 189 units against
+    128-wide embeddings at the step's shape (bytes: the embeddings read once
+    each way, h read twice, dh written); the LSTM's input side
+    (observation normalisation, pre-LSTM layer with
     the cross-hero pool, and its backward) at the step's shape with teams of
     five (B = 2040); the surgery that widens the LSTM from 2048 to 4096
     units; Adam at the step's parameter count and at 158,502,815.
@@ -319,6 +322,34 @@ def hbm_kernels(cfg, reps=20, warm=3):
     e["tflops_warm"] = round(fl / e["warm_us"] * 1e-6, 1)
     out.append(e)
     del oq, Wq, bq, yq, xq, dxq, dWq, dbq, pws, ows, ostats
+    # the PPO loss at the step's shape with a unit-selection head: head 1
+    # scores 189 units (the paper's count) against 128-wide embeddings
+    uheads = (cfg.head_sizes[0], 189) + tuple(cfg.head_sizes[2:])
+    Nu, Hu, du = cfg.T * cfg.B, cfg.H, 128
+    A1u = sum(uheads) + 1
+    dtu = o5.O5_BF16 if cfg.dtype == "bf16" else o5.O5_F32
+    etu = torch.bfloat16 if dtu == o5.O5_BF16 else torch.float32
+    hu = torch.tanh(torch.randn((Nu, Hu), generator=gen, device=dev)).to(etu)
+    Wpu = (torch.randn((A1u, Hu), generator=gen, device=dev) / Hu ** 0.5).to(etu)
+    bpu = torch.zeros(A1u, device=dev)
+    Wqu = (torch.randn((du, Hu), generator=gen, device=dev) / Hu ** 0.5).to(etu)
+    bqu = torch.zeros(du, device=dev)
+    Eu = (torch.randn((Nu, 189, du), generator=gen, device=dev) / du ** 0.5).to(etu)
+    actu = torch.stack([torch.randint(0, n, (Nu,), generator=gen, device=dev) for n in uheads], 1).to(torch.int32)
+    lpu = torch.full((Nu,), -10.0, device=dev)
+    advu, retu = torch.randn(Nu, generator=gen, device=dev), torch.randn(Nu, generator=gen, device=dev)
+    stu, dhu = torch.empty(8, device=dev), torch.empty((Nu, Hu), device=dev)
+    dWpu, dbpu = torch.empty((A1u, Hu), device=dev), torch.empty(A1u, device=dev)
+    dWqu, dbqu = torch.empty((du, Hu), device=dev), torch.empty(du, device=dev)
+    uh = o5.unit_head(1, du, Wqu, bqu, Eu, dWqu, dbqu)
+    uws = torch.empty(o5.o5_ppo_loss_grad_workspace_bytes(dtu, Nu, Hu, uheads, unit=uh), dtype=torch.uint8,
+                      device=dev)
+    ebytes = Nu * 189 * du * Eu.element_size()
+    out.append(entry("ppo_loss_grad_unit_head", f"N={Nu} H={Hu} heads={list(uheads)} unit head 1 d={du}",
+                     2 * ebytes + Nu * Hu * (2 * hu.element_size() + 4),
+                     lambda: o5.o5_ppo_loss_grad(dtu, Nu, Hu, uheads, hu, Wpu, bpu, actu, lpu, advu, retu, None, 0.2,
+                                                 1.0, 0.01, stu, dhu, dWpu, dbpu, uws, unit=uh)))
+    del hu, Wpu, Wqu, Eu, dhu, uws
     # surgery: the paper's LSTM widening 2048 -> 4096 units (input 4096,
     # heads 75), parameters and both moments
     A1q = sum(cfg.head_sizes) + 1

@@ -291,6 +291,7 @@ int o5_segments_to_samples(int L, int S, int T, const float* adv, const float* r
  *          with no available logit in a row adds nothing; an unavailable
  *          taken action has log-probability -inf (ratio 0).  A head with
  *          head_mask 0 adds nothing in every case.
+ * unit     host pointer to an o5_unit_head, or NULL.
  * hp       {clip_eps, vf_coef, ent_coef}.
  * stats    out [8] fp32: total, pg, vf, ent, clipfrac (mean |r-1| > eps),
  *          approx_kl (mean (r - 1) - log r), mean_ratio, nonfinite (rows
@@ -305,13 +306,34 @@ typedef struct {
   float ent_coef; /* 0.01 */
 } o5_ppo_hp;
 
+/* Unit-selection head (appendix "Neural Network Architecture": the unit
+ * embeddings of the observation processing travel beside the LSTM and the
+ * action heads use them to choose a unit to target).  Head `head` scores its
+ * n_head units against per-row embeddings instead of its rows of Wp, bp:
+ *
+ *   q = h Wq^T + bq [N, d],   z_head[n, u] = <q[n], E[n, u]>
+ *
+ * Those rows of Wp and bp are unused (o5_ppo_loss_grad writes zero gradient
+ * for them); the gradient reaches Wq, bq and h through q, none goes to E.
+ * Passed by host pointer; NULL = no such head. */
+typedef struct {
+  int head;        /* 0 <= head < K */
+  int d;           /* query and embedding width, a power of two in 8..512 */
+  const void* Wq;  /* [d, H] dt */
+  const float* bq; /* [d] */
+  const void* E;   /* [N, n_head, d] dt (rows as h) */
+  float* dWq;      /* out [d, H] (o5_ppo_loss_grad only) */
+  float* dbq;      /* out [d] (o5_ppo_loss_grad only) */
+} o5_unit_head;
+
 size_t o5_ppo_loss_grad_workspace_bytes(o5_dtype dt, int N, int H, int K,
-                                        const int* head_sizes);
+                                        const int* head_sizes,
+                                        const o5_unit_head* unit);
 int o5_ppo_loss_grad(o5_dtype dt, int N, int H, int K, const int* head_sizes,
                      const void* h, const void* Wp, const float* bp,
                      const int32_t* act, const float* logp_old, const float* adv,
                      const float* ret, const uint8_t* head_mask,
-                     const uint8_t* avail, o5_ppo_hp hp,
+                     const uint8_t* avail, const o5_unit_head* unit, o5_ppo_hp hp,
                      float* stats, float* dh, float* dWp, float* dbp,
                      void* ws, size_t ws_bytes, void* stream);
 
@@ -356,16 +378,19 @@ int o5_adam_step(size_t n, float* p, float* m, float* v, const float* g,
  *
  * dt, B, H, K, head_sizes, h [B, H], Wp, bp: as for o5_ppo_loss_grad.
  * avail    [B, A] uint8 or NULL (all available), as for o5_ppo_loss_grad.
+ * unit     host pointer to an o5_unit_head (dWq, dbq unused), or NULL.
  * act      out [B, K] int32; -1 for a head with no available logit.
  * logp     out [B] fp32, joint log-probability of the sampled action (heads
  *          with no available logit add nothing).   value: out [B] fp32.
  * ws       scratch of o5_policy_sample_workspace_bytes(...) bytes.
  * ------------------------------------------------------------------------ */
 size_t o5_policy_sample_workspace_bytes(o5_dtype dt, int B, int H, int K,
-                                        const int* head_sizes);
+                                        const int* head_sizes,
+                                        const o5_unit_head* unit);
 int o5_policy_sample(o5_dtype dt, int B, int H, int K, const int* head_sizes,
                      const void* h, const void* Wp, const float* bp,
-                     const uint8_t* avail, uint64_t seed, uint64_t counter,
+                     const uint8_t* avail, const o5_unit_head* unit,
+                     uint64_t seed, uint64_t counter,
                      int32_t* act, float* logp, float* value,
                      void* ws, size_t ws_bytes, void* stream);
 

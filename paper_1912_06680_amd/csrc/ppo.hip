@@ -63,7 +63,9 @@ __device__ __forceinline__ float column(const float (&z)[CPL], int c) {
 // not added).  avail [N][A] (or null = all available): an unavailable logit
 // is left out of its head's softmax and gets no gradient; a head with no
 // available logit adds nothing; an unavailable taken action has
-// log-probability -inf.  Writes dz [N][A1]; on the bf16 path the (hi, lo) pair in row
+// log-probability -inf.  Head kext (or none, -1) takes its logits from zext
+// [N][n_kext] (the unit-selection head) and returns their gradient in dzext
+// instead of dz and its sums.  Writes dz [N][A1]; on the bf16 path the (hi, lo) pair in row
 // layout [N][ld_hilo] and, when dzT is set, transposed as [2 ld_hilo][ldT]
 // (hi rows, then lo rows; columns n >= N zero).  Each block writes one row
 // of part: the column sums of its dz (A1 values), then the sums of its rows'
@@ -75,9 +77,9 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
     int N, int A1, int S, const float* __restrict__ zpart, const float* __restrict__ bp,
     const int32_t* __restrict__ act, const float* __restrict__ logp_old, const float* __restrict__ adv,
     const float* __restrict__ ret, const uint8_t* __restrict__ mask, const uint8_t* __restrict__ avail, HeadsMeta hm,
-    float clip_eps, float vf_coef,
+    const float* __restrict__ zext, float* __restrict__ dzext, int kext, float clip_eps, float vf_coef,
     float ent_coef, float invN, float* __restrict__ dz, float* __restrict__ part, uint16_t* __restrict__ dz_hi,
-    uint16_t* __restrict__ dz_lo, int ld_hilo, uint16_t* __restrict__ dzT, int ldT) {
+    uint16_t* __restrict__ dz_lo, int ncol_hilo, int ld_hilo, uint16_t* __restrict__ dzT, int ldT) {
   __shared__ float red[kWavesPerBlock][CPL * 64 + kStatCols];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int K = hm.K, A = hm.A;
@@ -92,8 +94,8 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
   float csum[CPL] = {};
   float st[kStatCols] = {};
   // the transposed pair is kept in registers (16 rows x 2 bytes per column)
-  // only for up to 128 logit columns; beyond that dzT must be null
-  constexpr bool kT = CPL <= 2;
+  // only for up to 256 logit columns; beyond that dzT must be null
+  constexpr bool kT = CPL <= 4;
   constexpr int TC = kT ? CPL : 1;
   uint32_t thi[TC][kRowsPerWave / 2] = {}, tlo[TC][kRowsPerWave / 2] = {};
   const size_t sstride = static_cast<size_t>(N) * A1;
@@ -106,7 +108,10 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
     for (int i = 0; i < CPL; ++i) {
       const int a = lane + 64 * i;
       float v = 0.0f;
-      if (a < A1) {
+      if (head[i] >= 0 && head[i] == kext) {
+        const int nk = hm.off[kext + 1] - hm.off[kext];
+        v = zext[static_cast<size_t>(n) * nk + (a - hm.off[kext])];
+      } else if (a < A1) {
         v = bp[a];
         for (int s2 = 0; s2 < S; ++s2) v += zpart[s2 * sstride + static_cast<size_t>(n) * A1 + a];
       }
@@ -178,9 +183,14 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
           const float onehot = (a - hm.off[k] == ak[k]) ? 1.0f : 0.0f;
           d = g_logpi * (onehot - p) + ent_scale * p * (z[i] - zbar[k]);
         }
+      if (head[i] >= 0 && head[i] == kext) {
+        const int nk = hm.off[kext + 1] - hm.off[kext];
+        dzext[static_cast<size_t>(n) * nk + (a - hm.off[kext])] = d;
+        d = 0.0f;  // these logits do not depend on Wp, bp
+      }
       if (a < A1) dz[static_cast<size_t>(n) * A1 + a] = d;
       csum[i] += d;
-      if (dz_hi != nullptr && a < ld_hilo) {
+      if (dz_hi != nullptr && a < ncol_hilo) {
         const uint16_t hb = f32_to_bf16_bits(d);
         const uint16_t lb = f32_to_bf16_bits(d - bf16_bits_to_f32(hb));
         dz_hi[static_cast<size_t>(n) * ld_hilo + a] = hb;
@@ -211,9 +221,10 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
 #pragma unroll
     for (int i = 0; i < TC; ++i) {
       const int a = lane + 64 * i;
-      if (a < ld_hilo) {
+      if (a < ncol_hilo) {
         *reinterpret_cast<uint2*>(dzT + static_cast<size_t>(a) * ldT + n0) = make_uint2(thi[i][0], thi[i][1]);
-        *reinterpret_cast<uint2*>(dzT + static_cast<size_t>(ld_hilo + a) * ldT + n0) = make_uint2(tlo[i][0], tlo[i][1]);
+        *reinterpret_cast<uint2*>(dzT + static_cast<size_t>(ncol_hilo + a) * ldT + n0) =
+            make_uint2(tlo[i][0], tlo[i][1]);
       }
     }
   }
@@ -237,31 +248,6 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
   }
 }
 
-// dWp[a, j] = sum over splits s of part[s, a, j] + part[s, A1p + a, j]
-// (the hi and lo halves), fixed order.
-__global__ void __launch_bounds__(256) sum_hilo_splits(int S, int A1, int A1p, int H, const float* __restrict__ part,
-                                                       float* __restrict__ out) {
-  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= static_cast<size_t>(A1) * H) return;
-  const size_t hs = static_cast<size_t>(A1p) * H;  // offset of the lo half
-  float v = 0.0f;
-  for (int s2 = 0; s2 < S; ++s2) {
-    const float* p = part + static_cast<size_t>(s2) * 2 * hs;
-    v += p[i] + p[hs + i];
-  }
-  out[i] = v;
-}
-
-// dst [R, H] bf16 = src [A1, H] with rows A1..R-1 zero.
-__global__ void __launch_bounds__(256) pad_rows_bf16(int A1, int R, int H, const uint16_t* __restrict__ src,
-                                                     uint16_t* __restrict__ dst) {
-  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  const size_t total = static_cast<size_t>(R) * H;
-  if (i >= total) return;
-  const int r = static_cast<int>(i / H);
-  dst[i] = r < A1 ? src[i] : static_cast<uint16_t>(0);
-}
-
 // stats from the summed block partials (sums = [dz column sums (A1) | row
 // stat sums (kStatCols)]); also copies the bias gradient out.
 __global__ void ppo_finalize(int A1, const float* __restrict__ sums, float invN, float vf_coef, float ent_coef,
@@ -281,29 +267,31 @@ __global__ void ppo_finalize(int A1, const float* __restrict__ sums, float invN,
 }
 
 struct PpoWs {
-  size_t zpart, dz, part, sums, wpart, dzhi, dzlo, dzT, wpad, total;
+  size_t zpart, dz, part, sums, wpart, dzhi, dzlo, dzT, wpad, unit, total;
+  UnitWs uw;  // the unit-selection head's scratch, at offset unit (if any)
   GemmPlan plan_z, plan_w, plan_h;
-  int nblk, A1, A1p, ldT, wsplits;
+  int nblk, A1, A1p, ldh, ldT, wsplits;  // ldh: row length of the (hi, lo) pair, A1p + the unit head's dp
   bool dwp_t;  // dWp from the transposed (hi; lo) pair, h read once
 };
 
-static PpoWs ppo_ws(o5_dtype dt, int N, int H, int A1) {
-  PpoWs w;
+static PpoWs ppo_ws(o5_dtype dt, int N, int H, int A1, int unit_nk = 0, int unit_d = 0) {
+  PpoWs w{};
   const bool bf = dt == O5_BF16;
   w.A1 = A1;
   w.A1p = cdiv(A1, 64) * 64;  // padded logit count: a multiple of the K tile
+  w.ldh = w.A1p + (unit_d > 0 ? cdiv(unit_d, 64) * 64 : 0);
   w.nblk = cdiv(N, kRowsPerBlock);
   w.ldT = w.nblk * kRowsPerBlock;
-  w.dwp_t = bf && w.A1p <= 128;
+  w.dwp_t = bf && w.A1p <= 256;
   w.plan_z = plan_gemm(bf, N, A1, H);
   w.plan_w = bf ? plan_gemm(true, A1, H, 2 * N) : plan_gemm(false, A1, H, N);
-  w.plan_h = bf ? plan_gemm(true, N, H, 2 * w.A1p) : GemmPlan{false, BfTile::k128x128, 1, 256};
+  w.plan_h = bf ? plan_gemm(true, N, H, 2 * w.ldh) : GemmPlan{false, BfTile::k128x128, 1, 256};
   w.plan_h.splits = 1;
   w.wsplits = 1;
   if (w.dwp_t) {
-    // M = 2 A1p (one 256-row tile), N = H, K = N: split K so the grid has
-    // about 256 blocks, each with at least 8 K tiles of 32
-    const int tiles = cdiv(H, 256);
+    // M = 2 A1p (one or two 256-row tiles), N = H, K = N: split K so the
+    // grid has about 256 blocks, each with at least 8 K tiles of 32
+    const int tiles = cdiv(2 * w.A1p, 256) * cdiv(H, 256);
     w.wsplits = std::max(1, std::min(cdiv(256, tiles), cdiv(N, 32) / 8));
   }
   size_t o = 0;
@@ -321,15 +309,20 @@ static PpoWs ppo_ws(o5_dtype dt, int N, int H, int A1) {
   w.dzhi = w.dzlo = w.dzT = w.wpad = 0;
   if (bf) {
     w.dzhi = o;
-    o += align_up(static_cast<size_t>(N) * w.A1p * 2);
+    o += align_up(static_cast<size_t>(N) * w.ldh * 2);
     w.dzlo = o;
-    o += align_up(static_cast<size_t>(N) * w.A1p * 2);
+    o += align_up(static_cast<size_t>(N) * w.ldh * 2);
     w.wpad = o;
-    o += align_up(static_cast<size_t>(w.A1p) * H * 2);
+    o += align_up(static_cast<size_t>(w.ldh) * H * 2);
     if (w.dwp_t) {
       w.dzT = o;
       o += align_up(static_cast<size_t>(2) * w.A1p * w.ldT * 2);
     }
+  }
+  w.unit = o;
+  if (unit_d > 0) {
+    w.uw = unit_ws(dt, N, H, unit_nk, unit_d, true);
+    o += align_up(w.uw.total);
   }
   w.total = o;
   return w;
@@ -357,17 +350,18 @@ int check_heads(const char* fn, o5_dtype dt, int N, int H, int K, const int* hea
 template <int CPL>
 static void launch_rows(const PpoWs& w, int N, int A1, int S, const float* zpart, const float* bp, const int32_t* act,
                         const float* logp_old, const float* adv, const float* ret, const uint8_t* mask,
-                        const uint8_t* avail, const HeadsMeta& hm, o5_ppo_hp hp, float invN, float* dz, float* part,
-                        uint16_t* dzhi, uint16_t* dzlo, uint16_t* dzT, hipStream_t s) {
+                        const uint8_t* avail, const HeadsMeta& hm, const float* zext, float* dzext, int kext,
+                        o5_ppo_hp hp, float invN, float* dz, float* part, uint16_t* dzhi, uint16_t* dzlo,
+                        uint16_t* dzT, hipStream_t s) {
   hipLaunchKernelGGL(ppo_rows<CPL>, dim3(w.nblk), dim3(kWavesPerBlock * 64), 0, s, N, A1, S, zpart, bp, act, logp_old,
-                     adv, ret, mask, avail, hm, hp.clip_eps, hp.vf_coef, hp.ent_coef, invN, dz, part, dzhi, dzlo, w.A1p, dzT,
-                     w.ldT);
+                     adv, ret, mask, avail, hm, zext, dzext, kext, hp.clip_eps, hp.vf_coef, hp.ent_coef, invN, dz, part, dzhi, dzlo, w.A1p,
+                     w.ldh, dzT, w.ldT);
 }
 
 template <typename E>
 static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, const float* bp, const int32_t* act,
                     const float* logp_old, const float* adv, const float* ret, const uint8_t* mask,
-                    const uint8_t* avail, o5_ppo_hp hp,
+                    const uint8_t* avail, const o5_unit_head* unit, o5_ppo_hp hp,
                     float* stats, float* dh, float* dWp, float* dbp, char* ws, const PpoWs& w, hipStream_t s) {
   const int A1 = hm.A + 1;
   float* zpart = reinterpret_cast<float*>(ws + w.zpart);
@@ -390,33 +384,51 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
     dzlo = reinterpret_cast<uint16_t*>(ws + w.dzlo);
     if (w.dwp_t) dzT = reinterpret_cast<uint16_t*>(ws + w.dzT);
   }
+  const float* zext = nullptr;
+  float* dzext = nullptr;
+  int kext = -1;
+  char* uws = ws + w.unit;
+  constexpr o5_dtype dt = sizeof(E) == 2 ? O5_BF16 : O5_F32;
+  if (unit != nullptr) {  // the unit-selection head's logits
+    kext = unit->head;
+    unit_forward(dt, N, H, w.uw.nk, *unit, h, uws, w.uw, s);
+    zext = reinterpret_cast<const float*>(uws + w.uw.zext);
+    dzext = reinterpret_cast<float*>(uws + w.uw.dzext);
+  }
   const int S = w.plan_z.splits;
   const int cpl = cdiv(A1, 64);
   if (cpl <= 1)
-    launch_rows<1>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, hp, invN, dz, part, dzhi, dzlo,
-                   dzT, s);
+    launch_rows<1>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz, part,
+                   dzhi, dzlo, dzT, s);
   else if (cpl <= 2)
-    launch_rows<2>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, hp, invN, dz, part, dzhi, dzlo,
-                   dzT, s);
+    launch_rows<2>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz, part,
+                   dzhi, dzlo, dzT, s);
   else if (cpl <= 4)
-    launch_rows<4>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, hp, invN, dz, part, dzhi, dzlo,
-                   dzT, s);
+    launch_rows<4>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz, part,
+                   dzhi, dzlo, dzT, s);
   else if (cpl <= 8)
-    launch_rows<8>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, hp, invN, dz, part, dzhi, dzlo,
-                   dzT, s);
+    launch_rows<8>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz, part,
+                   dzhi, dzlo, dzT, s);
   else
-    launch_rows<16>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, hp, invN, dz, part, dzhi, dzlo,
-                   dzT, s);
+    launch_rows<16>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz, part,
+                   dzhi, dzlo, dzT, s);
   if constexpr (sizeof(E) == 2) {
-    const int A1p = w.A1p;
+    const int A1p = w.A1p, ldh = w.ldh;
     uint16_t* wpad = reinterpret_cast<uint16_t*>(ws + w.wpad);
     hipLaunchKernelGGL(pad_rows_bf16, dim3(cdiv(static_cast<long long>(A1p) * H, 256)), dim3(256), 0, s, A1, A1p, H,
                        Wp, wpad);
-    {  // dh = [dz_hi | dz_lo] . [Wp ; Wp]  (K = 2 A1p)
-      KRows2<uint16_t> al{dzhi, dzlo, nullptr, A1p, A1p, A1p, 2 * A1p, N};
-      ICols2<uint16_t> bl{wpad, wpad, wpad, nullptr, H, H, 0, H, 2 * A1p, A1p};
+    if (unit != nullptr) {
+      // dq (hi, lo) into columns A1p .. ldh - 1 of the pair, Wq into the same rows of wpad
+      unit_grad(dt, N, H, w.uw.nk, *unit, h, uws, w.uw, dzhi, dzlo, A1p, ldh, s);
+      const int d = unit->d, dp = ldh - A1p;
+      hipLaunchKernelGGL(pad_rows_bf16, dim3(cdiv(static_cast<long long>(dp) * H, 256)), dim3(256), 0, s, d, dp, H,
+                         static_cast<const uint16_t*>(unit->Wq), wpad + static_cast<size_t>(A1p) * H);
+    }
+    {  // dh = [dz_hi dq_hi | dz_lo dq_lo] . [Wp Wq ; Wp Wq]  (K = 2 ldh)
+      KRows2<uint16_t> al{dzhi, dzlo, nullptr, ldh, ldh, ldh, 2 * ldh, N};
+      ICols2<uint16_t> bl{wpad, wpad, wpad, nullptr, H, H, 0, H, 2 * ldh, ldh};
       EpiStoreF32 epi{dh, H, 0};
-      run_gemm(w.plan_h, al, bl, epi, N, H, 2 * A1p, s);
+      run_gemm(w.plan_h, al, bl, epi, N, H, 2 * ldh, s);
     }
     if (w.dwp_t) {
       // [dWp_hi ; dWp_lo] = [hi ; lo]^T-rows . h  (M = 2 A1p, N = H, K = N), split over K
@@ -436,11 +448,19 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
                          w.plan_w.splits, A1 * H, wpart, dWp);
     }
   } else {
-    {  // dh = dz Wp  (fp32 FMA engine)
+    if (unit == nullptr) {  // dh = dz Wp  (fp32 FMA engine)
       KRows2<float> al{dz, nullptr, nullptr, A1, 0, A1, A1, N};
       ICols2<E> bl{Wp, nullptr, nullptr, nullptr, H, 0, H, H, A1, 0};
       EpiStoreF32 epi{dh, H, 0};
       launch_gemm_f32(al, bl, epi, N, H, A1, 1, s);
+    } else {  // dh = [dz | dq] . [Wp ; Wq]
+      unit_grad(dt, N, H, w.uw.nk, *unit, h, uws, w.uw, nullptr, nullptr, 0, 0, s);
+      const int d = unit->d;
+      const float* dq = reinterpret_cast<const float*>(uws + w.uw.dq);
+      KRows2<float> al{dz, dq, nullptr, A1, d, A1, A1 + d, N};
+      ICols2<E> bl{Wp, Wp, static_cast<const E*>(unit->Wq), nullptr, H, H, 0, H, A1 + d, A1};
+      EpiStoreF32 epi{dh, H, 0};
+      launch_gemm_f32(al, bl, epi, N, H, A1 + d, 1, s);
     }
     {  // dWp = dz^T h, split over rows
       ICols2<float> al{dz, nullptr, nullptr, nullptr, A1, 0, A1, A1, N, 0};
@@ -460,16 +480,19 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
 
 using namespace o5;
 
-extern "C" size_t o5_ppo_loss_grad_workspace_bytes(o5_dtype dt, int N, int H, int K, const int* head_sizes) {
+extern "C" size_t o5_ppo_loss_grad_workspace_bytes(o5_dtype dt, int N, int H, int K, const int* head_sizes,
+                                                   const o5_unit_head* unit) {
   HeadsMeta hm;
   if (check_heads("o5_ppo_loss_grad_workspace_bytes", dt, N, H, K, head_sizes, &hm) != O5_OK) return 0;
-  return ppo_ws(dt, N, H, hm.A + 1).total;
+  if (unit != nullptr && (unit->head < 0 || unit->head >= K || unit->d < 8 || unit->d > 512 || (unit->d & (unit->d - 1)) != 0)) return 0;
+  return unit ? ppo_ws(dt, N, H, hm.A + 1, hm.off[unit->head + 1] - hm.off[unit->head], unit->d).total
+              : ppo_ws(dt, N, H, hm.A + 1).total;
 }
 
 extern "C" int o5_ppo_loss_grad(o5_dtype dt, int N, int H, int K, const int* head_sizes, const void* h, const void* Wp,
                                 const float* bp, const int32_t* act, const float* logp_old, const float* adv,
-                                const float* ret, const uint8_t* head_mask, const uint8_t* avail, o5_ppo_hp hp,
-                                float* stats, float* dh,
+                                const float* ret, const uint8_t* head_mask, const uint8_t* avail,
+                                const o5_unit_head* unit, o5_ppo_hp hp, float* stats, float* dh,
                                 float* dWp, float* dbp, void* ws, size_t ws_bytes, void* stream) {
   HeadsMeta hm;
   int st = check_heads("o5_ppo_loss_grad", dt, N, H, K, head_sizes, &hm);
@@ -485,11 +508,16 @@ extern "C" int o5_ppo_loss_grad(o5_dtype dt, int N, int H, int K, const int* hea
   O5_PTR(ret, "ret");
   O5_OPT_PTR(head_mask, "head_mask");
   O5_OPT_PTR(avail, "avail");
+  if (unit != nullptr) {
+    st = check_unit("o5_ppo_loss_grad", hm, unit, true);
+    if (st != O5_OK) return st;
+  }
   O5_PTR(stats, "stats");
   O5_PTR(dh, "dh");
   O5_PTR(dWp, "dWp");
   O5_PTR(dbp, "dbp");
-  const PpoWs w = ppo_ws(dt, N, H, hm.A + 1);
+  const PpoWs w = unit ? ppo_ws(dt, N, H, hm.A + 1, hm.off[unit->head + 1] - hm.off[unit->head], unit->d)
+                       : ppo_ws(dt, N, H, hm.A + 1);
   O5_CHECK(ws != nullptr && ws_bytes >= w.total, O5_E_WORKSPACE,
            "o5_ppo_loss_grad: workspace needs %zu bytes, got %zu", w.total, ws ? ws_bytes : static_cast<size_t>(0));
   O5_CHECK(aligned16(ws), O5_E_ALIGN, "o5_ppo_loss_grad: ws is not 16-byte aligned");
@@ -498,10 +526,10 @@ extern "C" int o5_ppo_loss_grad(o5_dtype dt, int N, int H, int K, const int* hea
   ktimer_begin(kSitePpo, s);
   if (dt == O5_BF16)
     st = ppo_impl<uint16_t>(N, H, hm, static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(Wp), bp, act,
-                              logp_old, adv, ret, head_mask, avail, hp, stats, dh, dWp, dbp, wsp, w, s);
+                              logp_old, adv, ret, head_mask, avail, unit, hp, stats, dh, dWp, dbp, wsp, w, s);
   else
     st = ppo_impl<float>(N, H, hm, static_cast<const float*>(h), static_cast<const float*>(Wp), bp, act, logp_old, adv,
-                         ret, head_mask, avail, hp, stats, dh, dWp, dbp, wsp, w, s);
+                         ret, head_mask, avail, unit, hp, stats, dh, dWp, dbp, wsp, w, s);
   ktimer_end(kSitePpo, s);
   return st;
 }

@@ -55,6 +55,20 @@ class AdamHp(ctypes.Structure):
                 ("eps", ctypes.c_float), ("clip_k", ctypes.c_float)]
 
 
+class UnitHead(ctypes.Structure):
+    _fields_ = [("head", ctypes.c_int), ("d", ctypes.c_int), ("Wq", ctypes.c_void_p), ("bq", ctypes.c_void_p),
+                ("E", ctypes.c_void_p), ("dWq", ctypes.c_void_p), ("dbq", ctypes.c_void_p)]
+
+
+def unit_head(head, d, Wq, bq, E, dWq=None, dbq=None):
+    """An o5_unit_head over torch tensors (keep the tensors alive for the call)."""
+    return UnitHead(int(head), int(d), _p(Wq), _p(bq), _p(E), _p(dWq), _p(dbq))
+
+
+def _unit(u):
+    return None if u is None else ctypes.byref(u)
+
+
 class RewardHp(ctypes.Structure):
     _fields_ = [("tau", ctypes.c_float), ("decay_base", ctypes.c_float), ("decay_minutes", ctypes.c_float),
                 ("eps", ctypes.c_float)]
@@ -83,11 +97,12 @@ _SIGS = {
     "o5_prelstm_fwd": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp]),
     "o5_prelstm_bwd_workspace_bytes": (_sz, [_i, _i, _i, _i, _i]),
     "o5_prelstm_bwd": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
-    "o5_ppo_loss_grad_workspace_bytes": (_sz, [_i, _i, _i, _i, _vp]),
-    "o5_ppo_loss_grad": (_i, [_i, _i, _i, _i, _vp] + [_vp] * 9 + [PpoHp] + [_vp] * 5 + [_sz, _vp]),
+    "o5_ppo_loss_grad_workspace_bytes": (_sz, [_i, _i, _i, _i, _vp, _vp]),
+    "o5_ppo_loss_grad": (_i, [_i, _i, _i, _i, _vp] + [_vp] * 10 + [PpoHp] + [_vp] * 5 + [_sz, _vp]),
     "o5_adam_step": (_i, [_sz, _vp, _vp, _vp, _vp, _vp, AdamHp, _i, _vp]),
-    "o5_policy_sample_workspace_bytes": (_sz, [_i, _i, _i, _i, _vp]),
-    "o5_policy_sample": (_i, [_i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _u64, _u64, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "o5_policy_sample_workspace_bytes": (_sz, [_i, _i, _i, _i, _vp, _vp]),
+    "o5_policy_sample": (_i, [_i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _u64, _u64, _vp, _vp, _vp, _vp, _sz,
+                              _vp]),
     "o5_f32_to_bf16": (_i, [_sz, _vp, _vp, _vp]),
     "o5_param_count": (_sz, [_i, _i, _i]),
     "o5_surgery_widen": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _f, _u64, _vp]),
@@ -233,17 +248,17 @@ def o5_prelstm_bwd(dt, T, B, Do, D, o, y, dx, dW, db, ws, stream=None):
                                                   _stream(stream)))
 
 
-def o5_ppo_loss_grad_workspace_bytes(dt, N, H, head_sizes):
-    return lib().o5_ppo_loss_grad_workspace_bytes(dt, N, H, len(head_sizes), _heads(head_sizes))
+def o5_ppo_loss_grad_workspace_bytes(dt, N, H, head_sizes, unit=None):
+    return lib().o5_ppo_loss_grad_workspace_bytes(dt, N, H, len(head_sizes), _heads(head_sizes), _unit(unit))
 
 
 def o5_ppo_loss_grad(dt, N, H, head_sizes, h, Wp, bp, act, logp_old, adv, ret, head_mask,
-                     clip_eps, vf_coef, ent_coef, stats, dh, dWp, dbp, ws, stream=None, avail=None):
+                     clip_eps, vf_coef, ent_coef, stats, dh, dWp, dbp, ws, stream=None, avail=None, unit=None):
     wp, wn = _ws(ws)
     hp = PpoHp(clip_eps, vf_coef, ent_coef)
     _check("o5_ppo_loss_grad", lib().o5_ppo_loss_grad(
         dt, N, H, len(head_sizes), _heads(head_sizes), _p(h), _p(Wp), _p(bp), _p(act),
-        _p(logp_old), _p(adv), _p(ret), _p(head_mask), _p(avail), hp, _p(stats), _p(dh), _p(dWp),
+        _p(logp_old), _p(adv), _p(ret), _p(head_mask), _p(avail), _unit(unit), hp, _p(stats), _p(dh), _p(dWp),
         _p(dbp), wp, wn, _stream(stream)))
 
 
@@ -253,15 +268,15 @@ def o5_adam_step(n, p, m, v, g, p_bf16, lr, beta1, beta2, eps, clip_k, step, str
                                               int(step), _stream(stream)))
 
 
-def o5_policy_sample_workspace_bytes(dt, B, H, head_sizes):
-    return lib().o5_policy_sample_workspace_bytes(dt, B, H, len(head_sizes), _heads(head_sizes))
+def o5_policy_sample_workspace_bytes(dt, B, H, head_sizes, unit=None):
+    return lib().o5_policy_sample_workspace_bytes(dt, B, H, len(head_sizes), _heads(head_sizes), _unit(unit))
 
 
 def o5_policy_sample(dt, B, H, head_sizes, h, Wp, bp, seed, counter, act, logp, value, ws,
-                     stream=None, avail=None):
+                     stream=None, avail=None, unit=None):
     wp, wn = _ws(ws)
     _check("o5_policy_sample", lib().o5_policy_sample(
-        dt, B, H, len(head_sizes), _heads(head_sizes), _p(h), _p(Wp), _p(bp), _p(avail), int(seed),
+        dt, B, H, len(head_sizes), _heads(head_sizes), _p(h), _p(Wp), _p(bp), _p(avail), _unit(unit), int(seed),
         int(counter), _p(act), _p(logp), _p(value), wp, wn, _stream(stream)))
 
 

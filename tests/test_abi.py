@@ -85,7 +85,7 @@ def test_host_validation_errors(lib):
     assert L.o5_param_count(4096, 4096, 75) == 134541387
     # heads
     heads = (ctypes.c_int * 2)(3, 0)
-    assert L.o5_ppo_loss_grad_workspace_bytes(0, 8, 64, 2, heads) == 0
+    assert L.o5_ppo_loss_grad_workspace_bytes(0, 8, 64, 2, heads, None) == 0
     assert "head_sizes[1]" in o5.o5_last_error()
 
 
@@ -95,6 +95,11 @@ def test_workspace_queries_are_positive(lib):
         assert o5.o5_lstm_bptt_workspace_bytes(dt, 16, 2048, 4096, 4096) > 0
         assert o5.o5_ppo_loss_grad_workspace_bytes(dt, 32768, 4096, (30, 8, 32, 4)) > 0
         assert o5.o5_policy_sample_workspace_bytes(dt, 4096, 4096, (30, 8, 32, 4)) > 0
+    u = o5.UnitHead(1, 128, 16, 16, 16, 16, 16)
+    base = o5.o5_ppo_loss_grad_workspace_bytes(1, 32768, 4096, (30, 8, 32, 4))
+    assert o5.o5_ppo_loss_grad_workspace_bytes(1, 32768, 4096, (30, 8, 32, 4), u) > base
+    assert o5.o5_policy_sample_workspace_bytes(1, 4096, 4096, (30, 8, 32, 4), u) > 0
+    assert o5.o5_ppo_loss_grad_workspace_bytes(1, 64, 64, (3, 4), o5.UnitHead(2, 16, 16, 16, 16, 16, 16)) == 0
     assert o5.o5_reward_process_workspace_bytes(256, 13107) > 0
     assert o5.o5_reward_process_workspace_bytes(0, 1) == 0
 
