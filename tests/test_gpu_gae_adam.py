@@ -111,6 +111,33 @@ def test_adam_matches_oracle(n, step, clip_k, bf16_out):
         assert torch.equal(pb.view(torch.int16), tp.to(torch.bfloat16).view(torch.int16))
 
 
+def test_adam_full_size_sampled_elements():
+    """The full step's parameter count (the 4096-unit LSTM with 4096 inputs
+    and the heads, 134.5M; and 158.5M): the update is elementwise, so the
+    oracle checks a sample of elements, the first and last ones included."""
+    need_gpu()
+    for n in (134_541_387, 158_502_815):
+        banner(f"adam full size n={n}")
+        p, m, v, g = _adam_inputs(n, 7)
+        tp, tm, tv, tg = dev_f32(p), dev_f32(m), dev_f32(v), dev_f32(g)
+        pb = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+        o5.o5_adam_step(n, tp, tm, tv, tg, pb, 5e-5, 0.9, 0.999, 1e-8, 5.0, 3)
+        rng = np.random.Generator(np.random.PCG64(n))
+        idx = np.unique(np.concatenate([np.arange(64), n - 64 + np.arange(64), rng.integers(0, n, 1 << 20)]))
+        p_ref, m_ref, v_ref = adam_step(p[idx], m[idx], v[idx], g[idx], 5e-5, 0.9, 0.999, 1e-8, 5.0, 3)
+        ti = torch.from_numpy(idx).to("cuda")
+        pg = tp[ti].cpu().numpy().astype(np.float64)
+        dref = p_ref - p[idx].astype(np.float64)
+        ulp = np.spacing(np.abs(p_ref).astype(np.float32)).astype(np.float64)
+        bound = TOL_F32 * np.max(np.abs(dref)) + ulp
+        assert np.all(np.abs(pg - p_ref) <= bound)
+        assert_close("m", tm[ti].cpu().numpy(), m_ref, TOL_F32)
+        assert_close("v", tv[ti].cpu().numpy(), v_ref, TOL_F32)
+        assert torch.equal(pb[ti].view(torch.int16), tp[ti].to(torch.bfloat16).view(torch.int16))
+        del tp, tm, tv, tg, pb
+        torch.cuda.empty_cache()
+
+
 def test_adam_lr_zero_leaves_parameters_bitwise_and_is_deterministic():
     need_gpu()
     banner("adam lr=0 and determinism")

@@ -81,6 +81,8 @@ PPO_CASES = [
     # a single row; single-logit heads (certain actions)
     ("f32-one-row", 1, 64, HEADS, False, False, False),
     ("bf16-single-logit-heads", 100, 64, (1, 4, 1), True, True, False),
+    # the benchmark's shape: N = T B = 16 x 2048 rows of the 4096-unit LSTM
+    ("bf16-step-shape", 32768, 4096, HEADS, True, True, False),
 ]
 
 
