@@ -204,12 +204,14 @@ struct EpiLstmCell {
 };
 
 
+__device__ const uint8_t kZeroFlag = 0;
+
 // Backward cell for step t.  rec: [S][B][H] partial sums of dG_{t+1} W_h (or
 // NULL at t = T-1).  dc: in = dc arriving at c_t, out = dc for c_{t-1}.
 // Block: 64 hidden units x 32 rows; each thread owns 4 consecutive units of
 // 2 rows (16-byte fp32 and 8-byte bf16 accesses) and the block writes one
 // partial column sum of dG per gate and unit for the bias gradient.
-template <typename E>
+template <typename E, int NS>
 __global__ void __launch_bounds__(256) lstm_bwd_cell(
     int B, int H, int S, const float* __restrict__ rec, const uint8_t* __restrict__ reset_next,
     const float* __restrict__ dh_t, const float* __restrict__ dh_extra, const float* dc_in,
@@ -230,35 +232,62 @@ __global__ void __launch_bounds__(256) lstm_bwd_cell(
   // this thread's dG values (bf16 bits) of its two adjacent rows, for the
   // transposed copy; rows past B stay zero
   uint32_t tbits[2][16] = {};
+  constexpr int R = kPwRows / kRowGroups;  // rows per thread
+  // Every load of both rows is issued before any arithmetic, so a thread has
+  // all of them in flight at once (rows past B read row 0 and are dropped).
+  float4 dhv[R], exv[R], dcv[R], ctv[R], cpv[R], gin[R][4];
+  float4 recv[R][NS];
+  bool valid[R];
+  uint32_t rnb[R], rtb[R];  // reset flags of the next and this step, read like the rest
+  // absent reset flags read a zero byte, so no load sits behind a branch
+  const uint8_t* rnp = reset_next ? reset_next : &kZeroFlag;
+  const uint8_t* rtp = reset_t ? reset_t : &kZeroFlag;
+  const int rns = reset_next ? 1 : 0, rts = reset_t ? 1 : 0;
 #pragma unroll
-  for (int i = 0; i < kPwRows / kRowGroups; ++i) {
-    const int r = rg * (kPwRows / kRowGroups) + i;
-    const int b = blockIdx.y * kPwRows + r;
-    if (b >= B) continue;
+  for (int i = 0; i < R; ++i) {
+    const int b = blockIdx.y * kPwRows + rg * R + i;
+    valid[i] = b < B;
+    const int bc = valid[i] ? b : 0;
+    const size_t hj = static_cast<size_t>(bc) * H + j;
+    const size_t row = static_cast<size_t>(bc) * G;
+    dhv[i] = Vec4<float>::load(dh_t + hj);
+    exv[i] = dh_extra ? Vec4<float>::load(dh_extra + hj) : f4(0.f);
+#pragma unroll
+    for (int q = 0; q < NS; ++q) recv[i][q] = (rec && q < S) ? Vec4<float>::load(rec + q * sstride + hj) : f4(0.f);
+    rnb[i] = rnp[bc * rns];
+    rtb[i] = rtp[bc * rts];
+    dcv[i] = dc_in ? Vec4<float>::load(dc_in + hj) : f4(0.f);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) gin[i][g] = Vec4<E>::load(gates_t + row + g * H + j);
+    ctv[i] = Vec4<float>::load(c_t + hj);
+    cpv[i] = Vec4<float>::load(c_prev + hj);
+  }
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    if (!valid[i]) continue;
+    const int b = blockIdx.y * kPwRows + rg * R + i;
     const size_t hj = static_cast<size_t>(b) * H + j;
     const size_t row = static_cast<size_t>(b) * G;
-    float4 dh = Vec4<float>::load(dh_t + hj);
-    if (dh_extra) {
-      const float4 e = Vec4<float>::load(dh_extra + hj);
-      dh = make_float4(dh.x + e.x, dh.y + e.y, dh.z + e.z, dh.w + e.w);
-    }
+    float4 dh = dhv[i];
+    if (dh_extra) dh = make_float4(dh.x + exv[i].x, dh.y + exv[i].y, dh.z + exv[i].z, dh.w + exv[i].w);
     if (rec) {
-      float4 acc = f4(0.f);
-      for (int s = 0; s < S; ++s) {
-        const float4 v = Vec4<float>::load(rec + s * sstride + hj);
-        acc = make_float4(acc.x + v.x, acc.y + v.y, acc.z + v.z, acc.w + v.w);
-      }
-      const float kn = (reset_next && reset_next[b]) ? 0.0f : 1.0f;
-      dh = make_float4(dh.x + kn * acc.x, dh.y + kn * acc.y, dh.z + kn * acc.z, dh.w + kn * acc.w);
+      // the split partial sums in their fixed order
+      float4 acc = recv[i][0];
+#pragma unroll
+      for (int q = 1; q < NS; ++q)
+        if (q < S) acc = make_float4(acc.x + recv[i][q].x, acc.y + recv[i][q].y, acc.z + recv[i][q].z,
+                                     acc.w + recv[i][q].w);
+      const float k = rnb[i] ? 0.0f : 1.0f;
+      dh = make_float4(dh.x + k * acc.x, dh.y + k * acc.y, dh.z + k * acc.z, dh.w + k * acc.w);
     }
-    const float4 dcin = dc_in ? Vec4<float>::load(dc_in + hj) : f4(0.f);
-    const float4 ig = Vec4<E>::load(gates_t + row + j);
-    const float4 fg = Vec4<E>::load(gates_t + row + H + j);
-    const float4 gg = Vec4<E>::load(gates_t + row + 2 * H + j);
-    const float4 og = Vec4<E>::load(gates_t + row + 3 * H + j);
-    const float4 ct = Vec4<float>::load(c_t + hj);
-    const float4 cpr = Vec4<float>::load(c_prev + hj);
-    const float keep = (reset_t && reset_t[b]) ? 0.0f : 1.0f;
+    const float4 dcin = dcv[i];
+    const float4 ig = gin[i][0];
+    const float4 fg = gin[i][1];
+    const float4 gg = gin[i][2];
+    const float4 og = gin[i][3];
+    const float4 ct = ctv[i];
+    const float4 cpr = cpv[i];
+    const float keepf = rtb[i] ? 0.0f : 1.0f;
     const float* dhp = &dh.x;
     const float* dcp = &dcin.x;
     const float* ip = &ig.x;
@@ -276,13 +305,13 @@ __global__ void __launch_bounds__(256) lstm_bwd_cell(
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const float tc = tanh_f(cp_[q]);
-      const float cprev = keep * pp[q];
+      const float cprev = keepf * pp[q];
       const float dc = dcp[q] + dhp[q] * op[q] * (1.0f - tc * tc);
       aip[q] = dc * gp[q] * ip[q] * (1.0f - ip[q]);
       afp[q] = dc * cprev * fp[q] * (1.0f - fp[q]);
       agp[q] = dc * ip[q] * (1.0f - gp[q] * gp[q]);
       aop[q] = dhp[q] * tc * op[q] * (1.0f - op[q]);
-      dcop[q] = keep * dc * fp[q];
+      dcop[q] = keepf * dc * fp[q];
     }
     Vec4<float>::store(dc_out + hj, dco);
     Vec4<E>::store(dG_t + row + j, dai);
@@ -549,6 +578,10 @@ static int lstm_bptt_impl(int T, int B, int D, int H, const E* x, const E* Wx, c
     h0e = h0;
   }
   const dim3 pw_grid(cdiv(H, kPwCols), w.nbc);
+  // the cell unrolls its loads of the recurrent GEMM's split partials up to NS
+  auto cell = w.plan_dh.splits <= 2 ? lstm_bwd_cell<E, 2>
+              : w.plan_dh.splits <= 8 ? lstm_bwd_cell<E, 8>
+                                      : lstm_bwd_cell<E, 16>;
   for (int t = T - 1; t >= 0; --t) {
     const float* recp = nullptr;
     if (t < T - 1) {
@@ -572,7 +605,7 @@ static int lstm_bptt_impl(int T, int B, int D, int H, const E* x, const E* Wx, c
     const float* dhx = t == T - 1 ? dhT : nullptr;
     const float* cprev = t == 0 ? c0 : c + (t - 1) * BH;
     ktimer_begin(kSiteLstmBwdCell, s);
-    hipLaunchKernelGGL(lstm_bwd_cell<E>, pw_grid, dim3(256), 0, s, B, H, w.plan_dh.splits, recp, rn, dh + t * BH, dhx,
+    hipLaunchKernelGGL(cell, pw_grid, dim3(256), 0, s, B, H, w.plan_dh.splits, recp, rn, dh + t * BH, dhx,
                        dcin, dc, gates + t * BG, c + t * BH, cprev, rt, dG + t * BG, dbpart, t < T - 1 ? 1 : 0, dGT,
                        w.ldt, t * w.Bp);
     ktimer_end(kSiteLstmBwdCell, s);
