@@ -143,6 +143,7 @@ def test_head_mask_zero_removes_head():
     assert np.array_equal(dh1, dh2)
 
 
+@pytest.mark.filterwarnings("ignore:invalid value encountered:RuntimeWarning")
 def test_nonfinite_count():
     h, Wp, bp, act, adv, ret = _inputs(8, N=10, H=4, heads=(3,))
     adv[2] = np.nan
