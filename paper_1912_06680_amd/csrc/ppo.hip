@@ -37,25 +37,45 @@ constexpr int kRowsPerWave = 4;
 constexpr int kWavesPerBlock = 8;
 constexpr int kRowsPerBlock = kRowsPerWave * kWavesPerBlock;
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) v = fmaxf(v, __shfl_xor(v, d, 64));
-  return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
-  return v;
+// v combined with the value DPP control CTRL moves into each lane; lanes of
+// rows outside ROW_MASK take `id` instead.
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ float dpp(float id, float v) {
+  return __int_as_float(
+      __builtin_amdgcn_update_dpp(__float_as_int(id), __float_as_int(v), CTRL, ROW_MASK, 0xf, false));
 }
 
-// Column c of the row, held by lane c % 64 as its element c / 64.
+// Wave-wide reduction on the VALU's data-parallel lane moves: two quad
+// swaps and two rotations within each row of 16 lanes leave every lane with
+// its row's total, two row broadcasts carry them to lane 63, whose value is
+// returned to every lane.  A fixed combination order, so the result is the
+// same from call to call.
+template <class Op>
+__device__ __forceinline__ float wave_reduce(float v, float id, Op op) {
+  v = op(v, dpp<0xB1>(id, v));        // quad_perm [1, 0, 3, 2]
+  v = op(v, dpp<0x4E>(id, v));        // quad_perm [2, 3, 0, 1]
+  v = op(v, dpp<0x124>(id, v));       // row_ror 4
+  v = op(v, dpp<0x128>(id, v));       // row_ror 8
+  v = op(v, dpp<0x142, 0xa>(id, v));  // row_bcast 15: rows 1 and 3 add rows 0 and 2
+  v = op(v, dpp<0x143, 0xc>(id, v));  // row_bcast 31: rows 2 and 3 add rows 0 + 1
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+__device__ __forceinline__ float wave_max(float v) {
+  return wave_reduce(v, -INFINITY, [](float a, float b) { return fmaxf(a, b); });
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  return wave_reduce(v, 0.0f, [](float a, float b) { return a + b; });
+}
+
+// Column c (the same in every lane) of the row, held by lane c % 64 as its
+// element c / 64.
 template <int CPL>
 __device__ __forceinline__ float column(const float (&z)[CPL], int c) {
   float v = z[0];
 #pragma unroll
   for (int i = 1; i < CPL; ++i)
     if (c >> 6 == i) v = z[i];
-  return __shfl(v, c & 63, 64);
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), c & 63));
 }
 
 // One wave per row, kRowsPerWave consecutive rows per wave; lane l holds
@@ -72,7 +92,11 @@ __device__ __forceinline__ float column(const float (&z)[CPL], int c) {
 // surrogate, squared value error, entropy, clip indicator, approx-KL term,
 // ratio and non-finite indicator (kStatCols values); all sums in a fixed
 // order.
-template <int CPL>
+// Read in place of an absent availability mask and unit-head logits.
+__device__ const uint8_t kAllAvailable = 1;
+__device__ const float kNoLogit = 0.0f;
+
+template <int CPL, int SMAX>
 __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
     int N, int A1, int S, const float* __restrict__ zpart, const float* __restrict__ bp,
     const int32_t* __restrict__ act, const float* __restrict__ logp_old, const float* __restrict__ adv,
@@ -81,7 +105,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
     float ent_coef, float invN, float* __restrict__ dz, float* __restrict__ part, uint16_t* __restrict__ dz_hi,
     uint16_t* __restrict__ dz_lo, int ncol_hilo, int ld_hilo, uint16_t* __restrict__ dzT, int ldT) {
   __shared__ float red[kWavesPerBlock][CPL * 64 + kStatCols];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int K = hm.K, A = hm.A;
   int head[CPL];  // head of each column held, -1 for the value column and beyond
 #pragma unroll
@@ -100,28 +124,59 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
   uint32_t thi[TC][kRowsPerWave / 2] = {}, tlo[TC][kRowsPerWave / 2] = {};
   const size_t sstride = static_cast<size_t>(N) * A1;
   const int n0 = (blockIdx.x * kWavesPerBlock + wave) * kRowsPerWave;
+  // the logits and availability of the wave's rows, every request issued
+  // before the first row's reductions (rows past N read row N - 1, unused)
+  const int nke = kext >= 0 ? hm.off[kext + 1] - hm.off[kext] : 0;
+  float zr[kRowsPerWave][CPL];
+  uint32_t avr[kRowsPerWave][CPL];  // availability bytes as read (tested at use)
+  // per row: lane k < K holds head k's action and mask byte; the row's
+  // advantage, return and behaviour log-probability
+  int actr[kRowsPerWave];
+  uint32_t mkr[kRowsPerWave];
+  float advr[kRowsPerWave], retr[kRowsPerWave], lpor[kRowsPerWave];
+  const uint8_t* mkp = mask ? mask : &kAllAvailable;
+  const size_t mks = mask ? 1 : 0;
+  const int kl = min(lane, K - 1);
+  // (branch-free: every load reads a valid address, selects drop the ones
+  // not wanted, so no wait sits between two loads)
+  const uint8_t* avp = avail ? avail : &kAllAvailable;
+  const size_t avs = avail ? 1 : 0;
+  const float* zep = zext ? zext : &kNoLogit;
+  const size_t zes = zext ? 1 : 0;
+#pragma unroll
+  for (int rr = 0; rr < kRowsPerWave; ++rr) {
+    const size_t nc = static_cast<size_t>(min(n0 + rr, N - 1));
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      const int a = lane + 64 * i;
+      const bool ext = head[i] >= 0 && head[i] == kext;
+      const int ac = min(a, A1 - 1);
+      float p[SMAX];
+#pragma unroll
+      for (int s2 = 0; s2 < SMAX; ++s2) p[s2] = zpart[min(s2, S - 1) * sstride + nc * A1 + ac];
+      const float ze = zep[(nc * nke + (ext ? a - hm.off[kext] : 0)) * zes];
+      float v = bp[ac];
+#pragma unroll
+      for (int s2 = 0; s2 < SMAX; ++s2)
+        if (s2 < S) v += p[s2];
+      zr[rr][i] = ext ? ze : a < A1 ? v : 0.0f;
+      avr[rr][i] = avp[(nc * A + min(a, A - 1)) * avs];
+    }
+    actr[rr] = act[nc * K + kl];
+    mkr[rr] = mkp[(nc * K + kl) * mks];
+    advr[rr] = adv[nc];
+    retr[rr] = ret[nc];
+    lpor[rr] = logp_old[nc];
+  }
   for (int rr = 0; rr < kRowsPerWave; ++rr) {
     const int n = n0 + rr;
     if (n >= N) break;
     float z[CPL];
-#pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-      const int a = lane + 64 * i;
-      float v = 0.0f;
-      if (head[i] >= 0 && head[i] == kext) {
-        const int nk = hm.off[kext + 1] - hm.off[kext];
-        v = zext[static_cast<size_t>(n) * nk + (a - hm.off[kext])];
-      } else if (a < A1) {
-        v = bp[a];
-        for (int s2 = 0; s2 < S; ++s2) v += zpart[s2 * sstride + static_cast<size_t>(n) * A1 + a];
-      }
-      z[i] = v;
-    }
     bool av[CPL];
 #pragma unroll
     for (int i = 0; i < CPL; ++i) {
-      const int a = lane + 64 * i;
-      av[i] = avail == nullptr || a >= A || avail[static_cast<size_t>(n) * A + a] != 0;
+      z[i] = zr[0][i];
+      av[i] = lane + 64 * i >= A || avr[0][i] != 0;
     }
     float lse[kMaxHeads], zbar[kMaxHeads];
     bool mk[kMaxHeads], some[kMaxHeads];
@@ -148,21 +203,25 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
         some[k] = se > 0.0f;  // the maximum contributes e = 1
         lse[k] = some[k] ? mx + logf(se) : 0.0f;
         zbar[k] = some[k] ? sez / se : 0.0f;
-        ak[k] = act[static_cast<size_t>(n) * K + k];
-        mk[k] = mask == nullptr || mask[static_cast<size_t>(n) * K + k] != 0;
+        ak[k] = __builtin_amdgcn_readlane(actr[0], k);
+        mk[k] = __builtin_amdgcn_readlane(static_cast<int>(mkr[0]), k) != 0;
         const int nk = hm.off[k + 1] - hm.off[k];
         const int a_sel = min(max(ak[k], 0), nk - 1);
-        const float z_sel = column(z, hm.off[k] + a_sel);
-        bool taken = true;
-        if (avail != nullptr) taken = avail[static_cast<size_t>(n) * A + hm.off[k] + a_sel] != 0;
+        const int c_sel = hm.off[k] + a_sel;
+        const float z_sel = column(z, c_sel);
+        uint32_t tb = avr[0][0];
+#pragma unroll
+        for (int i = 1; i < CPL; ++i)
+          if (c_sel >> 6 == i) tb = avr[0][i];
+        const bool taken = __builtin_amdgcn_readlane(static_cast<int>(tb), c_sel & 63) != 0;
         if (mk[k] && some[k]) {
           logpi += taken ? z_sel - lse[k] : -INFINITY;
           ent += lse[k] - zbar[k];
         }
       }
     }
-    const float Ad = adv[n], R = ret[n];
-    const float dlog = logpi - logp_old[n];
+    const float Ad = advr[0], R = retr[0];
+    const float dlog = logpi - lpor[0];
     const float ratio = expf(dlog);
     const float rc = fminf(fmaxf(ratio, 1.0f - clip_eps), 1.0f + clip_eps);
     const float surr = fminf(ratio * Ad, rc * Ad);
@@ -184,8 +243,7 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
           d = g_logpi * (onehot - p) + ent_scale * p * (z[i] - zbar[k]);
         }
       if (head[i] >= 0 && head[i] == kext) {
-        const int nk = hm.off[kext + 1] - hm.off[kext];
-        dzext[static_cast<size_t>(n) * nk + (a - hm.off[kext])] = d;
+        dzext[static_cast<size_t>(n) * nke + (a - hm.off[kext])] = d;
         d = 0.0f;  // these logits do not depend on Wp, bp
       }
       if (a < A1) dz[static_cast<size_t>(n) * A1 + a] = d;
@@ -214,6 +272,21 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
     st[4] += expm1f(dlog) - dlog;  // (r - 1) - log r without the cancellation in r - 1
     st[5] += ratio;
     st[6] += isfinite(row_loss) ? 0.0f : 1.0f;
+    // the next row's inputs move to slot 0 (constant indices keep the
+    // prefetched values in registers)
+#pragma unroll
+    for (int q = 0; q + 1 < kRowsPerWave; ++q) {
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) {
+        zr[q][i] = zr[q + 1][i];
+        avr[q][i] = avr[q + 1][i];
+      }
+      actr[q] = actr[q + 1];
+      mkr[q] = mkr[q + 1];
+      advr[q] = advr[q + 1];
+      retr[q] = retr[q + 1];
+      lpor[q] = lpor[q + 1];
+    }
   }
   if (kT && dzT != nullptr) {
     // kRowsPerWave consecutive rows of each column held: 8 bytes of a dz^T row
@@ -347,15 +420,31 @@ int check_heads(const char* fn, o5_dtype dt, int N, int H, int K, const int* hea
   return O5_OK;
 }
 
+template <int CPL, int SMAX>
+static void launch_rows_s(const PpoWs& w, int N, int A1, int S, const float* zpart, const float* bp,
+                          const int32_t* act, const float* logp_old, const float* adv, const float* ret, const uint8_t* mask,
+                        const uint8_t* avail, const HeadsMeta& hm, const float* zext, float* dzext, int kext,
+                        o5_ppo_hp hp, float invN, float* dz, float* part, uint16_t* dzhi, uint16_t* dzlo,
+                        uint16_t* dzT, hipStream_t s) {
+  hipLaunchKernelGGL((ppo_rows<CPL, SMAX>), dim3(w.nblk), dim3(kWavesPerBlock * 64), 0, s, N, A1, S, zpart, bp, act,
+                     logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp.clip_eps, hp.vf_coef, hp.ent_coef, invN,
+                     dz, part, dzhi, dzlo, w.A1p, w.ldh, dzT, w.ldT);
+}
+
+// The row kernel unrolls its reads of the logits GEMM's split partials up
+// to SMAX (2 covers the usual split, 16 every plan).
 template <int CPL>
 static void launch_rows(const PpoWs& w, int N, int A1, int S, const float* zpart, const float* bp, const int32_t* act,
                         const float* logp_old, const float* adv, const float* ret, const uint8_t* mask,
                         const uint8_t* avail, const HeadsMeta& hm, const float* zext, float* dzext, int kext,
                         o5_ppo_hp hp, float invN, float* dz, float* part, uint16_t* dzhi, uint16_t* dzlo,
                         uint16_t* dzT, hipStream_t s) {
-  hipLaunchKernelGGL(ppo_rows<CPL>, dim3(w.nblk), dim3(kWavesPerBlock * 64), 0, s, N, A1, S, zpart, bp, act, logp_old,
-                     adv, ret, mask, avail, hm, zext, dzext, kext, hp.clip_eps, hp.vf_coef, hp.ent_coef, invN, dz, part, dzhi, dzlo, w.A1p,
-                     w.ldh, dzT, w.ldT);
+  if (S <= 2)
+    launch_rows_s<CPL, 2>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp,
+                          invN, dz, part, dzhi, dzlo, dzT, s);
+  else
+    launch_rows_s<CPL, 16>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp,
+                           invN, dz, part, dzhi, dzlo, dzT, s);
 }
 
 template <typename E>
