@@ -222,6 +222,100 @@ def cpu_baseline(cfg, target_s=15.0):
                       f"{synth.n_params(sub)} params, {dt:.2f} s on {cpu_model()}"}
 
 
+def other_configs(cfg, reps=5, warm=2):
+    """The two other single-GPU workloads of the method at paper scale, each
+    timed warm with events on the launch stream (median of `reps` after
+    `warm` untimed runs): the LSTM forward pass and truncated BPTT alone at
+    B = 1024 samples x T = 16 (D = H = 4096, no input gradient), and one
+    rollout inference step for B = 4096 environments (one LSTM step without
+    saved gates, then the heads and the Gumbel-max draw).  Inputs are
+    synthetic: x ~ N(0, 1), weights U(-1/sqrt(H), 1/sqrt(H)), h0, c0 and
+    the upstream gradient ~ N(0, 0.1^2) and N(0, 1)."""
+    import torch
+    from paper_1912_06680_amd import o5
+    dev = "cuda"
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1)
+    dt = o5.O5_BF16
+    et = torch.bfloat16
+    D = H = cfg.H
+    G = 4 * H
+    bound = H ** -0.5
+
+    def uni(shape):
+        return ((torch.rand(shape, generator=gen, device=dev) * 2 - 1) * bound).to(et)
+
+    def timed(fn):
+        ts = []
+        for i in range(warm + reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            if i >= warm:
+                ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts))
+
+    out = []
+    Wx, Wh = uni((G, D)), uni((G, H))
+    b = (torch.rand(G, generator=gen, device=dev) * 2 - 1) * bound
+    T, B = 16, 1024
+    x = torch.randn((T, B, D), generator=gen, device=dev).to(et)
+    h0 = torch.randn((B, H), generator=gen, device=dev) * 0.1
+    c0 = torch.randn((B, H), generator=gen, device=dev) * 0.1
+    h = torch.empty((T, B, H), dtype=et, device=dev)
+    c = torch.empty((T, B, H), device=dev)
+    gates = torch.empty((T, B, G), dtype=et, device=dev)
+    dh = torch.randn((T, B, H), generator=gen, device=dev)
+    dWx, dWh, db = torch.empty((G, D), device=dev), torch.empty((G, H), device=dev), torch.empty(G, device=dev)
+    ws = torch.empty(max(o5.o5_lstm_fwd_workspace_bytes(dt, T, B, D, H), o5.o5_lstm_bptt_workspace_bytes(dt, T, B, D, H)),
+                     dtype=torch.uint8, device=dev)
+
+    def lstm_step():
+        o5.o5_lstm_fwd(dt, T, B, D, H, x, Wx, Wh, b, h0, c0, None, h, c, gates, ws)
+        o5.o5_lstm_bptt(dt, T, B, D, H, x, Wx, Wh, h0, c0, None, h, c, gates, dh, None, None, dWx, dWh, db, None, ws)
+
+    ms = timed(lstm_step)
+    flop = 2.0 * T * B * G * (D + H) + 2.0 * G * ((T - 1) * B * H + T * B * H + T * B * D)
+    out.append({"workload": f"LSTM forward + truncated BPTT, B={B} x T={T}, D=H={H}, no input gradient",
+                "ms": round(ms, 3), "timesteps_per_s": round(B * T / (ms * 1e-3), 1),
+                "tflops": round(flop / (ms * 1e-3) / 1e12, 2),
+                "frac_mfma_peak": round(flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)})
+    del x, h0, c0, h, c, gates, dh, dWx, dWh, db, ws
+    B = 4096
+    heads = tuple(cfg.head_sizes)
+    A1 = sum(heads) + 1
+    Wp = uni((A1, H))
+    bp = torch.zeros(A1, device=dev)
+    x = torch.randn((1, B, D), generator=gen, device=dev).to(et)
+    h0 = torch.randn((B, H), generator=gen, device=dev) * 0.1
+    c0 = torch.randn((B, H), generator=gen, device=dev) * 0.1
+    h = torch.empty((1, B, H), dtype=et, device=dev)
+    c = torch.empty((1, B, H), device=dev)
+    ws = torch.empty(max(o5.o5_lstm_fwd_workspace_bytes(dt, 1, B, D, H), 256), dtype=torch.uint8, device=dev)
+    act = torch.empty((B, len(heads)), dtype=torch.int32, device=dev)
+    logp = torch.empty(B, device=dev)
+    val = torch.empty(B, device=dev)
+    sws = torch.empty(max(o5.o5_policy_sample_workspace_bytes(dt, B, H, heads), 256), dtype=torch.uint8, device=dev)
+    counter = [0]
+
+    def rollout():
+        o5.o5_lstm_fwd(dt, 1, B, D, H, x, Wx, Wh, b, h0, c0, None, h, c, None, ws)
+        o5.o5_policy_sample(dt, B, H, heads, h[0], Wp, bp, 0, counter[0], act, logp, val, sws)
+        counter[0] += 1
+
+    ms = timed(rollout)
+    flop = 2.0 * B * G * (D + H) + 2.0 * B * A1 * H
+    out.append({"workload": f"rollout inference: one LSTM step for B={B} environments (D=H={H}), heads "
+                            f"{list(heads)} + value, Gumbel-max sampling",
+                "ms": round(ms, 3), "env_steps_per_s": round(B / (ms * 1e-3), 1),
+                "tflops": round(flop / (ms * 1e-3) / 1e12, 2),
+                "frac_mfma_peak": round(flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)})
+    return out
+
+
 def hbm_kernels(cfg, reps=20, warm=3):
     """The HBM-bound kernels on their own, at the sizes their bandwidth is
     judged on: GAE over L=256-step segments at S = 128 (the step's size,
@@ -392,6 +486,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="full4096")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip the paper-scale LSTM-only and rollout-inference timings")
     ap.add_argument("--no-hbm-kernels", action="store_true",
                     help="skip the standalone GAE / Adam bandwidth measurements")
     ap.add_argument("--copy-ref", action="store_true",
@@ -487,6 +583,11 @@ def main():
     step_flop = 2.0 * T * B * 4 * H * (D + H) + 2.0 * 4 * H * ((T - 1) * B * H + T * B * H + T * B * D) + \
         3 * 2.0 * T * B * A1 * H
 
+    others = None
+    if not args.no_other_configs:
+        log("paper-scale LSTM fwd + BPTT and rollout inference")
+        others = other_configs(cfg)
+
     hbm = None
     if not args.no_hbm_kernels:
         log("standalone HBM-bound kernels (GAE, Adam), cold and warm")
@@ -512,6 +613,7 @@ def main():
         "lstm_gemm_tflops": round(lstm_gemm_tflops, 2),
         "step_tflops": round(step_flop / (ms_step * 1e-3) / 1e12, 2),
         "kernels": kernels,
+        "other_configs": others,
         "hbm_kernels": hbm,
         "loss_stats": [round(s, 6) for s in stats],
     }
