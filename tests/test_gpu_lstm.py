@@ -128,6 +128,59 @@ def test_lstm_inference_without_gates_and_determinism():
     assert_close("h", outs[0][0], ref["h"], TOL_BF16)
 
 
+def test_rollout_step_paper_scale():
+    """One rollout inference step at the paper's scale (B = 4096 environments,
+    D = H = 4096, bf16, no saved gates) followed by the heads and the
+    Gumbel-max draw, in the launch configuration the benchmark times.  The
+    LSTM step is checked on sampled rows (rows are independent); the draw
+    takes the device's bf16 h of every row through the oracle's heads and
+    Philox sampler."""
+    from oracle.philox import gumbel_max_sample
+    from oracle.ppo import heads_forward
+    need_gpu()
+    T, B, D, H = 1, 4096, 4096, 4096
+    heads = (30, 8, 32, 4)
+    A1 = sum(heads) + 1
+    banner(f"rollout step B={B} D={D} H={H} heads={heads}")
+    inp = _inputs(T, B, D, H, 41)
+    rng = np.random.Generator(np.random.PCG64(42))
+    Wp = ((rng.random((A1, H), dtype=np.float32) * 2 - 1) * 4 / np.sqrt(H)).astype(np.float32)
+    bp = ((rng.random(A1, dtype=np.float32) * 2 - 1) / np.sqrt(H)).astype(np.float32)
+    dt = o5.O5_BF16
+    x, Wx, Wh = dev_dt(inp["x"], True), dev_dt(inp["Wx"], True), dev_dt(inp["Wh"], True)
+    b, h0, c0 = dev_f32(inp["b"]), dev_f32(inp["h0"]), dev_f32(inp["c0"])
+    h = empty_dt((T, B, H), True)
+    c = torch.empty((T, B, H), dtype=torch.float32, device="cuda")
+    ws = workspace(o5.o5_lstm_fwd_workspace_bytes(dt, T, B, D, H))
+    o5.o5_lstm_fwd(dt, T, B, D, H, x, Wx, Wh, b, h0, c0, None, h, c, None, ws)
+    act = torch.empty((B, len(heads)), dtype=torch.int32, device="cuda")
+    logp = torch.empty(B, dtype=torch.float32, device="cuda")
+    value = torch.empty(B, dtype=torch.float32, device="cuda")
+    sws = workspace(o5.o5_policy_sample_workspace_bytes(dt, B, H, heads))
+    seed, counter = 5, 7
+    o5.o5_policy_sample(dt, B, H, heads, h[0], dev_dt(Wp, True), dev_f32(bp), seed, counter, act, logp, value, sws)
+    rows = np.array([0, 1234, 2048, B - 1])
+    h_ref, c_ref, _ = lstm_forward(round_to_bf16(inp["x"][:, rows]), round_to_bf16(inp["Wx"]),
+                                   round_to_bf16(inp["Wh"]), inp["b"], inp["h0"][rows], inp["c0"][rows], None,
+                                   store=round_to_bf16)
+    hg = host(h)
+    assert_close("h[rows]", hg[:, rows], h_ref, TOL_BF16)
+    assert_close("c[rows]", host(c)[:, rows], c_ref, TOL_BF16)
+    z = heads_forward(hg[0], round_to_bf16(Wp), bp)
+    act_ref, logp_ref, v_ref, scores = gumbel_max_sample(z, heads, seed, counter)
+    a = act.cpu().numpy()
+    agree = np.ones(B, bool)
+    for k in range(len(heads)):
+        srt = np.sort(scores[k], axis=1)
+        clear = srt[:, -1] - srt[:, -2] > 1e-4
+        mism = a[:, k] != act_ref[:, k]
+        assert not np.any(mism & clear), f"head {k}: {np.sum(mism & clear)} clear-cut mismatches"
+        agree &= ~mism
+    assert agree.mean() > 0.99
+    assert_close("logp", host(logp)[agree], logp_ref[agree], TOL_BF16)
+    assert_close("value", host(value), v_ref, TOL_BF16)
+
+
 @pytest.mark.parametrize("B", [1024, 2048])
 def test_lstm_paper_scale_sampled_rows(B):
     """B=1024 and the benchmark's B=2048, T=16, D=H=4096, in the benchmark's
