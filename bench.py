@@ -359,11 +359,18 @@ def hbm_kernels(cfg, reps=20, warm=3):
                 ts.append(e0.elapsed_time(e1) * 1e3)
         return float(np.median(ts))
 
-    def entry(kernel, size, nbytes, fn):
+    def entry(kernel, size, nbytes, fn, moved=None):
+        """`nbytes`: what the operation must move once; `moved`: what the
+        method moves when it is more (a second pass over inputs that exceed
+        the caches)."""
         cold, hot = timed(fn, True), timed(fn, False)
-        return {"kernel": kernel, "size": size, "bytes": int(nbytes), "cold_us": round(cold, 2),
-                "warm_us": round(hot, 2), "cold_gbs": round(nbytes / cold * 1e-3, 1),
-                "frac_hbm_peak_cold": round(nbytes / cold * 1e-3 / PEAK_HBM_GBS, 4)}
+        e = {"kernel": kernel, "size": size, "bytes": int(nbytes), "cold_us": round(cold, 2),
+             "warm_us": round(hot, 2), "cold_gbs": round(nbytes / cold * 1e-3, 1),
+             "frac_hbm_peak_cold": round(nbytes / cold * 1e-3 / PEAK_HBM_GBS, 4)}
+        if moved is not None:
+            e.update({"moved_bytes": int(moved), "cold_gbs_moved": round(moved / cold * 1e-3, 1),
+                      "frac_hbm_peak_cold_moved": round(moved / cold * 1e-3 / PEAK_HBM_GBS, 4)})
+        return e
 
     out = []
     L = 256
@@ -382,8 +389,11 @@ def hbm_kernels(cfg, reps=20, warm=3):
         stats = torch.zeros(3, dtype=torch.float64, device=dev)
         rr = torch.empty((L, 10 * G), device=dev)
         rws = torch.empty(max(o5.o5_reward_process_workspace_bytes(L, G), 256), dtype=torch.uint8, device=dev)
+        # two passes (the normalisation needs this call's statistics first):
+        # shaped, outcome and game time read twice, r written once
         out.append(entry("reward_process", f"L={L} G={G} (S={10 * G})", 12 * L * 10 * G + 4 * L * G,
-                         lambda: o5.o5_reward_process(L, G, sh, oc, gt, 0.3, 0.6, 10.0, 1e-8, stats, rr, rws)))
+                         lambda: o5.o5_reward_process(L, G, sh, oc, gt, 0.3, 0.6, 10.0, 1e-8, stats, rr, rws),
+                         moved=20 * L * 10 * G + 8 * L * G))
         del sh, oc, gt, stats, rr, rws
     # the LSTM's input side at the step's shape: 408 teams x 5 replicas x 16
     # steps of a 4096-wide observation into the 4096-wide LSTM input
@@ -395,8 +405,10 @@ def hbm_kernels(cfg, reps=20, warm=3):
     ostats = torch.zeros((3, Do), dtype=torch.float64, device=dev)
     oq = torch.empty((Nq, Do), dtype=et, device=dev)
     ows = torch.empty(o5.o5_obs_normalize_workspace_bytes(Nq, Do), dtype=torch.uint8, device=dev)
+    # two passes (statistics first, this call's rows included): obs read twice
     out.append(entry("obs_normalize", f"N={Nq} Do={Do}", Nq * Do * (4 + oq.element_size()),
-                     lambda: o5.o5_obs_normalize(dtq, Nq, Do, obs, ostats, 5.0, 1e-8, oq, ows)))
+                     lambda: o5.o5_obs_normalize(dtq, Nq, Do, obs, ostats, 5.0, 1e-8, oq, ows),
+                     moved=Nq * Do * (8 + oq.element_size())))
     del obs
     Wq = (torch.randn((D, Do), generator=gen, device=dev) / Do ** 0.5).to(et)
     bq = torch.zeros(D, device=dev)
