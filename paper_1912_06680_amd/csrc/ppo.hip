@@ -182,27 +182,48 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
     bool mk[kMaxHeads], some[kMaxHeads];
     int ak[kMaxHeads];
     float logpi = 0.0f, ent = 0.0f;
+    // per head: the maximum over its available logits; then one exponential
+    // per column; then the sums of e and e z per head (all reductions over
+    // the wave in a fixed order)
+    float mx[kMaxHeads];
 #pragma unroll
     for (int k = 0; k < kMaxHeads; ++k) {
+      mx[k] = -INFINITY;
       if (k < K) {
-        float mx = -INFINITY;
+        float m = -INFINITY;
 #pragma unroll
         for (int i = 0; i < CPL; ++i)
-          if (head[i] == k && av[i]) mx = fmaxf(mx, z[i]);
-        mx = wave_max(mx);
+          if (head[i] == k && av[i]) m = fmaxf(m, z[i]);
+        mx[k] = wave_max(m);
+      }
+    }
+    float e[CPL];
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      float m = 0.0f;
+#pragma unroll
+      for (int k = 0; k < kMaxHeads; ++k)
+        if (k < K && head[i] == k) m = mx[k];
+      e[i] = (head[i] >= 0 && av[i]) ? expf(z[i] - m) : 0.0f;
+    }
+    float inv_se[kMaxHeads];
+#pragma unroll
+    for (int k = 0; k < kMaxHeads; ++k) {
+      inv_se[k] = 0.0f;
+      if (k < K) {
         float se = 0.0f, sez = 0.0f;
 #pragma unroll
         for (int i = 0; i < CPL; ++i)
-          if (head[i] == k && av[i]) {
-            const float e = expf(z[i] - mx);
-            se += e;
-            sez += e * z[i];
+          if (head[i] == k) {
+            se += e[i];
+            sez += e[i] * z[i];
           }
         se = wave_sum(se);
         sez = wave_sum(sez);
         some[k] = se > 0.0f;  // the maximum contributes e = 1
-        lse[k] = some[k] ? mx + logf(se) : 0.0f;
+        lse[k] = some[k] ? mx[k] + logf(se) : 0.0f;
         zbar[k] = some[k] ? sez / se : 0.0f;
+        inv_se[k] = some[k] ? 1.0f / se : 0.0f;
         ak[k] = __builtin_amdgcn_readlane(actr[0], k);
         mk[k] = __builtin_amdgcn_readlane(static_cast<int>(mkr[0]), k) != 0;
         const int nk = hm.off[k + 1] - hm.off[k];
@@ -235,13 +256,23 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
       const int a = lane + 64 * i;
       float d = 0.0f;
       if (a == A) d = 2.0f * vf_coef * verr * invN;
+      // this column's head: its softmax normaliser, mean logit, taken action
+      bool use = false;
+      float is = 0.0f, zb = 0.0f;
+      int act_col = -1;
 #pragma unroll
       for (int k = 0; k < kMaxHeads; ++k)
-        if (k < K && head[i] == k && mk[k] && some[k] && av[i]) {
-          const float p = expf(z[i] - lse[k]);
-          const float onehot = (a - hm.off[k] == ak[k]) ? 1.0f : 0.0f;
-          d = g_logpi * (onehot - p) + ent_scale * p * (z[i] - zbar[k]);
+        if (k < K && head[i] == k) {
+          use = mk[k] && some[k];
+          is = inv_se[k];
+          zb = zbar[k];
+          act_col = hm.off[k] + ak[k];
         }
+      if (use && av[i]) {
+        const float p = e[i] * is;
+        const float onehot = a == act_col ? 1.0f : 0.0f;
+        d = g_logpi * (onehot - p) + ent_scale * p * (z[i] - zb);
+      }
       if (head[i] >= 0 && head[i] == kext) {
         dzext[static_cast<size_t>(n) * nke + (a - hm.off[kext])] = d;
         d = 0.0f;  // these logits do not depend on Wp, bp
