@@ -498,6 +498,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="full4096")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-timers", action="store_true",
+                    help="time the steps without the per-launch events (no roofline or per-kernel figures)")
     ap.add_argument("--no-other-configs", action="store_true",
                     help="skip the paper-scale LSTM-only and rollout-inference timings")
     ap.add_argument("--no-hbm-kernels", action="store_true",
@@ -535,8 +537,52 @@ def main():
     for _ in range(args.warmup):
         st.run()
     torch.cuda.synchronize()
+    # per-site device time and algorithmic work: one pass of K steps with an
+    # event pair around every launch site (the events add ~2 % to a step),
+    # then the K timed steps with events around the dominant kernel only
+    A1 = sum(cfg.head_sizes) + 1
+    n = st.n_params
+    flops = {
+        "lstm_fwd_gemm": 2.0 * B * 4 * H * (D + H),
+        "lstm_dh_gemm": 2.0 * B * H * 4 * H,
+        "lstm_dw_gemm": 2.0 * 4 * H * (D + H) * T * B,
+    }
+    bytes_ = {
+        "lstm_fwd_cell": 34.0 * B * H,
+        "lstm_bwd_cell": 40.0 * B * H,
+        "adam_step": 30.0 * n,
+        "gae": 17.0 * cfg.L * cfg.S + 4.0 * cfg.S,
+        "ppo_loss_grad": (2 * 2.0 * H + 4.0 * H + 4.0 * A1 + 16.0) * T * B,
+    }
+    kernels = {}
+    dom = None
+    if not args.no_kernel_timers:
+        log(f"per-kernel times over {args.steps} instrumented steps")
+        o5.o5_ktimer_enable(True)
+        for _ in range(args.steps):
+            st.run()
+        torch.cuda.synchronize()
+        o5.o5_ktimer_enable(False)
+        for site, name in enumerate(o5.KTIMER_SITES):
+            tot, cnt = o5.o5_ktimer_read(site)
+            if cnt == 0:
+                continue
+            per = tot / cnt
+            k = {"ms_per_launch": round(per, 5), "launches_per_step": cnt / args.steps,
+                 "ms_per_step": round(tot / args.steps, 4)}
+            if name in flops:
+                k["tflops"] = round(flops[name] / (per * 1e-3) / 1e12, 2)
+                k["frac_mfma_peak"] = round(k["tflops"] / PEAK_BF16_TFLOPS, 4)
+            if name in bytes_:
+                k["gbs"] = round(bytes_[name] / (per * 1e-3) / 1e9, 1)
+                k["frac_hbm_peak"] = round(k["gbs"] / PEAK_HBM_GBS, 4)
+            kernels[name] = k
+        if any(s_ in kernels for s_ in flops):
+            dom = max(flops, key=lambda s_: kernels.get(s_, {}).get("ms_per_step", 0.0))
+
     log(f"timing {args.steps} steps")
-    o5.o5_ktimer_enable(True)
+    if dom is not None:
+        o5.o5_ktimer_enable_sites([dom])
     t0 = time.perf_counter()
     for _ in range(args.steps):
         st.run()
@@ -553,45 +599,18 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     log(f"{ms_step:.3f} ms/step, {value:.0f} timesteps/s, loss {stats[0]:.5f}")
-
-    # per-site device time and algorithmic work per launch
-    A1 = sum(cfg.head_sizes) + 1
-    n = st.n_params
-    flops = {
-        "lstm_fwd_gemm": 2.0 * B * 4 * H * (D + H),
-        "lstm_dh_gemm": 2.0 * B * H * 4 * H,
-        "lstm_dw_gemm": 2.0 * 4 * H * (D + H) * T * B,
-    }
-    bytes_ = {
-        "lstm_fwd_cell": 34.0 * B * H,
-        "lstm_bwd_cell": 40.0 * B * H,
-        "adam_step": 30.0 * n,
-        "gae": 17.0 * cfg.L * cfg.S + 4.0 * cfg.S,
-        "ppo_loss_grad": (2 * 2.0 * H + 4.0 * H + 4.0 * A1 + 16.0) * T * B,
-    }
-    kernels = {}
-    for site, name in enumerate(o5.KTIMER_SITES):
-        tot, cnt = o5.o5_ktimer_read(site)
-        if cnt == 0:
-            continue
-        per = tot / cnt
-        k = {"ms_per_launch": round(per, 5), "launches_per_step": cnt / args.steps,
-             "ms_per_step": round(tot / args.steps, 4)}
-        if name in flops:
-            k["tflops"] = round(flops[name] / (per * 1e-3) / 1e12, 2)
-            k["frac_mfma_peak"] = round(k["tflops"] / PEAK_BF16_TFLOPS, 4)
-        if name in bytes_:
-            k["gbs"] = round(bytes_[name] / (per * 1e-3) / 1e9, 1)
-            k["frac_hbm_peak"] = round(k["gbs"] / PEAK_HBM_GBS, 4)
-        kernels[name] = k
-    gemm_ms = sum(kernels[s]["ms_per_step"] for s in flops if s in kernels)
-    gemm_flop = sum(flops[s] * kernels[s]["launches_per_step"] for s in flops if s in kernels)
+    gemm_ms = sum(kernels[s_]["ms_per_step"] for s_ in flops if s_ in kernels)
+    gemm_flop = sum(flops[s_] * kernels[s_]["launches_per_step"] for s_ in flops if s_ in kernels)
     lstm_gemm_tflops = gemm_flop / (gemm_ms * 1e-3) / 1e12 if gemm_ms > 0 else 0.0
-    dom = max(flops, key=lambda s: kernels.get(s, {}).get("ms_per_step", 0.0))
-    dk = kernels[dom]
-    roofline = {"bound": "mfma", "achieved": dk["tflops"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(dk["tflops"] / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic(dom), "kernel": dom,
-                "flop_per_launch": flops[dom], "ms_per_launch": dk["ms_per_launch"]}
+    roofline = None
+    if dom is not None:
+        # the dominant kernel's launches inside the timed steps
+        tot, cnt = o5.o5_ktimer_read(o5.KTIMER_SITES.index(dom))
+        per = tot / cnt
+        tf = flops[dom] / (per * 1e-3) / 1e12
+        roofline = {"bound": "mfma", "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic(dom),
+                    "kernel": dom, "flop_per_launch": flops[dom], "ms_per_launch": round(per, 5)}
     step_flop = 2.0 * T * B * 4 * H * (D + H) + 2.0 * 4 * H * ((T - 1) * B * H + T * B * H + T * B * D) + \
         3 * 2.0 * T * B * A1 * H
 

@@ -450,9 +450,14 @@ int o5_f32_to_bf16(size_t n, const float* src, uint16_t* dst, void* stream);
  * call), 7 adam_step, 8 gae, 9 policy_sample (whole call), 10
  * reward_process, 11 obs_normalize, 12 prelstm_fwd, 13 prelstm_bwd (whole
  * calls).
+ * o5_ktimer_enable_sites(mask) does the same for the sites whose bit
+ * (1 << site) is set in mask (0 stops recording): every recorded pair adds
+ * two event packets to the stream, so a timed run can record only the sites
+ * it needs.
  * o5_ktimer_site_name returns the site's name ("" if out of range).
  * ------------------------------------------------------------------------ */
 int o5_ktimer_enable(int on);
+int o5_ktimer_enable_sites(unsigned int mask);
 int o5_ktimer_read(int site, double* total_ms, int* launches);
 const char* o5_ktimer_site_name(int site);
 

@@ -34,6 +34,7 @@ int check_launch(const char* where) {
 namespace {
 struct KTimer {
   bool on = false;
+  unsigned mask = 0;  // sites recorded while on
   std::vector<hipEvent_t> pool;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> done[kSiteCount];
   hipEvent_t open[kSiteCount] = {};
@@ -56,7 +57,7 @@ const char* kSiteNames[kSiteCount] = {"lstm_fwd_gemm", "lstm_fwd_cell", "lstm_dh
 }  // namespace
 
 void ktimer_begin(int site, hipStream_t s) {
-  if (!g_kt.on) return;
+  if (!g_kt.on || !((g_kt.mask >> site) & 1u)) return;
   hipEvent_t e = g_kt.get();
   if (e && hipEventRecord(e, s) == hipSuccess) g_kt.open[site] = e;
 }
@@ -112,8 +113,8 @@ extern "C" const char* o5_status_str(int status) {
 
 extern "C" const char* o5_last_error(void) { return o5::g_last_error; }
 
-extern "C" int o5_ktimer_enable(int on) {
-  if (!on) {  // stop recording; keep what was recorded
+extern "C" int o5_ktimer_enable_sites(unsigned mask) {
+  if (mask == 0) {  // stop recording; keep what was recorded
     g_kt.on = false;
     return O5_OK;
   }
@@ -125,9 +126,12 @@ extern "C" int o5_ktimer_enable(int on) {
     g_kt.done[i].clear();
     g_kt.open[i] = nullptr;
   }
+  g_kt.mask = mask;
   g_kt.on = true;
   return O5_OK;
 }
+
+extern "C" int o5_ktimer_enable(int on) { return o5_ktimer_enable_sites(on ? ~0u : 0u); }
 
 extern "C" int o5_ktimer_read(int site, double* total_ms, int* launches) {
   O5_CHECK(site >= 0 && site < kSiteCount, O5_E_ARG, "o5_ktimer_read: site %d out of range", site);

@@ -32,7 +32,7 @@ EXPORTED = (
     "o5_policy_sample_workspace_bytes", "o5_policy_sample",
     "o5_f32_to_bf16",
     "o5_param_count", "o5_surgery_widen", "o5_surgery_fold_input",
-    "o5_ktimer_enable", "o5_ktimer_read", "o5_ktimer_site_name",
+    "o5_ktimer_enable", "o5_ktimer_enable_sites", "o5_ktimer_read", "o5_ktimer_site_name",
 )
 
 KTIMER_SITES = ("lstm_fwd_gemm", "lstm_fwd_cell", "lstm_dh_gemm", "lstm_bwd_cell", "lstm_dw_gemm",
@@ -108,6 +108,7 @@ _SIGS = {
     "o5_surgery_widen": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _f, _u64, _vp]),
     "o5_surgery_fold_input": (_i, [_i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "o5_ktimer_enable": (_i, [_i]),
+    "o5_ktimer_enable_sites": (_i, [ctypes.c_uint]),
     "o5_ktimer_read": (_i, [_i, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int)]),
     "o5_ktimer_site_name": (ctypes.c_char_p, [_i]),
 }
@@ -302,6 +303,14 @@ def o5_f32_to_bf16(n, src, dst, stream=None):
 
 def o5_ktimer_enable(on):
     _check("o5_ktimer_enable", lib().o5_ktimer_enable(1 if on else 0))
+
+
+def o5_ktimer_enable_sites(names):
+    """Record only the named sites (an empty list stops recording)."""
+    mask = 0
+    for nm in names:
+        mask |= 1 << KTIMER_SITES.index(nm)
+    _check("o5_ktimer_enable_sites", lib().o5_ktimer_enable_sites(mask))
 
 
 def o5_ktimer_read(site):
