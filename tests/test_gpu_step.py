@@ -91,3 +91,33 @@ def test_two_steps_equal_checkpoint_resume():
     c.run()
     for k in ("p32", "m", "v", "g"):
         assert torch.equal(getattr(a, k), getattr(c, k)), k
+
+
+def test_full_size_step_is_deterministic():
+    """The benchmark's step (B = 2048 x T = 16, D = H = 4096, bf16) run twice
+    from the same state gives bitwise identical parameters, Adam moments,
+    gradients and loss statistics: every reduction has a fixed order."""
+    need_gpu()
+    cfg = synth.CONFIGS["full4096"]
+    banner(f"full-size determinism: B={cfg.B} T={cfg.T} D={cfg.D} H={cfg.H} {cfg.dtype}")
+    inp = synth.make_inputs(cfg, 0)
+    rng = np.random.Generator(np.random.PCG64(3))
+    N = cfg.T * cfg.B
+    act = np.stack([rng.integers(0, n, N) for n in cfg.head_sizes], axis=1).astype(np.int32)
+    logp_old = (rng.standard_normal(N) - 8.0).astype(np.float32)
+    values = rng.standard_normal((cfg.L + 1, cfg.S)).astype(np.float32)
+    st = PPOStep(cfg)
+    st.load_x(inp["x"])
+    st.load_rollout(inp["h0"], inp["c0"], inp["rewards"], inp["dones"], values, act, logp_old)
+    outs = []
+    for _ in range(2):
+        st.load_params({k: inp[k] for k in PARAM_ORDER})
+        st.m.zero_()
+        st.v.zero_()
+        st.step_count = 0
+        st.run()
+        torch.cuda.synchronize()
+        outs.append({k: getattr(st, k).clone() for k in ("p32", "m", "v", "g", "stats")})
+    for k in outs[0]:
+        assert torch.equal(outs[0][k], outs[1][k]), k
+    assert torch.isfinite(outs[0]["stats"]).all()
