@@ -1,7 +1,7 @@
 """fp32 -> bfloat16 round-to-nearest-even, as plain integer arithmetic.
 
 Test infrastructure (see the package docstring).  The paper names no numeric
-precision; the bf16 path of this build rounds GEMM inputs (x, W_x, W_h, W_p
+precision; the library's bf16 path rounds GEMM inputs (x, W_x, W_h, W_p
 and the hidden states fed back into the recurrence) to bfloat16.  The oracle
 reference for that path takes the same rounded inputs and keeps everything
 else in fp64.

@@ -4,7 +4,7 @@ Test infrastructure (see the package docstring).
 
 The rollout policy samples an action from its output distribution at every
 timestep (section "Training System", subsection "Playing Dota using AI").  The
-paper does not say how; this build draws each categorical head with the
+paper does not say how; here each categorical head is drawn with the
 Gumbel-max rule, argmax_a (z_a + G_a) with G = -ln(-ln U), U uniform on
 (0, 1), using the counter-based generator Philox4x64 with 10 rounds
 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as easy as 1, 2, 3",
@@ -19,7 +19,7 @@ with M0 = 0xD2E7470EE14C6C93, M1 = 0xCA5A826395121157 and the Weyl
 increments W0 = 0x9E3779B97F4A7C15 (golden ratio), W1 = 0xBB67AE8584CAA73B
 (sqrt(3) - 1).  The key update happens between rounds.
 
-Counter assignment (this build's convention): the noise for logit ``a`` of
+Counter assignment (the convention used here): the noise for logit ``a`` of
 head ``k`` in row ``b`` is output word ``a mod 4`` of the block with counter
 (a div 4, k, b, counter) and key (seed, 0).  U = ((word >> 40) + 1/2) / 2^24.
 """

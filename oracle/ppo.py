@@ -39,7 +39,7 @@ q = h Wq^T + bq [N, d], logits z_k[n, u] = <q[n], E[n, u]>.  Reading: the
 query is a linear projection of the LSTM state, the score a plain dot
 product; the rows of Wp and bp that belong to head k are then unused (zero
 gradient).  The gradient reaches Wq, bq and h through q; none is taken into
-E (the observation encoder is not part of this build).
+E (the observation encoder that would produce E is not modelled).
 """
 import numpy as np
 
