@@ -318,7 +318,7 @@ def other_configs(cfg, reps=5, warm=2):
 
 def hbm_kernels(cfg, reps=20, warm=3):
     """The HBM-bound kernels on their own, at the sizes their bandwidth is
-    judged on: GAE over L=256-step segments at S = 128 (the step's size,
+    quoted at: GAE over L=256-step segments at S = 128 (the step's size,
     latency-bound), 11,520 (the paper's 2.9M-timestep batch) and 131,072
     (33.5M timesteps, beyond the 256 MB infinity cache); the reward
     post-processing ahead of GAE at 1,152 and 13,107 games of ten heroes;
