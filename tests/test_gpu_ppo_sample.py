@@ -83,6 +83,11 @@ PPO_CASES = [
     ("bf16-single-logit-heads", 100, 64, (1, 4, 1), True, True, False),
     # the benchmark's shape: N = T B = 16 x 2048 rows of the 4096-unit LSTM
     ("bf16-step-shape", 32768, 4096, HEADS, True, True, False),
+    # the largest logit count (A + 1 = 1024: 16 columns per lane, dWp without
+    # the transposed pair) and the largest head count
+    ("bf16-max-logits", 300, 128, (512, 300, 211), True, True, False),
+    ("f32-max-logits-avail", 200, 64, (512, 300, 211), False, True, True),
+    ("f32-max-heads", 200, 64, (3, 5, 7, 2, 9, 4, 6, 8), False, True, True),
 ]
 
 
@@ -140,30 +145,35 @@ def test_ppo_ratio_one_invariant_on_gpu():
     assert st[4] == 0.0 and abs(st[6] - 1.0) < 1e-5
 
 
-SAMPLE_CASES = [("f32", 512, 256, False, False), ("bf16", 1000, 512, True, False),
-                ("f32-avail", 600, 128, False, True), ("bf16-avail", 700, 256, True, True)]
+# the largest logit count (A + 1 = 1024) and the largest head count (8)
+MAX_LOGITS = (512, 300, 211)
+MAX_HEADS = (3, 5, 7, 2, 9, 4, 6, 8)
+SAMPLE_CASES = [("f32", 512, 256, False, False, HEADS), ("bf16", 1000, 512, True, False, HEADS),
+                ("f32-avail", 600, 128, False, True, HEADS), ("bf16-avail", 700, 256, True, True, HEADS),
+                ("bf16-max-logits", 300, 128, True, False, MAX_LOGITS),
+                ("f32-max-heads-avail", 300, 64, False, True, MAX_HEADS)]
 
 
-@pytest.mark.parametrize("name,B,H,bf16,with_avail", SAMPLE_CASES, ids=[c[0] for c in SAMPLE_CASES])
-def test_policy_sample_matches_oracle(name, B, H, bf16, with_avail):
+@pytest.mark.parametrize("name,B,H,bf16,with_avail,heads", SAMPLE_CASES, ids=[c[0] for c in SAMPLE_CASES])
+def test_policy_sample_matches_oracle(name, B, H, bf16, with_avail, heads):
     need_gpu()
-    banner(f"policy_sample {name} B={B} H={H} avail={with_avail}")
-    inp = _inputs(B, H, HEADS, seed=B, bf16=bf16, with_mask=with_avail, with_avail=with_avail)
+    banner(f"policy_sample {name} B={B} H={H} heads={heads} avail={with_avail}")
+    inp = _inputs(B, H, heads, seed=B, bf16=bf16, with_mask=with_avail, with_avail=with_avail)
     seed, counter = 12345, 7
-    act_ref, logp_ref, v_ref, scores = gumbel_max_sample(heads_forward(inp["hh"], inp["ww"], inp["bp"]), HEADS,
+    act_ref, logp_ref, v_ref, scores = gumbel_max_sample(heads_forward(inp["hh"], inp["ww"], inp["bp"]), heads,
                                                           seed, counter, inp["avail"])
     dt = o5.O5_BF16 if bf16 else o5.O5_F32
-    act = torch.empty((B, len(HEADS)), dtype=torch.int32, device="cuda")
+    act = torch.empty((B, len(heads)), dtype=torch.int32, device="cuda")
     logp = torch.empty(B, dtype=torch.float32, device="cuda")
     value = torch.empty(B, dtype=torch.float32, device="cuda")
-    ws = workspace(o5.o5_policy_sample_workspace_bytes(dt, B, H, HEADS))
-    o5.o5_policy_sample(dt, B, H, HEADS, dev_dt(inp["h"], bf16), dev_dt(inp["Wp"], bf16), dev_f32(inp["bp"]), seed,
+    ws = workspace(o5.o5_policy_sample_workspace_bytes(dt, B, H, heads))
+    o5.o5_policy_sample(dt, B, H, heads, dev_dt(inp["h"], bf16), dev_dt(inp["Wp"], bf16), dev_f32(inp["bp"]), seed,
                         counter, act, logp, value, ws,
                         avail=dev(inp["avail"]) if inp["avail"] is not None else None)
     a = act.cpu().numpy()
     if inp["avail"] is not None:
-        off = np.concatenate([[0], np.cumsum(HEADS)])
-        for k in range(len(HEADS)):
+        off = np.concatenate([[0], np.cumsum(heads)])
+        for k in range(len(heads)):
             blk = inp["avail"][:, off[k]:off[k + 1]]
             empty = ~blk.any(axis=1)
             assert np.all(a[empty, k] == -1) and np.all(act_ref[empty, k] == -1)
@@ -171,7 +181,7 @@ def test_policy_sample_matches_oracle(name, B, H, bf16, with_avail):
             assert np.all(blk[~empty][np.arange(taken.size), taken] == 1), "an unavailable action was drawn"
     # unique where the oracle's best score leads the runner-up by > 1e-4
     agree = np.ones(B, bool)
-    for k in range(len(HEADS)):
+    for k in range(len(heads)):
         s = np.sort(scores[k], axis=1)
         with np.errstate(invalid="ignore"):       # empty heads: -inf - -inf
             clear = ~(s[:, -1] - s[:, -2] <= 1e-4)  # (a single available logit leads by +inf)
