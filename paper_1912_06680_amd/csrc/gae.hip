@@ -8,15 +8,15 @@
 // its end, and maps compose, so a segment can be cut into chunks that are
 // reduced in parallel, combined, and replayed from their carry-in.  Three
 // kernels:
-//  * wave per segment (S <= 4096): the 64 lanes of a wave take 64 chunks of
-//    one segment and combine their maps with a wavefront suffix scan
-//    (shuffles): L/64 + log2(64) dependent steps;
-//  * chunked lanes (S > 4096, L <= 256): lane = segment, wave = one of 8
-//    chunks of at most 32 steps, kept in registers between the reduce and
-//    the replay; the 8 maps of a segment combine through LDS.  A wave reads
-//    64 consecutive segments at each step (coalesced), every input is read
-//    once, and a block of 8 waves covers 64 segments, so 11,520 segments
-//    (the paper's batch) already give 1,440 waves;
+//  * wave per segment (S <= 256, or L > 256 and S <= 4096): the 64 lanes of
+//    a wave take 64 chunks of one segment and combine their maps with a
+//    wavefront suffix scan (shuffles): L/64 + log2(64) dependent steps;
+//  * chunked lanes (256 < S < 32768, L <= 256): lane = segment, wave = one
+//    of 16 chunks of at most 16 steps, kept in registers between the reduce
+//    and the replay; the 16 maps of a segment combine through LDS.  A wave
+//    reads 64 consecutive segments at each step (coalesced), every input is
+//    read once, and a block of 16 waves covers 64 segments, so 11,520
+//    segments (the paper's batch) already give 2,880 waves;
 //  * otherwise (S >= 32768, or L > 256): a lane per 4 segments with 16-byte
 //    accesses when S is a multiple of 4, else a lane per segment; each lane
 //    walks its segments backwards, coalesced as above.
@@ -73,10 +73,10 @@ __global__ void __launch_bounds__(256) gae_lane_per_segment(int L, int S, const 
   }
 }
 
-constexpr int kGaeChunks = 8;      // waves per block = chunks per segment
-constexpr int kGaeChunkMax = 32;   // steps per chunk (so L <= 256)
+constexpr int kGaeChunks = 16;     // waves per block = chunks per segment
+constexpr int kGaeChunkMax = 16;   // steps per chunk (so L <= 256)
 
-// Lane = segment (64 per block), wave c = chunk c of ceil(L / 8) steps.
+// Lane = segment (64 per block), wave c = chunk c of ceil(L / 16) steps.
 __global__ void __launch_bounds__(kGaeChunks * 64) gae_chunked(int L, int S, const float* __restrict__ r,
                                                                const float* __restrict__ v,
                                                                const uint8_t* __restrict__ done, float gamma,
@@ -295,10 +295,14 @@ __global__ void __launch_bounds__(256) segments_to_samples_kernel(int L, int S, 
 
 using namespace o5;
 
-// Segments per launch up to which the wave-per-segment scan is used, and
-// below which the chunked-lane kernel is (above it there are enough lanes
-// for one per segment, and 16-byte accesses stream better).
-static constexpr int kGaeWaveScanMaxS = 4096;
+// Segments per launch up to which the wave-per-segment scan is used (for
+// segments longer than the chunked kernel takes: up to kGaeWaveScanLongMaxS),
+// and below which the chunked-lane kernel is (above it there are enough
+// lanes for one per segment, and 16-byte accesses stream better).  At L =
+// 256 the chunked kernel (16 chunks of 16 steps) beats the wave scan from a
+// few hundred segments on: 16 against 57 us at S = 4096.
+static constexpr int kGaeWaveScanMaxS = 256;
+static constexpr int kGaeWaveScanLongMaxS = 4096;
 static constexpr int kGaeChunkedMaxS = 32768;
 static constexpr int kGaeLaneV = 4;  // segments per lane of the large-S kernel
 
@@ -315,10 +319,11 @@ extern "C" int o5_gae(int L, int S, const float* r, const float* v, const uint8_
   O5_PTR(ret, "ret");
   const float gl = gamma * lambda;
   ktimer_begin(kSiteGae, as_stream(stream));
-  if (S <= kGaeWaveScanMaxS) {
+  const bool chunkable = L <= kGaeChunks * kGaeChunkMax;
+  if (S <= kGaeWaveScanMaxS || (!chunkable && S <= kGaeWaveScanLongMaxS)) {
     hipLaunchKernelGGL(gae_wave_per_segment, dim3((S + 3) / 4), dim3(256), 0, as_stream(stream), L, S,
                        r, v, done, gamma, gl, adv, ret);
-  } else if (S < kGaeChunkedMaxS && L <= kGaeChunks * kGaeChunkMax) {
+  } else if (S < kGaeChunkedMaxS && chunkable) {
     hipLaunchKernelGGL(gae_chunked, dim3((S + 63) / 64), dim3(kGaeChunks * 64), 0, as_stream(stream), L, S, r, v,
                        done, gamma, gl, adv, ret);
   } else if (S % kGaeLaneV == 0 && aligned16(r) && aligned16(v) && aligned16(adv) && aligned16(ret) &&

@@ -21,17 +21,18 @@ def _gae_inputs(L, S, p_done, seed):
     return r, v, d
 
 
-# (L, S): the four kernels (wave scan for S <= 4096; chunked lanes for L <=
-# 256 and S < 32768; otherwise a lane per 4 segments when S % 4 == 0, else a
-# lane per segment), ragged L (not a multiple of 64, of the 8 chunks or of the
-# unroll; empty trailing chunks), ragged S (not a multiple of 64), a single
-# segment/step.
+# (L, S): the four kernels (wave scan for S <= 256, and for L > 256 up to S
+# = 4096; chunked lanes for L <= 256 and 256 < S < 32768; otherwise a lane
+# per 4 segments when S % 4 == 0, else a lane per segment), ragged L (not a
+# multiple of 64, of the 16 chunks or of the unroll; empty trailing chunks),
+# ragged S (not a multiple of 64), a single segment/step.
 @pytest.mark.parametrize("L,S,gamma,lam", [
     (1, 1, 0.998, 0.95), (16, 8, 0.998, 0.95), (256, 128, 0.998, 0.95), (37, 3, 0.9, 0.8),
     (300, 7, 0.998, 0.95), (256, 4097, 0.998, 0.95), (45, 5000, 0.99, 0.9), (256, 128, 0.998, 0.0),
     (256, 4100, 0.998, 1.0), (250, 4500, 0.998, 0.95), (9, 5000, 0.998, 0.95), (1, 4200, 0.998, 0.95),
     (256, 20000, 0.998, 0.95), (257, 4201, 0.998, 0.95), (600, 4160, 0.99, 0.9), (256, 32772, 0.998, 0.95),
     (37, 40000, 0.99, 0.9), (3, 32769, 0.998, 0.95),
+    (256, 1000, 0.998, 0.95), (255, 257, 0.99, 0.9), (17, 300, 0.998, 0.95), (300, 1000, 0.998, 0.95),
 ])
 def test_gae_matches_oracle(L, S, gamma, lam):
     need_gpu()
