@@ -49,10 +49,11 @@ def source_digest():
     return h.hexdigest()
 
 
-def measured_traffic(kernel):
+def measured_traffic(kernel, path=None):
     """HBM bytes per launch of `kernel` from the counter runs summarised in
-    profiles/traffic.json, or None when absent or taken on other sources."""
-    path = os.path.join(ROOT, "profiles", "traffic.json")
+    profiles/traffic.json (or `path`), or None when absent or taken on other
+    sources."""
+    path = path or os.path.join(ROOT, "profiles", "traffic.json")
     try:
         with open(path) as fh:
             t = json.load(fh)
@@ -80,7 +81,7 @@ SITE_SYMBOLS = {
 COPY_REF_N = 1 << 26   # fp32 elements of the reference conversion (256 MiB read, 128 MiB written)
 
 
-def summarize_counters(fetch_dir, write_dir):
+def summarize_counters(fetch_dir, write_dir, path=None):
     """Turn two `rocprofv3 --pmc FETCH_SIZE` / `--pmc WRITE_SIZE` runs of
     `bench.py --copy-ref` into profiles/traffic.json.  Both counters read KiB
     per dispatch; each is scaled by bytes/counter of the reference conversion
@@ -123,11 +124,12 @@ def summarize_counters(fetch_dir, write_dir):
             e["dispatches_" + name.lower()] = len(v)
     out["kernels"] = {k: v for k, v in out["kernels"].items()
                       if "fetch_bytes_per_launch" in v and "write_bytes_per_launch" in v}
-    path = os.path.join(ROOT, "profiles", "traffic.json")
+    path = path or os.path.join(ROOT, "profiles", "traffic.json")
     with open(path, "w") as fh:
         json.dump(out, fh, indent=1)
         fh.write("\n")
     print(json.dumps(out, indent=1))
+    return out
 
 
 def gpu_behaviour(st, inp):
