@@ -150,3 +150,63 @@ def test_nonfinite_count():
     ret[7] = np.inf
     stats, *_ = ppo_loss_grad(h, Wp, bp, act, np.zeros(10), adv, ret, (3,))
     assert stats["nonfinite"] == 2.0
+
+
+def _one_head_rows(z_row, counts):
+    """Rows that all share one logit vector z_row (a single head), with
+    action a repeated counts[a] times."""
+    act = np.concatenate([np.full(c, a) for a, c in enumerate(counts)])[:, None]
+    N = len(act)
+    Wp = np.zeros((len(z_row) + 1, 1))
+    bp = np.append(np.asarray(z_row, np.float64), 0.0)
+    h = np.ones((N, 1))
+    return h, Wp, bp, act
+
+
+def test_approx_kl_is_the_exact_kl_when_rows_follow_the_old_policy():
+    """Statistics at r != 1 pinned by an identity that does not involve the
+    estimator's formula: when the taken actions occur exactly in proportion
+    to the behaviour policy p (action a in k_a of M rows, p_a = k_a / M),
+    the row mean of (r - 1) - log r with r = q_a / p_a is
+    sum_a q_a - 1 + sum_a p_a log(p_a / q_a) = KL(p || q), the exact
+    Kullback-Leibler divergence of the new policy q from p; the row mean of
+    r is sum_a q_a = 1."""
+    from scipy.special import softmax
+    from scipy.stats import entropy
+    counts = np.array([1, 3, 6, 2, 8])          # p = (1, 3, 6, 2, 8) / 20
+    p = counts / counts.sum()
+    z = np.array([0.7, -0.2, 0.4, 1.1, -0.5])   # the new policy's logits
+    q = softmax(z)
+    h, Wp, bp, act = _one_head_rows(z, counts)
+    N = len(act)
+    logp_old = np.log(p[act[:, 0]])
+    adv, ret = np.ones(N), np.zeros(N)
+    stats, *_ = ppo_loss_grad(h, Wp, bp, act, logp_old, adv, ret, (5,))
+    kl = entropy(p, q)                          # scipy: sum p log(p / q)
+    assert kl > 0.1                              # far from r = 1
+    assert abs(stats["approx_kl"] - kl) < 1e-14
+    assert abs(stats["mean_ratio"] - 1.0) < 1e-14
+    # swapping the roles of the two policies (the ratio inverted) gives a
+    # different number, so the sign convention of the log-ratio is pinned
+    inv = np.mean(p[act[:, 0]] / q[act[:, 0]] - 1.0 - np.log(p[act[:, 0]] / q[act[:, 0]]))
+    assert abs(inv - kl) > 1e-3
+
+
+def test_ratio_statistics_at_hand_chosen_log_ratios():
+    """Rows whose log-ratio d = log pi - log pi_old is set by hand: r = e^d.
+    The clip range (1 - 0.2, 1 + 0.2) is (e^-0.22314, e^0.18232) in d, so
+    of d = (0.18, 0.19, -0.22, -0.23, 0, 1) exactly three rows (0.19, -0.23,
+    1) lie outside it; one row of d = 0.3 gives approx_kl = e^0.3 - 1.3 and
+    mean_ratio = e^0.3 (e^0.3 = 1.3498588075760032), and one of d = -0.3
+    gives e^-0.3 - 0.7 and e^-0.3 (e^-0.3 = 0.7408182206817179)."""
+    heads = (4, 3)
+    h, Wp, bp, act, adv, ret = _inputs(11, N=6, H=5, heads=heads)
+    lp = _logpi(h, Wp, bp, act, heads)
+    d = np.array([0.18, 0.19, -0.22, -0.23, 0.0, 1.0])
+    stats, *_ = ppo_loss_grad(h, Wp, bp, act, lp - d, adv, ret, heads)
+    assert stats["clipfrac"] == 0.5
+    for dd, e_d in ((0.3, 1.3498588075760032), (-0.3, 0.7408182206817179)):
+        s1, *_ = ppo_loss_grad(h[:1], Wp, bp, act[:1], lp[:1] - dd, adv[:1], ret[:1], heads)
+        assert abs(s1["mean_ratio"] - e_d) < 1e-15
+        assert abs(s1["approx_kl"] - (e_d - 1.0 - dd)) < 1e-15
+        assert s1["clipfrac"] == 1.0
