@@ -15,13 +15,15 @@ the bias-corrected second moment that already includes the current
 """
 import numpy as np
 
+from .precision import F
+
 
 def adam_step(p, m, v, g, lr, beta1, beta2, eps, clip_k, step):
     """One update.  Returns new (p, m, v) as fp64 arrays; inputs untouched."""
-    p = np.asarray(p, np.float64)
-    m = np.asarray(m, np.float64)
-    v = np.asarray(v, np.float64)
-    g = np.asarray(g, np.float64)
+    p = np.asarray(p, F())
+    m = np.asarray(m, F())
+    v = np.asarray(v, F())
+    g = np.asarray(g, F())
     v_new = beta2 * v + (1.0 - beta2) * g * g
     v_hat = v_new / (1.0 - beta2 ** step)
     if clip_k > 0:

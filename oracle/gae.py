@@ -20,15 +20,17 @@ Layout is time-major: r, done [L, S]; v [L+1, S] with row L the bootstrap.
 """
 import numpy as np
 
+from .precision import F
+
 
 def gae(r, v, done, gamma, lam):
     """Sequential reverse loop over t = L-1 .. 0.  Returns (adv, ret) [L, S]."""
-    r = np.asarray(r, np.float64)
-    v = np.asarray(v, np.float64)
-    nd = 1.0 - np.asarray(done, np.float64)
+    r = np.asarray(r, F())
+    v = np.asarray(v, F())
+    nd = 1.0 - np.asarray(done, F())
     L, S = r.shape
-    adv = np.zeros((L, S))
-    carry = np.zeros(S)
+    adv = np.zeros((L, S), F())
+    carry = np.zeros(S, F())
     for t in reversed(range(L)):
         delta = r[t] + gamma * nd[t] * v[t + 1] - v[t]
         carry = delta + gamma * lam * nd[t] * carry
@@ -47,8 +49,8 @@ def segments_to_samples(adv, ret, done, T):
     """
     L, S = adv.shape
     J = L // T
-    adv_s = np.empty((T, S * J))
-    ret_s = np.empty((T, S * J))
+    adv_s = np.empty((T, S * J), F())
+    ret_s = np.empty((T, S * J), F())
     reset = np.zeros((T, S * J), dtype=np.uint8)
     for s in range(S):
         for j in range(J):

@@ -27,10 +27,12 @@ arithmetic stay fp64.  Without it every value is fp64.
 """
 import numpy as np
 
+from .precision import F
+
 
 def sigmoid(a):
     """Logistic function, evaluated without overflow for either sign."""
-    a = np.asarray(a, dtype=np.float64)
+    a = np.asarray(a, dtype=F())
     out = np.empty_like(a)
     pos = a >= 0
     out[pos] = 1.0 / (1.0 + np.exp(-a[pos]))
@@ -41,8 +43,8 @@ def sigmoid(a):
 
 def _keep(reset, t, B):
     if reset is None:
-        return np.ones((B, 1))
-    return 1.0 - np.asarray(reset[t], dtype=np.float64).reshape(B, 1)
+        return np.ones((B, 1), F())
+    return 1.0 - np.asarray(reset[t], dtype=F()).reshape(B, 1)
 
 
 def _identity(a):
@@ -58,17 +60,17 @@ def lstm_forward(x, Wx, Wh, b, h0, c0, reset=None, store=None):
     computed from the exact gates) and the recurrent input is the stored h.
     """
     store = store or _identity
-    x = np.asarray(x, np.float64)
-    Wx = np.asarray(Wx, np.float64)
-    Wh = np.asarray(Wh, np.float64)
-    b = np.asarray(b, np.float64)
+    x = np.asarray(x, F())
+    Wx = np.asarray(Wx, F())
+    Wh = np.asarray(Wh, F())
+    b = np.asarray(b, F())
     T, B, _ = x.shape
     H = Wh.shape[1]
-    h = np.empty((T, B, H))
-    c = np.empty((T, B, H))
-    gates = np.empty((T, B, 4 * H))
-    h_prev = store(np.asarray(h0, np.float64))
-    c_prev = np.asarray(c0, np.float64)
+    h = np.empty((T, B, H), F())
+    c = np.empty((T, B, H), F())
+    gates = np.empty((T, B, 4 * H), F())
+    h_prev = store(np.asarray(h0, F()))
+    c_prev = np.asarray(c0, F())
     for t in range(T):
         keep = _keep(reset, t, B)
         h_tilde = keep * h_prev
@@ -102,22 +104,22 @@ def lstm_bptt(x, Wx, Wh, h0, c0, reset, h, c, gates, dh, dhT=None, dcT=None,
     Returns (dWx [4H,D], dWh [4H,H], db [4H], dx [T,B,D] or None).
     """
     store = store or _identity
-    x = np.asarray(x, np.float64)
-    Wx = np.asarray(Wx, np.float64)
-    Wh = np.asarray(Wh, np.float64)
+    x = np.asarray(x, F())
+    Wx = np.asarray(Wx, F())
+    Wh = np.asarray(Wh, F())
     T, B, D = x.shape
     H = Wh.shape[1]
     dWx = np.zeros_like(Wx)
     dWh = np.zeros_like(Wh)
-    db = np.zeros(4 * H)
-    dx = np.zeros((T, B, D)) if want_dx else None
+    db = np.zeros(4 * H, F())
+    dx = np.zeros((T, B, D), F()) if want_dx else None
 
-    dh_next = np.zeros((B, H)) if dhT is None else np.array(dhT, np.float64)
-    dc_next = np.zeros((B, H)) if dcT is None else np.array(dcT, np.float64)
+    dh_next = np.zeros((B, H), F()) if dhT is None else np.array(dhT, F())
+    dc_next = np.zeros((B, H), F()) if dcT is None else np.array(dcT, F())
     for t in reversed(range(T)):
         keep = _keep(reset, t, B)
-        h_prev = store(np.asarray(h0, np.float64)) if t == 0 else h[t - 1]
-        c_prev = np.asarray(c0, np.float64) if t == 0 else c[t - 1]
+        h_prev = store(np.asarray(h0, F())) if t == 0 else h[t - 1]
+        c_prev = np.asarray(c0, F()) if t == 0 else c[t - 1]
         h_tilde = keep * h_prev
         c_tilde = keep * c_prev
         i = gates[t][:, 0 * H:1 * H]

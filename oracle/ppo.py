@@ -43,6 +43,8 @@ E (the observation encoder that would produce E is not modelled).
 """
 import numpy as np
 
+from .precision import F
+
 STAT_NAMES = ("total", "pg", "vf", "ent", "clipfrac", "approx_kl",
               "mean_ratio", "nonfinite")
 
@@ -56,8 +58,8 @@ def head_offsets(head_sizes):
 
 def heads_forward(h, Wp, bp):
     """Logits and value: z = h Wp^T + bp, an [N, A+1] array."""
-    return np.asarray(h, np.float64) @ np.asarray(Wp, np.float64).T + \
-        np.asarray(bp, np.float64)
+    return np.asarray(h, F()) @ np.asarray(Wp, F()).T + \
+        np.asarray(bp, F())
 
 
 def head_logprob_entropy(z, act, head_sizes, avail=None):
@@ -70,8 +72,8 @@ def head_logprob_entropy(z, act, head_sizes, avail=None):
     off = head_offsets(head_sizes)
     K = len(head_sizes)
     av_all = np.ones((N, off[-1]), bool) if avail is None else np.asarray(avail) != 0
-    logp = np.empty((N, K))
-    ent = np.empty((N, K))
+    logp = np.empty((N, K), F())
+    ent = np.empty((N, K), F())
     probs = []
     rows = np.arange(N)
     for k in range(K):
@@ -93,8 +95,8 @@ def head_logprob_entropy(z, act, head_sizes, avail=None):
 
 def unit_logits(h, Wq, bq, E):
     """Query q = h Wq^T + bq and logits z[n, u] = <q[n], E[n, u]>."""
-    q = np.asarray(h, np.float64) @ np.asarray(Wq, np.float64).T + np.asarray(bq, np.float64)
-    return q, np.einsum("nj,nuj->nu", q, np.asarray(E, np.float64))
+    q = np.asarray(h, F()) @ np.asarray(Wq, F()).T + np.asarray(bq, F())
+    return q, np.einsum("nj,nuj->nu", q, np.asarray(E, F()))
 
 
 def ppo_loss_grad(h, Wp, bp, act, logp_old, adv, ret, head_sizes,
@@ -106,18 +108,18 @@ def ppo_loss_grad(h, Wp, bp, act, logp_old, adv, ret, head_sizes,
     ``unit`` = dict(head=k, Wq=[d,H], bq=[d], E=[N,n_k,d]) also
     (dWq [d,H], dbq [d]) as a sixth element.
     """
-    h = np.asarray(h, np.float64)
-    Wp = np.asarray(Wp, np.float64)
+    h = np.asarray(h, F())
+    Wp = np.asarray(Wp, F())
     act = np.asarray(act, np.int64)
-    logp_old = np.asarray(logp_old, np.float64)
-    A_ = np.asarray(adv, np.float64)
-    R_ = np.asarray(ret, np.float64)
+    logp_old = np.asarray(logp_old, F())
+    A_ = np.asarray(adv, F())
+    R_ = np.asarray(ret, F())
     N = h.shape[0]
     K = len(head_sizes)
     off = head_offsets(head_sizes)
     A = off[-1]
-    mask = np.ones((N, K)) if head_mask is None else \
-        np.asarray(head_mask, np.float64)
+    mask = np.ones((N, K), F()) if head_mask is None else \
+        np.asarray(head_mask, F())
 
     z = heads_forward(h, Wp, bp)
     if unit is not None:
@@ -179,8 +181,8 @@ def ppo_loss_grad(h, Wp, bp, act, logp_old, adv, ret, head_sizes,
     ku = unit["head"]
     dz_u = dz[:, off[ku]:off[ku + 1]].copy()
     dz[:, off[ku]:off[ku + 1]] = 0.0
-    Wq = np.asarray(unit["Wq"], np.float64)
-    dq = np.einsum("nu,nuj->nj", dz_u, np.asarray(unit["E"], np.float64))
+    Wq = np.asarray(unit["Wq"], F())
+    dq = np.einsum("nu,nuj->nj", dz_u, np.asarray(unit["E"], F()))
     dh = dz @ Wp + dq @ Wq
     dWp = dz.T @ h
     dbp = dz.sum(axis=0)
