@@ -268,7 +268,8 @@ __global__ void __launch_bounds__(256) gae_wave_per_segment(int L, int S, const 
   }
 }
 
-// One thread per (t, b) of the sample layout.
+// One thread per (t, b) of the sample layout, grid-stride; every index is
+// 64-bit, so T * B = L * S may exceed 2^31.
 __global__ void __launch_bounds__(256) segments_to_samples_kernel(int L, int S, int T,
                                                                   const float* __restrict__ adv,
                                                                   const float* __restrict__ ret,
@@ -276,19 +277,21 @@ __global__ void __launch_bounds__(256) segments_to_samples_kernel(int L, int S, 
                                                                   float* __restrict__ adv_s,
                                                                   float* __restrict__ ret_s,
                                                                   uint8_t* __restrict__ reset) {
-  const int J = L / T;
-  const int B = S * J;
+  const size_t J = static_cast<size_t>(L / T);
+  const size_t S_ = static_cast<size_t>(S);
+  const size_t B = S_ * J;
   const size_t total = static_cast<size_t>(T) * B;
-  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= total) return;
-  const int t = static_cast<int>(i / B);
-  const int b = static_cast<int>(i % B);
-  const int s = b / J;
-  const int j = b % J;
-  const size_t src = static_cast<size_t>(T * j + t) * S + s;
-  adv_s[i] = adv[src];
-  ret_s[i] = ret[src];
-  reset[i] = (t > 0 && done[src - S] != 0) ? 1 : 0;
+  const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
+  for (size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < total; i += stride) {
+    const size_t t = i / B;
+    const size_t b = i - t * B;
+    const size_t s = b / J;
+    const size_t j = b - s * J;
+    const size_t src = (static_cast<size_t>(T) * j + t) * S_ + s;
+    adv_s[i] = adv[src];
+    ret_s[i] = ret[src];
+    reset[i] = (t > 0 && done[src - S_] != 0) ? 1 : 0;
+  }
 }
 
 }  // namespace o5
@@ -351,7 +354,8 @@ extern "C" int o5_segments_to_samples(int L, int S, int T, const float* adv, con
   O5_PTR(ret_s, "ret_s");
   O5_PTR(reset, "reset");
   const size_t total = static_cast<size_t>(L) * S;
-  hipLaunchKernelGGL(segments_to_samples_kernel, dim3(static_cast<unsigned>((total + 255) / 256)),
-                     dim3(256), 0, as_stream(stream), L, S, T, adv, ret, done, adv_s, ret_s, reset);
+  const size_t blocks = std::min<size_t>((total + 255) / 256, size_t{1} << 20);
+  hipLaunchKernelGGL(segments_to_samples_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                     as_stream(stream), L, S, T, adv, ret, done, adv_s, ret_s, reset);
   return check_launch("o5_segments_to_samples");
 }

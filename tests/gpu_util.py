@@ -71,3 +71,23 @@ def assert_close(name, gpu, ref, tol):
     e = rel_err(gpu, ref)
     print(f"    {name}: rel_err={e:.3e} (tol {tol:g})", flush=True)
     assert e <= tol, f"{name}: rel_err {e:.3e} > {tol:g}"
+
+
+def assert_close_both(name, gpu, ref, ref_plain, tol):
+    """bf16 path: compare with the oracle that rounds where the device stores
+    a bf16 operand (``ref``) and with the plain definition that rounds only
+    the inputs (``ref_plain``); both at ``tol``, both printed."""
+    e = rel_err(gpu, ref)
+    e2 = rel_err(gpu, ref_plain)
+    print(f"    {name}: rel_err={e:.3e} storage-point oracle, {e2:.3e} plain oracle (tol {tol:g})", flush=True)
+    assert e <= tol, f"{name}: rel_err {e:.3e} > {tol:g} (storage-point oracle)"
+    assert e2 <= tol, f"{name}: rel_err {e2:.3e} > {tol:g} (plain oracle)"
+
+
+def tile_rows(B, tile=256):
+    """One row inside every `tile`-row block of B rows (its middle, or the
+    middle of the partial last block), plus the first and last row."""
+    rows = {0, B - 1}
+    for t0 in range(0, B, tile):
+        rows.add(min(t0 + tile // 2, (t0 + B - 1) // 2 if t0 + tile > B else t0 + tile // 2))
+    return sorted(rows)

@@ -74,6 +74,37 @@ def test_segments_to_samples_bit_exact(L, S, T):
     assert np.array_equal(reset.cpu().numpy(), erst)
 
 
+def test_segments_to_samples_beyond_2_pow_31_elements():
+    """L * S = 16 * (2^27 + 8) > 2^31 elements (about 38 GB of buffers): the
+    cut indexes in 64 bits.  Values are distinct integers (exact in fp32)
+    so a misplaced element cannot pass; sampled segments are cut by the
+    oracle from their own columns and compared bit for bit."""
+    need_gpu()
+    L, T = 16, 4
+    S = (1 << 27) + 8
+    J = L // T
+    banner(f"segments_to_samples L={L} S={S} T={T} (L*S = {L * S} > 2^31)")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(5)
+    adv = torch.randint(0, 1 << 24, (L, S), generator=gen, device="cuda").to(torch.float32)
+    ret = torch.randint(0, 1 << 24, (L, S), generator=gen, device="cuda").to(torch.float32)
+    done = (torch.rand((L, S), generator=gen, device="cuda") < 0.3).to(torch.uint8)
+    B = S * J
+    a_s = torch.empty((T, B), dtype=torch.float32, device="cuda")
+    r_s = torch.empty_like(a_s)
+    reset = torch.empty((T, B), dtype=torch.uint8, device="cuda")
+    o5.o5_segments_to_samples(L, S, T, adv, ret, done, a_s, r_s, reset)
+    torch.cuda.synchronize()
+    segs = torch.tensor([0, 1, 12345, (1 << 27) - 1, 1 << 27, S - 1], device="cuda")
+    cols = (segs[:, None] * J + torch.arange(J, device="cuda")[None]).reshape(-1)
+    ea, er, erst = segments_to_samples(host(adv[:, segs]), host(ret[:, segs]), done[:, segs].cpu().numpy(), T)
+    assert np.array_equal(host(a_s[:, cols]), ea)
+    assert np.array_equal(host(r_s[:, cols]), er)
+    assert np.array_equal(reset[:, cols].cpu().numpy(), erst)
+    del adv, ret, done, a_s, r_s, reset
+    torch.cuda.empty_cache()
+
+
 def _adam_inputs(n, seed):
     rng = np.random.Generator(np.random.PCG64(seed))
     p = rng.standard_normal(n, dtype=np.float32) * 0.05

@@ -123,6 +123,43 @@ def test_ppo_loss_grad_matches_oracle(name, N, H, heads, bf16, with_mask, with_a
     assert_close("dbp", host(dbp), dbp_ref, tol)
 
 
+@pytest.mark.parametrize("bf16", [False, True])
+def test_ppo_nonfinite_rows_are_counted_on_gpu(bf16):
+    """NaN advantages on two rows and an infinite return on a third: the
+    device's stats[7] counts exactly those three rows, and the gradient dh
+    of every other row (which depends on its own row only) stays finite and
+    matches the oracle."""
+    need_gpu()
+    N, H, heads = 300, 128, HEADS
+    banner(f"ppo non-finite rows N={N} H={H} bf16={bf16}")
+    inp = _inputs(N, H, heads, seed=17, bf16=bf16, with_mask=True)
+    bad = np.array([3, 100, 257])
+    inp["adv"][bad[:2]] = np.nan
+    inp["ret"][bad[2]] = np.inf
+    with np.errstate(invalid="ignore"):
+        stats_ref, dh_ref, _, _, _ = ppo_loss_grad(
+            inp["hh"], inp["ww"], inp["bp"], inp["act"], inp["logp_old"], inp["adv"], inp["ret"], heads,
+            0.2, 1.0, 0.01, inp["mask"])
+    assert stats_ref["nonfinite"] == 3.0
+    dt = o5.O5_BF16 if bf16 else o5.O5_F32
+    A1 = sum(heads) + 1
+    stats = torch.empty(8, dtype=torch.float32, device="cuda")
+    dh = torch.empty((N, H), dtype=torch.float32, device="cuda")
+    dWp = torch.empty((A1, H), dtype=torch.float32, device="cuda")
+    dbp = torch.empty(A1, dtype=torch.float32, device="cuda")
+    ws = workspace(o5.o5_ppo_loss_grad_workspace_bytes(dt, N, H, heads))
+    o5.o5_ppo_loss_grad(dt, N, H, heads, dev_dt(inp["h"], bf16), dev_dt(inp["Wp"], bf16), dev_f32(inp["bp"]),
+                        dev(inp["act"]), dev_f32(inp["logp_old"]), dev_f32(inp["adv"]), dev_f32(inp["ret"]),
+                        dev(inp["mask"]), 0.2, 1.0, 0.01, stats, dh, dWp, dbp, ws)
+    st = host(stats)
+    print(f"    nonfinite: gpu={st[7]} oracle={stats_ref['nonfinite']}", flush=True)
+    assert st[7] == 3.0
+    clean = np.setdiff1d(np.arange(N), bad)
+    dh_h = host(dh)
+    assert not np.all(np.isfinite(dh_h[bad]))
+    assert_close("dh[clean rows]", dh_h[clean], dh_ref[clean], TOL_BF16 if bf16 else TOL_F32)
+
+
 def test_ppo_ratio_one_invariant_on_gpu():
     """logp_old = logpi makes every ratio 1: pg = -mean(A) and clipfrac = 0."""
     need_gpu()
