@@ -439,7 +439,12 @@ int o5_surgery_fold_input(int D, int H, int A1, int Dk, const float* E,
 int o5_f32_to_bf16(size_t n, const float* src, uint16_t* dst, void* stream);
 
 /* ------------------------------------------------------------------------
- * Kernel timing (instrumentation for benchmarks, not thread-safe).
+ * Kernel timing (instrumentation for benchmarks).  The timer is
+ * process-wide state and so lies outside the stateless contract of the
+ * compute calls above: its records are guarded by a lock, so calls from
+ * several threads do not race, but the two events of one site are paired
+ * in recording order, so a site should not be timed from two streams at
+ * once.
  * o5_ktimer_enable(1) clears previous records and starts recording a pair
  * of hipEvents on the caller's stream around every launch site listed
  * below; o5_ktimer_enable(0) stops recording (records are kept until the

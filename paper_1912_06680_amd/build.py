@@ -31,8 +31,8 @@ def _hipcc():
     raise RuntimeError("hipcc not found (ROCm is required to build libo5)")
 
 
-def _compile(hipcc, src, obj, defines=()):
-    cmd = [hipcc, *HIPCC_FLAGS, *[f"-D{d}" for d in defines], "-c", src, "-o", obj]
+def _compile(hipcc, src, obj):
+    cmd = [hipcc, *HIPCC_FLAGS, "-c", src, "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     msgs = "\n".join(l for l in (res.stdout + res.stderr).splitlines()
                      if "is not a recognized feature" not in l)
@@ -41,9 +41,8 @@ def _compile(hipcc, src, obj, defines=()):
     return msgs
 
 
-def build(verbose=False, out=None, defines=()):
-    """Compile all HIP sources and link libo5.so (or `out`).  Always rebuilds.
-    `defines` are extra -D flags (tuning variants)."""
+def build(verbose=False, out=None):
+    """Compile all HIP sources and link libo5.so (or `out`).  Always rebuilds."""
     hipcc = _hipcc()
     lib_path = out or LIB_PATH
     build_dir = BUILD_DIR if out is None else out + ".build"
@@ -52,7 +51,7 @@ def build(verbose=False, out=None, defines=()):
     objs = [os.path.join(build_dir, s[:-4] + ".o") for s in srcs]
     jobs = min(len(srcs), max(1, min(8, os.cpu_count() or 1)))
     with _cf.ThreadPoolExecutor(jobs) as ex:
-        futs = [ex.submit(_compile, hipcc, os.path.join(CSRC, s), o, defines) for s, o in zip(srcs, objs)]
+        futs = [ex.submit(_compile, hipcc, os.path.join(CSRC, s), o) for s, o in zip(srcs, objs)]
         for s, f in zip(srcs, futs):
             msgs = f.result()
             if verbose and msgs.strip():

@@ -1,6 +1,8 @@
 // Status strings, per-thread error messages, fp32 -> bf16 conversion.
 #include "common.h"
 
+#include <atomic>
+#include <mutex>
 #include <utility>
 #include <vector>
 
@@ -29,12 +31,16 @@ int check_launch(const char* where) {
 // ----------------------------------------------------------- kernel timer
 // Events are recorded on the caller's stream around each timed launch site;
 // elapsed times are read (and the events returned to the pool) by
-// o5_ktimer_read.  Host-side state only; meant for single-threaded
-// benchmarking.
+// o5_ktimer_read.  Process-wide host state, outside the stateless contract
+// of the compute calls: `active` (the recorded sites, 0 = off) is read
+// atomically at every launch site, and everything else is touched under
+// `lock`, so concurrent callers never race on it; a begin/end pair of one
+// site is only meaningful when that site is not timed from two streams at
+// once.
 namespace {
 struct KTimer {
-  bool on = false;
-  unsigned mask = 0;  // sites recorded while on
+  std::atomic<unsigned> active{0};
+  std::mutex lock;
   std::vector<hipEvent_t> pool;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> done[kSiteCount];
   hipEvent_t open[kSiteCount] = {};
@@ -57,13 +63,16 @@ const char* kSiteNames[kSiteCount] = {"lstm_fwd_gemm", "lstm_fwd_cell", "lstm_dh
 }  // namespace
 
 void ktimer_begin(int site, hipStream_t s) {
-  if (!g_kt.on || !((g_kt.mask >> site) & 1u)) return;
+  if (!((g_kt.active.load(std::memory_order_acquire) >> site) & 1u)) return;
+  std::lock_guard<std::mutex> g(g_kt.lock);
   hipEvent_t e = g_kt.get();
   if (e && hipEventRecord(e, s) == hipSuccess) g_kt.open[site] = e;
 }
 
 void ktimer_end(int site, hipStream_t s) {
-  if (!g_kt.on || !g_kt.open[site]) return;
+  if (!((g_kt.active.load(std::memory_order_acquire) >> site) & 1u)) return;
+  std::lock_guard<std::mutex> g(g_kt.lock);
+  if (!g_kt.open[site]) return;
   hipEvent_t e = g_kt.get();
   if (e && hipEventRecord(e, s) == hipSuccess) g_kt.done[site].emplace_back(g_kt.open[site], e);
   g_kt.open[site] = nullptr;
@@ -115,9 +124,10 @@ extern "C" const char* o5_last_error(void) { return o5::g_last_error; }
 
 extern "C" int o5_ktimer_enable_sites(unsigned mask) {
   if (mask == 0) {  // stop recording; keep what was recorded
-    g_kt.on = false;
+    g_kt.active.store(0, std::memory_order_release);
     return O5_OK;
   }
+  std::lock_guard<std::mutex> g(g_kt.lock);
   for (int i = 0; i < kSiteCount; ++i) {
     for (auto& pr : g_kt.done[i]) {
       g_kt.pool.push_back(pr.first);
@@ -126,8 +136,7 @@ extern "C" int o5_ktimer_enable_sites(unsigned mask) {
     g_kt.done[i].clear();
     g_kt.open[i] = nullptr;
   }
-  g_kt.mask = mask;
-  g_kt.on = true;
+  g_kt.active.store(mask & ((1u << kSiteCount) - 1u), std::memory_order_release);
   return O5_OK;
 }
 
@@ -136,6 +145,7 @@ extern "C" int o5_ktimer_enable(int on) { return o5_ktimer_enable_sites(on ? ~0u
 extern "C" int o5_ktimer_read(int site, double* total_ms, int* launches) {
   O5_CHECK(site >= 0 && site < kSiteCount, O5_E_ARG, "o5_ktimer_read: site %d out of range", site);
   O5_CHECK(total_ms != nullptr && launches != nullptr, O5_E_NULL, "o5_ktimer_read: NULL output");
+  std::lock_guard<std::mutex> g(g_kt.lock);
   double t = 0.0;
   for (auto& pr : g_kt.done[site]) {
     float ms = 0.0f;

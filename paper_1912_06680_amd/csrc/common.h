@@ -86,20 +86,11 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
 }
 
 // ------------------------------------------------------------- activations
-#ifndef O5_FAST_ACT
-#define O5_FAST_ACT 1
-#endif
-#if O5_FAST_ACT
 // sigma(a) = 1 / (1 + e^-a) and tanh(a) = 1 - 2 / (1 + e^2a) with the
 // hardware exp2 and reciprocal (about 1 ulp each); both saturate correctly
 // when the exponential overflows or underflows.
 __device__ __forceinline__ float sigmoid_f(float a) { return __builtin_amdgcn_rcpf(1.0f + __expf(-a)); }
 __device__ __forceinline__ float tanh_f(float a) { return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + __expf(2.0f * a)); }
-#else
-// IEEE division and the math library's tanh (slower, for comparison runs)
-__device__ __forceinline__ float sigmoid_f(float a) { return 1.0f / (1.0f + __expf(-a)); }
-__device__ __forceinline__ float tanh_f(float a) { return tanhf(a); }
-#endif
 
 // Element type tags used by templates: float (fp32 path) or uint16_t
 // holding bf16 bits (bf16 path).

@@ -364,10 +364,7 @@ __global__ void __launch_bounds__(256) gemm_f32_fma(AL al, BL bl, Epi epi, int M
 
 // ------------------------------------------------------ bf16 MFMA engine
 
-#ifndef O5_GROUP_M
-#define O5_GROUP_M 4
-#endif
-constexpr int kGroupM = O5_GROUP_M;
+constexpr int kGroupM = 4;
 
 // Map the linear block id to a (tile_m, tile_n) pair.  Blocks are dealt
 // round-robin to the 8 XCDs, so each XCD first gets a contiguous run of
@@ -509,22 +506,19 @@ inline void launch_gemm_f32(const AL& al, const BL& bl, const Epi& epi, int M, i
 }
 
 // Tile configurations of the bf16 engines: block tile, waves (x 64 threads).
-//   kDma256    256 x 256, 8 waves, direct-to-LDS 4-stage pipeline (gemm_dma.h)
-//   k256x256   256 x 256, 4 waves of 128 x 128 (one wave per SIMD)
-//   k256x256w8 256 x 256, 8 waves of 128 x 64 (two waves per SIMD)
-//   k128x128   128 x 128, 4 waves of 64 x 64
-enum class BfTile { kDma256, k256x256, k256x256w8, k128x128 };
+//   kDma256    256 x 256, 8 waves, buffer loads straight to LDS (gemm_kk.h for
+//              two K-contiguous operands, else gemm_dma.h)
+//   k256x256w8 256 x 256, 8 waves of 128 x 64, register-staged (operands the
+//              direct-to-LDS engines cannot take: a masked second source)
+//   k128x128   128 x 128, 4 waves of 64 x 64, register-staged (small grids)
+enum class BfTile { kDma256, k256x256w8, k128x128 };
 
 template <class AL, class BL, class Epi>
 inline void launch_gemm_bf16(const AL& al, const BL& bl, const Epi& epi, int M, int N, int K, int splits,
                              BfTile tile, hipStream_t s) {
   const int nkt = (K + 63) / 64;
   const int kps = (nkt + splits - 1) / splits;
-  if (tile == BfTile::k256x256) {
-    const unsigned tiles = ((M + 255) / 256) * ((N + 255) / 256);
-    hipLaunchKernelGGL((gemm_bf16_mfma<256, 256, 128, 128, AL, BL, Epi>), dim3(tiles, 1, splits), dim3(256), 0, s,
-                       al, bl, epi, M, N, K, kps);
-  } else if (tile == BfTile::k256x256w8) {
+  if (tile == BfTile::k256x256w8) {
     const unsigned tiles = ((M + 255) / 256) * ((N + 255) / 256);
     hipLaunchKernelGGL((gemm_bf16_mfma<256, 256, 128, 64, AL, BL, Epi>), dim3(tiles, 1, splits), dim3(512), 0, s,
                        al, bl, epi, M, N, K, kps);

@@ -38,29 +38,14 @@
 
 #include "gemm.h"
 
-#ifndef O5_DMA_READ_AHEAD
-#define O5_DMA_READ_AHEAD 0
-#endif
-#ifndef O5_DMA_WAVES
-#define O5_DMA_WAVES 8
-#endif
-#ifndef O5_DMA_STAGES
-#define O5_DMA_STAGES 4
-#endif
-
 namespace o5 {
 
 namespace dma {
 
-constexpr int BM = 256, BN = 256, BK = 32, STAGES = O5_DMA_STAGES;
+constexpr int BM = 256, BN = 256, BK = 32, STAGES = 4;
 static_assert(STAGES >= 3 && STAGES <= 5, "3..5 stages fit in 160 KB of LDS");
-#if O5_DMA_WAVES == 4
-// 4 waves (2 x 2) of 128 x 128, one wave per SIMD
-constexpr int WM = 128, WN = 128;
-#else
 // 8 waves (2 x 4) of 128 x 64, two waves per SIMD
 constexpr int WM = 128, WN = 64;
-#endif
 constexpr int WAVES_M = BM / WM, WAVES_N = BN / WN;
 constexpr int NWAVES = WAVES_M * WAVES_N;
 constexpr int NT = NWAVES * 64;
@@ -326,25 +311,6 @@ __global__ void __launch_bounds__(dma::NT, 1)
       ta.issue(al, (kt + STAGES - 1) * BK, an, wave);
       tb.issue(bl, (kt + STAGES - 1) * BK, bn, wave);
     }
-#if O5_DMA_READ_AHEAD
-    // both k steps' fragments are requested before the first MFMA, so the
-    // second step's LDS latency hides under the first step's MFMAs
-    bf16x8_t af[2][MB], bfr[2][NB];
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      Op<AL>::template read<MB>(as, wm0, lane, kk, af[kk]);
-      Op<BL>::template read<NB>(bs, wn0, lane, kk, bfr[kk]);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x100, 2 * (MB + NB) * 2, 0);  // all LDS reads first
-    __builtin_amdgcn_sched_group_barrier(0x008, 2 * MB * NB, 0);        // then the MFMAs
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk)
-#pragma unroll
-      for (int a = 0; a < MB; ++a)
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kk][a], bfr[kk][b], acc[a][b], 0, 0, 0);
-#else
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
       bf16x8_t af[MB], bfr[NB];
@@ -356,7 +322,6 @@ __global__ void __launch_bounds__(dma::NT, 1)
         for (int b = 0; b < NB; ++b)
           acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
     }
-#endif
   };
   // the stage of tile kt is (kt - kt0) % STAGES; unrolling by STAGES keeps
   // every stage address a compile-time constant

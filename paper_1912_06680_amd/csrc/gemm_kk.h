@@ -35,10 +35,6 @@
 
 #include "gemm_dma.h"
 
-#ifndef O5_KK_WAVES
-#define O5_KK_WAVES 8
-#endif
-
 namespace o5 {
 
 namespace kk {
@@ -49,7 +45,7 @@ constexpr int ROW_BYTES = BK * 2;      // one stage row
 constexpr int CPR = BK / 8;            // 16-byte chunks per row
 constexpr int RPI = 1024 / ROW_BYTES;  // rows per 1 KB copy
 constexpr int R256 = 256 / ROW_BYTES;  // rows per 256 bytes
-constexpr int NWAVES = O5_KK_WAVES;    // 8, or 4 (one wave per SIMD)
+constexpr int NWAVES = 8;              // two per SIMD
 constexpr int NT = NWAVES * 64;
 
 // Block and wave tiling of a 256 x BN block tile.
@@ -320,16 +316,6 @@ inline bool kk_fits(const KRows2<E>& l) {
   const size_t b1 = l.p1 != nullptr ? static_cast<size_t>(l.rows) * l.ld1 * sizeof(E) : 0;
   return l.K >= kk::BK && l.K % kk::BK == 0 && l.K0 % kk::BK == 0 && b0 < (size_t{1} << 31) &&
          b1 < (size_t{1} << 31);
-}
-
-// The K-contiguous engine is the default for two K-contiguous bf16 operands;
-// O5_GEMM_ENGINE=dma selects the 8-wave direct-to-LDS engine instead.
-inline bool kk_engine_enabled() {
-  static const bool v = [] {
-    const char* e = std::getenv("O5_GEMM_ENGINE");
-    return !(e && e[0] == 'd');
-  }();
-  return v;
 }
 
 }  // namespace o5

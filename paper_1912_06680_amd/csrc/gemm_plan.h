@@ -18,31 +18,6 @@ struct GemmPlan {
 
 inline int cdiv(long long a, long long b) { return static_cast<int>((a + b - 1) / b); }
 
-// Engine used for 256 x 256 blocks; O5_BF16_TILE=w4|w8|128 selects one of the
-// register-staged engines instead (for comparison runs).
-inline int bf16_tile_override() {
-  static const int v = [] {
-    const char* e = std::getenv("O5_BF16_TILE");
-    if (!e) return 0;
-    if (e[0] == 'w' && e[1] == '4') return 1;
-    if (e[0] == 'w' && e[1] == '8') return 2;
-    if (e[0] == '1') return 3;
-    return 0;
-  }();
-  return v;
-}
-
-// Column tile of the K-contiguous engine; O5_KK_BN=256|128 forces one (for
-// comparison runs).
-inline int kk_bn_override() {
-  static const int v = [] {
-    const char* e = std::getenv("O5_KK_BN");
-    if (!e) return 0;
-    return e[0] == '1' ? 128 : e[0] == '2' ? 256 : 0;
-  }();
-  return v;
-}
-
 // Choose engine, tile and split-K so the launch has >= ~256 blocks (one per
 // CU) while every split keeps a reasonable number of K tiles.  256 x 128
 // tiles replace 256 x 256 ones where half of a 256-wide column tile would be
@@ -62,15 +37,12 @@ inline GemmPlan plan_gemm(bool bf16, int M, int N, int K) {
   }
   const int nkt = cdiv(K, 64);
   const int t256 = cdiv(M, 256) * cdiv(N, 256);
-  const int ov = bf16_tile_override();
-  if (t256 >= 64 && ov != 3) {
+  if (t256 >= 64) {
     const bool narrow = N % 256 != 0 && N % 256 <= 128;
-    const int bo = kk_bn_override();
-    p.bn = bo != 0 ? bo : narrow ? 128 : 256;
+    p.bn = narrow ? 128 : 256;
     const int t = p.bn == 128 ? cdiv(M, 256) * cdiv(N, 128) : t256;
     int s = cdiv(256, t);
     s = std::min(s, std::max(1, nkt / 16));
-    p.tile = ov == 1 ? BfTile::k256x256 : ov == 2 ? BfTile::k256x256w8 : BfTile::kDma256;
     p.splits = std::max(1, std::min(s, 8));
     return p;
   }
@@ -94,7 +66,7 @@ inline void run_gemm(const GemmPlan& p, const AL& al, const BL& bl, const Epi& e
   if constexpr (AL::kBf16 && BL::kBf16) {
     if (p.bf16) {
       if constexpr (std::is_same_v<AL, KRows2<uint16_t>> && std::is_same_v<BL, KRows2<uint16_t>>) {
-        if (p.tile == BfTile::kDma256 && kk_engine_enabled() && kk_fits(al) && kk_fits(bl)) {
+        if (p.tile == BfTile::kDma256 && kk_fits(al) && kk_fits(bl)) {
           if (p.bn == 128)
             launch_gemm_kk<128>(al, bl, epi, M, N, K, p.splits, s);
           else

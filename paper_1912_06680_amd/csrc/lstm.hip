@@ -519,7 +519,7 @@ static int lstm_fwd_impl(int T, int B, int D, int H, const E* x, const E* Wx, co
         E* gt = gates ? gates + static_cast<size_t>(t) * B * 4 * H : nullptr;
         EpiLstmCell<E> epi{bias, cprev, rt, h + t * BH, c + t * BH, gt, H};
         ktimer_begin(kSiteLstmFwdGemm, s);
-        if (kk_engine_enabled() && kk_fits(al) && kk_fits(bl))
+        if (kk_fits(al) && kk_fits(bl))
           launch_gemm_kk(al, bl, epi, B, 4 * H, D + H, 1, s);
         else
           launch_gemm_bf16_dma(al, bl, epi, B, 4 * H, D + H, 1, s);

@@ -13,8 +13,7 @@ import os
 
 import torch
 
-# O5_LIB may name another build of the library (comparison runs)
-LIB_PATH = os.environ.get("O5_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libo5.so")
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libo5.so")
 
 O5_F32 = 0
 O5_BF16 = 1
