@@ -66,4 +66,15 @@ void unit_forward(o5_dtype dt, int N, int H, int nk, const o5_unit_head& u, cons
 void unit_grad(o5_dtype dt, int N, int H, int nk, const o5_unit_head& u, const void* h, char* ws, const UnitWs& w,
                uint16_t* dzhi, uint16_t* dzlo, int col0, int ld, hipStream_t s);
 
+// ------------------------------------------------ rollout sampling
+// The two halves of o5_policy_sample: argument validation (everything but
+// the workspace; fills hm and the scratch bytes needed) and the enqueueing
+// of its kernels with a scratch buffer of at least that size.
+int policy_sample_check(const char* fn, o5_dtype dt, int B, int H, int K, const int* head_sizes, const void* h,
+                        const void* Wp, const float* bp, const uint8_t* avail, const o5_unit_head* unit,
+                        const int32_t* act, const float* logp, const float* value, HeadsMeta* hm, size_t* need);
+int policy_sample_run(o5_dtype dt, int B, int H, const HeadsMeta& hm, const void* h, const void* Wp, const float* bp,
+                      const uint8_t* avail, const o5_unit_head* unit, uint64_t seed, uint64_t counter, int32_t* act,
+                      float* logp, float* value, char* ws, hipStream_t s);
+
 }  // namespace o5

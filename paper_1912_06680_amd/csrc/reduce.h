@@ -45,4 +45,47 @@ static __global__ void __launch_bounds__(256) colsum_tree(int P, int N, const fl
   if (threadIdx.x == 0) out[n] = red[0];
 }
 
+// ------------------------------------------------------ wave reductions
+
+// v combined with the value DPP control CTRL moves into each lane; lanes of
+// rows outside ROW_MASK take `id` instead.
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ float dpp(float id, float v) {
+  return __int_as_float(
+      __builtin_amdgcn_update_dpp(__float_as_int(id), __float_as_int(v), CTRL, ROW_MASK, 0xf, false));
+}
+
+// Wave-wide reduction on the VALU's data-parallel lane moves: two quad
+// swaps and two rotations within each row of 16 lanes leave every lane with
+// its row's total, two row broadcasts carry them to lane 63, whose value is
+// returned to every lane.  A fixed combination order, so the result is the
+// same from call to call.
+template <class Op>
+__device__ __forceinline__ float wave_reduce(float v, float id, Op op) {
+  v = op(v, dpp<0xB1>(id, v));        // quad_perm [1, 0, 3, 2]
+  v = op(v, dpp<0x4E>(id, v));        // quad_perm [2, 3, 0, 1]
+  v = op(v, dpp<0x124>(id, v));       // row_ror 4
+  v = op(v, dpp<0x128>(id, v));       // row_ror 8
+  v = op(v, dpp<0x142, 0xa>(id, v));  // row_bcast 15: rows 1 and 3 add rows 0 and 2
+  v = op(v, dpp<0x143, 0xc>(id, v));  // row_bcast 31: rows 2 and 3 add rows 0 + 1
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+__device__ __forceinline__ float wave_max(float v) {
+  return wave_reduce(v, -INFINITY, [](float a, float b) { return fmaxf(a, b); });
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  return wave_reduce(v, 0.0f, [](float a, float b) { return a + b; });
+}
+
+// Column c (the same in every lane) of the row, held by lane c % 64 as its
+// element c / 64.
+template <int CPL>
+__device__ __forceinline__ float column(const float (&z)[CPL], int c) {
+  float v = z[0];
+#pragma unroll
+  for (int i = 1; i < CPL; ++i)
+    if (c >> 6 == i) v = z[i];
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), c & 63));
+}
+
 }  // namespace o5
