@@ -395,6 +395,29 @@ int o5_policy_sample(o5_dtype dt, int B, int H, int K, const int* head_sizes,
                      void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * o5_policy_sample_static -- o5_policy_sample without a workspace, for the
+ * callers that cannot allocate: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation.  Arguments, outputs and errors
+ * are those of o5_policy_sample, and so are the results (the same kernels:
+ * bitwise the same outputs).  It allocates nothing: its scratch is a device
+ * array of O5_STATIC_SCRATCH_BYTES inside the library, one per GPU, held
+ * until the process ends; its address on a GPU is looked up on the first
+ * call there (with that GPU current) and kept.  A shape whose
+ * o5_policy_sample_workspace_bytes exceeds O5_STATIC_SCRATCH_BYTES is
+ * rejected with O5_E_SHAPE (with the paper's 75 logits at H = 4096 every
+ * batch of up to 16,128 rows fits).  Every call on one GPU shares that GPU's array, which
+ * keeps the last call's contents (no part of it needs to start at zero:
+ * each call writes all it reads), so calls that overlap on one GPU -- two
+ * streams, or two host threads -- race: serialise them.
+ * ------------------------------------------------------------------------ */
+#define O5_STATIC_SCRATCH_BYTES (16 << 20)
+int o5_policy_sample_static(o5_dtype dt, int B, int H, int K, const int* head_sizes,
+                            const void* h, const void* Wp, const float* bp,
+                            const uint8_t* avail, const o5_unit_head* unit,
+                            uint64_t seed, uint64_t counter,
+                            int32_t* act, float* logp, float* value, void* stream);
+
+/* ------------------------------------------------------------------------
  * Surgery on the flat parameter vector (appendix "Surgery"; subsection
  * "Continual Transfer via Surgery").  Layout of a vector for (D, H, A1):
  * Wx [4H, D], Wh [4H, H], b [4H], Wp [A1, H], bp [A1], fp32, gate blocks

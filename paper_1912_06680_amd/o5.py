@@ -28,7 +28,7 @@ EXPORTED = (
     "o5_prelstm_bwd_workspace_bytes", "o5_prelstm_bwd",
     "o5_ppo_loss_grad_workspace_bytes", "o5_ppo_loss_grad",
     "o5_adam_step",
-    "o5_policy_sample_workspace_bytes", "o5_policy_sample",
+    "o5_policy_sample_workspace_bytes", "o5_policy_sample", "o5_policy_sample_static",
     "o5_f32_to_bf16",
     "o5_param_count", "o5_surgery_widen", "o5_surgery_fold_input",
     "o5_ktimer_enable", "o5_ktimer_enable_sites", "o5_ktimer_read", "o5_ktimer_site_name",
@@ -102,6 +102,8 @@ _SIGS = {
     "o5_policy_sample_workspace_bytes": (_sz, [_i, _i, _i, _i, _vp, _vp]),
     "o5_policy_sample": (_i, [_i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _u64, _u64, _vp, _vp, _vp, _vp, _sz,
                               _vp]),
+    "o5_policy_sample_static": (_i, [_i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _u64, _u64, _vp, _vp, _vp,
+                                     _vp]),
     "o5_f32_to_bf16": (_i, [_sz, _vp, _vp, _vp]),
     "o5_param_count": (_sz, [_i, _i, _i]),
     "o5_surgery_widen": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _f, _u64, _vp]),
@@ -278,6 +280,13 @@ def o5_policy_sample(dt, B, H, head_sizes, h, Wp, bp, seed, counter, act, logp, 
     _check("o5_policy_sample", lib().o5_policy_sample(
         dt, B, H, len(head_sizes), _heads(head_sizes), _p(h), _p(Wp), _p(bp), _p(avail), _unit(unit), int(seed),
         int(counter), _p(act), _p(logp), _p(value), wp, wn, _stream(stream)))
+
+
+def o5_policy_sample_static(dt, B, H, head_sizes, h, Wp, bp, seed, counter, act, logp, value, stream=None,
+                            avail=None, unit=None):
+    _check("o5_policy_sample_static", lib().o5_policy_sample_static(
+        dt, B, H, len(head_sizes), _heads(head_sizes), _p(h), _p(Wp), _p(bp), _p(avail), _unit(unit), int(seed),
+        int(counter), _p(act), _p(logp), _p(value), _stream(stream)))
 
 
 def o5_param_count(D, H, A1):
