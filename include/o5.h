@@ -61,8 +61,11 @@ enum {
 
 /* Arithmetic type of the GEMM inputs (x, weights, hidden state).  Cell
  * state, gradients, optimizer state, advantages and losses are always fp32;
- * GEMMs always accumulate in fp32. */
-typedef enum { O5_F32 = 0, O5_BF16 = 1 } o5_dtype;
+ * GEMMs always accumulate in fp32.  Any other non-negative value is
+ * rejected with O5_E_DTYPE (the last enumerator only widens the type's
+ * range to every such value, so that a C caller's bad value is defined
+ * behaviour on the C++ side as well). */
+typedef enum { O5_F32 = 0, O5_BF16 = 1, O5_DTYPE_MAX_ENUM = 0x7fffffff } o5_dtype;
 
 /* O5_VERSION of the loaded library. */
 int o5_version(void);

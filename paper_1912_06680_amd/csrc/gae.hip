@@ -312,7 +312,7 @@ static constexpr int kGaeLaneV = 4;  // segments per lane of the large-S kernel
 extern "C" int o5_gae(int L, int S, const float* r, const float* v, const uint8_t* done, float gamma,
                       float lambda, float* adv, float* ret, void* stream) {
   O5_CHECK(L >= 1 && S >= 1, O5_E_SHAPE, "o5_gae: L=%d and S=%d must be >= 1", L, S);
-  O5_CHECK(static_cast<long long>(L + 1) * S < (1ll << 40), O5_E_SHAPE, "o5_gae: L*S too large");
+  O5_CHECK((static_cast<long long>(L) + 1) * S < (1ll << 40), O5_E_SHAPE, "o5_gae: L*S too large");
   O5_CHECK(gamma >= 0.0f && gamma <= 1.0f && lambda >= 0.0f && lambda <= 1.0f, O5_E_ARG,
            "o5_gae: gamma=%g and lambda=%g must lie in [0, 1]", gamma, lambda);
   O5_PTR(r, "r");

@@ -175,17 +175,25 @@ static RewardWs reward_ws(int L, int G) {
 
 using namespace o5;
 
+static int check_reward_shape(const char* fn, int L, int G) {
+  O5_CHECK(L >= 1 && G >= 1, O5_E_SHAPE, "%s: L=%d and G=%d must be >= 1", fn, L, G);
+  O5_CHECK(static_cast<long long>(L) * G < (1ll << 31) && static_cast<long long>(L) * G * kHeroes < (1ll << 31),
+           O5_E_SHAPE, "%s: L*G*10 must stay below 2^31", fn);
+  return O5_OK;
+}
+
 extern "C" size_t o5_reward_process_workspace_bytes(int L, int G) {
-  if (L < 1 || G < 1) return 0;
+  if (check_reward_shape("o5_reward_process_workspace_bytes", L, G) != O5_OK) return 0;
   return reward_ws(L, G).total;
 }
 
 extern "C" int o5_reward_process(int L, int G, const float* shaped, const float* outcome, const float* game_time,
                                  o5_reward_hp hp, double* stats, float* r, void* ws, size_t ws_bytes,
                                  void* stream) {
-  O5_CHECK(L >= 1 && G >= 1, O5_E_SHAPE, "o5_reward_process: L=%d and G=%d must be >= 1", L, G);
-  O5_CHECK(static_cast<long long>(L) * G * kHeroes < (1ll << 31), O5_E_SHAPE,
-           "o5_reward_process: L*G*10 must stay below 2^31");
+  {
+    const int st = check_reward_shape("o5_reward_process", L, G);
+    if (st != O5_OK) return st;
+  }
   O5_CHECK(hp.tau >= 0.0f && hp.tau <= 1.0f, O5_E_ARG, "o5_reward_process: tau=%g must lie in [0, 1]", hp.tau);
   O5_CHECK(hp.decay_base > 0.0f && hp.decay_base <= 1.0f && hp.decay_minutes > 0.0f && hp.eps > 0.0f, O5_E_ARG,
            "o5_reward_process: need 0 < decay_base <= 1, decay_minutes > 0 and eps > 0");

@@ -159,7 +159,10 @@ __global__ void __launch_bounds__(256) fold_bias(Shape5 o, Shape5 n, int Dk, con
 
 static int check_shape(const char* fn, int D, int H, int A1) {
   O5_CHECK(D >= 1 && H >= 1 && A1 >= 1, O5_E_SHAPE, "%s: D=%d H=%d A1=%d must be >= 1", fn, D, H, A1);
-  O5_CHECK(static_cast<long long>(4) * H * (D + H + 1) + static_cast<long long>(A1) * (H + 1) < (1ll << 40),
+  O5_CHECK(D <= (1 << 24) && H <= (1 << 24) && A1 <= (1 << 24), O5_E_SHAPE, "%s: D, H and A1 must be <= 2^24", fn);
+  O5_CHECK(static_cast<long long>(4) * H * (static_cast<long long>(D) + H + 1) +
+                   static_cast<long long>(A1) * (static_cast<long long>(H) + 1) <
+               (1ll << 40),
            O5_E_SHAPE, "%s: parameter vector too large", fn);
   return O5_OK;
 }
@@ -169,7 +172,7 @@ static int check_shape(const char* fn, int D, int H, int A1) {
 using namespace o5;
 
 extern "C" size_t o5_param_count(int D, int H, int A1) {
-  if (D < 1 || H < 1 || A1 < 1) return 0;
+  if (check_shape("o5_param_count", D, H, A1) != O5_OK) return 0;
   return shape5(D, H, A1).total;
 }
 
