@@ -48,13 +48,14 @@ constexpr int R256 = 256 / ROW_BYTES;  // rows per 256 bytes
 constexpr int NWAVES = 8;              // two per SIMD
 constexpr int NT = NWAVES * 64;
 
-// Block and wave tiling of a 256 x BN block tile.
+// Block and wave tiling of a 256 x BN block tile: 256 x 256 (2 x 4 waves of
+// 128 x 64) or 256 x 128 (4 x 2 waves of 64 x 64).
 template <int BN_>
 struct Shape {
   static_assert(BN_ == 256 || BN_ == 128, "BN is 256 or 128");
-  static_assert(NWAVES == 8 || NWAVES == 4, "8 or 4 waves");
+  static_assert(NWAVES == 8, "8 waves");
   static constexpr int BM = 256, BN = BN_;
-  static constexpr int WAVES_M = (NWAVES == 8 && BN == 128) ? 4 : 2;
+  static constexpr int WAVES_M = BN == 128 ? 4 : 2;
   static constexpr int WAVES_N = NWAVES / WAVES_M;
   static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   static constexpr int MB = WM / 32, NB = WN / 32;  // 32 x 32 MFMA blocks per wave
@@ -91,38 +92,49 @@ constexpr uint32_t kOutOfRange = 0xfffffff0u;  // a byte offset past every opera
 // and masked rows of the second source, get an offset past the buffer and so
 // read zeros.  Requires K0 and K multiples of BK (no tile straddles a source
 // boundary or the end) and sources below 2^31 bytes.
-template <typename E, int NC>
+template <typename E, int NC, bool TWO>
 struct Tile {
   rsrc_t rs0, rs1;
-  uint32_t voff0[NC], voff1[NC];
+  uint32_t voff0[NC], voff1[TWO ? NC : 1];  // (TWO: the operand has a second source)
   int K0, kmax;
 
   __device__ __forceinline__ void init(const KRows2<E>& l, int row0, int wave, int lane) {
     K0 = l.K0;
     kmax = l.K - BK;
     rs0 = make_rsrc(l.p0, static_cast<uint32_t>(static_cast<size_t>(l.rows) * l.ld0 * sizeof(E)));
-    rs1 = make_rsrc(l.p1 != nullptr ? l.p1 : l.p0,
-                    l.p1 != nullptr ? static_cast<uint32_t>(static_cast<size_t>(l.rows) * l.ld1 * sizeof(E)) : 0u);
+    if constexpr (TWO)
+      rs1 = make_rsrc(l.p1 != nullptr ? l.p1 : l.p0,
+                      l.p1 != nullptr ? static_cast<uint32_t>(static_cast<size_t>(l.rows) * l.ld1 * sizeof(E)) : 0u);
 #pragma unroll
     for (int q = 0; q < NC; ++q) {
       const int r = (wave * NC + q) * RPI + lane / CPR;  // tile row this lane fills
       const int row = l.gstride > 0 ? (r >> 6) * l.gstride + (row0 >> 2) + (r & 63) : row0 + r;
       const uint32_t koff = slot(r, lane % CPR) * 16;
       const bool valid = row < l.rows;
-      const bool masked = valid && l.mask1 != nullptr && l.mask1[row] != 0;
       voff0[q] = valid ? static_cast<uint32_t>(row) * l.ld0 * sizeof(E) + koff : kOutOfRange;
-      voff1[q] = (valid && !masked && l.p1 != nullptr) ? static_cast<uint32_t>(row) * l.ld1 * sizeof(E) + koff
-                                                        : kOutOfRange;
+      if constexpr (TWO) {
+        const bool masked = valid && l.mask1 != nullptr && l.mask1[row] != 0;
+        voff1[q] = (valid && !masked && l.p1 != nullptr) ? static_cast<uint32_t>(row) * l.ld1 * sizeof(E) + koff
+                                                          : kOutOfRange;
+      }
     }
   }
   // copy q of the tile starting at k0 into the stage at LDS address `stage`;
   // a tile past the end re-reads the last tile
   __device__ __forceinline__ void issue_one(int k0, uint32_t stage, int wave, int q) const {
     k0 = min(k0, kmax);
-    const bool seg0 = k0 < K0;
-    const uint32_t soff = static_cast<uint32_t>(seg0 ? k0 : k0 - K0) * sizeof(E);
-    const uint32_t voff = seg0 ? voff0[q] : voff1[q];
-    const rsrc_t rs = seg0 ? rs0 : rs1;
+    uint32_t soff, voff;
+    rsrc_t rs;
+    if constexpr (TWO) {
+      const bool seg0 = k0 < K0;
+      soff = static_cast<uint32_t>(seg0 ? k0 : k0 - K0) * sizeof(E);
+      voff = seg0 ? voff0[q] : voff1[q];
+      rs = seg0 ? rs0 : rs1;
+    } else {
+      soff = static_cast<uint32_t>(k0) * sizeof(E);
+      voff = voff0[q];
+      rs = rs0;
+    }
     const uint32_t lds = stage + (wave * NC + q) * 1024;
     // (s_nop: one wait state between the M0 write and the LDS DMA reading it)
     asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(voff), "s"(rs),
@@ -170,9 +182,10 @@ __device__ __forceinline__ void mfma_all(const Frags<MB, NB>& f, f32x16_t (&acc)
 // The same MFMAs with the wave's copies of one A and one B tile (k0, stages
 // as and bs) spread evenly among them (the order is pinned by scheduling
 // barriers).
-template <typename E, int MB, int NB, int NCA, int NCB>
-__device__ __forceinline__ void mfma_copies(const Frags<MB, NB>& f, f32x16_t (&acc)[MB][NB], const Tile<E, NCA>& ta,
-                                            const Tile<E, NCB>& tb, int k0, uint32_t as, uint32_t bs, int wave) {
+template <typename E, int MB, int NB, int NCA, int NCB, bool TWO>
+__device__ __forceinline__ void mfma_copies(const Frags<MB, NB>& f, f32x16_t (&acc)[MB][NB],
+                                            const Tile<E, NCA, TWO>& ta, const Tile<E, NCB, TWO>& tb, int k0,
+                                            uint32_t as, uint32_t bs, int wave) {
   constexpr int NQ = NCA + NCB;
   dma::unroll<0, MB * NB>([&](auto I) {
     constexpr int m = decltype(I)::value;
@@ -194,7 +207,7 @@ __device__ __forceinline__ void mfma_copies(const Frags<MB, NB>& f, f32x16_t (&a
 
 }  // namespace kk
 
-template <int BN, class Epi, typename E>
+template <int BN, bool TWO, class Epi, typename E>
 __global__ void __launch_bounds__(kk::NT, 1)
     gemm_kk(KRows2<E> al, KRows2<E> bl, Epi epi, int M, int N, int K, int ktiles_per_split) {
   using namespace kk;
@@ -227,8 +240,8 @@ __global__ void __launch_bounds__(kk::NT, 1)
       for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.0f;
 
   if (n > 0) {
-    Tile<E, S::NCA> ta;
-    Tile<E, S::NCB> tb;
+    Tile<E, S::NCA, TWO> ta;
+    Tile<E, S::NCB, TWO> tb;
     ta.init(al, m0, wave, lane);
     tb.init(bl, n0, wave, lane);
     // stage t % 2 of A at (t % 2) * TA, of B at 2 * TA + (t % 2) * TB
@@ -305,7 +318,13 @@ inline void launch_gemm_kk(const KRows2<E>& al, const KRows2<E>& bl, const Epi& 
   const int nkt = (K + kk::BK - 1) / kk::BK;
   const int kps = (nkt + splits - 1) / splits;
   const unsigned tiles = ((M + 255) / 256) * ((N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kk<BN, Epi, E>), dim3(tiles, 1, splits), dim3(kk::NT), 0, s, al, bl, epi, M, N, K, kps);
+  // operands with a second source (or a row mask) take the two-source copies
+  if (al.p1 != nullptr || bl.p1 != nullptr || al.mask1 != nullptr || bl.mask1 != nullptr)
+    hipLaunchKernelGGL((gemm_kk<BN, true, Epi, E>), dim3(tiles, 1, splits), dim3(kk::NT), 0, s, al, bl, epi, M, N, K,
+                       kps);
+  else
+    hipLaunchKernelGGL((gemm_kk<BN, false, Epi, E>), dim3(tiles, 1, splits), dim3(kk::NT), 0, s, al, bl, epi, M, N, K,
+                       kps);
 }
 
 // Operands the buffer-load copies can take: K and the source split K0 whole

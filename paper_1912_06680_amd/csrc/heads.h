@@ -34,16 +34,6 @@ static __global__ void __launch_bounds__(256) sum_hilo_splits(int S, int A1, int
   out[i] = v;
 }
 
-// dst [R, H] bf16 = src [A1, H] with rows A1..R-1 zero.
-static __global__ void __launch_bounds__(256) pad_rows_bf16(int A1, int R, int H, const uint16_t* __restrict__ src,
-                                                     uint16_t* __restrict__ dst) {
-  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  const size_t total = static_cast<size_t>(R) * H;
-  if (i >= total) return;
-  const int r = static_cast<int>(i / H);
-  dst[i] = r < A1 ? src[i] : static_cast<uint16_t>(0);
-}
-
 // ------------------------------------------------- unit-selection head
 // Head `unit->head` scored against per-row unit embeddings (o5_unit_head):
 // q = h Wq^T + bq, logits <q[n], E[n, u]>.  Scratch of the loss and the

@@ -484,7 +484,8 @@ static int check_dims(const char* fn, o5_dtype dt, int T, int B, int D, int H) {
   O5_CHECK(T >= 1 && B >= 1, O5_E_SHAPE, "%s: T=%d and B=%d must be >= 1", fn, T, B);
   O5_CHECK(D >= 64 && H >= 64 && D % 64 == 0 && H % 64 == 0 && D <= 65536 && H <= 65536, O5_E_SHAPE,
            "%s: D=%d and H=%d must be positive multiples of 64 (<= 65536)", fn, D, H);
-  O5_CHECK(static_cast<long long>(T) * B * 4 * H < (1ll << 31) && static_cast<long long>(T) * B * D < (1ll << 31),
+  O5_CHECK(static_cast<long long>(T) * B < (1ll << 31) && static_cast<long long>(T) * B * 4 * H < (1ll << 31) &&
+               static_cast<long long>(T) * B * D < (1ll << 31),
            O5_E_SHAPE, "%s: T*B*4H and T*B*D must stay below 2^31", fn);
   return O5_OK;
 }
@@ -635,7 +636,7 @@ static int lstm_bptt_impl(int T, int B, int D, int H, const E* x, const E* Wx, c
       ktimer_end(kSiteLstmDwGemm, s);
     }
   }
-  hipLaunchKernelGGL(colsum_rows, dim3(cdiv(4 * H, 256)), dim3(256), 0, s, w.nbc, 4 * H, dbpart, db);
+  hipLaunchKernelGGL(colsum_rows4, dim3(cdiv(4 * H, 64)), dim3(256), 0, s, w.nbc, 4 * H, dbpart, db);
   if (dx) {
     // dx = dG . W_x :  A(i=r, k=n) = dG[r, n];  B(j=d, k=n) = W_x[n, d]
     const int R = T * B;

@@ -37,24 +37,215 @@ constexpr int kRowsPerWave = 4;
 constexpr int kWavesPerBlock = 8;
 constexpr int kRowsPerBlock = kRowsPerWave * kWavesPerBlock;
 
-// One wave per row, kRowsPerWave consecutive rows per wave; lane l holds
-// logit columns l + 64 i (i < CPL).  zpart: [S][N][A1] partial logits (bias
-// not added).  avail [N][A] (or null = all available): an unavailable logit
-// is left out of its head's softmax and gets no gradient; a head with no
-// available logit adds nothing; an unavailable taken action has
-// log-probability -inf.  Head kext (or none, -1) takes its logits from zext
-// [N][n_kext] (the unit-selection head) and returns their gradient in dzext
-// instead of dz and its sums.  Writes dz [N][A1]; on the bf16 path the (hi, lo) pair in row
-// layout [N][ld_hilo] and, when dzT is set, transposed as [2 ld_hilo][ldT]
-// (hi rows, then lo rows; columns n >= N zero).  Each block writes one row
-// of part: the column sums of its dz (A1 values), then the sums of its rows'
-// surrogate, squared value error, entropy, clip indicator, approx-KL term,
-// ratio and non-finite indicator (kStatCols values); all sums in a fixed
-// order.
-// Read in place of an absent availability mask and unit-head logits.
+// Read in place of an absent availability mask, head mask and unit-head
+// logits.
 __device__ const uint8_t kAllAvailable = 1;
 __device__ const float kNoLogit = 0.0f;
 
+// The head of each logit column a lane holds (columns l + 64 i), -1 for the
+// value column and beyond.
+template <int CPL>
+__device__ __forceinline__ void column_heads(const HeadsMeta& hm, int lane, int (&head)[CPL]) {
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) {
+    const int a = lane + 64 * i;
+    head[i] = -1;
+    for (int k = 0; k < hm.K; ++k)
+      if (a >= hm.off[k] && a < hm.off[k + 1]) head[i] = k;
+  }
+}
+
+// The loss terms of one row and their gradient with respect to its logits,
+// computed by one wave.  Lane l holds columns a = l + 64 i: the logit z[i]
+// (bias added; the unit head's own logit for its columns), the availability
+// byte avb[i] as read, and the column's head.  Lane k < K holds head k's
+// action `actl` and mask byte `mkl`.  Writes d[i] = dL/dz for each column
+// held (0 where a logit does not count) and adds the row's surrogate,
+// squared value error, entropy, clip indicator, approx-KL term, ratio and
+// non-finite indicator to st.  An unavailable logit is left out of its
+// head's softmax and gets no gradient; a head with no available logit adds
+// nothing; an unavailable taken action has log-probability -inf.  All
+// reductions over the wave run in a fixed order.
+template <int CPL>
+__device__ __forceinline__ void ppo_row(const float (&z)[CPL], const uint32_t (&avb)[CPL], const int (&head)[CPL],
+                                        int lane, int actl, uint32_t mkl, float Ad, float R, float lpo,
+                                        const HeadsMeta& hm, float clip_eps, float vf_coef, float ent_coef,
+                                        float invN, float (&d)[CPL], float (&st)[kStatCols]) {
+  const int K = hm.K, A = hm.A;
+  bool av[CPL];
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) av[i] = lane + 64 * i >= A || avb[i] != 0;
+  float lse[kMaxHeads], zbar[kMaxHeads];
+  bool mk[kMaxHeads], some[kMaxHeads];
+  int ak[kMaxHeads];
+  float logpi = 0.0f, ent = 0.0f;
+  // per head: the maximum over its available logits; then one exponential
+  // per column; then the sums of e and e z per head
+  float mx[kMaxHeads];
+#pragma unroll
+  for (int k = 0; k < kMaxHeads; ++k) {
+    mx[k] = -INFINITY;
+    if (k < K) {
+      float m = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < CPL; ++i)
+        if (head[i] == k && av[i]) m = fmaxf(m, z[i]);
+      mx[k] = wave_max(m);
+    }
+  }
+  float e[CPL];
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) {
+    float m = 0.0f;
+#pragma unroll
+    for (int k = 0; k < kMaxHeads; ++k)
+      if (k < K && head[i] == k) m = mx[k];
+    e[i] = (head[i] >= 0 && av[i]) ? expf(z[i] - m) : 0.0f;
+  }
+  float inv_se[kMaxHeads];
+#pragma unroll
+  for (int k = 0; k < kMaxHeads; ++k) {
+    inv_se[k] = 0.0f;
+    some[k] = false;
+    mk[k] = false;
+    ak[k] = 0;
+    if (k < K) {
+      float se = 0.0f, sez = 0.0f;
+#pragma unroll
+      for (int i = 0; i < CPL; ++i)
+        if (head[i] == k) {
+          se += e[i];
+          sez += e[i] * z[i];
+        }
+      se = wave_sum(se);
+      sez = wave_sum(sez);
+      some[k] = se > 0.0f;  // the maximum contributes e = 1
+      lse[k] = some[k] ? mx[k] + logf(se) : 0.0f;
+      zbar[k] = some[k] ? sez / se : 0.0f;
+      inv_se[k] = some[k] ? 1.0f / se : 0.0f;
+      ak[k] = __builtin_amdgcn_readlane(actl, k);
+      mk[k] = __builtin_amdgcn_readlane(static_cast<int>(mkl), k) != 0;
+      const int nk = hm.off[k + 1] - hm.off[k];
+      const int a_sel = min(max(ak[k], 0), nk - 1);
+      const int c_sel = hm.off[k] + a_sel;
+      const float z_sel = column(z, c_sel);
+      uint32_t tb = avb[0];
+#pragma unroll
+      for (int i = 1; i < CPL; ++i)
+        if (c_sel >> 6 == i) tb = avb[i];
+      const bool taken = __builtin_amdgcn_readlane(static_cast<int>(tb), c_sel & 63) != 0;
+      if (mk[k] && some[k]) {
+        logpi += taken ? z_sel - lse[k] : -INFINITY;
+        ent += lse[k] - zbar[k];
+      }
+    }
+  }
+  const float dlog = logpi - lpo;
+  const float ratio = expf(dlog);
+  const float rc = fminf(fmaxf(ratio, 1.0f - clip_eps), 1.0f + clip_eps);
+  const float surr = fminf(ratio * Ad, rc * Ad);
+  const float V = column(z, A);
+  const float verr = V - R;
+  const bool flow = (Ad >= 0.0f && ratio <= 1.0f + clip_eps) || (Ad < 0.0f && ratio >= 1.0f - clip_eps);
+  const float g_logpi = flow ? -ratio * Ad * invN : 0.0f;
+  const float ent_scale = ent_coef * invN;
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) {
+    const int a = lane + 64 * i;
+    float di = 0.0f;
+    if (a == A) di = 2.0f * vf_coef * verr * invN;
+    // this column's head: its softmax normaliser, mean logit, taken action
+    bool use = false;
+    float is = 0.0f, zb = 0.0f;
+    int act_col = -1;
+#pragma unroll
+    for (int k = 0; k < kMaxHeads; ++k)
+      if (k < K && head[i] == k) {
+        use = mk[k] && some[k];
+        is = inv_se[k];
+        zb = zbar[k];
+        act_col = hm.off[k] + ak[k];
+      }
+    if (use && av[i]) {
+      const float p = e[i] * is;
+      const float onehot = a == act_col ? 1.0f : 0.0f;
+      di = g_logpi * (onehot - p) + ent_scale * p * (z[i] - zb);
+    }
+    d[i] = di;
+  }
+  const float row_loss = -surr + vf_coef * verr * verr - ent_coef * ent;
+  st[0] += surr;
+  st[1] += verr * verr;
+  st[2] += ent;
+  st[3] += fabsf(ratio - 1.0f) > clip_eps ? 1.0f : 0.0f;
+  st[4] += expm1f(dlog) - dlog;  // (r - 1) - log r without the cancellation in r - 1
+  st[5] += ratio;
+  st[6] += isfinite(row_loss) ? 0.0f : 1.0f;
+}
+
+// Where the gradient of row n (from ppo_row) goes: the unit head's columns
+// to dzext [N][nke] (and 0 in every other output), the rest to dz [N][A1]
+// (if set) and to the column sums csum; on the bf16 path the pair hi =
+// bf16(d), lo = bf16(d - hi) to dz_hi, dz_lo [N][ld_hilo] (if set).
+template <int CPL>
+__device__ __forceinline__ void ppo_row_store(float (&d)[CPL], const int (&head)[CPL], int lane, int n,
+                                              const HeadsMeta& hm, int kext, int nke, int A1, float* dzext, float* dz,
+                                              float (&csum)[CPL], uint16_t* dz_hi, uint16_t* dz_lo, int ncol_hilo,
+                                              int ld_hilo) {
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) {
+    const int a = lane + 64 * i;
+    if (head[i] >= 0 && head[i] == kext) {
+      dzext[static_cast<size_t>(n) * nke + (a - hm.off[kext])] = d[i];
+      d[i] = 0.0f;  // these logits do not depend on Wp, bp
+    }
+    if (dz != nullptr && a < A1) dz[static_cast<size_t>(n) * A1 + a] = d[i];
+    csum[i] += d[i];
+    if (dz_hi != nullptr && a < ncol_hilo) {
+      const uint16_t hb = f32_to_bf16_bits(d[i]);
+      const uint16_t lb = f32_to_bf16_bits(d[i] - bf16_bits_to_f32(hb));
+      dz_hi[static_cast<size_t>(n) * ld_hilo + a] = hb;
+      dz_lo[static_cast<size_t>(n) * ld_hilo + a] = lb;
+    }
+  }
+}
+
+// The block's column sums of dz and its row statistics, reduced over its
+// waves in a fixed order through red [waves][CPL 64 + kStatCols] in LDS,
+// then written as row `prow` of part: the A1 column sums, then the
+// kStatCols statistics.
+template <int CPL, int NW>
+__device__ __forceinline__ void block_partials(const float (&csum)[CPL], const float (&st)[kStatCols], float* red,
+                                               int wave, int lane, int A1, float* part, int prow) {
+  constexpr int RW = CPL * 64 + kStatCols;
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) red[wave * RW + 64 * i + lane] = csum[i];
+  if (lane < kStatCols) {
+    float v = 0.0f;
+#pragma unroll
+    for (int q = 0; q < kStatCols; ++q)
+      if (q == lane) v = st[q];
+    red[wave * RW + CPL * 64 + lane] = v;
+  }
+  __syncthreads();
+  const int W = A1 + kStatCols;
+  for (int t = threadIdx.x; t < W; t += blockDim.x) {
+    const int c = t < A1 ? t : CPL * 64 + (t - A1);
+    float v = 0.0f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) v += red[w * RW + c];
+    part[static_cast<size_t>(prow) * W + t] = v;
+  }
+}
+
+// One wave per row, kRowsPerWave consecutive rows per wave; lane l holds
+// logit columns l + 64 i (i < CPL).  zpart: [S][N][A1] partial logits (bias
+// not added).  avail [N][A] (or null = all available).  Head kext (or none,
+// -1) takes its logits from zext [N][n_kext] (the unit-selection head) and
+// returns their gradient in dzext instead of dz and its sums.  Writes dz
+// [N][A1] (if set); on the bf16 path the (hi, lo) pair in row layout
+// [N][ld_hilo].  Each block writes row blockIdx.x of part (see
+// block_partials).
 template <int CPL, int SMAX>
 __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
     int N, int A1, int S, const float* __restrict__ zpart, const float* __restrict__ bp,
@@ -62,25 +253,14 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
     const float* __restrict__ ret, const uint8_t* __restrict__ mask, const uint8_t* __restrict__ avail, HeadsMeta hm,
     const float* __restrict__ zext, float* __restrict__ dzext, int kext, float clip_eps, float vf_coef,
     float ent_coef, float invN, float* __restrict__ dz, float* __restrict__ part, uint16_t* __restrict__ dz_hi,
-    uint16_t* __restrict__ dz_lo, int ncol_hilo, int ld_hilo, uint16_t* __restrict__ dzT, int ldT) {
-  __shared__ float red[kWavesPerBlock][CPL * 64 + kStatCols];
+    uint16_t* __restrict__ dz_lo, int ncol_hilo, int ld_hilo) {
+  __shared__ float red[kWavesPerBlock * (CPL * 64 + kStatCols)];
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int K = hm.K, A = hm.A;
-  int head[CPL];  // head of each column held, -1 for the value column and beyond
-#pragma unroll
-  for (int i = 0; i < CPL; ++i) {
-    const int a = lane + 64 * i;
-    head[i] = -1;
-    for (int k = 0; k < K; ++k)
-      if (a >= hm.off[k] && a < hm.off[k + 1]) head[i] = k;
-  }
+  int head[CPL];
+  column_heads(hm, lane, head);
   float csum[CPL] = {};
   float st[kStatCols] = {};
-  // the transposed pair is kept in registers (16 rows x 2 bytes per column)
-  // only for up to 256 logit columns; beyond that dzT must be null
-  constexpr bool kT = CPL <= 4;
-  constexpr int TC = kT ? CPL : 1;
-  uint32_t thi[TC][kRowsPerWave / 2] = {}, tlo[TC][kRowsPerWave / 2] = {};
   const size_t sstride = static_cast<size_t>(N) * A1;
   const int n0 = (blockIdx.x * kWavesPerBlock + wave) * kRowsPerWave;
   // the logits and availability of the wave's rows, every request issued
@@ -130,138 +310,10 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
   for (int rr = 0; rr < kRowsPerWave; ++rr) {
     const int n = n0 + rr;
     if (n >= N) break;
-    float z[CPL];
-    bool av[CPL];
-#pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-      z[i] = zr[0][i];
-      av[i] = lane + 64 * i >= A || avr[0][i] != 0;
-    }
-    float lse[kMaxHeads], zbar[kMaxHeads];
-    bool mk[kMaxHeads], some[kMaxHeads];
-    int ak[kMaxHeads];
-    float logpi = 0.0f, ent = 0.0f;
-    // per head: the maximum over its available logits; then one exponential
-    // per column; then the sums of e and e z per head (all reductions over
-    // the wave in a fixed order)
-    float mx[kMaxHeads];
-#pragma unroll
-    for (int k = 0; k < kMaxHeads; ++k) {
-      mx[k] = -INFINITY;
-      if (k < K) {
-        float m = -INFINITY;
-#pragma unroll
-        for (int i = 0; i < CPL; ++i)
-          if (head[i] == k && av[i]) m = fmaxf(m, z[i]);
-        mx[k] = wave_max(m);
-      }
-    }
-    float e[CPL];
-#pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-      float m = 0.0f;
-#pragma unroll
-      for (int k = 0; k < kMaxHeads; ++k)
-        if (k < K && head[i] == k) m = mx[k];
-      e[i] = (head[i] >= 0 && av[i]) ? expf(z[i] - m) : 0.0f;
-    }
-    float inv_se[kMaxHeads];
-#pragma unroll
-    for (int k = 0; k < kMaxHeads; ++k) {
-      inv_se[k] = 0.0f;
-      if (k < K) {
-        float se = 0.0f, sez = 0.0f;
-#pragma unroll
-        for (int i = 0; i < CPL; ++i)
-          if (head[i] == k) {
-            se += e[i];
-            sez += e[i] * z[i];
-          }
-        se = wave_sum(se);
-        sez = wave_sum(sez);
-        some[k] = se > 0.0f;  // the maximum contributes e = 1
-        lse[k] = some[k] ? mx[k] + logf(se) : 0.0f;
-        zbar[k] = some[k] ? sez / se : 0.0f;
-        inv_se[k] = some[k] ? 1.0f / se : 0.0f;
-        ak[k] = __builtin_amdgcn_readlane(actr[0], k);
-        mk[k] = __builtin_amdgcn_readlane(static_cast<int>(mkr[0]), k) != 0;
-        const int nk = hm.off[k + 1] - hm.off[k];
-        const int a_sel = min(max(ak[k], 0), nk - 1);
-        const int c_sel = hm.off[k] + a_sel;
-        const float z_sel = column(z, c_sel);
-        uint32_t tb = avr[0][0];
-#pragma unroll
-        for (int i = 1; i < CPL; ++i)
-          if (c_sel >> 6 == i) tb = avr[0][i];
-        const bool taken = __builtin_amdgcn_readlane(static_cast<int>(tb), c_sel & 63) != 0;
-        if (mk[k] && some[k]) {
-          logpi += taken ? z_sel - lse[k] : -INFINITY;
-          ent += lse[k] - zbar[k];
-        }
-      }
-    }
-    const float Ad = advr[0], R = retr[0];
-    const float dlog = logpi - lpor[0];
-    const float ratio = expf(dlog);
-    const float rc = fminf(fmaxf(ratio, 1.0f - clip_eps), 1.0f + clip_eps);
-    const float surr = fminf(ratio * Ad, rc * Ad);
-    const float V = column(z, A);
-    const float verr = V - R;
-    const bool flow = (Ad >= 0.0f && ratio <= 1.0f + clip_eps) || (Ad < 0.0f && ratio >= 1.0f - clip_eps);
-    const float g_logpi = flow ? -ratio * Ad * invN : 0.0f;
-    const float ent_scale = ent_coef * invN;
-#pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-      const int a = lane + 64 * i;
-      float d = 0.0f;
-      if (a == A) d = 2.0f * vf_coef * verr * invN;
-      // this column's head: its softmax normaliser, mean logit, taken action
-      bool use = false;
-      float is = 0.0f, zb = 0.0f;
-      int act_col = -1;
-#pragma unroll
-      for (int k = 0; k < kMaxHeads; ++k)
-        if (k < K && head[i] == k) {
-          use = mk[k] && some[k];
-          is = inv_se[k];
-          zb = zbar[k];
-          act_col = hm.off[k] + ak[k];
-        }
-      if (use && av[i]) {
-        const float p = e[i] * is;
-        const float onehot = a == act_col ? 1.0f : 0.0f;
-        d = g_logpi * (onehot - p) + ent_scale * p * (z[i] - zb);
-      }
-      if (head[i] >= 0 && head[i] == kext) {
-        dzext[static_cast<size_t>(n) * nke + (a - hm.off[kext])] = d;
-        d = 0.0f;  // these logits do not depend on Wp, bp
-      }
-      if (a < A1) dz[static_cast<size_t>(n) * A1 + a] = d;
-      csum[i] += d;
-      if (dz_hi != nullptr && a < ncol_hilo) {
-        const uint16_t hb = f32_to_bf16_bits(d);
-        const uint16_t lb = f32_to_bf16_bits(d - bf16_bits_to_f32(hb));
-        dz_hi[static_cast<size_t>(n) * ld_hilo + a] = hb;
-        dz_lo[static_cast<size_t>(n) * ld_hilo + a] = lb;
-        if constexpr (kT) {
-          const int sh = (rr & 1) * 16;
-#pragma unroll
-          for (int q = 0; q < kRowsPerWave / 2; ++q)
-            if (q == rr >> 1) {
-              thi[i][q] |= static_cast<uint32_t>(hb) << sh;
-              tlo[i][q] |= static_cast<uint32_t>(lb) << sh;
-            }
-        }
-      }
-    }
-    const float row_loss = -surr + vf_coef * verr * verr - ent_coef * ent;
-    st[0] += surr;
-    st[1] += verr * verr;
-    st[2] += ent;
-    st[3] += fabsf(ratio - 1.0f) > clip_eps ? 1.0f : 0.0f;
-    st[4] += expm1f(dlog) - dlog;  // (r - 1) - log r without the cancellation in r - 1
-    st[5] += ratio;
-    st[6] += isfinite(row_loss) ? 0.0f : 1.0f;
+    float d[CPL];
+    ppo_row<CPL>(zr[0], avr[0], head, lane, actr[0], mkr[0], advr[0], retr[0], lpor[0], hm, clip_eps, vf_coef,
+                 ent_coef, invN, d, st);
+    ppo_row_store<CPL>(d, head, lane, n, hm, kext, nke, A1, dzext, dz, csum, dz_hi, dz_lo, ncol_hilo, ld_hilo);
     // the next row's inputs move to slot 0 (constant indices keep the
     // prefetched values in registers)
 #pragma unroll
@@ -278,36 +330,206 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
       lpor[q] = lpor[q + 1];
     }
   }
-  if (kT && dzT != nullptr) {
-    // kRowsPerWave consecutive rows of each column held: 8 bytes of a dz^T row
-    static_assert(kRowsPerWave == 4, "one 8-byte store per column and half");
-#pragma unroll
-    for (int i = 0; i < TC; ++i) {
-      const int a = lane + 64 * i;
-      if (a < ncol_hilo) {
-        *reinterpret_cast<uint2*>(dzT + static_cast<size_t>(a) * ldT + n0) = make_uint2(thi[i][0], thi[i][1]);
-        *reinterpret_cast<uint2*>(dzT + static_cast<size_t>(ncol_hilo + a) * ldT + n0) =
-            make_uint2(tlo[i][0], tlo[i][1]);
-      }
+  block_partials<CPL, kWavesPerBlock>(csum, st, red, wave, lane, A1, part, blockIdx.x);
+}
+
+// The row kernel with one thread per row, for up to MAXC logit columns: the
+// block's 64 rows of logits (the GEMM's partial sums plus bias, or the unit
+// head's own logits) and availability bytes are staged in LDS by all 256
+// threads with coalesced loads; the first wave then takes one row per lane
+// through the same definition as ppo_row, serially (max, exponentials and
+// sums per head, the joint ratio, clipped surrogate, value error and
+// entropy, then dL/dz per column, written back over the row's logits);
+// finally the block writes the gradient rows (dz, the (hi, lo) pair, the
+// unit head's columns) and its column sums with coalesced stores.  No cross-lane operation; every sum in a fixed order.
+// Writes row blockIdx.x of part (64 rows per partial).
+constexpr int kRtRows = 64;
+constexpr int kRtThreads = 256;
+
+template <int MAXC>
+__global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
+    int N, int A1, int S, const float* __restrict__ zpart, const float* __restrict__ bp,
+    const int32_t* __restrict__ act, const float* __restrict__ logp_old, const float* __restrict__ adv,
+    const float* __restrict__ ret, const uint8_t* __restrict__ mask, const uint8_t* __restrict__ avail, HeadsMeta hm,
+    const float* __restrict__ zext, float* __restrict__ dzext, int kext, float clip_eps, float vf_coef,
+    float ent_coef, float invN, float* __restrict__ dz, float* __restrict__ part, uint16_t* __restrict__ dz_hi,
+    uint16_t* __restrict__ dz_lo, int ncol_hilo, int ld_hilo) {
+  constexpr int ZP = MAXC + 1;  // floats per staged row (odd: a column read hits distinct banks)
+  __shared__ float zs[kRtRows][ZP];
+  __shared__ uint8_t avs[kRtRows][MAXC];
+  __shared__ float st_red[kStatCols][kRtRows];
+  const int t = threadIdx.x;
+  const int n0 = blockIdx.x * kRtRows;
+  const int rows = min(kRtRows, N - n0);
+  const int K = hm.K, A = hm.A;
+  const size_t sstride = static_cast<size_t>(N) * A1;
+  const int nke = kext >= 0 ? hm.off[kext + 1] - hm.off[kext] : 0;
+  const int e0 = kext >= 0 ? hm.off[kext] : 0;
+  // stage the rows: element e = (r, a) of the block's [rows x A1] slice
+  // (the block's rows are contiguous in every source)
+  {
+    const int ne = rows * A1;
+#pragma unroll 4
+    for (int e = t; e < ne; e += kRtThreads) {
+      const size_t g = static_cast<size_t>(n0) * A1 + e;
+      const int r = e / A1, a = e - r * A1;
+      float v = bp[a];
+      for (int s2 = 0; s2 < S; ++s2) v += zpart[s2 * sstride + g];
+      zs[r][a] = v;
+    }
+    for (int e = t; e < rows * nke; e += kRtThreads) {
+      const int r = e / nke, u = e - r * nke;
+      zs[r][e0 + u] = zext[static_cast<size_t>(n0) * nke + e];
+    }
+#pragma unroll 4
+    for (int e = t; e < rows * A; e += kRtThreads) {
+      const int r = e / A, a = e - r * A;
+      avs[r][a] = avail ? avail[static_cast<size_t>(n0) * A + e] : 1;
     }
   }
+  __syncthreads();
+  if (t < kRtRows) {
+    float st[kStatCols] = {};
+    if (t < rows) {
+      const int n = n0 + t;
+      float* z = zs[t];
+      const uint8_t* av = avs[t];
+      float mx[kMaxHeads], inv[kMaxHeads], zbar[kMaxHeads];
+      bool use[kMaxHeads];
+      int ak[kMaxHeads];
+      float logpi = 0.0f, ent = 0.0f;
 #pragma unroll
-  for (int i = 0; i < CPL; ++i) red[wave][64 * i + lane] = csum[i];
-  if (lane < kStatCols) {
-    float v = 0.0f;
+      for (int k = 0; k < kMaxHeads; ++k) {
+        mx[k] = 0.0f;
+        inv[k] = 0.0f;
+        zbar[k] = 0.0f;
+        use[k] = false;
+        ak[k] = 0;
+        if (k < K) {
+          const int o = hm.off[k], nk = hm.off[k + 1] - o;
+          float m = -INFINITY;
+          for (int a = 0; a < nk; ++a)
+            if (av[o + a]) m = fmaxf(m, z[o + a]);
+          float sum = 0.0f, sz = 0.0f;
+          for (int a = 0; a < nk; ++a)
+            if (av[o + a]) {
+              const float e = expf(z[o + a] - m);
+              sum += e;
+              sz += e * z[o + a];
+            }
+          const bool some = sum > 0.0f;  // the maximum contributes e = 1
+          const bool mk = mask == nullptr || mask[static_cast<size_t>(n) * K + k] != 0;
+          const float lse = some ? m + logf(sum) : 0.0f;
+          mx[k] = m;
+          inv[k] = some ? 1.0f / sum : 0.0f;
+          zbar[k] = some ? sz / sum : 0.0f;
+          use[k] = mk && some;
+          ak[k] = act[static_cast<size_t>(n) * K + k];
+          if (use[k]) {
+            const int a_sel = min(max(ak[k], 0), nk - 1);
+            logpi += av[o + a_sel] ? z[o + a_sel] - lse : -INFINITY;
+            ent += lse - zbar[k];
+          }
+        }
+      }
+      const float Ad = adv[n], R = ret[n];
+      const float dlog = logpi - logp_old[n];
+      const float ratio = expf(dlog);
+      const float rc = fminf(fmaxf(ratio, 1.0f - clip_eps), 1.0f + clip_eps);
+      const float surr = fminf(ratio * Ad, rc * Ad);
+      const float verr = z[A] - R;
+      const bool flow = (Ad >= 0.0f && ratio <= 1.0f + clip_eps) || (Ad < 0.0f && ratio >= 1.0f - clip_eps);
+      const float g_logpi = flow ? -ratio * Ad * invN : 0.0f;
+      const float ent_scale = ent_coef * invN;
 #pragma unroll
-    for (int q = 0; q < kStatCols; ++q)
-      if (q == lane) v = st[q];
-    red[wave][CPL * 64 + lane] = v;
+      for (int k = 0; k < kMaxHeads; ++k) {
+        if (k < K) {
+          const int o = hm.off[k], nk = hm.off[k + 1] - o;
+          for (int a = 0; a < nk; ++a) {
+            float d = 0.0f;
+            if (use[k] && av[o + a]) {
+              const float p = expf(z[o + a] - mx[k]) * inv[k];
+              const float onehot = a == ak[k] ? 1.0f : 0.0f;
+              d = g_logpi * (onehot - p) + ent_scale * p * (z[o + a] - zbar[k]);
+            }
+            z[o + a] = d;
+          }
+        }
+      }
+      z[A] = 2.0f * vf_coef * verr * invN;
+      for (int a = A1; a < MAXC; ++a) z[a] = 0.0f;
+      const float row_loss = -surr + vf_coef * verr * verr - ent_coef * ent;
+      st[0] = surr;
+      st[1] = verr * verr;
+      st[2] = ent;
+      st[3] = fabsf(ratio - 1.0f) > clip_eps ? 1.0f : 0.0f;
+      st[4] = expm1f(dlog) - dlog;  // (r - 1) - log r without the cancellation in r - 1
+      st[5] = ratio;
+      st[6] = isfinite(row_loss) ? 0.0f : 1.0f;
+    } else {
+      for (int a = 0; a < MAXC; ++a) zs[t][a] = 0.0f;  // rows past N: defined, never stored
+    }
+#pragma unroll
+    for (int q = 0; q < kStatCols; ++q) st_red[q][t] = st[q];
   }
   __syncthreads();
+  // the unit head's gradient leaves; its columns are 0 in every other output
+  if (nke > 0) {
+    for (int e = t; e < rows * nke; e += kRtThreads) {
+      const int r = e / nke, u = e - r * nke;
+      dzext[static_cast<size_t>(n0) * nke + e] = zs[r][e0 + u];
+    }
+    __syncthreads();
+    for (int e = t; e < kRtRows * nke; e += kRtThreads) zs[e / nke][e0 + e % nke] = 0.0f;
+    __syncthreads();
+  }
+  if (dz != nullptr)
+    for (int e = t; e < rows * A1; e += kRtThreads) dz[static_cast<size_t>(n0) * A1 + e] = zs[e / A1][e % A1];
+  if (dz_hi != nullptr) {
+    for (int e = t; e < rows * ncol_hilo; e += kRtThreads) {
+      const int r = e / ncol_hilo, a = e - r * ncol_hilo;
+      const float d = zs[r][a];
+      const uint16_t hb = f32_to_bf16_bits(d);
+      dz_hi[static_cast<size_t>(n0 + r) * ld_hilo + a] = hb;
+      dz_lo[static_cast<size_t>(n0 + r) * ld_hilo + a] = f32_to_bf16_bits(d - bf16_bits_to_f32(hb));
+    }
+  }
+  // column sums over the block's rows, then its statistics, in row order
   const int W = A1 + kStatCols;
-  for (int t = threadIdx.x; t < W; t += blockDim.x) {
-    const int c = t < A1 ? t : CPL * 64 + (t - A1);
+  for (int c = t; c < W; c += kRtThreads) {
     float v = 0.0f;
-#pragma unroll
-    for (int w = 0; w < kWavesPerBlock; ++w) v += red[w][c];
-    part[static_cast<size_t>(blockIdx.x) * W + t] = v;
+    if (c < A1)
+      for (int r = 0; r < rows; ++r) v += zs[r][c];
+    else
+      for (int r = 0; r < rows; ++r) v += st_red[c - A1][r];
+    part[static_cast<size_t>(blockIdx.x) * W + c] = v;
+  }
+}
+
+// The weights of the dh product, transposed and repeated for the (hi, lo)
+// pair: row j of wT [H][2 ldh] is [w(0..ldh) | w(0..ldh)] with w(k) = Wp[k][j]
+// for k < A1, Wq[k - A1p][j] for A1p <= k < A1p + d (the unit head's query
+// weights, if any) and 0 elsewhere.  One 64 x 64 tile per block through LDS.
+__global__ void __launch_bounds__(256) pair_weights_t(int A1, int A1p, int ldh, int H, const uint16_t* __restrict__ Wp,
+                                                      const uint16_t* __restrict__ Wq, int d,
+                                                      uint16_t* __restrict__ wT) {
+  __shared__ uint16_t t[64][66];
+  const int j0 = blockIdx.x * 64, k0 = blockIdx.y * 64;
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int kk = e >> 6, jj = e & 63, k = k0 + kk, j = j0 + jj;
+    uint16_t v = 0;
+    if (k < A1)
+      v = Wp[static_cast<size_t>(k) * H + j];
+    else if (Wq != nullptr && k >= A1p && k < A1p + d)
+      v = Wq[static_cast<size_t>(k - A1p) * H + j];
+    t[kk][jj] = v;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int jj = e >> 6, kk = e & 63;
+    const size_t row = static_cast<size_t>(j0 + jj) * 2 * ldh;
+    wT[row + k0 + kk] = t[kk][jj];
+    wT[row + ldh + k0 + kk] = t[kk][jj];
   }
 }
 
@@ -330,11 +552,13 @@ __global__ void ppo_finalize(int A1, const float* __restrict__ sums, float invN,
 }
 
 struct PpoWs {
-  size_t zpart, dz, part, sums, wpart, dzhi, dzlo, dzT, wpad, unit, total;
+  size_t zpart, dz, part, sums, wpart, dzp, wT, unit, total;
   UnitWs uw;  // the unit-selection head's scratch, at offset unit (if any)
   GemmPlan plan_z, plan_w, plan_h;
-  int nblk, A1, A1p, ldh, ldT, wsplits;  // ldh: row length of the (hi, lo) pair, A1p + the unit head's dp
-  bool dwp_t;  // dWp from the transposed (hi; lo) pair, h read once
+  int nblk, A1, A1p, ldh, wsplits;  // ldh: row length of the (hi, lo) pair, A1p + the unit head's dp
+  bool dwp_t;  // dWp as one product of the (hi, lo) pair with h (h read once)
+  bool rows_t;  // the row kernel with one thread per row (ppo_rows_t)
+  int nblk_t;   // its blocks (= partial rows)
 };
 
 static PpoWs ppo_ws(o5_dtype dt, int N, int H, int A1, int unit_nk = 0, int unit_d = 0) {
@@ -344,17 +568,19 @@ static PpoWs ppo_ws(o5_dtype dt, int N, int H, int A1, int unit_nk = 0, int unit
   w.A1p = cdiv(A1, 64) * 64;  // padded logit count: a multiple of the K tile
   w.ldh = w.A1p + (unit_d > 0 ? cdiv(unit_d, 64) * 64 : 0);
   w.nblk = cdiv(N, kRowsPerBlock);
-  w.ldT = w.nblk * kRowsPerBlock;
-  w.dwp_t = bf && w.A1p <= 256;
+  // (the thread-per-row kernel stages every column of the pair: ldh <= 256)
+  w.rows_t = w.ldh <= 256;
+  w.nblk_t = cdiv(N, kRtRows);
+  w.dwp_t = bf && w.ldh <= 256;
   w.plan_z = plan_gemm(bf, N, A1, H);
   w.plan_w = bf ? plan_gemm(true, A1, H, 2 * N) : plan_gemm(false, A1, H, N);
-  w.plan_h = bf ? plan_gemm(true, N, H, 2 * w.ldh) : GemmPlan{false, BfTile::k128x128, 1, 256};
+  w.plan_h = plan_gemm(bf, N, H, 2 * w.ldh);
   w.plan_h.splits = 1;
   w.wsplits = 1;
   if (w.dwp_t) {
-    // M = 2 A1p (one or two 256-row tiles), N = H, K = N: split K so the
+    // M = 2 ldh (one or two 256-row tiles), N = H, K = N: split K so the
     // grid has about 256 blocks, each with at least 8 K tiles of 32
-    const int tiles = cdiv(2 * w.A1p, 256) * cdiv(H, 256);
+    const int tiles = cdiv(2 * w.ldh, 256) * cdiv(H, 256);
     w.wsplits = std::max(1, std::min(cdiv(256, tiles), cdiv(N, 32) / 8));
   }
   size_t o = 0;
@@ -367,20 +593,16 @@ static PpoWs ppo_ws(o5_dtype dt, int N, int H, int A1, int unit_nk = 0, int unit
   w.sums = o;
   o += align_up(static_cast<size_t>(A1 + kStatCols) * 4);
   w.wpart = o;
-  o += align_up(w.dwp_t ? static_cast<size_t>(w.wsplits) * 2 * w.A1p * H * 4
+  o += align_up(w.dwp_t ? static_cast<size_t>(w.wsplits) * 2 * w.ldh * H * 4
                         : static_cast<size_t>(w.plan_w.splits) * A1 * H * 4);
-  w.dzhi = w.dzlo = w.dzT = w.wpad = 0;
+  w.dzp = w.wT = 0;
   if (bf) {
-    w.dzhi = o;
-    o += align_up(static_cast<size_t>(N) * w.ldh * 2);
-    w.dzlo = o;
-    o += align_up(static_cast<size_t>(N) * w.ldh * 2);
-    w.wpad = o;
-    o += align_up(static_cast<size_t>(w.ldh) * H * 2);
-    if (w.dwp_t) {
-      w.dzT = o;
-      o += align_up(static_cast<size_t>(2) * w.A1p * w.ldT * 2);
-    }
+    // the (hi, lo) pair, row n = [hi (ldh) | lo (ldh)], and the weights
+    // transposed and repeated for it, row j = [W[., j] | W[., j]]
+    w.dzp = o;
+    o += align_up(static_cast<size_t>(N) * 2 * w.ldh * 2);
+    w.wT = o;
+    o += align_up(static_cast<size_t>(H) * 2 * w.ldh * 2);
   }
   w.unit = o;
   if (unit_d > 0) {
@@ -415,10 +637,10 @@ static void launch_rows_s(const PpoWs& w, int N, int A1, int S, const float* zpa
                           const int32_t* act, const float* logp_old, const float* adv, const float* ret, const uint8_t* mask,
                         const uint8_t* avail, const HeadsMeta& hm, const float* zext, float* dzext, int kext,
                         o5_ppo_hp hp, float invN, float* dz, float* part, uint16_t* dzhi, uint16_t* dzlo,
-                        uint16_t* dzT, hipStream_t s) {
+                        hipStream_t s) {
   hipLaunchKernelGGL((ppo_rows<CPL, SMAX>), dim3(w.nblk), dim3(kWavesPerBlock * 64), 0, s, N, A1, S, zpart, bp, act,
                      logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp.clip_eps, hp.vf_coef, hp.ent_coef, invN,
-                     dz, part, dzhi, dzlo, w.A1p, w.ldh, dzT, w.ldT);
+                     dz, part, dzhi, dzlo, w.A1p, 2 * w.ldh);
 }
 
 // The row kernel unrolls its reads of the logits GEMM's split partials up
@@ -428,13 +650,13 @@ static void launch_rows(const PpoWs& w, int N, int A1, int S, const float* zpart
                         const float* logp_old, const float* adv, const float* ret, const uint8_t* mask,
                         const uint8_t* avail, const HeadsMeta& hm, const float* zext, float* dzext, int kext,
                         o5_ppo_hp hp, float invN, float* dz, float* part, uint16_t* dzhi, uint16_t* dzlo,
-                        uint16_t* dzT, hipStream_t s) {
+                        hipStream_t s) {
   if (S <= 2)
     launch_rows_s<CPL, 2>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp,
-                          invN, dz, part, dzhi, dzlo, dzT, s);
+                          invN, dz, part, dzhi, dzlo, s);
   else
     launch_rows_s<CPL, 16>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp,
-                           invN, dz, part, dzhi, dzlo, dzT, s);
+                           invN, dz, part, dzhi, dzlo, s);
 }
 
 template <typename E>
@@ -449,19 +671,12 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
   float* sums = reinterpret_cast<float*>(ws + w.sums);
   float* wpart = reinterpret_cast<float*>(ws + w.wpart);
   const float invN = 1.0f / static_cast<float>(N);
-  {  // z = h Wp^T
-    KRows2<E> al{h, nullptr, nullptr, H, 0, H, H, N};
-    KRows2<E> bl{Wp, nullptr, nullptr, H, 0, H, H, A1};
-    EpiLogits epi{{zpart, A1, static_cast<size_t>(N) * A1}};
-    run_gemm(w.plan_z, al, bl, epi, N, A1, H, s);
-  }
   uint16_t* dzhi = nullptr;
   uint16_t* dzlo = nullptr;
-  uint16_t* dzT = nullptr;
   if constexpr (sizeof(E) == 2) {
-    dzhi = reinterpret_cast<uint16_t*>(ws + w.dzhi);
-    dzlo = reinterpret_cast<uint16_t*>(ws + w.dzlo);
-    if (w.dwp_t) dzT = reinterpret_cast<uint16_t*>(ws + w.dzT);
+    dzhi = reinterpret_cast<uint16_t*>(ws + w.dzp);
+    dzlo = dzhi + w.ldh;
+    dz = nullptr;  // the bf16 products read the (hi, lo) pair only
   }
   const float* zext = nullptr;
   float* dzext = nullptr;
@@ -474,52 +689,68 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
     zext = reinterpret_cast<const float*>(uws + w.uw.zext);
     dzext = reinterpret_cast<float*>(uws + w.uw.dzext);
   }
+  {  // z = h Wp^T
+    KRows2<E> hl{h, nullptr, nullptr, H, 0, H, H, N};
+    KRows2<E> wl{Wp, nullptr, nullptr, H, 0, H, H, A1};
+    EpiLogits epi{{zpart, A1, static_cast<size_t>(N) * A1}};
+    run_gemm(w.plan_z, hl, wl, epi, N, A1, H, s);
+  }
   const int S = w.plan_z.splits;
   const int cpl = cdiv(A1, 64);
-  if (cpl <= 1)
-    launch_rows<1>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz, part,
-                   dzhi, dzlo, dzT, s);
+  if (w.rows_t && w.A1p <= 128)
+    hipLaunchKernelGGL(ppo_rows_t<128>, dim3(w.nblk_t), dim3(kRtThreads), 0, s, N, A1, S, zpart, bp, act, logp_old,
+                       adv, ret, mask, avail, hm, zext, dzext, kext, hp.clip_eps, hp.vf_coef, hp.ent_coef, invN, dz,
+                       part, dzhi, dzlo, w.A1p, 2 * w.ldh);
+  else if (w.rows_t)
+    hipLaunchKernelGGL(ppo_rows_t<256>, dim3(w.nblk_t), dim3(kRtThreads), 0, s, N, A1, S, zpart, bp, act, logp_old,
+                       adv, ret, mask, avail, hm, zext, dzext, kext, hp.clip_eps, hp.vf_coef, hp.ent_coef, invN, dz,
+                       part, dzhi, dzlo, w.A1p, 2 * w.ldh);
+  else if (cpl <= 1)
+    launch_rows<1>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz,
+                   part, dzhi, dzlo, s);
   else if (cpl <= 2)
-    launch_rows<2>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz, part,
-                   dzhi, dzlo, dzT, s);
+    launch_rows<2>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz,
+                   part, dzhi, dzlo, s);
   else if (cpl <= 4)
-    launch_rows<4>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz, part,
-                   dzhi, dzlo, dzT, s);
+    launch_rows<4>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz,
+                   part, dzhi, dzlo, s);
   else if (cpl <= 8)
-    launch_rows<8>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz, part,
-                   dzhi, dzlo, dzT, s);
+    launch_rows<8>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz,
+                   part, dzhi, dzlo, s);
   else
-    launch_rows<16>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz, part,
-                   dzhi, dzlo, dzT, s);
+    launch_rows<16>(w, N, A1, S, zpart, bp, act, logp_old, adv, ret, mask, avail, hm, zext, dzext, kext, hp, invN, dz,
+                    part, dzhi, dzlo, s);
   if constexpr (sizeof(E) == 2) {
     const int A1p = w.A1p, ldh = w.ldh;
-    uint16_t* wpad = reinterpret_cast<uint16_t*>(ws + w.wpad);
-    hipLaunchKernelGGL(pad_rows_bf16, dim3(cdiv(static_cast<long long>(A1p) * H, 256)), dim3(256), 0, s, A1, A1p, H,
-                       Wp, wpad);
+    uint16_t* wT = reinterpret_cast<uint16_t*>(ws + w.wT);
+    const uint16_t* Wq = nullptr;
+    int d = 0;
     if (unit != nullptr) {
-      // dq (hi, lo) into columns A1p .. ldh - 1 of the pair, Wq into the same rows of wpad
-      unit_grad(dt, N, H, w.uw.nk, *unit, h, uws, w.uw, dzhi, dzlo, A1p, ldh, s);
-      const int d = unit->d, dp = ldh - A1p;
-      hipLaunchKernelGGL(pad_rows_bf16, dim3(cdiv(static_cast<long long>(dp) * H, 256)), dim3(256), 0, s, d, dp, H,
-                         static_cast<const uint16_t*>(unit->Wq), wpad + static_cast<size_t>(A1p) * H);
+      // dq (hi, lo) into columns A1p .. ldh - 1 of the pair, Wq into the same columns of wT
+      unit_grad(dt, N, H, w.uw.nk, *unit, h, uws, w.uw, dzhi, dzlo, A1p, 2 * ldh, s);
+      Wq = static_cast<const uint16_t*>(unit->Wq);
+      d = unit->d;
     }
-    {  // dh = [dz_hi dq_hi | dz_lo dq_lo] . [Wp Wq ; Wp Wq]  (K = 2 ldh)
-      KRows2<uint16_t> al{dzhi, dzlo, nullptr, ldh, ldh, ldh, 2 * ldh, N};
-      ICols2<uint16_t> bl{wpad, wpad, wpad, nullptr, H, H, 0, H, 2 * ldh, ldh};
+    hipLaunchKernelGGL(pair_weights_t, dim3(H / 64, ldh / 64), dim3(256), 0, s, A1, A1p, ldh, H, Wp, Wq, d, wT);
+    {  // dh = [dz_hi dq_hi | dz_lo dq_lo] . [Wp Wq ; Wp Wq]  (K = 2 ldh), both operands K-contiguous
+      KRows2<uint16_t> al{dzhi, nullptr, nullptr, 2 * ldh, 0, 2 * ldh, 2 * ldh, N};
+      KRows2<uint16_t> bl{wT, nullptr, nullptr, 2 * ldh, 0, 2 * ldh, 2 * ldh, H};
       EpiStoreF32 epi{dh, H, 0};
       run_gemm(w.plan_h, al, bl, epi, N, H, 2 * ldh, s);
     }
     if (w.dwp_t) {
-      // [dWp_hi ; dWp_lo] = [hi ; lo]^T-rows . h  (M = 2 A1p, N = H, K = N), split over K
-      KRows2<uint16_t> al{dzT, nullptr, nullptr, w.ldT, 0, N, N, 2 * A1p};
+      // [dWp_hi ; dWp_lo] = pair^T . h  (M = 2 ldh rows: hi columns, then lo
+      // columns; N = H, K = N), both operands read I-contiguous (the row
+      // layouts of the pair and of h), split over K; then hi + lo per split
+      ICols2<uint16_t> al{dzhi, nullptr, nullptr, nullptr, 2 * ldh, 0, 2 * ldh, 2 * ldh, N, 0};
       ICols2<uint16_t> bl{h, nullptr, nullptr, nullptr, H, 0, H, H, N, 0};
-      EpiStoreF32 epi{wpart, H, static_cast<size_t>(2) * A1p * H};
-      launch_gemm_bf16_dma(al, bl, epi, 2 * A1p, H, N, w.wsplits, s);
+      EpiStoreF32 epi{wpart, H, static_cast<size_t>(2) * ldh * H};
+      launch_gemm_bf16_dma(al, bl, epi, 2 * ldh, H, N, w.wsplits, s);
       hipLaunchKernelGGL(sum_hilo_splits, dim3(cdiv(static_cast<long long>(A1) * H, 256)), dim3(256), 0, s,
-                         w.wsplits, A1, A1p, H, wpart, dWp);
+                         w.wsplits, A1, ldh, H, wpart, dWp);
     } else {
       // dWp = [dz_hi ; dz_lo]^T . [h ; h]  (K = 2N), split over K, fixed-order sum
-      ICols2<uint16_t> al{dzhi, dzhi, dzlo, nullptr, A1p, A1p, 0, A1p, 2 * N, N};
+      ICols2<uint16_t> al{dzhi, dzhi, dzlo, nullptr, 2 * ldh, 2 * ldh, 0, A1p, 2 * N, N};
       ICols2<uint16_t> bl{h, h, h, nullptr, H, H, 0, H, 2 * N, N};
       EpiStoreF32 epi{wpart, H, static_cast<size_t>(A1) * H};
       run_gemm(w.plan_w, al, bl, epi, A1, H, 2 * N, s);
@@ -550,7 +781,8 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
     hipLaunchKernelGGL(colsum_rows, dim3(cdiv(static_cast<long long>(A1) * H, 256)), dim3(256), 0, s, w.plan_w.splits,
                        A1 * H, wpart, dWp);
   }
-  hipLaunchKernelGGL(colsum_tree, dim3(A1 + kStatCols), dim3(256), 0, s, w.nblk, A1 + kStatCols, part, sums);
+  hipLaunchKernelGGL(colsum_tree, dim3(A1 + kStatCols), dim3(256), 0, s, w.rows_t ? w.nblk_t : w.nblk,
+                     A1 + kStatCols, part, sums);
   hipLaunchKernelGGL(ppo_finalize, dim3(1), dim3(256), 0, s, A1, sums, invN, hp.vf_coef, hp.ent_coef, stats, dbp);
   return check_launch("o5_ppo_loss_grad");
 }

@@ -247,7 +247,7 @@ static void prelstm_bwd_impl(int N, int Do, int D, const E* o, const float* y, c
   const int groups = N / kReplicas;
   hipLaunchKernelGGL(pool_bwd<E>, dim3(cdiv(D, 256), w.nby), dim3(256), 0, s, groups, D, D / 4, kPoolGroupsPerBlock, y,
                      dx, dpre, dbpart);
-  hipLaunchKernelGGL(colsum_rows, dim3(cdiv(D, 256)), dim3(256), 0, s, w.nby, D, dbpart, db);
+  hipLaunchKernelGGL(colsum_rows4, dim3(cdiv(D, 64)), dim3(256), 0, s, w.nby, D, dbpart, db);
   // dW[d, k] = sum_n dpre[n, d] o[n, k]: both operands I-contiguous
   GemmPlan plan = plan_gemm(sizeof(E) == 2, D, Do, N);
   plan.splits = 1;
@@ -262,8 +262,8 @@ static int check_prelstm(const char* fn, o5_dtype dt, int T, int B, int Do, int 
            "%s: need T >= 1 and B a positive multiple of 5 (T=%d B=%d)", fn, T, B);
   O5_CHECK(Do >= 64 && Do % 64 == 0 && D >= 64 && D % 64 == 0, O5_E_SHAPE,
            "%s: Do=%d and D=%d must be positive multiples of 64", fn, Do, D);
-  O5_CHECK(static_cast<long long>(T) * B * (Do > D ? Do : D) < (1ll << 31), O5_E_SHAPE, "%s: T*B*max(Do, D) too large",
-           fn);
+  O5_CHECK(static_cast<long long>(T) * B < (1ll << 31) && static_cast<long long>(T) * B * (Do > D ? Do : D) < (1ll << 31),
+           O5_E_SHAPE, "%s: T*B*max(Do, D) too large", fn);
   O5_CHECK(T * B / kReplicas <= 65535, O5_E_SHAPE, "%s: T*B/5 must be <= 65535", fn);
   return O5_OK;
 }
@@ -272,17 +272,25 @@ static int check_prelstm(const char* fn, o5_dtype dt, int T, int B, int Do, int 
 
 using namespace o5;
 
+static int check_obs_shape(const char* fn, int N, int Do) {
+  O5_CHECK(N >= 1 && Do >= 4 && Do % 4 == 0, O5_E_SHAPE, "%s: need N >= 1 and Do a positive multiple of 4", fn);
+  O5_CHECK(static_cast<long long>(N) * Do < (1ll << 40) && cdiv(N, kObsRowsPerChunk) <= 65535, O5_E_SHAPE,
+           "%s: N*Do too large", fn);
+  return O5_OK;
+}
+
 extern "C" size_t o5_obs_normalize_workspace_bytes(int N, int Do) {
-  if (N < 1 || Do < 1) return 0;
+  if (check_obs_shape("o5_obs_normalize_workspace_bytes", N, Do) != O5_OK) return 0;
   return obs_ws(N, Do).total;
 }
 
 extern "C" int o5_obs_normalize(o5_dtype dt, int N, int Do, const float* obs, double* stats, float clip, float eps,
                                 void* o, void* ws, size_t ws_bytes, void* stream) {
   O5_CHECK(dt == O5_F32 || dt == O5_BF16, O5_E_DTYPE, "o5_obs_normalize: unknown dtype %d", static_cast<int>(dt));
-  O5_CHECK(N >= 1 && Do >= 4 && Do % 4 == 0, O5_E_SHAPE, "o5_obs_normalize: need N >= 1 and Do a positive multiple of 4");
-  O5_CHECK(static_cast<long long>(N) * Do < (1ll << 40) && cdiv(N, kObsRowsPerChunk) <= 65535, O5_E_SHAPE,
-           "o5_obs_normalize: N*Do too large");
+  {
+    const int st = check_obs_shape("o5_obs_normalize", N, Do);
+    if (st != O5_OK) return st;
+  }
   O5_CHECK(clip > 0.0f && eps > 0.0f, O5_E_ARG, "o5_obs_normalize: need clip > 0 and eps > 0");
   O5_PTR(obs, "obs");
   O5_PTR(stats, "stats");
@@ -334,7 +342,7 @@ extern "C" int o5_prelstm_fwd(o5_dtype dt, int T, int B, int Do, int D, const vo
 }
 
 extern "C" size_t o5_prelstm_bwd_workspace_bytes(o5_dtype dt, int T, int B, int Do, int D) {
-  if (T < 1 || B < kReplicas || D < 1 || Do < 1) return 0;
+  if (check_prelstm("o5_prelstm_bwd_workspace_bytes", dt, T, B, Do, D) != O5_OK) return 0;
   return prelstm_bwd_ws(dt, T * B, D).total;
 }
 

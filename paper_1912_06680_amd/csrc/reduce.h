@@ -26,6 +26,23 @@ static __global__ void __launch_bounds__(256) colsum_rows(int P, int N, const fl
   out[n] = s;
 }
 
+// out[n] = sum over the P rows of part for many rows and few columns: a
+// block takes 64 columns; its 4 waves sum rows g, g + 4, g + 8, ... (g the
+// wave), each in order, and the 4 sums are added in the order g = 0..3.
+// Launch with cdiv(N, 64) blocks of 256 threads.
+static __global__ void __launch_bounds__(256) colsum_rows4(int P, int N, const float* __restrict__ part,
+                                                          float* __restrict__ out) {
+  __shared__ float red[4][64];
+  const int c = threadIdx.x & 63, g = threadIdx.x >> 6;
+  const int n = blockIdx.x * 64 + c;
+  float s = 0.0f;
+  if (n < N)
+    for (int p = g; p < P; p += 4) s += part[static_cast<size_t>(p) * N + n];
+  red[g][c] = s;
+  __syncthreads();
+  if (g == 0 && n < N) out[n] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
+}
+
 // out[n] = sum over the P rows of part, one block of 256 threads per column:
 // thread t sums rows t, t + 256, ... in order, then a fixed-shape tree in LDS.
 // For short columns of many rows (where one thread per column would walk all
