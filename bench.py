@@ -132,6 +132,118 @@ def summarize_counters(fetch_dir, write_dir, path=None):
     return out
 
 
+def _pmc_groups(d, counters):
+    """{(kernel, grid threads): {counter: [values per dispatch]}} from the
+    counter_collection CSVs of one rocprofv3 --pmc run."""
+    import csv
+    import glob
+    out = {}
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] in counters:
+                    g = out.setdefault((r["Kernel_Name"], int(r["Grid_Size"])), {})
+                    g.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    return out
+
+
+def _trace_groups(d):
+    """{(kernel, grid threads): [durations in us]} from a --kernel-trace run."""
+    import csv
+    import glob
+    out = {}
+    for f in glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                grid = int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])
+                us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+                out.setdefault((r["Kernel_Name"], grid), []).append(us)
+    return out
+
+
+def _short(name):
+    """Kernel symbol without namespaces and parameter list, template
+    arguments kept (shortened)."""
+    n = name.replace("void ", "").replace("o5::", "").replace("unsigned short", "bf16")
+    depth, cut = 0, len(n)
+    for i, ch in enumerate(n):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            cut = i
+            break
+    return n[:cut][:70]
+
+
+N_XCD, N_SIMD = 8, 1024   # MI355X: 8 XCDs, 256 CUs x 4 SIMDs
+
+
+def counter_table(fetch_dir, write_dir, mfma_dir, trace_dir, out_md, command):
+    """Per-kernel table of the step from four rocprofv3 runs of bench.py:
+    FETCH_SIZE and WRITE_SIZE (scaled by the reference conversion as in
+    summarize_counters), SQ_INSTS_MFMA / SQ_VALU_MFMA_BUSY_CYCLES /
+    GRBM_GUI_ACTIVE, and the kernel trace.  MFMA busy is the fraction of
+    SIMD cycles the matrix pipes were busy: SQ_VALU_MFMA_BUSY_CYCLES /
+    (1024 SIMDs x GRBM_GUI_ACTIVE / 8 XCDs) (GRBM_GUI_ACTIVE sums the 8
+    XCDs' busy cycles); the clock is those cycles over the traced duration.
+    One row per (kernel, grid) group with at least 2 dispatches."""
+    tr = _trace_groups(trace_dir)
+    fe = _pmc_groups(fetch_dir, {"FETCH_SIZE"})
+    wr = _pmc_groups(write_dir, {"WRITE_SIZE"})
+    mf = _pmc_groups(mfma_dir, {"SQ_INSTS_MFMA", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE", "SQ_BUSY_CYCLES"})
+
+    def scale(groups, counter, ref_bytes):
+        ref = [v[counter] for (k, grid), v in groups.items() if "f32_to_bf16_kernel" in k and grid == COPY_REF_N // 8]
+        if len(ref) != 1:
+            raise SystemExit(f"{counter}: reference conversion not found exactly once")
+        return ref_bytes / (1024.0 * sum(ref[0]) / len(ref[0]))
+
+    sf, sw = scale(fe, "FETCH_SIZE", 4.0 * COPY_REF_N), scale(wr, "WRITE_SIZE", 2.0 * COPY_REF_N)
+    mean = lambda v: sum(v) / len(v)  # noqa: E731
+    rows = []
+    for key, durs in tr.items():
+        if len(durs) < 2 or "at::native" in key[0] or "rocclr" in key[0]:
+            continue
+        r = {"kernel": _short(key[0]), "grid": key[1], "n": len(durs), "us": mean(durs)}
+        if key in fe:
+            r["fetch_mb"] = sf * 1024.0 * mean(fe[key]["FETCH_SIZE"]) / 1e6
+        if key in wr:
+            r["write_mb"] = sw * 1024.0 * mean(wr[key]["WRITE_SIZE"]) / 1e6
+        if "fetch_mb" in r and "write_mb" in r:
+            r["gbs"] = (r["fetch_mb"] + r["write_mb"]) * 1e6 / (r["us"] * 1e-6) / 1e9
+        m = mf.get(key)
+        if m and "SQ_INSTS_MFMA" in m and mean(m["SQ_INSTS_MFMA"]) > 0:
+            grbm = mean(m["GRBM_GUI_ACTIVE"]) / N_XCD
+            r["mfma_instr"] = mean(m["SQ_INSTS_MFMA"])
+            r["mfma_tflops"] = r["mfma_instr"] * 32768.0 / (r["us"] * 1e-6) / 1e12
+            r["mfma_busy"] = mean(m["SQ_VALU_MFMA_BUSY_CYCLES"]) / (N_SIMD * grbm)
+            r["clock_ghz"] = grbm / (r["us"] * 1e3)
+        rows.append(r)
+    rows.sort(key=lambda r: -r["us"] * r["n"])
+    f = lambda r, k, fmt: (fmt.format(r[k]) if k in r else "")  # noqa: E731
+    lines = ["# Per-kernel counters: one PPO step at H = 4096 (B = 2048 x T = 16) and the other configurations",
+             "", "Command (four runs on one MI355X; the summary by the last line, on the CPU):", "", "```", command,
+             "```", "",
+             f"Counter scaling from the reference conversion (2^26 fp32 read, 2^26 bf16 written): FETCH_SIZE x "
+             f"{sf:.3f}, WRITE_SIZE x {sw:.3f}. WRITE_SIZE misses lines still dirty in the L2 when a kernel "
+             f"ends, so it can read below the bytes a kernel writes. MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / "
+             f"(1024 SIMDs x GRBM_GUI_ACTIVE / 8), at the clock the kernel ran at (column `GHz`); MFMA TFLOP/s = "
+             f"SQ_INSTS_MFMA x 32768 FLOP (v_mfma_f32_32x32x16_bf16) / traced time.", "",
+             "| kernel | grid threads | dispatches | avg us | fetch MB | write MB | GB/s (counted) | MFMA instr | "
+             "MFMA TFLOP/s | MFMA busy | GHz |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    for r in rows:
+        lines.append(f"| `{r['kernel']}` | {r['grid']} | {r['n']} | {r['us']:.1f} | {f(r, 'fetch_mb', '{:.1f}')} | "
+                     f"{f(r, 'write_mb', '{:.1f}')} | {f(r, 'gbs', '{:.0f}')} | {f(r, 'mfma_instr', '{:.0f}')} | "
+                     f"{f(r, 'mfma_tflops', '{:.0f}')} | {f(r, 'mfma_busy', '{:.3f}')} | {f(r, 'clock_ghz', '{:.2f}')} |")
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+    return rows
+
+
 def gpu_behaviour(st, inp):
     """Untimed: actions, log-probabilities and values of a perturbed policy,
     produced by the library itself (forward pass + sampler)."""
@@ -182,46 +294,125 @@ def gpu_behaviour(st, inp):
     torch.cuda.synchronize()
 
 
-def cpu_baseline(cfg, target_s=15.0):
-    """Time the CPU oracle's composed step on a bounded sample: the same
-    per-sample shapes (T, D, H, heads, segment length) with fewer segments."""
-    from oracle.step import ppo_step
+def _oracle_step_inputs(sub, seed=1):
+    """Seeded inputs of one oracle step at config `sub` (behaviour data drawn
+    at random: the timing does not depend on it)."""
     from paper_1912_06680_amd import synth
+    inp = synth.make_inputs(sub, seed)
+    rng = np.random.default_rng(2)
+    N = sub.T * sub.B
+    act = np.stack([rng.integers(0, n, N) for n in sub.head_sizes], axis=1)
+    logp_old = -np.log(np.prod(sub.head_sizes)) + rng.normal(0, 0.05, N)
+    values = rng.standard_normal((sub.L + 1, sub.S))
+    return inp, act, logp_old, values
+
+
+def _time_oracle_step(sub, dtype, reps=1):
+    """Median wall time of `reps` full oracle steps (GAE, LSTM forward, heads
+    and loss, BPTT, Adam over every parameter) at config `sub`, with arrays
+    of `dtype`; bf16 configs round their GEMM inputs as the oracle does."""
+    from oracle.precision import working
+    from oracle.step import ppo_step
+    inp, act, logp_old, values = _oracle_step_inputs(sub)
+    params = {k: inp[k] for k in ("Wx", "Wh", "b", "Wp", "bp")}
+    ts = []
+    with working(dtype):
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            ppo_step(params, inp["x"], inp["h0"], inp["c0"], inp["rewards"], inp["dones"], values, act, logp_old,
+                     sub.head_sizes, sub.T, sub.gamma, sub.lam, sub.clip_eps, sub.vf_coef, sub.ent_coef, None, sub.lr,
+                     sub.beta1, sub.beta2, sub.adam_eps, sub.clip_k, 1, bf16=sub.dtype == "bf16")
+            ts.append(time.perf_counter() - t0)
+    return float(np.median(ts))
+
+
+def _time_oracle_lstm(T, B, D, H, dtype, reps=1, seed=3):
+    """Median wall time of the oracle's LSTM forward pass and truncated BPTT
+    (no input gradient) over B samples of T steps, arrays of `dtype`."""
+    from oracle.lstm import lstm_bptt, lstm_forward
+    from oracle.precision import working
+    rng = np.random.Generator(np.random.PCG64(seed))
+    bound = 1.0 / np.sqrt(H)
+    Wx = (rng.random((4 * H, D), dtype=np.float32) * 2 - 1) * bound
+    Wh = (rng.random((4 * H, H), dtype=np.float32) * 2 - 1) * bound
+    b = (rng.random(4 * H, dtype=np.float32) * 2 - 1) * bound
+    x = rng.standard_normal((T, B, D), dtype=np.float32)
+    h0 = rng.standard_normal((B, H), dtype=np.float32) * 0.1
+    c0 = rng.standard_normal((B, H), dtype=np.float32) * 0.1
+    dh = rng.standard_normal((T, B, H), dtype=np.float32)
+    ts = []
+    with working(dtype):
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            h, c, g = lstm_forward(x, Wx, Wh, b, h0, c0)
+            lstm_bptt(x, Wx, Wh, h0, c0, None, h, c, g, dh)
+            ts.append(time.perf_counter() - t0)
+    return float(np.median(ts))
+
+
+def cpu_threads():
+    """Threads the oracle's BLAS actually uses (the pool size it reports)."""
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
-        threads = os.cpu_count() or 1
+        return os.cpu_count() or 1
 
-    def run(nb):
-        # nb samples, each its own GAE segment of T steps (same per-timestep work)
+
+def cpu_baseline(cfg, target_s=12.0):
+    """Time the CPU oracle (plain NumPy, as it stands) on the host.
+
+    Headline: the full step at the benchmark shape (T = 16, D = H = 4096,
+    four heads) on a bounded sample in fp64 -- the same per-sample shapes
+    with fewer samples, each its own GAE segment of T steps, plus Adam over
+    every parameter (a fixed cost, found from a 2- and a 6-sample run; the
+    third run is sized to about target_s).  Beside it, the other workloads
+    in fp64 and with the same code in fp32 (``oracle.precision.working``):
+    the tiny step (8 x 16, H = 128) and the mid step (256 x 16, H = 1024)
+    whole, median of 3 and 1 repetitions; the LSTM forward + BPTT at
+    D = H = 4096 on a sample of 8 of its 1024 sequences; the headline slice
+    again in fp32."""
+    from paper_1912_06680_amd import synth
+    threads = cpu_threads()
+
+    def run5(nb, dtype=np.float64):
         sub = synth.scaled(cfg, S=nb, B=nb, L=cfg.T)
-        inp = synth.make_inputs(sub, 1)
-        rng = np.random.default_rng(2)
-        N = sub.T * sub.B
-        act = np.stack([rng.integers(0, n, N) for n in sub.head_sizes], axis=1)
-        logp_old = -np.log(np.prod(sub.head_sizes)) + rng.normal(0, 0.05, N)
-        values = rng.standard_normal((sub.L + 1, sub.S))
-        params = {k: inp[k] for k in ("Wx", "Wh", "b", "Wp", "bp")}
-        t0 = time.perf_counter()
-        ppo_step(params, inp["x"], inp["h0"], inp["c0"], inp["rewards"], inp["dones"], values, act, logp_old,
-                 sub.head_sizes, sub.T, sub.gamma, sub.lam, sub.clip_eps, sub.vf_coef, sub.ent_coef, None, sub.lr,
-                 sub.beta1, sub.beta2, sub.adam_eps, sub.clip_k, 1, bf16=sub.dtype == "bf16")
-        return time.perf_counter() - t0, sub
+        return _time_oracle_step(sub, dtype), sub
 
-    # the step has a fixed part (Adam over every parameter) and a part linear
-    # in the samples: two small runs give both, the third is sized to target_s
-    dt1, _ = run(2)
-    dt2, sub = run(6)
+    dt1, _ = run5(2)
+    dt2, sub = run5(6)
     dt = dt2
     per = max((dt2 - dt1) / 4, 0.02 * dt2 / 6)   # floor against timing noise
-    nb = int(min(cfg.B, 256, max(6, round(6 + (target_s - dt2) / per))))
+    nb = int(min(cfg.B, max(6, round(6 + (target_s - dt2) / per))))
     if nb > 6:
-        dt, sub = run(nb)
-    return {"value": sub.B * sub.T / dt, "unit": "timesteps/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{sub.B} samples x T={sub.T} (D=H={sub.H}, heads {tuple(sub.head_sizes)}, each sample "
-                      f"its own GAE segment), one full step of the fp64 NumPy oracle incl. Adam over all "
-                      f"{synth.n_params(sub)} params, {dt:.2f} s on {cpu_model()}"}
+        dt, sub = run5(nb)
+    out = {"value": sub.B * sub.T / dt, "unit": "timesteps/s", "cores": int(threads), "kind": "oracle",
+           "sample": f"{sub.B} samples x T={sub.T} (D=H={sub.H}, heads {tuple(sub.head_sizes)}, each sample "
+                     f"its own GAE segment), one full step of the fp64 NumPy oracle incl. Adam over all "
+                     f"{synth.n_params(sub)} params, {dt:.2f} s",
+           "host": {"cpu_model": cpu_model(), "os_cpu_count": os.cpu_count(),
+                    "threads_env": {k: os.environ.get(k) for k in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS",
+                                                                      "MKL_NUM_THREADS")}}}
+    others = []
+    # fp32: the same code on the plain fp32 configuration (no bf16 operand rounding)
+    sub32 = synth.scaled(sub, dtype="f32")
+    dt32 = _time_oracle_step(sub32, np.float32)
+    others.append({"config": f"full step, sample of the benchmark shape ({sub.B} samples x T={sub.T}, D=H={sub.H})",
+                   "dtype": "f32", "s": round(dt32, 3), "timesteps_per_s": round(sub.B * sub.T / dt32, 1)})
+    for name, reps in (("tiny", 3), ("mid", 1)):
+        c = synth.CONFIGS[name]
+        for dtype, dn in ((np.float64, "f64"), (np.float32, "f32")):
+            t = _time_oracle_step(c, dtype, reps)
+            others.append({"config": f"full step {name}: B={c.B} x T={c.T}, D={c.D} H={c.H}, heads "
+                                     f"{list(c.head_sizes)}", "dtype": dn, "s": round(t, 4),
+                           "timesteps_per_s": round(c.B * c.T / t, 1)})
+    B3 = 8
+    for dtype, dn in ((np.float64, "f64"), (np.float32, "f32")):
+        t = _time_oracle_lstm(16, B3, 4096, 4096, dtype)
+        others.append({"config": f"LSTM forward + BPTT, sample of {B3} of 1024 sequences x T=16, "
+                                 f"D=H=4096", "dtype": dn, "s": round(t, 3), "timesteps_per_s": round(B3 * 16 / t, 1)})
+    out["other_configs"] = others
+    return out
 
 
 def other_configs(cfg, reps=5, warm=2):
@@ -261,6 +452,24 @@ def other_configs(cfg, reps=5, warm=2):
         return float(np.median(ts))
 
     out = []
+    # configs 1 and 2: the whole optimizer step at the tiny and mid sizes
+    # (latency-bound), as the step runs in the benchmark
+    from paper_1912_06680_amd import synth
+    from paper_1912_06680_amd.step import PARAM_ORDER, PPOStep
+    for name in ("tiny", "mid", "mid_bf16"):
+        c = synth.CONFIGS[name]
+        inp = synth.make_inputs(c, 0)
+        st = PPOStep(c)
+        gpu_behaviour(st, inp)
+        st.load_params({k: inp[k] for k in PARAM_ORDER})
+        st.m.zero_()
+        st.v.zero_()
+        ms_small = timed(st.run)
+        out.append({"workload": f"full PPO step {name}: B={c.B} x T={c.T}, D={c.D} H={c.H}, heads "
+                                f"{list(c.head_sizes)} + value, GAE {c.S} x {c.L}, Adam over {st.n_params} params",
+                    "dtype": c.dtype, "ms": round(ms_small, 4), "timesteps_per_s": round(c.B * c.T / (ms_small * 1e-3), 1)})
+        del st
+    torch.cuda.empty_cache()
     Wx, Wh = uni((G, D)), uni((G, H))
     b = (torch.rand(G, generator=gen, device=dev) * 2 - 1) * bound
     T, B = 16, 1024
@@ -482,6 +691,30 @@ def hbm_kernels(cfg, reps=20, warm=3):
     return out
 
 
+def stream_copy_gbs(reps=10, warm=3):
+    """Device-to-device copy of 1 GiB of fp32 (torch's copy kernel): bytes
+    read plus written per second, median of `reps` -- the bandwidth a plain
+    streaming kernel reaches on this GPU, a second reference beside the
+    published 8 TB/s."""
+    import torch
+    n = 1 << 28
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    ts = []
+    for i in range(warm + reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        if i >= warm:
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2.0 * 4 * n / float(np.median(ts)) / 1e9
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as fh:
@@ -510,9 +743,15 @@ def main():
                     help="after timing, run one conversion of 2^26 fp32 elements (counter scale reference)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write profiles/traffic.json from two rocprofv3 --pmc runs and exit (no GPU)")
+    ap.add_argument("--counter-table", nargs=5, metavar=("FETCH_DIR", "WRITE_DIR", "MFMA_DIR", "TRACE_DIR", "OUT_MD"),
+                    help="write the per-kernel counter table from four rocprofv3 runs and exit (no GPU)")
+    ap.add_argument("--command", default="", help="the command recorded in the counter table")
     args = ap.parse_args()
     if args.summarize_counters:
         summarize_counters(*args.summarize_counters)
+        return
+    if args.counter_table:
+        counter_table(*args.counter_table, command=args.command)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU path "
@@ -556,6 +795,8 @@ def main():
         "gae": 17.0 * cfg.L * cfg.S + 4.0 * cfg.S,
         "ppo_loss_grad": (2 * 2.0 * H + 4.0 * H + 4.0 * A1 + 16.0) * T * B,
     }
+    copy_gbs = stream_copy_gbs()
+    log(f"streaming copy: {copy_gbs:.0f} GB/s")
     kernels = {}
     dom = None
     if not args.no_kernel_timers:
@@ -578,6 +819,7 @@ def main():
             if name in bytes_:
                 k["gbs"] = round(bytes_[name] / (per * 1e-3) / 1e9, 1)
                 k["frac_hbm_peak"] = round(k["gbs"] / PEAK_HBM_GBS, 4)
+                k["frac_stream_copy"] = round(k["gbs"] / copy_gbs, 4)
             kernels[name] = k
         if any(s_ in kernels for s_ in flops):
             dom = max(flops, key=lambda s_: kernels.get(s_, {}).get("ms_per_step", 0.0))
@@ -625,6 +867,8 @@ def main():
     if not args.no_hbm_kernels:
         log("standalone HBM-bound kernels (GAE, Adam), cold and warm")
         hbm = hbm_kernels(cfg)
+        for e in hbm:
+            e["frac_stream_copy_cold"] = round(e["cold_gbs"] / copy_gbs, 4)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -642,6 +886,7 @@ def main():
                                f"{n} params", "global_batch": B * T, "seq_len": T, "parallelism": "none (1 GPU)"},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "stream_copy_gbs": round(copy_gbs, 1),
         "lstm_gemm_mfma_frac": round(lstm_gemm_tflops / PEAK_BF16_TFLOPS, 4),
         "lstm_gemm_tflops": round(lstm_gemm_tflops, 2),
         "step_tflops": round(step_flop / (ms_step * 1e-3) / 1e12, 2),
