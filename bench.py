@@ -83,44 +83,28 @@ COPY_REF_N = 1 << 26   # fp32 elements of the reference conversion (256 MiB read
 
 def summarize_counters(fetch_dir, write_dir, path=None):
     """Turn two `rocprofv3 --pmc FETCH_SIZE` / `--pmc WRITE_SIZE` runs of
-    `bench.py --copy-ref` into profiles/traffic.json.  Both counters read KiB
-    per dispatch; each is scaled by bytes/counter of the reference conversion
-    (COPY_REF_N fp32 elements read, as many bf16 written), which is the only
-    o5_f32_to_bf16 dispatch with COPY_REF_N / 8 threads."""
-    import csv
-    import glob
-
-    def load(d, counter):
-        groups = {}
-        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
-            with open(f) as fh:
-                for r in csv.DictReader(fh):
-                    if r["Counter_Name"] != counter:
-                        continue
-                    key = (r["Kernel_Name"], int(r["Grid_Size"]))
-                    groups.setdefault(key, []).append(float(r["Counter_Value"]) * 1024.0)
-        if not groups:
-            raise SystemExit(f"no {counter} rows under {d}")
-        return groups
-
+    `bench.py --copy-ref` into profiles/traffic.json: bytes per launch of
+    each timed site's kernel within the step (dispatches before the
+    reference conversion).  Both counters read KiB per dispatch; each is
+    scaled by bytes/counter of the reference conversion (COPY_REF_N fp32
+    elements read, as many bf16 written)."""
     out = {"source_digest": source_digest(), "kernels": {}}
-    scale = {}
     for name, d, ref_bytes in (("FETCH_SIZE", fetch_dir, 4.0 * COPY_REF_N), ("WRITE_SIZE", write_dir, 2.0 * COPY_REF_N)):
-        g = load(d, name)
-        ref = [v for (k, grid), v in g.items() if "f32_to_bf16_kernel" in k and grid == COPY_REF_N // 8]
+        g = _pmc_groups(d, {name})
+        ref = [v[name] for (ph, k, grid), v in g.items() if ph == "ref"]
         if len(ref) != 1:
             raise SystemExit(f"{name}: reference conversion not found exactly once")
-        counted = sum(ref[0]) / len(ref[0])
-        scale[name] = ref_bytes / counted
-        out[name] = {"copy_ref_counted_bytes": counted, "copy_ref_bytes": ref_bytes, "scale": scale[name]}
+        counted = 1024.0 * sum(ref[0]) / len(ref[0])
+        scale = ref_bytes / counted
+        out[name] = {"copy_ref_counted_bytes": counted, "copy_ref_bytes": ref_bytes, "scale": scale}
         for site, sym in SITE_SYMBOLS.items():
-            cand = [(len(v), k, v) for k, v in g.items() if sym in k[0]]
+            cand = [(len(v[name]), k, grid, v[name]) for (ph, k, grid), v in g.items() if ph == "step" and sym in k]
             if not cand:
                 continue
-            _, (kname, grid), v = max(cand, key=lambda c: c[0])
+            _, kname, grid, v = max(cand, key=lambda c: c[0])
             e = out["kernels"].setdefault(site, {"symbol": kname[:160], "grid_threads": grid})
             key = "fetch_bytes_per_launch" if name == "FETCH_SIZE" else "write_bytes_per_launch"
-            e[key] = round(scale[name] * sum(v) / len(v))
+            e[key] = round(scale * 1024.0 * sum(v) / len(v))
             e["dispatches_" + name.lower()] = len(v)
     out["kernels"] = {k: v for k, v in out["kernels"].items()
                       if "fetch_bytes_per_launch" in v and "write_bytes_per_launch" in v}
@@ -132,32 +116,54 @@ def summarize_counters(fetch_dir, write_dir, path=None):
     return out
 
 
+def _copy_ref_dispatch(rows, grid_of):
+    """Dispatch id of the reference conversion (the one o5_f32_to_bf16 launch
+    with COPY_REF_N / 8 threads), which bench.py --copy-ref runs right after
+    the timed steps and before the other workloads."""
+    ids = [int(r["Dispatch_Id"]) for r in rows
+           if "f32_to_bf16_kernel" in r["Kernel_Name"] and grid_of(r) == COPY_REF_N // 8]
+    if len(set(ids)) != 1:
+        raise SystemExit("reference conversion not found exactly once")
+    return ids[0]
+
+
+def _phase(dispatch, ref):
+    return "step" if dispatch < ref else ("ref" if dispatch == ref else "other")
+
+
 def _pmc_groups(d, counters):
-    """{(kernel, grid threads): {counter: [values per dispatch]}} from the
-    counter_collection CSVs of one rocprofv3 --pmc run."""
+    """{(phase, kernel, grid threads): {counter: [values per dispatch]}} from
+    the counter_collection CSVs of one rocprofv3 --pmc run; phase "step" for
+    dispatches before the reference conversion, "ref" for it, "other" after."""
     import csv
     import glob
-    out = {}
+    rows = []
     for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
         with open(f) as fh:
-            for r in csv.DictReader(fh):
-                if r["Counter_Name"] in counters:
-                    g = out.setdefault((r["Kernel_Name"], int(r["Grid_Size"])), {})
-                    g.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+            rows += [r for r in csv.DictReader(fh) if r["Counter_Name"] in counters]
+    ref = _copy_ref_dispatch(rows, lambda r: int(r["Grid_Size"]))
+    out = {}
+    for r in rows:
+        key = (_phase(int(r["Dispatch_Id"]), ref), r["Kernel_Name"], int(r["Grid_Size"]))
+        out.setdefault(key, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
     return out
 
 
 def _trace_groups(d):
-    """{(kernel, grid threads): [durations in us]} from a --kernel-trace run."""
+    """{(phase, kernel, grid threads): [durations in us]} from a
+    --kernel-trace run (phases as in _pmc_groups)."""
     import csv
     import glob
-    out = {}
+    rows = []
     for f in glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True):
         with open(f) as fh:
-            for r in csv.DictReader(fh):
-                grid = int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])
-                us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-                out.setdefault((r["Kernel_Name"], grid), []).append(us)
+            rows += list(csv.DictReader(fh))
+    grid = lambda r: int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])  # noqa: E731
+    ref = _copy_ref_dispatch(rows, grid)
+    out = {}
+    for r in rows:
+        us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        out.setdefault((_phase(int(r["Dispatch_Id"]), ref), r["Kernel_Name"], grid(r)), []).append(us)
     return out
 
 
@@ -181,21 +187,23 @@ N_XCD, N_SIMD = 8, 1024   # MI355X: 8 XCDs, 256 CUs x 4 SIMDs
 
 
 def counter_table(fetch_dir, write_dir, mfma_dir, trace_dir, out_md, command):
-    """Per-kernel table of the step from four rocprofv3 runs of bench.py:
+    """Per-kernel table from four rocprofv3 runs of bench.py --copy-ref:
     FETCH_SIZE and WRITE_SIZE (scaled by the reference conversion as in
     summarize_counters), SQ_INSTS_MFMA / SQ_VALU_MFMA_BUSY_CYCLES /
     GRBM_GUI_ACTIVE, and the kernel trace.  MFMA busy is the fraction of
     SIMD cycles the matrix pipes were busy: SQ_VALU_MFMA_BUSY_CYCLES /
     (1024 SIMDs x GRBM_GUI_ACTIVE / 8 XCDs) (GRBM_GUI_ACTIVE sums the 8
     XCDs' busy cycles); the clock is those cycles over the traced duration.
-    One row per (kernel, grid) group with at least 2 dispatches."""
+    Two sections: the optimizer step at the benchmark shape (dispatches
+    before the reference conversion: warmup, instrumented and timed steps)
+    and the other workloads (after it).  One row per (kernel, grid) group."""
     tr = _trace_groups(trace_dir)
     fe = _pmc_groups(fetch_dir, {"FETCH_SIZE"})
     wr = _pmc_groups(write_dir, {"WRITE_SIZE"})
     mf = _pmc_groups(mfma_dir, {"SQ_INSTS_MFMA", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE", "SQ_BUSY_CYCLES"})
 
     def scale(groups, counter, ref_bytes):
-        ref = [v[counter] for (k, grid), v in groups.items() if "f32_to_bf16_kernel" in k and grid == COPY_REF_N // 8]
+        ref = [v[counter] for (ph, k, grid), v in groups.items() if ph == "ref"]
         if len(ref) != 1:
             raise SystemExit(f"{counter}: reference conversion not found exactly once")
         return ref_bytes / (1024.0 * sum(ref[0]) / len(ref[0]))
@@ -204,9 +212,9 @@ def counter_table(fetch_dir, write_dir, mfma_dir, trace_dir, out_md, command):
     mean = lambda v: sum(v) / len(v)  # noqa: E731
     rows = []
     for key, durs in tr.items():
-        if len(durs) < 2 or "at::native" in key[0] or "rocclr" in key[0]:
+        if key[0] == "ref" or "at::native" in key[1] or "rocclr" in key[1]:
             continue
-        r = {"kernel": _short(key[0]), "grid": key[1], "n": len(durs), "us": mean(durs)}
+        r = {"phase": key[0], "kernel": _short(key[1]), "grid": key[2], "n": len(durs), "us": mean(durs)}
         if key in fe:
             r["fetch_mb"] = sf * 1024.0 * mean(fe[key]["FETCH_SIZE"]) / 1e6
         if key in wr:
@@ -221,25 +229,33 @@ def counter_table(fetch_dir, write_dir, mfma_dir, trace_dir, out_md, command):
             r["mfma_busy"] = mean(m["SQ_VALU_MFMA_BUSY_CYCLES"]) / (N_SIMD * grbm)
             r["clock_ghz"] = grbm / (r["us"] * 1e3)
         rows.append(r)
-    rows.sort(key=lambda r: -r["us"] * r["n"])
+    rows.sort(key=lambda r: (r["phase"] != "step", -r["us"] * r["n"]))
     f = lambda r, k, fmt: (fmt.format(r[k]) if k in r else "")  # noqa: E731
-    lines = ["# Per-kernel counters: one PPO step at H = 4096 (B = 2048 x T = 16) and the other configurations",
-             "", "Command (four runs on one MI355X; the summary by the last line, on the CPU):", "", "```", command,
-             "```", "",
+    head = ["| kernel | grid threads | dispatches | avg us | fetch MB | write MB | GB/s (counted) | MFMA instr | "
+            "MFMA TFLOP/s | MFMA busy | GHz |",
+            "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    lines = ["# Per-kernel counters: the PPO optimizer step at H = 4096 (B = 2048 x T = 16), then the other "
+             "workloads", "", "Command (four runs on one MI355X; the table by the last line, on the CPU):", "", "```",
+             command, "```", "",
              f"Counter scaling from the reference conversion (2^26 fp32 read, 2^26 bf16 written): FETCH_SIZE x "
              f"{sf:.3f}, WRITE_SIZE x {sw:.3f}. WRITE_SIZE misses lines still dirty in the L2 when a kernel "
              f"ends, so it can read below the bytes a kernel writes. MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / "
              f"(1024 SIMDs x GRBM_GUI_ACTIVE / 8), at the clock the kernel ran at (column `GHz`); MFMA TFLOP/s = "
-             f"SQ_INSTS_MFMA x 32768 FLOP (v_mfma_f32_32x32x16_bf16) / traced time.", "",
-             "| kernel | grid threads | dispatches | avg us | fetch MB | write MB | GB/s (counted) | MFMA instr | "
-             "MFMA TFLOP/s | MFMA busy | GHz |",
-             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
-    for r in rows:
-        lines.append(f"| `{r['kernel']}` | {r['grid']} | {r['n']} | {r['us']:.1f} | {f(r, 'fetch_mb', '{:.1f}')} | "
-                     f"{f(r, 'write_mb', '{:.1f}')} | {f(r, 'gbs', '{:.0f}')} | {f(r, 'mfma_instr', '{:.0f}')} | "
-                     f"{f(r, 'mfma_tflops', '{:.0f}')} | {f(r, 'mfma_busy', '{:.3f}')} | {f(r, 'clock_ghz', '{:.2f}')} |")
+             f"SQ_INSTS_MFMA x 32768 FLOP (v_mfma_f32_32x32x16_bf16) / traced time.", ""]
+    for phase, title in (("step", "## The optimizer step (warmup, instrumented and timed steps)"),
+                         ("other", "## The other workloads (tiny and mid steps, LSTM forward + BPTT at B = 1024, "
+                                   "rollout inference at B = 4096)")):
+        lines += [title, ""] + head
+        for r in rows:
+            if r["phase"] != phase:
+                continue
+            lines.append(f"| `{r['kernel']}` | {r['grid']} | {r['n']} | {r['us']:.1f} | {f(r, 'fetch_mb', '{:.1f}')} | "
+                         f"{f(r, 'write_mb', '{:.1f}')} | {f(r, 'gbs', '{:.0f}')} | {f(r, 'mfma_instr', '{:.0f}')} | "
+                         f"{f(r, 'mfma_tflops', '{:.0f}')} | {f(r, 'mfma_busy', '{:.3f}')} | "
+                         f"{f(r, 'clock_ghz', '{:.2f}')} |")
+        lines.append("")
     with open(out_md, "w") as fh:
-        fh.write("\n".join(lines) + "\n")
+        fh.write("\n".join(lines))
     print("\n".join(lines))
     return rows
 

@@ -336,12 +336,14 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
 // The row kernel with one thread per row, for up to MAXC logit columns: the
 // block's 64 rows of logits (the GEMM's partial sums plus bias, or the unit
 // head's own logits) and availability bytes are staged in LDS by all 256
-// threads with coalesced loads; the first wave then takes one row per lane
-// through the same definition as ppo_row, serially (max, exponentials and
-// sums per head, the joint ratio, clipped surrogate, value error and
-// entropy, then dL/dz per column, written back over the row's logits);
-// finally the block writes the gradient rows (dz, the (hi, lo) pair, the
-// unit head's columns) and its column sums with coalesced stores.  No cross-lane operation; every sum in a fixed order.
+// threads with coalesced loads; then, one row per lane, the same definition
+// as ppo_row in three passes: each wave takes whole heads (max,
+// exponentials and sums, the taken action's log-probability), the first
+// wave the row (joint ratio, clipped surrogate, value error, entropy), and
+// the waves their heads again for dL/dz per column, written back over the
+// row's logits; finally the block writes the gradient rows (dz, the (hi,
+// lo) pair, the unit head's columns) and its column sums with coalesced
+// stores.  No cross-lane operation; every sum in a fixed order.
 // Writes row blockIdx.x of part (64 rows per partial).
 constexpr int kRtRows = 64;
 constexpr int kRtThreads = 256;
@@ -355,9 +357,13 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
     float ent_coef, float invN, float* __restrict__ dz, float* __restrict__ part, uint16_t* __restrict__ dz_hi,
     uint16_t* __restrict__ dz_lo, int ncol_hilo, int ld_hilo) {
   constexpr int ZP = MAXC + 1;  // floats per staged row (odd: a column read hits distinct banks)
+  constexpr int AP = MAXC + 4;  // bytes per availability row (an odd number of dwords, for the same reason)
   __shared__ float zs[kRtRows][ZP];
-  __shared__ uint8_t avs[kRtRows][MAXC];
+  __shared__ uint8_t avs[kRtRows][AP];
   __shared__ float st_red[kStatCols][kRtRows];
+  __shared__ float hd_mx[kMaxHeads][kRtRows], hd_inv[kMaxHeads][kRtRows], hd_zbar[kMaxHeads][kRtRows];
+  __shared__ float hd_lp[kMaxHeads][kRtRows], hd_ent[kMaxHeads][kRtRows], row_g[kRtRows];
+  __shared__ int hd_act[kMaxHeads][kRtRows], hd_use[kMaxHeads][kRtRows];
   const int t = threadIdx.x;
   const int n0 = blockIdx.x * kRtRows;
   const int rows = min(kRtRows, N - n0);
@@ -381,57 +387,72 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
       const int r = e / nke, u = e - r * nke;
       zs[r][e0 + u] = zext[static_cast<size_t>(n0) * nke + e];
     }
+    if (avail != nullptr) {
 #pragma unroll 4
-    for (int e = t; e < rows * A; e += kRtThreads) {
-      const int r = e / A, a = e - r * A;
-      avs[r][a] = avail ? avail[static_cast<size_t>(n0) * A + e] : 1;
+      for (int e = t; e < rows * A; e += kRtThreads) {
+        const int r = e / A, a = e - r * A;
+        avs[r][a] = avail[static_cast<size_t>(n0) * A + e];
+      }
     }
   }
   __syncthreads();
+  // heads: wave w takes heads w, w + 4, ... of every row (lane = row): the
+  // head's maximum, normaliser, mean logit and the taken action's
+  // log-probability, kept in LDS per (head, row)
+  const int r = t & (kRtRows - 1), w0 = t / kRtRows;
+  const bool all_av = avail == nullptr;  // uniform: no availability bytes read
+  if (r < rows) {
+    const int n = n0 + r;
+    const float* z = zs[r];
+    const uint8_t* av = avs[r];
+    for (int k = w0; k < K; k += kRtThreads / kRtRows) {
+      const int o = hm.off[k], nk = hm.off[k + 1] - o;
+      float m = -INFINITY;
+      for (int a = 0; a < nk; ++a)
+        if (all_av || av[o + a]) m = fmaxf(m, z[o + a]);
+      float sum = 0.0f, sz = 0.0f;
+      for (int a = 0; a < nk; ++a)
+        if (all_av || av[o + a]) {
+          const float e = expf(z[o + a] - m);
+          sum += e;
+          sz += e * z[o + a];
+        }
+      const bool some = sum > 0.0f;  // the maximum contributes e = 1
+      const bool mk = mask == nullptr || mask[static_cast<size_t>(n) * K + k] != 0;
+      const float lse = some ? m + logf(sum) : 0.0f;
+      const float zb = some ? sz / sum : 0.0f;
+      const int ak = act[static_cast<size_t>(n) * K + k];
+      const bool use = mk && some;
+      float lp = 0.0f, en = 0.0f;
+      if (use) {
+        const int a_sel = min(max(ak, 0), nk - 1);
+        lp = (all_av || av[o + a_sel]) ? z[o + a_sel] - lse : -INFINITY;
+        en = lse - zb;
+      }
+      hd_mx[k][r] = m;
+      hd_inv[k][r] = some ? 1.0f / sum : 0.0f;
+      hd_zbar[k][r] = zb;
+      hd_lp[k][r] = lp;
+      hd_ent[k][r] = en;
+      hd_act[k][r] = ak;
+      hd_use[k][r] = use;
+    }
+  }
+  __syncthreads();
+  // the row: joint ratio (log-probabilities summed over heads in order),
+  // clipped surrogate, value error, entropy, the scale of the log-probability
+  // gradient; the value column's gradient and the padding columns
   if (t < kRtRows) {
     float st[kStatCols] = {};
     if (t < rows) {
       const int n = n0 + t;
       float* z = zs[t];
-      const uint8_t* av = avs[t];
-      float mx[kMaxHeads], inv[kMaxHeads], zbar[kMaxHeads];
-      bool use[kMaxHeads];
-      int ak[kMaxHeads];
       float logpi = 0.0f, ent = 0.0f;
-#pragma unroll
-      for (int k = 0; k < kMaxHeads; ++k) {
-        mx[k] = 0.0f;
-        inv[k] = 0.0f;
-        zbar[k] = 0.0f;
-        use[k] = false;
-        ak[k] = 0;
-        if (k < K) {
-          const int o = hm.off[k], nk = hm.off[k + 1] - o;
-          float m = -INFINITY;
-          for (int a = 0; a < nk; ++a)
-            if (av[o + a]) m = fmaxf(m, z[o + a]);
-          float sum = 0.0f, sz = 0.0f;
-          for (int a = 0; a < nk; ++a)
-            if (av[o + a]) {
-              const float e = expf(z[o + a] - m);
-              sum += e;
-              sz += e * z[o + a];
-            }
-          const bool some = sum > 0.0f;  // the maximum contributes e = 1
-          const bool mk = mask == nullptr || mask[static_cast<size_t>(n) * K + k] != 0;
-          const float lse = some ? m + logf(sum) : 0.0f;
-          mx[k] = m;
-          inv[k] = some ? 1.0f / sum : 0.0f;
-          zbar[k] = some ? sz / sum : 0.0f;
-          use[k] = mk && some;
-          ak[k] = act[static_cast<size_t>(n) * K + k];
-          if (use[k]) {
-            const int a_sel = min(max(ak[k], 0), nk - 1);
-            logpi += av[o + a_sel] ? z[o + a_sel] - lse : -INFINITY;
-            ent += lse - zbar[k];
-          }
+      for (int k = 0; k < K; ++k)
+        if (hd_use[k][t]) {
+          logpi += hd_lp[k][t];
+          ent += hd_ent[k][t];
         }
-      }
       const float Ad = adv[n], R = ret[n];
       const float dlog = logpi - logp_old[n];
       const float ratio = expf(dlog);
@@ -439,23 +460,7 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
       const float surr = fminf(ratio * Ad, rc * Ad);
       const float verr = z[A] - R;
       const bool flow = (Ad >= 0.0f && ratio <= 1.0f + clip_eps) || (Ad < 0.0f && ratio >= 1.0f - clip_eps);
-      const float g_logpi = flow ? -ratio * Ad * invN : 0.0f;
-      const float ent_scale = ent_coef * invN;
-#pragma unroll
-      for (int k = 0; k < kMaxHeads; ++k) {
-        if (k < K) {
-          const int o = hm.off[k], nk = hm.off[k + 1] - o;
-          for (int a = 0; a < nk; ++a) {
-            float d = 0.0f;
-            if (use[k] && av[o + a]) {
-              const float p = expf(z[o + a] - mx[k]) * inv[k];
-              const float onehot = a == ak[k] ? 1.0f : 0.0f;
-              d = g_logpi * (onehot - p) + ent_scale * p * (z[o + a] - zbar[k]);
-            }
-            z[o + a] = d;
-          }
-        }
-      }
+      row_g[t] = flow ? -ratio * Ad * invN : 0.0f;
       z[A] = 2.0f * vf_coef * verr * invN;
       for (int a = A1; a < MAXC; ++a) z[a] = 0.0f;
       const float row_loss = -surr + vf_coef * verr * verr - ent_coef * ent;
@@ -471,6 +476,30 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
     }
 #pragma unroll
     for (int q = 0; q < kStatCols; ++q) st_red[q][t] = st[q];
+  }
+  __syncthreads();
+  // dL/dz of every head column, written back over the row's logits (same
+  // head-to-wave assignment as above)
+  if (r < rows) {
+    float* z = zs[r];
+    const uint8_t* av = avs[r];
+    const float g_logpi = row_g[r];
+    const float ent_scale = ent_coef * invN;
+    for (int k = w0; k < K; k += kRtThreads / kRtRows) {
+      const int o = hm.off[k], nk = hm.off[k + 1] - o;
+      const int ak = hd_act[k][r];
+      const bool use = hd_use[k][r] != 0;
+      const float mx = hd_mx[k][r], inv = hd_inv[k][r], zbar = hd_zbar[k][r];
+      for (int a = 0; a < nk; ++a) {
+        float d = 0.0f;
+        if (use && (all_av || av[o + a])) {
+          const float p = expf(z[o + a] - mx) * inv;
+          const float onehot = a == ak ? 1.0f : 0.0f;
+          d = g_logpi * (onehot - p) + ent_scale * p * (z[o + a] - zbar);
+        }
+        z[o + a] = d;
+      }
+    }
   }
   __syncthreads();
   // the unit head's gradient leaves; its columns are 0 in every other output

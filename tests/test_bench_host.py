@@ -1,7 +1,8 @@
 """Host logic of bench.py (CPU only): the HBM-counter summary scales each
 counter by what it reads for the reference conversion, takes the most
-frequent (symbol, grid) group of each site, and the traffic it writes is
-used only while the kernel sources it was taken on are unchanged."""
+frequent (symbol, grid) group of each site among the step's dispatches
+(those before the reference conversion), and the traffic it writes is used
+only while the kernel sources it was taken on are unchanged."""
 import csv
 import json
 
@@ -11,20 +12,23 @@ import bench
 def _write(d, counter, rows):
     d.mkdir(parents=True)
     with open(d / "x_counter_collection.csv", "w", newline="") as fh:
-        w = csv.DictWriter(fh, fieldnames=["Kernel_Name", "Grid_Size", "Counter_Name", "Counter_Value"])
+        w = csv.DictWriter(fh, fieldnames=["Dispatch_Id", "Kernel_Name", "Grid_Size", "Counter_Name", "Counter_Value"])
         w.writeheader()
-        for name, grid, kib in rows:
-            w.writerow({"Kernel_Name": name, "Grid_Size": grid, "Counter_Name": counter, "Counter_Value": kib})
+        for i, (name, grid, kib) in enumerate(rows, 1):
+            w.writerow({"Dispatch_Id": i, "Kernel_Name": name, "Grid_Size": grid, "Counter_Name": counter,
+                        "Counter_Value": kib})
 
 
 def test_counter_summary_scales_by_the_reference_and_picks_the_frequent_group(tmp_path):
     ref = ("o5::f32_to_bf16_kernel(unsigned long, float const*, unsigned short*)", bench.COPY_REF_N // 8)
     fwd = "void o5::gemm_kk<256, o5::EpiLstmCell<unsigned short>, unsigned short>(...)"
     # FETCH_SIZE counts half of the reference's bytes read; WRITE_SIZE all of them
-    fetch = [(ref[0], ref[1], 4.0 * bench.COPY_REF_N / 1024 / 2)]
-    fetch += [(fwd, 262144, 1000.0)] * 16 + [(fwd, 131072, 5.0)]      # the behaviour pass's other grid
-    write = [(ref[0], ref[1], 2.0 * bench.COPY_REF_N / 1024)]
-    write += [(fwd, 262144, 100.0)] * 16 + [(fwd, 131072, 1.0)]
+    # the step's dispatches, then the reference, then other workloads (the
+    # same symbol and grid as the step's, which must not count)
+    fetch = [(fwd, 262144, 1000.0)] * 16 + [(fwd, 131072, 5.0)]      # the behaviour pass's other grid
+    fetch += [(ref[0], ref[1], 4.0 * bench.COPY_REF_N / 1024 / 2)] + [(fwd, 262144, 7.0)] * 40
+    write = [(fwd, 262144, 100.0)] * 16 + [(fwd, 131072, 1.0)]
+    write += [(ref[0], ref[1], 2.0 * bench.COPY_REF_N / 1024)] + [(fwd, 262144, 3.0)] * 40
     _write(tmp_path / "f", "FETCH_SIZE", fetch)
     _write(tmp_path / "w", "WRITE_SIZE", write)
     out = bench.summarize_counters(str(tmp_path / "f"), str(tmp_path / "w"), str(tmp_path / "t.json"))
