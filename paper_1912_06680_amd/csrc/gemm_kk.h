@@ -9,7 +9,8 @@
 // MFMAs, measured a few percent slower overall.)
 //
 // Operands go global -> LDS by buffer loads with the LDS flag (16 bytes per
-// lane, written at M0 + 16 * lane) through two stages of BK = 64 k: a copy
+// lane, written at M0 + 16 * lane) through NS stages of BK = 64 k (two of
+// 64 KB for 256 x 256 tiles, three of 48 KB for 256 x 128 ones): a copy
 // instruction moves 8 rows x 128 bytes, i.e. whole cache lines (stages of 32
 // k move 16 half lines, which halves the rate at which the L2 feeds the CU;
 // a ring of more, smaller slots measured slower).  Each lane's byte offset
@@ -19,14 +20,15 @@
 //
 // The wave software-pipelines its fragments: those of k step s + 1 are read
 // while the MFMAs of step s run.  Before the last k step of tile r the wave
-// waits for its own copies of tile r + 1, meets the other waves at the
-// barrier (after which the stage of tile r is free: every wave has finished
-// reading it), reads the first fragments of tile r + 1, and then issues the
-// copies that refill the stage with tile r + 2, interleaved with the MFMAs of
-// that last k step.  The copies are inline asm, so the compiler neither waits
-// for them before LDS reads nor edits the explicit waits; each wave issues
-// copies for tiles 0 .. n (the one past the K range re-reads the last tile
-// into a stage no one reads again).
+// waits for its own copies of tile r + 1 (those of the NS - 2 tiles after it
+// may stay in flight), meets the other waves at the barrier (after which the
+// stage of tile r is free: every wave has finished reading it), reads the
+// first fragments of tile r + 1, and then issues the copies that refill the
+// stage with tile r + NS, interleaved with the MFMAs of that last k step.
+// The copies are inline asm, so the compiler neither waits for them before
+// LDS reads nor edits the explicit waits; each wave issues copies for tiles
+// 0 .. n + NS - 2 (those past the K range re-read the last tile into stages
+// no one reads again).
 //
 // LDS layout of one operand stage: [rows][64 k] bf16, the 16-byte chunk c of
 // row r stored at slot c ^ ((r / 2) % 8), so the 16 rows of a fragment read
@@ -63,7 +65,11 @@ struct Shape {
   static constexpr int TB = BN * ROW_BYTES;        // B stage bytes
   static constexpr int NCA = TA / 1024 / NWAVES;   // copies per wave per A tile
   static constexpr int NCB = TB / 1024 / NWAVES;   // copies per wave per B tile
-  static constexpr int SMEM = 2 * (TA + TB);       // two stages
+  // stages: two of 64 KB (256 x 256), three of 48 KB (256 x 128): with
+  // three, two tiles' copies are in flight while a third is read
+  static constexpr int NS = BN == 128 ? 3 : 2;
+  static constexpr int SMEM = NS * (TA + TB);
+  static_assert(SMEM <= 160 * 1024, "LDS");
 };
 
 __device__ __forceinline__ int slot(int r, int c) { return c ^ ((r / R256) % CPR); }
@@ -244,19 +250,25 @@ __global__ void __launch_bounds__(kk::NT, 1)
     Tile<E, S::NCB, TWO> tb;
     ta.init(al, m0, wave, lane);
     tb.init(bl, n0, wave, lane);
-    // stage t % 2 of A at (t % 2) * TA, of B at 2 * TA + (t % 2) * TB
-    auto aoff = [&](int t) { return (t & 1) * TA; };
-    auto boff = [&](int t) { return 2 * TA + (t & 1) * TB; };
+    // stage t % NS of A at (t % NS) * TA, of B at NS * TA + (t % NS) * TB
+    constexpr int NS = S::NS;
+    constexpr int NC = S::NCA + S::NCB;  // copies per wave and tile
+    auto aoff = [&](int t) { return (t % NS) * TA; };
+    auto boff = [&](int t) { return NS * TA + (t % NS) * TB; };
     // the same memory as an LDS address, for the copies' M0
     const uint32_t l0 = static_cast<uint32_t>(reinterpret_cast<size_t>((__attribute__((address_space(3))) char*)smem));
 
-    // prologue: tile 0, wait, barrier, tile 1, first fragments
-    ta.issue(kt0 * BK, l0 + aoff(0), wave);
-    tb.issue(kt0 * BK, l0 + boff(0), wave);
-    dma::vm_wait<0>();
+    // prologue: tiles 0 .. NS - 2, wait for tile 0, barrier, tile NS - 1,
+    // first fragments
+#pragma unroll
+    for (int t = 0; t + 1 < NS; ++t) {
+      ta.issue((kt0 + t) * BK, l0 + aoff(t), wave);
+      tb.issue((kt0 + t) * BK, l0 + boff(t), wave);
+    }
+    dma::vm_wait<(NS - 2) * NC>();
     dma::wave_barrier();
-    ta.issue((kt0 + 1) * BK, l0 + aoff(1), wave);
-    tb.issue((kt0 + 1) * BK, l0 + boff(1), wave);
+    ta.issue((kt0 + NS - 1) * BK, l0 + aoff(NS - 1), wave);
+    tb.issue((kt0 + NS - 1) * BK, l0 + boff(NS - 1), wave);
     Frags<MB, NB> f[2];
     read(smem + aoff(0), smem + boff(0), wm0, wn0, lane, 0, f[0]);
 
@@ -271,14 +283,15 @@ __global__ void __launch_bounds__(kk::NT, 1)
         mfma_all(f[s & 1], acc);
         __builtin_amdgcn_sched_barrier(0);
       });
-      // every wave done reading tile r; tile r + 1 landed (nothing else is in flight)
+      // every wave done reading tile r; tile r + 1 landed (the copies of
+      // tiles r + 2 .. r + NS - 1 may still be in flight)
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      dma::vm_wait<0>();
+      dma::vm_wait<(NS - 2) * NC>();
       dma::wave_barrier();
       read(smem + aoff(r + 1), smem + boff(r + 1), wm0, wn0, lane, 0, f[0]);
       __builtin_amdgcn_sched_barrier(0);
-      // last k step of tile r; its stage refills with tile r + 2
-      mfma_copies<E>(f[1], acc, ta, tb, (kt0 + r + 2) * BK, l0 + ao, l0 + bo, wave);
+      // last k step of tile r; its stage refills with tile r + NS
+      mfma_copies<E>(f[1], acc, ta, tb, (kt0 + r + NS) * BK, l0 + ao, l0 + bo, wave);
     }
     {
       // the last tile; its first fragments are in f[0]
