@@ -480,7 +480,8 @@ int o5_f32_to_bf16(size_t n, const float* src, uint16_t* dst, void* stream);
  * 3 lstm_bwd_cell, 4 lstm_dw_gemm, 5 lstm_dx_gemm, 6 ppo_loss_grad (whole
  * call), 7 adam_step, 8 gae, 9 policy_sample (whole call), 10
  * reward_process, 11 obs_normalize, 12 prelstm_fwd, 13 prelstm_bwd (whole
- * calls).
+ * calls), 14 lstm_fwd_call (a whole o5_lstm_fwd call: one pair of events
+ * for all its steps, where site 0 adds a pair around each step's launch).
  * o5_ktimer_enable_sites(mask) does the same for the sites whose bit
  * (1 << site) is set in mask (0 stops recording): every recorded pair adds
  * two event packets to the stream, so a timed run can record only the sites

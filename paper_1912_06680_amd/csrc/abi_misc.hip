@@ -59,7 +59,7 @@ KTimer g_kt;
 const char* kSiteNames[kSiteCount] = {"lstm_fwd_gemm", "lstm_fwd_cell", "lstm_dh_gemm", "lstm_bwd_cell",
                                       "lstm_dw_gemm",  "lstm_dx_gemm",  "ppo_loss_grad", "adam_step",
                                       "gae",           "policy_sample", "reward_process",
-                                      "obs_normalize", "prelstm_fwd",   "prelstm_bwd"};
+                                      "obs_normalize", "prelstm_fwd",   "prelstm_bwd",   "lstm_fwd_call"};
 }  // namespace
 
 void ktimer_begin(int site, hipStream_t s) {

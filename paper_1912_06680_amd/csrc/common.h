@@ -64,6 +64,7 @@ enum KSite {
   kSiteObsNorm,
   kSitePreFwd,
   kSitePreBwd,
+  kSiteLstmFwdCall,  // the whole o5_lstm_fwd call (all T steps)
   kSiteCount
 };
 // When timing is on, record an event on `s` before / after a launch site.

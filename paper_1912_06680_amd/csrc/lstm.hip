@@ -680,13 +680,17 @@ extern "C" int o5_lstm_fwd(o5_dtype dt, int T, int B, int D, int H, const void* 
   O5_CHECK(aligned16(ws), O5_E_ALIGN, "o5_lstm_fwd: ws is not 16-byte aligned");
   char* wsp = static_cast<char*>(ws);
   hipStream_t s = as_stream(stream);
-  if (dt == O5_BF16)
-    return lstm_fwd_impl<uint16_t>(T, B, D, H, static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(Wx),
-                                   static_cast<const uint16_t*>(Wh), b, h0, c0, reset, static_cast<uint16_t*>(h), c,
-                                   static_cast<uint16_t*>(gates), wsp, w, s);
-  return lstm_fwd_impl<float>(T, B, D, H, static_cast<const float*>(x), static_cast<const float*>(Wx),
-                              static_cast<const float*>(Wh), b, h0, c0, reset, static_cast<float*>(h), c,
-                              static_cast<float*>(gates), wsp, w, s);
+  ktimer_begin(kSiteLstmFwdCall, s);
+  const int rc =
+      dt == O5_BF16
+          ? lstm_fwd_impl<uint16_t>(T, B, D, H, static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(Wx),
+                                    static_cast<const uint16_t*>(Wh), b, h0, c0, reset, static_cast<uint16_t*>(h), c,
+                                    static_cast<uint16_t*>(gates), wsp, w, s)
+          : lstm_fwd_impl<float>(T, B, D, H, static_cast<const float*>(x), static_cast<const float*>(Wx),
+                                 static_cast<const float*>(Wh), b, h0, c0, reset, static_cast<float*>(h), c,
+                                 static_cast<float*>(gates), wsp, w, s);
+  ktimer_end(kSiteLstmFwdCall, s);
+  return rc;
 }
 
 extern "C" size_t o5_lstm_bptt_workspace_bytes(o5_dtype dt, int T, int B, int D, int H) {
