@@ -799,17 +799,22 @@ def main():
     # then the K timed steps with events around the dominant kernel only
     A1 = sum(cfg.head_sizes) + 1
     n = st.n_params
+    # the bf16 step passes the heads' gradient in factored form: the
+    # recurrent product of each step t < T-1 also takes the heads' K = ld
+    # columns, the last step has those alone (T launches), the loss call
+    # writes P (ld bf16 per row) instead of dh, and the cell reads no dh
+    ld = st.ld if st.bf16 else 0
     flops = {
         "lstm_fwd_gemm": 2.0 * B * 4 * H * (D + H),
-        "lstm_dh_gemm": 2.0 * B * H * 4 * H,
+        "lstm_dh_gemm": (2.0 * B * H * ((T - 1) * (4 * H + ld) + ld) / T) if st.bf16 else 2.0 * B * H * 4 * H,
         "lstm_dw_gemm": 2.0 * 4 * H * (D + H) * T * B,
     }
     bytes_ = {
         "lstm_fwd_cell": 34.0 * B * H,
-        "lstm_bwd_cell": 40.0 * B * H,
+        "lstm_bwd_cell": (36.0 if st.bf16 else 40.0) * B * H,
         "adam_step": 30.0 * n,
         "gae": 17.0 * cfg.L * cfg.S + 4.0 * cfg.S,
-        "ppo_loss_grad": (2 * 2.0 * H + 4.0 * H + 4.0 * A1 + 16.0) * T * B,
+        "ppo_loss_grad": (2 * 2.0 * H + (2.0 * ld if st.bf16 else 4.0 * H) + 4.0 * A1 + 16.0) * T * B,
     }
     copy_gbs = stream_copy_gbs()
     log(f"streaming copy: {copy_gbs:.0f} GB/s")

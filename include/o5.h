@@ -130,6 +130,22 @@ int o5_lstm_bptt(o5_dtype dt, int T, int B, int D, int H,
                  float* dWx, float* dWh, float* db, void* dx,
                  void* ws, size_t ws_bytes, void* stream);
 
+/* o5_lstm_bptt_factored -- o5_lstm_bptt (dt = O5_BF16 only) with the heads'
+ * gradient given in factored form, dh[t] = P[t] W^T (P [T*B, ld] and W
+ * [H, ld] bf16 as written by o5_ppo_loss_grad_factored over the N = T*B
+ * rows; ld a multiple of 64, at most 4096): each step's recurrent product
+ * takes [P_t | dG_{t+1}] against [W | W_h^T], so dh is never stored.  Same
+ * workspace query as o5_lstm_bptt.  O5_E_DTYPE for fp32, O5_E_SHAPE for a
+ * bad ld. */
+int o5_lstm_bptt_factored(o5_dtype dt, int T, int B, int D, int H,
+                          const void* x, const void* Wx, const void* Wh,
+                          const float* h0, const float* c0,
+                          const uint8_t* reset, const void* h, const float* c,
+                          const void* gates, const uint16_t* P,
+                          const uint16_t* W, int ld, const float* dhT,
+                          const float* dcT, float* dWx, float* dWh, float* db,
+                          void* dx, void* ws, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------------
  * o5_gae -- generalized advantage estimation over S rollout segments of L
  * steps (subsection "Optimizing the Policy": PPO with GAE, advantages
@@ -339,6 +355,38 @@ int o5_ppo_loss_grad(o5_dtype dt, int N, int H, int K, const int* head_sizes,
                      const uint8_t* avail, const o5_unit_head* unit, o5_ppo_hp hp,
                      float* stats, float* dh, float* dWp, float* dbp,
                      void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * The heads' gradient in factored form (bf16 only; the same loss and
+ * gradient as o5_ppo_loss_grad, appendix "Neural Network Architecture" and
+ * subsection "Optimizing the Policy").  dL/dh is a product of a narrow
+ * per-row gradient and the heads' weights, dh = P W^T, and the backward pass
+ * can form it inside its own recurrent product instead of reading a
+ * [N, H] fp32 dh:
+ *
+ *   P [N, ld] bf16: row n = [hi | lo], hi = bf16(g_n), lo = bf16(g_n - hi),
+ *       g_n = (dL/dz_n, then dL/dq_n for a unit head), zero-padded to ld/2
+ *   W [H, ld] bf16: row j = [w_j | w_j], w_j = (Wp[:, j], then Wq[:, j])
+ *
+ * o5_ppo_head_grad_ld returns ld for these heads (a multiple of 64; 0 if
+ * they are invalid).  o5_ppo_loss_grad_factored takes the arguments of
+ * o5_ppo_loss_grad, dt = O5_BF16, with P, W and ld in place of dh
+ * (O5_E_DTYPE for fp32, O5_E_SHAPE if ld is not the value above); its
+ * workspace query is o5_ppo_loss_grad_workspace_bytes.  stats, dWp, dbp and
+ * the unit head's gradients are those of o5_ppo_loss_grad bit for bit.
+ * ------------------------------------------------------------------------ */
+int o5_ppo_head_grad_ld(int H, int K, const int* head_sizes,
+                        const o5_unit_head* unit);
+int o5_ppo_loss_grad_factored(o5_dtype dt, int N, int H, int K,
+                              const int* head_sizes, const void* h,
+                              const void* Wp, const float* bp,
+                              const int32_t* act, const float* logp_old,
+                              const float* adv, const float* ret,
+                              const uint8_t* head_mask, const uint8_t* avail,
+                              const o5_unit_head* unit, o5_ppo_hp hp,
+                              float* stats, uint16_t* P, uint16_t* W, int ld,
+                              float* dWp, float* dbp,
+                              void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * o5_adam_step -- Adam with the per-parameter clip of each gradient element

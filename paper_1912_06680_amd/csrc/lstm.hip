@@ -250,7 +250,7 @@ __global__ void __launch_bounds__(256) lstm_bwd_cell(
     const int bc = valid[i] ? b : 0;
     const size_t hj = static_cast<size_t>(bc) * H + j;
     const size_t row = static_cast<size_t>(bc) * G;
-    dhv[i] = Vec4<float>::load(dh_t + hj);
+    dhv[i] = dh_t ? Vec4<float>::load(dh_t + hj) : f4(0.f);
     exv[i] = dh_extra ? Vec4<float>::load(dh_extra + hj) : f4(0.f);
 #pragma unroll
     for (int q = 0; q < NS; ++q) recv[i][q] = (rec && q < S) ? Vec4<float>::load(rec + q * sstride + hj) : f4(0.f);
@@ -555,7 +555,10 @@ template <typename E>
 static int lstm_bptt_impl(int T, int B, int D, int H, const E* x, const E* Wx, const E* Wh, const float* h0,
                           const float* c0, const uint8_t* reset, const E* h, const float* c, const E* gates,
                           const float* dh, const float* dhT, const float* dcT, float* dWx, float* dWh, float* db,
-                          E* dx, char* ws, const BwdWs& w, hipStream_t s) {
+                          E* dx, char* ws, const BwdWs& w, hipStream_t s, const E* P = nullptr,
+                          const E* Wf = nullptr, int ldp = 0) {
+  // P, Wf (bf16 only): the heads' gradient in factored form, dh_t = P_t Wf^T
+  // with P [T*B][ldp] and Wf [H][ldp], instead of dh
   constexpr bool kBf = sizeof(E) == 2;
   const size_t BH = static_cast<size_t>(B) * H;
   const size_t BG = static_cast<size_t>(B) * 4 * H;
@@ -583,9 +586,31 @@ static int lstm_bptt_impl(int T, int B, int D, int H, const E* x, const E* Wx, c
   auto cell = w.plan_dh.splits <= 2 ? lstm_bwd_cell<E, 2>
               : w.plan_dh.splits <= 8 ? lstm_bwd_cell<E, 8>
                                       : lstm_bwd_cell<E, 16>;
+  const bool fact = P != nullptr;
   for (int t = T - 1; t >= 0; --t) {
     const float* recp = nullptr;
-    if (t < T - 1) {
+    int S = w.plan_dh.splits;  // partial sums the cell adds
+    if (fact) {
+      if constexpr (kBf) {
+        // R = [P_t | dG_{t+1}] . [Wf | W_h^T]^T: the heads' dh_t plus, for the
+        // rows whose state carried into step t + 1 (the reset mask zeroes the
+        // second source's rows), dG_{t+1} W_h; the last step has the first
+        // part only
+        const int K = t < T - 1 ? ldp + 4 * H : ldp;
+        const uint8_t* rn = (reset && t < T - 1) ? reset + static_cast<size_t>(t + 1) * B : nullptr;
+        KRows2<E> al{P + static_cast<size_t>(t) * B * ldp, t < T - 1 ? dG + (t + 1) * BG : nullptr, rn, ldp,
+                     t < T - 1 ? 4 * H : 0, ldp, K, B};
+        KRows2<E> bl{Wf, t < T - 1 ? WhT : nullptr, nullptr, ldp, t < T - 1 ? 4 * H : 0, ldp, K, H};
+        EpiStoreF32 epi{rec, H, BH};
+        GemmPlan plan = w.plan_dh;
+        if (t == T - 1) plan.splits = 1;
+        S = plan.splits;
+        ktimer_begin(kSiteLstmDhGemm, s);
+        run_gemm(plan, al, bl, epi, B, H, K, s);
+        ktimer_end(kSiteLstmDhGemm, s);
+        recp = rec;
+      }
+    } else if (t < T - 1) {
       // R = dG_{t+1} . W_h :  A(i=b, k=n) = dG_{t+1}[b, n];  B(j, k=n) = W_h[n, j]
       KRows2<E> al{dG + (t + 1) * BG, nullptr, nullptr, 4 * H, 0, 4 * H, 4 * H, B};
       EpiStoreF32 epi{rec, H, BH};
@@ -601,12 +626,13 @@ static int lstm_bptt_impl(int T, int B, int D, int H, const E* x, const E* Wx, c
       recp = rec;
     }
     const uint8_t* rt = reset ? reset + static_cast<size_t>(t) * B : nullptr;
-    const uint8_t* rn = (reset && t < T - 1) ? reset + static_cast<size_t>(t + 1) * B : nullptr;
+    // (the factored path has applied the next step's reset inside its product)
+    const uint8_t* rn = (reset && t < T - 1 && !fact) ? reset + static_cast<size_t>(t + 1) * B : nullptr;
     const float* dcin = t == T - 1 ? dcT : dc;
     const float* dhx = t == T - 1 ? dhT : nullptr;
     const float* cprev = t == 0 ? c0 : c + (t - 1) * BH;
     ktimer_begin(kSiteLstmBwdCell, s);
-    hipLaunchKernelGGL(cell, pw_grid, dim3(256), 0, s, B, H, w.plan_dh.splits, recp, rn, dh + t * BH, dhx,
+    hipLaunchKernelGGL(cell, pw_grid, dim3(256), 0, s, B, H, S, recp, rn, fact ? nullptr : dh + t * BH, dhx,
                        dcin, dc, gates + t * BG, c + t * BH, cprev, rt, dG + t * BG, dbpart, t < T - 1 ? 1 : 0, dGT,
                        w.ldt, t * w.Bp);
     ktimer_end(kSiteLstmBwdCell, s);
@@ -698,11 +724,12 @@ extern "C" size_t o5_lstm_bptt_workspace_bytes(o5_dtype dt, int T, int B, int D,
   return bwd_ws(dt, T, B, D, H).total;
 }
 
-extern "C" int o5_lstm_bptt(o5_dtype dt, int T, int B, int D, int H, const void* x, const void* Wx, const void* Wh,
-                            const float* h0, const float* c0, const uint8_t* reset, const void* h, const float* c,
-                            const void* gates, const float* dh, const float* dhT, const float* dcT, float* dWx,
-                            float* dWh, float* db, void* dx, void* ws, size_t ws_bytes, void* stream) {
-  int st = check_dims("o5_lstm_bptt", dt, T, B, D, H);
+// Validation shared by the two backward calls (all but the heads' gradient).
+static int bptt_check(const char* fn, o5_dtype dt, int T, int B, int D, int H, const void* x, const void* Wx,
+                      const void* Wh, const float* h0, const float* c0, const uint8_t* reset, const void* h,
+                      const float* c, const void* gates, const float* dhT, const float* dcT, float* dWx, float* dWh,
+                      float* db, void* dx, void* ws, size_t ws_bytes, BwdWs* w) {
+  int st = check_dims(fn, dt, T, B, D, H);
   if (st != O5_OK) return st;
   O5_PTR(x, "x");
   O5_PTR(Wx, "Wx");
@@ -713,17 +740,28 @@ extern "C" int o5_lstm_bptt(o5_dtype dt, int T, int B, int D, int H, const void*
   O5_PTR(h, "h");
   O5_PTR(c, "c");
   O5_PTR(gates, "gates");
-  O5_PTR(dh, "dh");
   O5_OPT_PTR(dhT, "dhT");
   O5_OPT_PTR(dcT, "dcT");
   O5_PTR(dWx, "dWx");
   O5_PTR(dWh, "dWh");
   O5_PTR(db, "db");
   O5_OPT_PTR(dx, "dx");
-  const BwdWs w = bwd_ws(dt, T, B, D, H);
-  O5_CHECK(ws != nullptr && ws_bytes >= w.total, O5_E_WORKSPACE,
-           "o5_lstm_bptt: workspace needs %zu bytes, got %zu", w.total, ws ? ws_bytes : static_cast<size_t>(0));
-  O5_CHECK(aligned16(ws), O5_E_ALIGN, "o5_lstm_bptt: ws is not 16-byte aligned");
+  *w = bwd_ws(dt, T, B, D, H);
+  O5_CHECK(ws != nullptr && ws_bytes >= w->total, O5_E_WORKSPACE, "%s: workspace needs %zu bytes, got %zu", fn,
+           w->total, ws ? ws_bytes : static_cast<size_t>(0));
+  O5_CHECK(aligned16(ws), O5_E_ALIGN, "%s: ws is not 16-byte aligned", fn);
+  return O5_OK;
+}
+
+extern "C" int o5_lstm_bptt(o5_dtype dt, int T, int B, int D, int H, const void* x, const void* Wx, const void* Wh,
+                            const float* h0, const float* c0, const uint8_t* reset, const void* h, const float* c,
+                            const void* gates, const float* dh, const float* dhT, const float* dcT, float* dWx,
+                            float* dWh, float* db, void* dx, void* ws, size_t ws_bytes, void* stream) {
+  BwdWs w;
+  const int st = bptt_check("o5_lstm_bptt", dt, T, B, D, H, x, Wx, Wh, h0, c0, reset, h, c, gates, dhT, dcT, dWx,
+                            dWh, db, dx, ws, ws_bytes, &w);
+  if (st != O5_OK) return st;
+  O5_PTR(dh, "dh");
   char* wsp = static_cast<char*>(ws);
   hipStream_t s = as_stream(stream);
   if (dt == O5_BF16)
@@ -735,4 +773,25 @@ extern "C" int o5_lstm_bptt(o5_dtype dt, int T, int B, int D, int H, const void*
                                static_cast<const float*>(Wh), h0, c0, reset, static_cast<const float*>(h), c,
                                static_cast<const float*>(gates), dh, dhT, dcT, dWx, dWh, db,
                                static_cast<float*>(dx), wsp, w, s);
+}
+
+extern "C" int o5_lstm_bptt_factored(o5_dtype dt, int T, int B, int D, int H, const void* x, const void* Wx,
+                                     const void* Wh, const float* h0, const float* c0, const uint8_t* reset,
+                                     const void* h, const float* c, const void* gates, const uint16_t* P,
+                                     const uint16_t* W, int ld, const float* dhT, const float* dcT, float* dWx,
+                                     float* dWh, float* db, void* dx, void* ws, size_t ws_bytes, void* stream) {
+  O5_CHECK(dt == O5_BF16, O5_E_DTYPE, "o5_lstm_bptt_factored: the factored gradient is bf16 only (dt=%d)",
+           static_cast<int>(dt));
+  BwdWs w;
+  const int st = bptt_check("o5_lstm_bptt_factored", dt, T, B, D, H, x, Wx, Wh, h0, c0, reset, h, c, gates, dhT,
+                            dcT, dWx, dWh, db, dx, ws, ws_bytes, &w);
+  if (st != O5_OK) return st;
+  O5_CHECK(ld >= 64 && ld % 64 == 0 && ld <= 4096, O5_E_SHAPE,
+           "o5_lstm_bptt_factored: ld=%d must be a multiple of 64 in 64..4096", ld);
+  O5_PTR(P, "P");
+  O5_PTR(W, "W");
+  return lstm_bptt_impl<uint16_t>(T, B, D, H, static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(Wx),
+                                  static_cast<const uint16_t*>(Wh), h0, c0, reset, static_cast<const uint16_t*>(h), c,
+                                  static_cast<const uint16_t*>(gates), nullptr, dhT, dcT, dWx, dWh, db,
+                                  static_cast<uint16_t*>(dx), static_cast<char*>(ws), w, as_stream(stream), P, W, ld);
 }

@@ -692,7 +692,10 @@ template <typename E>
 static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, const float* bp, const int32_t* act,
                     const float* logp_old, const float* adv, const float* ret, const uint8_t* mask,
                     const uint8_t* avail, const o5_unit_head* unit, o5_ppo_hp hp,
-                    float* stats, float* dh, float* dWp, float* dbp, char* ws, const PpoWs& w, hipStream_t s) {
+                    float* stats, float* dh, float* dWp, float* dbp, char* ws, const PpoWs& w, hipStream_t s,
+                    uint16_t* P_out = nullptr, uint16_t* W_out = nullptr) {
+  // bf16 path: the (hi, lo) pair and its repeated weights go to P_out and
+  // W_out when given (then dh may be null and is not formed)
   const int A1 = hm.A + 1;
   float* zpart = reinterpret_cast<float*>(ws + w.zpart);
   float* dz = reinterpret_cast<float*>(ws + w.dz);
@@ -703,7 +706,7 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
   uint16_t* dzhi = nullptr;
   uint16_t* dzlo = nullptr;
   if constexpr (sizeof(E) == 2) {
-    dzhi = reinterpret_cast<uint16_t*>(ws + w.dzp);
+    dzhi = P_out != nullptr ? P_out : reinterpret_cast<uint16_t*>(ws + w.dzp);
     dzlo = dzhi + w.ldh;
     dz = nullptr;  // the bf16 products read the (hi, lo) pair only
   }
@@ -751,7 +754,7 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
                     part, dzhi, dzlo, s);
   if constexpr (sizeof(E) == 2) {
     const int A1p = w.A1p, ldh = w.ldh;
-    uint16_t* wT = reinterpret_cast<uint16_t*>(ws + w.wT);
+    uint16_t* wT = W_out != nullptr ? W_out : reinterpret_cast<uint16_t*>(ws + w.wT);
     const uint16_t* Wq = nullptr;
     int d = 0;
     if (unit != nullptr) {
@@ -761,7 +764,7 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
       d = unit->d;
     }
     hipLaunchKernelGGL(pair_weights_t, dim3(H / 64, ldh / 64), dim3(256), 0, s, A1, A1p, ldh, H, Wp, Wq, d, wT);
-    {  // dh = [dz_hi dq_hi | dz_lo dq_lo] . [Wp Wq ; Wp Wq]  (K = 2 ldh), both operands K-contiguous
+    if (dh != nullptr) {  // dh = [dz_hi dq_hi | dz_lo dq_lo] . [Wp Wq ; Wp Wq]  (K = 2 ldh), both K-contiguous
       KRows2<uint16_t> al{dzhi, nullptr, nullptr, 2 * ldh, 0, 2 * ldh, 2 * ldh, N};
       KRows2<uint16_t> bl{wT, nullptr, nullptr, 2 * ldh, 0, 2 * ldh, 2 * ldh, H};
       EpiStoreF32 epi{dh, H, 0};
@@ -829,15 +832,16 @@ extern "C" size_t o5_ppo_loss_grad_workspace_bytes(o5_dtype dt, int N, int H, in
               : ppo_ws(dt, N, H, hm.A + 1).total;
 }
 
-extern "C" int o5_ppo_loss_grad(o5_dtype dt, int N, int H, int K, const int* head_sizes, const void* h, const void* Wp,
-                                const float* bp, const int32_t* act, const float* logp_old, const float* adv,
-                                const float* ret, const uint8_t* head_mask, const uint8_t* avail,
-                                const o5_unit_head* unit, o5_ppo_hp hp, float* stats, float* dh,
-                                float* dWp, float* dbp, void* ws, size_t ws_bytes, void* stream) {
-  HeadsMeta hm;
-  int st = check_heads("o5_ppo_loss_grad", dt, N, H, K, head_sizes, &hm);
+// Validation shared by the two loss calls (everything but the gradient
+// outputs that differ); fills hm and w.
+static int ppo_check(const char* fn, o5_dtype dt, int N, int H, int K, const int* head_sizes, const void* h,
+                     const void* Wp, const float* bp, const int32_t* act, const float* logp_old, const float* adv,
+                     const float* ret, const uint8_t* head_mask, const uint8_t* avail, const o5_unit_head* unit,
+                     o5_ppo_hp hp, float* stats, float* dWp, float* dbp, void* ws, size_t ws_bytes, HeadsMeta* hm,
+                     PpoWs* w) {
+  int st = check_heads(fn, dt, N, H, K, head_sizes, hm);
   if (st != O5_OK) return st;
-  O5_CHECK(hp.clip_eps >= 0.0f && hp.clip_eps < 1.0f, O5_E_ARG, "o5_ppo_loss_grad: clip_eps=%g must be in [0, 1)",
+  O5_CHECK(hp.clip_eps >= 0.0f && hp.clip_eps < 1.0f, O5_E_ARG, "%s: clip_eps=%g must be in [0, 1)", fn,
            hp.clip_eps);
   O5_PTR(h, "h");
   O5_PTR(Wp, "Wp");
@@ -849,27 +853,77 @@ extern "C" int o5_ppo_loss_grad(o5_dtype dt, int N, int H, int K, const int* hea
   O5_OPT_PTR(head_mask, "head_mask");
   O5_OPT_PTR(avail, "avail");
   if (unit != nullptr) {
-    st = check_unit("o5_ppo_loss_grad", hm, unit, true);
+    st = check_unit(fn, *hm, unit, true);
     if (st != O5_OK) return st;
   }
   O5_PTR(stats, "stats");
-  O5_PTR(dh, "dh");
   O5_PTR(dWp, "dWp");
   O5_PTR(dbp, "dbp");
-  const PpoWs w = unit ? ppo_ws(dt, N, H, hm.A + 1, hm.off[unit->head + 1] - hm.off[unit->head], unit->d)
-                       : ppo_ws(dt, N, H, hm.A + 1);
-  O5_CHECK(ws != nullptr && ws_bytes >= w.total, O5_E_WORKSPACE,
-           "o5_ppo_loss_grad: workspace needs %zu bytes, got %zu", w.total, ws ? ws_bytes : static_cast<size_t>(0));
-  O5_CHECK(aligned16(ws), O5_E_ALIGN, "o5_ppo_loss_grad: ws is not 16-byte aligned");
+  *w = unit ? ppo_ws(dt, N, H, hm->A + 1, hm->off[unit->head + 1] - hm->off[unit->head], unit->d)
+            : ppo_ws(dt, N, H, hm->A + 1);
+  O5_CHECK(ws != nullptr && ws_bytes >= w->total, O5_E_WORKSPACE, "%s: workspace needs %zu bytes, got %zu", fn,
+           w->total, ws ? ws_bytes : static_cast<size_t>(0));
+  O5_CHECK(aligned16(ws), O5_E_ALIGN, "%s: ws is not 16-byte aligned", fn);
+  return O5_OK;
+}
+
+extern "C" int o5_ppo_loss_grad(o5_dtype dt, int N, int H, int K, const int* head_sizes, const void* h, const void* Wp,
+                                const float* bp, const int32_t* act, const float* logp_old, const float* adv,
+                                const float* ret, const uint8_t* head_mask, const uint8_t* avail,
+                                const o5_unit_head* unit, o5_ppo_hp hp, float* stats, float* dh,
+                                float* dWp, float* dbp, void* ws, size_t ws_bytes, void* stream) {
+  HeadsMeta hm;
+  PpoWs w;
+  int st = ppo_check("o5_ppo_loss_grad", dt, N, H, K, head_sizes, h, Wp, bp, act, logp_old, adv, ret, head_mask,
+                     avail, unit, hp, stats, dWp, dbp, ws, ws_bytes, &hm, &w);
+  if (st != O5_OK) return st;
+  O5_PTR(dh, "dh");
   char* wsp = static_cast<char*>(ws);
   hipStream_t s = as_stream(stream);
   ktimer_begin(kSitePpo, s);
   if (dt == O5_BF16)
     st = ppo_impl<uint16_t>(N, H, hm, static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(Wp), bp, act,
-                              logp_old, adv, ret, head_mask, avail, unit, hp, stats, dh, dWp, dbp, wsp, w, s);
+                            logp_old, adv, ret, head_mask, avail, unit, hp, stats, dh, dWp, dbp, wsp, w, s);
   else
     st = ppo_impl<float>(N, H, hm, static_cast<const float*>(h), static_cast<const float*>(Wp), bp, act, logp_old, adv,
                          ret, head_mask, avail, unit, hp, stats, dh, dWp, dbp, wsp, w, s);
+  ktimer_end(kSitePpo, s);
+  return st;
+}
+
+extern "C" int o5_ppo_head_grad_ld(int H, int K, const int* head_sizes, const o5_unit_head* unit) {
+  HeadsMeta hm;
+  if (check_heads("o5_ppo_head_grad_ld", O5_BF16, 1, H, K, head_sizes, &hm) != O5_OK) return 0;
+  if (unit != nullptr &&
+      (unit->head < 0 || unit->head >= K || unit->d < 8 || unit->d > 512 || (unit->d & (unit->d - 1)) != 0))
+    return 0;
+  const PpoWs w = unit ? ppo_ws(O5_BF16, 1, H, hm.A + 1, hm.off[unit->head + 1] - hm.off[unit->head], unit->d)
+                       : ppo_ws(O5_BF16, 1, H, hm.A + 1);
+  return 2 * w.ldh;
+}
+
+extern "C" int o5_ppo_loss_grad_factored(o5_dtype dt, int N, int H, int K, const int* head_sizes, const void* h,
+                                         const void* Wp, const float* bp, const int32_t* act, const float* logp_old,
+                                         const float* adv, const float* ret, const uint8_t* head_mask,
+                                         const uint8_t* avail, const o5_unit_head* unit, o5_ppo_hp hp, float* stats,
+                                         uint16_t* P, uint16_t* W, int ld, float* dWp, float* dbp, void* ws,
+                                         size_t ws_bytes, void* stream) {
+  O5_CHECK(dt == O5_BF16, O5_E_DTYPE, "o5_ppo_loss_grad_factored: the factored gradient is bf16 only (dt=%d)",
+           static_cast<int>(dt));
+  HeadsMeta hm;
+  PpoWs w;
+  int st = ppo_check("o5_ppo_loss_grad_factored", dt, N, H, K, head_sizes, h, Wp, bp, act, logp_old, adv, ret,
+                     head_mask, avail, unit, hp, stats, dWp, dbp, ws, ws_bytes, &hm, &w);
+  if (st != O5_OK) return st;
+  O5_CHECK(ld == 2 * w.ldh, O5_E_SHAPE, "o5_ppo_loss_grad_factored: ld=%d, the heads need %d (o5_ppo_head_grad_ld)",
+           ld, 2 * w.ldh);
+  O5_PTR(P, "P");
+  O5_PTR(W, "W");
+  hipStream_t s = as_stream(stream);
+  ktimer_begin(kSitePpo, s);
+  st = ppo_impl<uint16_t>(N, H, hm, static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(Wp), bp, act,
+                          logp_old, adv, ret, head_mask, avail, unit, hp, stats, nullptr, dWp, dbp,
+                          static_cast<char*>(ws), w, s, P, W);
   ktimer_end(kSitePpo, s);
   return st;
 }

@@ -21,12 +21,12 @@ O5_BF16 = 1
 EXPORTED = (
     "o5_version", "o5_status_str", "o5_last_error",
     "o5_lstm_fwd_workspace_bytes", "o5_lstm_fwd",
-    "o5_lstm_bptt_workspace_bytes", "o5_lstm_bptt",
+    "o5_lstm_bptt_workspace_bytes", "o5_lstm_bptt", "o5_lstm_bptt_factored",
     "o5_gae", "o5_segments_to_samples",
     "o5_reward_process_workspace_bytes", "o5_reward_process",
     "o5_obs_normalize_workspace_bytes", "o5_obs_normalize", "o5_prelstm_fwd",
     "o5_prelstm_bwd_workspace_bytes", "o5_prelstm_bwd",
-    "o5_ppo_loss_grad_workspace_bytes", "o5_ppo_loss_grad",
+    "o5_ppo_loss_grad_workspace_bytes", "o5_ppo_loss_grad", "o5_ppo_head_grad_ld", "o5_ppo_loss_grad_factored",
     "o5_adam_step",
     "o5_policy_sample_workspace_bytes", "o5_policy_sample", "o5_policy_sample_static",
     "o5_f32_to_bf16",
@@ -87,6 +87,7 @@ _SIGS = {
     "o5_lstm_fwd": (_i, [_i, _i, _i, _i, _i] + [_vp] * 11 + [_sz, _vp]),
     "o5_lstm_bptt_workspace_bytes": (_sz, [_i, _i, _i, _i, _i]),
     "o5_lstm_bptt": (_i, [_i, _i, _i, _i, _i] + [_vp] * 17 + [_sz, _vp]),
+    "o5_lstm_bptt_factored": (_i, [_i, _i, _i, _i, _i] + [_vp] * 11 + [_i] + [_vp] * 7 + [_sz, _vp]),
     "o5_gae": (_i, [_i, _i, _vp, _vp, _vp, _f, _f, _vp, _vp, _vp]),
     "o5_segments_to_samples": (_i, [_i, _i, _i] + [_vp] * 6 + [_vp]),
     "o5_reward_process_workspace_bytes": (_sz, [_i, _i]),
@@ -98,6 +99,9 @@ _SIGS = {
     "o5_prelstm_bwd": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "o5_ppo_loss_grad_workspace_bytes": (_sz, [_i, _i, _i, _i, _vp, _vp]),
     "o5_ppo_loss_grad": (_i, [_i, _i, _i, _i, _vp] + [_vp] * 10 + [PpoHp] + [_vp] * 5 + [_sz, _vp]),
+    "o5_ppo_head_grad_ld": (_i, [_i, _i, _vp, _vp]),
+    "o5_ppo_loss_grad_factored": (_i, [_i, _i, _i, _i, _vp] + [_vp] * 10 + [PpoHp] + [_vp] * 3 + [_i] + [_vp] * 3
+                                  + [_sz, _vp]),
     "o5_adam_step": (_i, [_sz, _vp, _vp, _vp, _vp, _vp, AdamHp, _i, _vp]),
     "o5_policy_sample_workspace_bytes": (_sz, [_i, _i, _i, _i, _vp, _vp]),
     "o5_policy_sample": (_i, [_i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _u64, _u64, _vp, _vp, _vp, _vp, _sz,
@@ -203,6 +207,15 @@ def o5_lstm_bptt(dt, T, B, D, H, x, Wx, Wh, h0, c0, reset, h, c, gates, dh, dhT,
         _stream(stream)))
 
 
+def o5_lstm_bptt_factored(dt, T, B, D, H, x, Wx, Wh, h0, c0, reset, h, c, gates, P, W, ld, dhT, dcT,
+                          dWx, dWh, db, dx, ws, stream=None):
+    wp, wn = _ws(ws)
+    _check("o5_lstm_bptt_factored", lib().o5_lstm_bptt_factored(
+        dt, T, B, D, H, _p(x), _p(Wx), _p(Wh), _p(h0), _p(c0), _p(reset), _p(h), _p(c),
+        _p(gates), _p(P), _p(W), int(ld), _p(dhT), _p(dcT), _p(dWx), _p(dWh), _p(db), _p(dx), wp, wn,
+        _stream(stream)))
+
+
 def o5_gae(L, S, r, v, done, gamma, lam, adv, ret, stream=None):
     _check("o5_gae", lib().o5_gae(L, S, _p(r), _p(v), _p(done), float(gamma), float(lam),
                                   _p(adv), _p(ret), _stream(stream)))
@@ -262,6 +275,21 @@ def o5_ppo_loss_grad(dt, N, H, head_sizes, h, Wp, bp, act, logp_old, adv, ret, h
         dt, N, H, len(head_sizes), _heads(head_sizes), _p(h), _p(Wp), _p(bp), _p(act),
         _p(logp_old), _p(adv), _p(ret), _p(head_mask), _p(avail), _unit(unit), hp, _p(stats), _p(dh), _p(dWp),
         _p(dbp), wp, wn, _stream(stream)))
+
+
+def o5_ppo_head_grad_ld(H, head_sizes, unit=None):
+    return lib().o5_ppo_head_grad_ld(H, len(head_sizes), _heads(head_sizes), _unit(unit))
+
+
+def o5_ppo_loss_grad_factored(dt, N, H, head_sizes, h, Wp, bp, act, logp_old, adv, ret, head_mask,
+                              clip_eps, vf_coef, ent_coef, stats, P, W, ld, dWp, dbp, ws, stream=None,
+                              avail=None, unit=None):
+    wp, wn = _ws(ws)
+    hp = PpoHp(clip_eps, vf_coef, ent_coef)
+    _check("o5_ppo_loss_grad_factored", lib().o5_ppo_loss_grad_factored(
+        dt, N, H, len(head_sizes), _heads(head_sizes), _p(h), _p(Wp), _p(bp), _p(act),
+        _p(logp_old), _p(adv), _p(ret), _p(head_mask), _p(avail), _unit(unit), hp, _p(stats), _p(P), _p(W),
+        int(ld), _p(dWp), _p(dbp), wp, wn, _stream(stream)))
 
 
 def o5_adam_step(n, p, m, v, g, p_bf16, lr, beta1, beta2, eps, clip_k, step, stream=None):

@@ -5,7 +5,10 @@ Policy"): GAE over each 256-step segment, the cut into 16-step samples, the
 LSTM forward pass from each sample's stored state, the heads with the PPO
 loss and its gradient, truncated BPTT, and Adam with the per-parameter clip.
 This module only allocates device buffers (torch) and calls the library in
-order on one stream; all arithmetic runs in libo5's kernels.
+order on one stream; all arithmetic runs in libo5's kernels.  On the bf16
+path the heads hand their gradient to the backward pass in factored form
+(dh = P W^T, o5_ppo_loss_grad_factored and o5_lstm_bptt_factored), so the
+[T*B, H] fp32 dh is never stored; the fp32 path passes dh itself.
 
 Parameter storage: one flat fp32 master vector in the order
 (W_x, W_h, b, W_p, b_p), each row-major, with a flat bf16 mirror for the bf16
@@ -79,7 +82,12 @@ class PPOStep:
         self.h = torch.empty((T, B, H), **edt)
         self.c = torch.empty((T, B, H), **f32)
         self.gates = torch.empty((T, B, 4 * H), **edt)
-        self.dh = torch.empty((self.N, H), **f32)
+        if self.bf16:
+            self.ld = o5.o5_ppo_head_grad_ld(H, self.heads)
+            self.hgP = torch.empty((self.N, self.ld), dtype=torch.bfloat16, device=device)
+            self.hgW = torch.empty((H, self.ld), dtype=torch.bfloat16, device=device)
+        else:
+            self.dh = torch.empty((self.N, H), **f32)
         self.stats = torch.empty(8, **f32)
         ws = max(o5.o5_lstm_fwd_workspace_bytes(self.dt, T, B, D, H),
                  o5.o5_lstm_bptt_workspace_bytes(self.dt, T, B, D, H),
@@ -123,11 +131,20 @@ class PPOStep:
                                   self.reset, stream)
         o5.o5_lstm_fwd(self.dt, T, B, D, H, self.x, W["Wx"], W["Wh"], self.P["b"], self.h0, self.c0,
                        self.reset, self.h, self.c, self.gates, self.ws, stream)
-        o5.o5_ppo_loss_grad(self.dt, self.N, H, self.heads, self.h, W["Wp"], self.P["bp"], self.act,
-                            self.logp_old, self.adv_s, self.ret_s, None, c.clip_eps, c.vf_coef, c.ent_coef,
-                            self.stats, self.dh, G["Wp"], G["bp"], self.ws, stream)
-        o5.o5_lstm_bptt(self.dt, T, B, D, H, self.x, W["Wx"], W["Wh"], self.h0, self.c0, self.reset,
-                        self.h, self.c, self.gates, self.dh, None, None, G["Wx"], G["Wh"], G["b"], None,
-                        self.ws, stream)
+        if self.bf16:
+            o5.o5_ppo_loss_grad_factored(self.dt, self.N, H, self.heads, self.h, W["Wp"], self.P["bp"], self.act,
+                                         self.logp_old, self.adv_s, self.ret_s, None, c.clip_eps, c.vf_coef,
+                                         c.ent_coef, self.stats, self.hgP, self.hgW, self.ld, G["Wp"], G["bp"],
+                                         self.ws, stream)
+            o5.o5_lstm_bptt_factored(self.dt, T, B, D, H, self.x, W["Wx"], W["Wh"], self.h0, self.c0, self.reset,
+                                     self.h, self.c, self.gates, self.hgP, self.hgW, self.ld, None, None, G["Wx"],
+                                     G["Wh"], G["b"], None, self.ws, stream)
+        else:
+            o5.o5_ppo_loss_grad(self.dt, self.N, H, self.heads, self.h, W["Wp"], self.P["bp"], self.act,
+                                self.logp_old, self.adv_s, self.ret_s, None, c.clip_eps, c.vf_coef, c.ent_coef,
+                                self.stats, self.dh, G["Wp"], G["bp"], self.ws, stream)
+            o5.o5_lstm_bptt(self.dt, T, B, D, H, self.x, W["Wx"], W["Wh"], self.h0, self.c0, self.reset,
+                            self.h, self.c, self.gates, self.dh, None, None, G["Wx"], G["Wh"], G["b"], None,
+                            self.ws, stream)
         o5.o5_adam_step(self.n_params, self.p32, self.m, self.v, self.g, self.p16, c.lr, c.beta1, c.beta2,
                         c.adam_eps, c.clip_k, self.step_count, stream)

@@ -141,6 +141,36 @@ static void check_heads_and_sampler() {
         ++g_checks;
       }
   }
+  // the factored loss and backward calls: bf16 only, ld as the heads need
+  {
+    const o5_ppo_hp hp{0.2f, 1.0f, 0.01f};
+    const int ld = o5_ppo_head_grad_ld(4096, 4, heads, nullptr);
+    EXPECT(ld == 256);
+    o5_unit_head u{1, 128, P(), F(), P(), F(), F()};
+    EXPECT(o5_ppo_head_grad_ld(4096, 4, heads, &u) == 512);
+    EXPECT(o5_ppo_head_grad_ld(4096, 4, nullptr, nullptr) == 0);
+    EXPECT(o5_ppo_head_grad_ld(-1, 4, heads, nullptr) == 0);
+    const size_t need = o5_ppo_loss_grad_workspace_bytes(O5_BF16, 2048, 4096, 4, heads, nullptr);
+    uint16_t* p16 = static_cast<uint16_t*>(P());
+    EXPECT(o5_ppo_loss_grad_factored(O5_F32, 2048, 4096, 4, heads, P(), P(), F(), static_cast<int32_t*>(P()), F(),
+                                     F(), F(), U8(), nullptr, nullptr, hp, F(), p16, p16, ld, F(), F(), P(), need,
+                                     nullptr) == O5_E_DTYPE);
+    EXPECT(o5_ppo_loss_grad_factored(O5_BF16, 2048, 4096, 4, heads, P(), P(), F(), static_cast<int32_t*>(P()), F(),
+                                     F(), F(), U8(), nullptr, nullptr, hp, F(), p16, p16, ld + 64, F(), F(), P(), need,
+                                     nullptr) == O5_E_SHAPE);
+    EXPECT(o5_ppo_loss_grad_factored(O5_BF16, 2048, 4096, 4, heads, P(), P(), F(), static_cast<int32_t*>(P()), F(),
+                                     F(), F(), U8(), nullptr, nullptr, hp, F(), nullptr, p16, ld, F(), F(), P(), need,
+                                     nullptr) == O5_E_NULL);
+    const size_t bneed = o5_lstm_bptt_workspace_bytes(O5_BF16, 16, 8, 64, 128);
+    EXPECT(o5_lstm_bptt_factored(O5_F32, 16, 8, 64, 128, P(), P(), P(), F(), F(), U8(), P(), F(), P(), p16, p16, 256,
+                                 nullptr, nullptr, F(), F(), F(), nullptr, P(), bneed, nullptr) == O5_E_DTYPE);
+    EXPECT(o5_lstm_bptt_factored(O5_BF16, 16, 8, 64, 128, P(), P(), P(), F(), F(), U8(), P(), F(), P(), p16, p16, 100,
+                                 nullptr, nullptr, F(), F(), F(), nullptr, P(), bneed, nullptr) == O5_E_SHAPE);
+    EXPECT(o5_lstm_bptt_factored(O5_BF16, 16, 8, 64, 128, P(), P(), P(), F(), F(), U8(), P(), F(), P(), p16, p16, 256,
+                                 nullptr, nullptr, F(), F(), F(), nullptr, P(), bneed - 1, nullptr) == O5_E_WORKSPACE);
+    EXPECT(o5_lstm_bptt_factored(O5_BF16, 16, 8, 64, 128, P(), P(), P(), F(), F(), U8(), P(), F(), P(), nullptr, p16,
+                                 256, nullptr, nullptr, F(), F(), F(), nullptr, P(), bneed, nullptr) == O5_E_NULL);
+  }
   // many large heads: the total is capped
   int wide[8];
   for (int& w : wide) w = INT_MAX / 4;
