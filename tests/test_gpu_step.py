@@ -7,7 +7,7 @@ import torch
 
 from oracle.adam import adam_step
 from oracle.step import flatten, ppo_step, unflatten
-from paper_1912_06680_amd import synth
+from paper_1912_06680_amd import o5, synth
 from paper_1912_06680_amd.step import PARAM_ORDER, PPOStep
 from tests.behaviour import oracle_behaviour
 from tests.gpu_util import TOL_BF16, TOL_F32, assert_close, assert_close_both, banner, host, need_gpu
@@ -292,3 +292,52 @@ def test_full_size_step_is_deterministic():
     for k in outs[0]:
         assert torch.equal(outs[0][k], outs[1][k]), k
     assert torch.isfinite(outs[0]["stats"]).all()
+
+
+def test_full_size_backward_is_additive_over_samples():
+    """At the benchmark's shape (B = 2048 x T = 16, D = H = 4096, bf16, in the
+    launch configuration bench.py times) the weight gradients are a sum over
+    samples, a property that holds at any size: the step's backward pass over
+    all 2048 samples equals the sum of the same call over samples 0..1023
+    and 1024..2047 (each from the step's own forward outputs and factored
+    head gradient), up to the order of the fp32 sums.  The halves run in
+    another launch configuration (another K split of the recurrent product,
+    half the weight-gradient product's K), and the B = 1024 backward pass is
+    compared with the oracle in tests/test_gpu_lstm.py."""
+    need_gpu()
+    cfg = synth.CONFIGS["full4096"]
+    T, B, D, H = cfg.T, cfg.B, cfg.D, cfg.H
+    banner(f"full-size additivity over samples: B={B} T={T} D={D} H={H} {cfg.dtype}")
+    inp = synth.make_inputs(cfg, 0)
+    rng = np.random.Generator(np.random.PCG64(4))
+    N = T * B
+    act = np.stack([rng.integers(0, n, N) for n in cfg.head_sizes], axis=1).astype(np.int32)
+    logp_old = (rng.standard_normal(N) - 8.0).astype(np.float32)
+    values = rng.standard_normal((cfg.L + 1, cfg.S)).astype(np.float32)
+    st = PPOStep(cfg)
+    st.load_x(inp["x"])
+    st.load_rollout(inp["h0"], inp["c0"], inp["rewards"], inp["dones"], values, act, logp_old)
+    st.load_params({k: inp[k] for k in PARAM_ORDER})
+    st.run()
+    st.load_params({k: inp[k] for k in PARAM_ORDER})   # the weights the step's passes used
+    torch.cuda.synchronize()
+    full = {k: st.G[k].clone() for k in ("Wx", "Wh", "b")}
+    Bh = B // 2
+    ws = torch.empty(o5.o5_lstm_bptt_workspace_bytes(st.dt, T, Bh, D, H), dtype=torch.uint8, device="cuda")
+    P3 = st.hgP.view(T, B, st.ld)
+    total = None
+    for half in (slice(0, Bh), slice(Bh, B)):
+        part = {"Wx": torch.empty((4 * H, D), device="cuda"), "Wh": torch.empty((4 * H, H), device="cuda"),
+                "b": torch.empty(4 * H, device="cuda")}
+        o5.o5_lstm_bptt_factored(st.dt, T, Bh, D, H, st.x[:, half].contiguous(), st.W["Wx"], st.W["Wh"],
+                                 st.h0[half].contiguous(), st.c0[half].contiguous(), st.reset[:, half].contiguous(),
+                                 st.h[:, half].contiguous(), st.c[:, half].contiguous(),
+                                 st.gates[:, half].contiguous(), P3[:, half].contiguous().view(T * Bh, st.ld),
+                                 st.hgW, st.ld, None, None, part["Wx"], part["Wh"], part["b"], None, ws)
+        torch.cuda.synchronize()
+        total = part if total is None else {k: total[k] + part[k] for k in total}
+    for k in ("Wx", "Wh", "b"):
+        err = float((total[k] - full[k]).abs().max() / full[k].abs().max())
+        print(f"    d{k}: max|sum of halves - full| / max|full| = {err:.2e}", flush=True)
+        assert err <= 1e-3, k
+
