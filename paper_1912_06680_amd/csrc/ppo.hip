@@ -585,7 +585,6 @@ struct PpoWs {
   UnitWs uw;  // the unit-selection head's scratch, at offset unit (if any)
   GemmPlan plan_z, plan_w, plan_h;
   int nblk, A1, A1p, ldh, wsplits;  // ldh: row length of the (hi, lo) pair, A1p + the unit head's dp
-  bool dwp_t;  // dWp as one product of the (hi, lo) pair with h (h read once)
   bool rows_t;  // the row kernel with one thread per row (ppo_rows_t)
   int nblk_t;   // its blocks (= partial rows)
 };
@@ -600,16 +599,15 @@ static PpoWs ppo_ws(o5_dtype dt, int N, int H, int A1, int unit_nk = 0, int unit
   // (the thread-per-row kernel stages every column of the pair: ldh <= 256)
   w.rows_t = w.ldh <= 256;
   w.nblk_t = cdiv(N, kRtRows);
-  w.dwp_t = bf && w.ldh <= 256;
   w.plan_z = plan_gemm(bf, N, A1, H);
-  w.plan_w = bf ? plan_gemm(true, A1, H, 2 * N) : plan_gemm(false, A1, H, N);
+  w.plan_w = plan_gemm(false, A1, H, N);  // fp32 dWp (bf16: the pair product below)
   w.plan_h = plan_gemm(bf, N, H, 2 * w.ldh);
   w.plan_h.splits = 1;
   w.wsplits = 1;
-  if (w.dwp_t) {
-    // M = 2 ldh (one or two 256-row tiles), N = H, K = N: split K so the
-    // grid has about 256 blocks, each with at least 8 K tiles of 32
-    const int tiles = cdiv(2 * w.ldh, 256) * cdiv(H, 256);
+  if (bf) {
+    // dWp: M = 2 A1p, N = H, K = N: split K so the grid has about 256
+    // blocks, each with at least 8 K tiles of 32
+    const int tiles = cdiv(2 * w.A1p, 256) * cdiv(H, 256);
     w.wsplits = std::max(1, std::min(cdiv(256, tiles), cdiv(N, 32) / 8));
   }
   size_t o = 0;
@@ -622,7 +620,7 @@ static PpoWs ppo_ws(o5_dtype dt, int N, int H, int A1, int unit_nk = 0, int unit
   w.sums = o;
   o += align_up(static_cast<size_t>(A1 + kStatCols) * 4);
   w.wpart = o;
-  o += align_up(w.dwp_t ? static_cast<size_t>(w.wsplits) * 2 * w.ldh * H * 4
+  o += align_up(bf ? static_cast<size_t>(w.wsplits) * 2 * w.A1p * H * 4
                         : static_cast<size_t>(w.plan_w.splits) * A1 * H * 4);
   w.dzp = w.wT = 0;
   if (bf) {
@@ -770,24 +768,18 @@ static int ppo_impl(int N, int H, const HeadsMeta& hm, const E* h, const E* Wp, 
       EpiStoreF32 epi{dh, H, 0};
       run_gemm(w.plan_h, al, bl, epi, N, H, 2 * ldh, s);
     }
-    if (w.dwp_t) {
-      // [dWp_hi ; dWp_lo] = pair^T . h  (M = 2 ldh rows: hi columns, then lo
-      // columns; N = H, K = N), both operands read I-contiguous (the row
-      // layouts of the pair and of h), split over K; then hi + lo per split
-      ICols2<uint16_t> al{dzhi, nullptr, nullptr, nullptr, 2 * ldh, 0, 2 * ldh, 2 * ldh, N, 0};
+    {
+      // [dWp_hi ; dWp_lo] = [dz_hi | dz_lo]^T . h  (M = 2 A1p rows: the hi
+      // logit columns of the pair, then its lo logit columns (a unit head's
+      // dq columns in between are skipped); N = H, K = N), both operands read
+      // I-contiguous (the row layouts of the pair and of h, h read once),
+      // split over K; then hi + lo per split
+      ICols2<uint16_t> al{dzhi, dzlo, dzlo, nullptr, 2 * ldh, 2 * ldh, A1p, 2 * A1p, N, N};
       ICols2<uint16_t> bl{h, nullptr, nullptr, nullptr, H, 0, H, H, N, 0};
-      EpiStoreF32 epi{wpart, H, static_cast<size_t>(2) * ldh * H};
-      launch_gemm_bf16_dma(al, bl, epi, 2 * ldh, H, N, w.wsplits, s);
+      EpiStoreF32 epi{wpart, H, static_cast<size_t>(2) * A1p * H};
+      launch_gemm_bf16_dma(al, bl, epi, 2 * A1p, H, N, w.wsplits, s);
       hipLaunchKernelGGL(sum_hilo_splits, dim3(cdiv(static_cast<long long>(A1) * H, 256)), dim3(256), 0, s,
-                         w.wsplits, A1, ldh, H, wpart, dWp);
-    } else {
-      // dWp = [dz_hi ; dz_lo]^T . [h ; h]  (K = 2N), split over K, fixed-order sum
-      ICols2<uint16_t> al{dzhi, dzhi, dzlo, nullptr, 2 * ldh, 2 * ldh, 0, A1p, 2 * N, N};
-      ICols2<uint16_t> bl{h, h, h, nullptr, H, H, 0, H, 2 * N, N};
-      EpiStoreF32 epi{wpart, H, static_cast<size_t>(A1) * H};
-      run_gemm(w.plan_w, al, bl, epi, A1, H, 2 * N, s);
-      hipLaunchKernelGGL(colsum_rows, dim3(cdiv(static_cast<long long>(A1) * H, 256)), dim3(256), 0, s,
-                         w.plan_w.splits, A1 * H, wpart, dWp);
+                         w.wsplits, A1, A1p, H, wpart, dWp);
     }
   } else {
     if (unit == nullptr) {  // dh = dz Wp  (fp32 FMA engine)
