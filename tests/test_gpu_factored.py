@@ -67,6 +67,9 @@ def _both_loss_calls(N, H, heads, seed, with_mask, with_avail, unit_d):
     ("ragged-avail", 1001, 256, (5, 3, 7), True, True, 0),
     ("unit-head", 2048, 512, (30, 40, 32, 4), False, True, 128),
     ("wide-heads", 500, 128, (100, 60, 30), True, False, 0),
+    # 1023 logits + value: the widest heads the call takes, 2048 pair columns
+    ("widest", 300, 64, (512, 511), True, False, 0),
+    ("unit-d512", 700, 128, (7, 9), True, True, 512),
 ])
 def test_factored_loss_matches_the_plain_call(name, N, H, heads, with_mask, with_avail, unit_d):
     need_gpu()
@@ -131,6 +134,7 @@ def _lstm_case(T, B, D, H, seed, p_reset):
 @pytest.mark.parametrize("T,B,D,H,heads,p_reset,with_dx", [
     (16, 256, 1024, 1024, HEADS, 0.05, True),
     (5, 77, 128, 192, (5, 3, 7), 0.2, False),
+    (1, 130, 64, 64, (4,), 0.5, True),
     (16, 1024, 4096, 4096, HEADS, 0.01, False),
 ])
 def test_factored_bptt_matches_the_dh_bptt(T, B, D, H, heads, p_reset, with_dx):
