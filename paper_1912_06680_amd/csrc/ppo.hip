@@ -372,16 +372,34 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
   const int nke = kext >= 0 ? hm.off[kext + 1] - hm.off[kext] : 0;
   const int e0 = kext >= 0 ? hm.off[kext] : 0;
   // stage the rows: element e = (r, a) of the block's [rows x A1] slice
-  // (the block's rows are contiguous in every source)
+  // (the block's rows are contiguous in every source), in groups of kGrp
+  // elements per thread whose loads are all issued before their LDS stores
   {
+    constexpr int kGrp = 8;
     const int ne = rows * A1;
-#pragma unroll 4
-    for (int e = t; e < ne; e += kRtThreads) {
-      const size_t g = static_cast<size_t>(n0) * A1 + e;
-      const int r = e / A1, a = e - r * A1;
-      float v = bp[a];
-      for (int s2 = 0; s2 < S; ++s2) v += zpart[s2 * sstride + g];
-      zs[r][a] = v;
+    const float* zp = zpart + static_cast<size_t>(n0) * A1;
+    for (int e0g = 0; e0g < ne; e0g += kGrp * kRtThreads) {
+      float v[kGrp];
+#pragma unroll
+      for (int q = 0; q < kGrp; ++q) {
+        const int e = e0g + t + q * kRtThreads;
+        v[q] = 0.0f;
+        if (e < ne) {
+          float acc = bp[e % A1] + zp[e];
+          for (int s2 = 1; s2 < S; ++s2) acc += zp[s2 * sstride + e];
+          v[q] = acc;
+        }
+      }
+      // (the unit head's columns come from zext below, written by other
+      // threads: no store here may race with those)
+#pragma unroll
+      for (int q = 0; q < kGrp; ++q) {
+        const int e = e0g + t + q * kRtThreads;
+        if (e < ne) {
+          const int r = e / A1, a = e - r * A1;
+          if (a < e0 || a >= e0 + nke) zs[r][a] = v[q];
+        }
+      }
     }
     for (int e = t; e < rows * nke; e += kRtThreads) {
       const int r = e / nke, u = e - r * nke;
@@ -515,12 +533,23 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
   if (dz != nullptr)
     for (int e = t; e < rows * A1; e += kRtThreads) dz[static_cast<size_t>(n0) * A1 + e] = zs[e / A1][e % A1];
   if (dz_hi != nullptr) {
-    for (int e = t; e < rows * ncol_hilo; e += kRtThreads) {
-      const int r = e / ncol_hilo, a = e - r * ncol_hilo;
-      const float d = zs[r][a];
-      const uint16_t hb = f32_to_bf16_bits(d);
-      dz_hi[static_cast<size_t>(n0 + r) * ld_hilo + a] = hb;
-      dz_lo[static_cast<size_t>(n0 + r) * ld_hilo + a] = f32_to_bf16_bits(d - bf16_bits_to_f32(hb));
+    // 8 columns of one row per item: two 16-byte stores (hi, lo)
+    const int cpr = ncol_hilo / 8;  // ncol_hilo is a multiple of 64
+    for (int c = t; c < rows * cpr; c += kRtThreads) {
+      const int r = c / cpr, a0 = (c - r * cpr) * 8;
+      uint32_t hw[4], lw[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float d0 = zs[r][a0 + 2 * j], d1 = zs[r][a0 + 2 * j + 1];
+        const uint16_t h0 = f32_to_bf16_bits(d0), h1 = f32_to_bf16_bits(d1);
+        const uint16_t l0 = f32_to_bf16_bits(d0 - bf16_bits_to_f32(h0));
+        const uint16_t l1 = f32_to_bf16_bits(d1 - bf16_bits_to_f32(h1));
+        hw[j] = h0 | (static_cast<uint32_t>(h1) << 16);
+        lw[j] = l0 | (static_cast<uint32_t>(l1) << 16);
+      }
+      const size_t o = static_cast<size_t>(n0 + r) * ld_hilo + a0;
+      *reinterpret_cast<uint4*>(dz_hi + o) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+      *reinterpret_cast<uint4*>(dz_lo + o) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
     }
   }
   // column sums over the block's rows, then its statistics, in row order
