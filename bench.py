@@ -260,6 +260,64 @@ def counter_table(fetch_dir, write_dir, mfma_dir, trace_dir, out_md, command):
     return rows
 
 
+def trace_summary(trace_dir, out_md, command, bench_log=None):
+    """The rocprofv3 --kernel-trace --stats summary of a bench.py --copy-ref
+    run as a table (every symbol's calls and durations), and, for the
+    forward GEMM, the average over the launches of the timed steps (the last
+    `steps` x T forward launches before the reference conversion) beside the
+    per-launch time bench.py printed for the same steps (from its JSON line
+    in bench_log)."""
+    import csv
+    import glob
+    stats = []
+    for f in glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True):
+        with open(f) as fh:
+            stats += list(csv.DictReader(fh))
+    rows = []
+    for f in glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True):
+        with open(f) as fh:
+            rows += list(csv.DictReader(fh))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    line = None
+    if bench_log:
+        with open(bench_log) as fh:
+            for ln in fh:
+                if ln.startswith("{"):
+                    line = json.loads(ln)
+    lines = ["# Kernel trace: the PPO optimizer step at H = 4096 (B = 2048 x T = 16, bf16), then the other workloads",
+             "", "Command (from the repository root, `TMPDIR=/tmp`, on one MI355X; the table by `bench.py "
+             "--trace-summary` on the CPU):", "", "```", command, "```", "",
+             "The run holds 2 warmup, 5 instrumented (an event pair around every launch site) and 5 timed steps, "
+             "then the other workloads (tiny and mid steps, LSTM forward + BPTT at B = 1024, rollout inference at "
+             "B = 4096); `--stats` pools every dispatch of a symbol, so a symbol that serves several shapes averages "
+             "over them (the counter table splits them by grid and phase)."]
+    if line is not None:
+        grid = lambda r: int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])  # noqa: E731
+        ref = _copy_ref_dispatch(rows, grid)
+        fwd = [r for r in rows if int(r["Dispatch_Id"]) < ref and "EpiLstmCell" in r["Kernel_Name"]
+               and grid(r) == 262144]
+        n = line["steps"] * line["config"]["seq_len"]
+        us = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in fwd]
+        timed, inst = us[-n:], us[-2 * n:-n]
+        lines += ["", f"The timed steps of this run under the profiler: {line['ms_per_step']:.2f} ms per step. The "
+                      f"dominant kernel, the fused forward GEMM (`gemm_kk<256, true, EpiLstmCell<bf16>, bf16>`, grid "
+                      f"262144): its {n} launches inside the timed steps average {sum(timed) / n:.1f} µs in this "
+                      f"trace, and bench.py's HIP events over the same steps gave "
+                      f"{1e3 * line['roofline']['ms_per_launch']:.1f} µs per launch (`roofline.ms_per_launch`); "
+                      f"the {n} launches of the instrumented pass, with an event pair around each, average "
+                      f"{sum(inst) / n:.1f} µs."]
+    lines += ["", "| kernel | calls | avg µs | min µs | max µs | total ms | % |", "|---|---:|---:|---:|---:|---:|---:|"]
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"])):
+        if float(r["Percentage"]) < 0.05:
+            continue
+        lines.append(f"| `{_short(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                     f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
+                     f"{float(r['TotalDurationNs']) / 1e6:.2f} | {float(r['Percentage']):.2f} |")
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def gpu_behaviour(st, inp):
     """Untimed: actions, log-probabilities and values of a perturbed policy,
     produced by the library itself (forward pass + sampler)."""
@@ -761,13 +819,19 @@ def main():
                     help="write profiles/traffic.json from two rocprofv3 --pmc runs and exit (no GPU)")
     ap.add_argument("--counter-table", nargs=5, metavar=("FETCH_DIR", "WRITE_DIR", "MFMA_DIR", "TRACE_DIR", "OUT_MD"),
                     help="write the per-kernel counter table from four rocprofv3 runs and exit (no GPU)")
-    ap.add_argument("--command", default="", help="the command recorded in the counter table")
+    ap.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "OUT_MD"),
+                    help="write the kernel-trace summary of a rocprofv3 --kernel-trace --stats run and exit (no GPU)")
+    ap.add_argument("--bench-log", default=None, help="the traced run's output (its JSON line), for --trace-summary")
+    ap.add_argument("--command", default="", help="the command recorded in the counter table or trace summary")
     args = ap.parse_args()
     if args.summarize_counters:
         summarize_counters(*args.summarize_counters)
         return
     if args.counter_table:
         counter_table(*args.counter_table, command=args.command)
+        return
+    if args.trace_summary:
+        trace_summary(*args.trace_summary, command=args.command, bench_log=args.bench_log)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU path "
