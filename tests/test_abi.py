@@ -89,6 +89,29 @@ def test_host_validation_errors(lib):
     assert "head_sizes[1]" in o5.o5_last_error()
 
 
+def test_factored_calls_validate_on_the_host(lib):
+    L = lib
+    heads = (ctypes.c_int * 4)(30, 8, 32, 4)
+    assert L.o5_ppo_head_grad_ld(4096, 4, heads, None) == 256
+    u = o5.UnitHead(1, 128, 16, 16, 16, 16, 16)
+    assert L.o5_ppo_head_grad_ld(4096, 4, heads, ctypes.byref(u)) == 512
+    assert L.o5_ppo_head_grad_ld(4096, 4, None, None) == 0
+    need = L.o5_ppo_loss_grad_workspace_bytes(1, 2048, 4096, 4, heads, None)
+    hp = o5.PpoHp(0.2, 1.0, 0.01)
+    # h, Wp, bp, act, logp_old, adv, ret; no head mask, availability or unit
+    # head (a host pointer); stats, P, W
+    args = [2048, 4096, 4, heads] + [16] * 7 + [None, None, None] + [hp, 16, 16, 16]
+    # fp32 is refused; ld must be the heads' value
+    assert L.o5_ppo_loss_grad_factored(0, *args, 256, 16, 16, 16, need, None) == 3
+    assert L.o5_ppo_loss_grad_factored(1, *args, 320, 16, 16, 16, need, None) == 2
+    assert "o5_ppo_head_grad_ld" in o5.o5_last_error()
+    bneed = L.o5_lstm_bptt_workspace_bytes(1, 16, 8, 64, 128)
+    bargs = [16, 8, 64, 128] + [16] * 11
+    assert L.o5_lstm_bptt_factored(0, *bargs, 256, *([16] * 6), 16, bneed, None) == 3
+    assert L.o5_lstm_bptt_factored(1, *bargs, 100, *([16] * 6), 16, bneed, None) == 2
+    assert L.o5_lstm_bptt_factored(1, *bargs, 256, *([16] * 6), 16, bneed - 1, None) == 5
+
+
 def test_workspace_queries_are_positive(lib):
     for dt in (0, 1):
         assert o5.o5_lstm_fwd_workspace_bytes(dt, 16, 2048, 4096, 4096) > 0
