@@ -9,8 +9,9 @@
 // MFMAs, measured a few percent slower overall.)
 //
 // Operands go global -> LDS by buffer loads with the LDS flag (16 bytes per
-// lane, written at M0 + 16 * lane) through NS stages of BK = 64 k (two of
-// 64 KB for 256 x 256 tiles, three of 48 KB for 256 x 128 ones): a copy
+// lane, written at M0 + 16 * lane) through stages of BK = 64 k (for 256 x
+// 256 tiles two of A and three of B, 32 KB each; for 256 x 128 tiles three
+// of each): a copy
 // instruction moves 8 rows x 128 bytes, i.e. whole cache lines (stages of 32
 // k move 16 half lines, which halves the rate at which the L2 feeds the CU;
 // a ring of more, smaller slots measured slower).  Each lane's byte offset
@@ -20,15 +21,14 @@
 //
 // The wave software-pipelines its fragments: those of k step s + 1 are read
 // while the MFMAs of step s run.  Before the last k step of tile r the wave
-// waits for its own copies of tile r + 1 (those of the NS - 2 tiles after it
-// may stay in flight), meets the other waves at the barrier (after which the
-// stage of tile r is free: every wave has finished reading it), reads the
-// first fragments of tile r + 1, and then issues the copies that refill the
-// stage with tile r + NS, interleaved with the MFMAs of that last k step.
-// The copies are inline asm, so the compiler neither waits for them before
-// LDS reads nor edits the explicit waits; each wave issues copies for tiles
-// 0 .. n + NS - 2 (those past the K range re-read the last tile into stages
-// no one reads again).
+// waits for its own copies of tile r + 1 (those of later tiles may stay in
+// flight), meets the other waves at the barrier (after which the stages of
+// tile r are free: every wave has finished reading them), reads the first
+// fragments of tile r + 1, and then issues the copies that refill them with
+// A tile r + NSA and B tile r + NSB, interleaved with the MFMAs of that last
+// k step.  The copies are inline asm, so the compiler neither waits for them
+// before LDS reads nor edits the explicit waits; copies past the K range
+// re-read the last tile into stages no one reads again.
 //
 // LDS layout of one operand stage: [rows][64 k] bf16, the 16-byte chunk c of
 // row r stored at slot c ^ ((r / 2) % 8), so the 16 rows of a fragment read
@@ -65,10 +65,15 @@ struct Shape {
   static constexpr int TB = BN * ROW_BYTES;        // B stage bytes
   static constexpr int NCA = TA / 1024 / NWAVES;   // copies per wave per A tile
   static constexpr int NCB = TB / 1024 / NWAVES;   // copies per wave per B tile
-  // stages: two of 64 KB (256 x 256), three of 48 KB (256 x 128): with
-  // three, two tiles' copies are in flight while a third is read
-  static constexpr int NS = BN == 128 ? 3 : 2;
-  static constexpr int SMEM = NS * (TA + TB);
+  // stages per operand: with NS of them, NS - 1 tiles' copies are in
+  // flight while one is read.  256 x 128 tiles: three of each (48 KB per
+  // stage pair); 256 x 256 tiles: two of A and three of B, 32 KB each,
+  // which fills the 160 KB (a third B stage: forward GEMM 471 against 478
+  // us, weight gradient 6.69 against 6.76 ms)
+  static constexpr int NSA = BN == 128 ? 3 : 2;
+  static constexpr int NSB = 3;
+  static_assert(NSB >= NSA && NSB <= NSA + 1, "the wait below assumes NSA <= NSB <= NSA + 1");
+  static constexpr int SMEM = NSA * TA + NSB * TB;
   static_assert(SMEM <= 160 * 1024, "LDS");
 };
 
@@ -190,8 +195,8 @@ __device__ __forceinline__ void mfma_all(const Frags<MB, NB>& f, f32x16_t (&acc)
 // barriers).
 template <typename E, int MB, int NB, int NCA, int NCB, bool TWO>
 __device__ __forceinline__ void mfma_copies(const Frags<MB, NB>& f, f32x16_t (&acc)[MB][NB],
-                                            const Tile<E, NCA, TWO>& ta, const Tile<E, NCB, TWO>& tb, int k0,
-                                            uint32_t as, uint32_t bs, int wave) {
+                                            const Tile<E, NCA, TWO>& ta, const Tile<E, NCB, TWO>& tb, int k0a,
+                                            int k0b, uint32_t as, uint32_t bs, int wave) {
   constexpr int NQ = NCA + NCB;
   dma::unroll<0, MB * NB>([&](auto I) {
     constexpr int m = decltype(I)::value;
@@ -202,9 +207,9 @@ __device__ __forceinline__ void mfma_copies(const Frags<MB, NB>& f, f32x16_t (&a
       constexpr int q = decltype(J)::value;
       if constexpr (q * MB * NB / NQ == m) {
         if constexpr (q < NCA)
-          ta.issue_one(k0, as, wave, q);
+          ta.issue_one(k0a, as, wave, q);
         else
-          tb.issue_one(k0, bs, wave, q - NCA);
+          tb.issue_one(k0b, bs, wave, q - NCA);
       }
     });
     __builtin_amdgcn_sched_barrier(0);
@@ -250,25 +255,29 @@ __global__ void __launch_bounds__(kk::NT, 1)
     Tile<E, S::NCB, TWO> tb;
     ta.init(al, m0, wave, lane);
     tb.init(bl, n0, wave, lane);
-    // stage t % NS of A at (t % NS) * TA, of B at NS * TA + (t % NS) * TB
-    constexpr int NS = S::NS;
-    constexpr int NC = S::NCA + S::NCB;  // copies per wave and tile
-    auto aoff = [&](int t) { return (t % NS) * TA; };
-    auto boff = [&](int t) { return NS * TA + (t % NS) * TB; };
+    // stage t % NSA of A at (t % NSA) * TA, of B at NSA * TA + (t % NSB) * TB
+    constexpr int NSA = S::NSA, NSB = S::NSB;
+    // copies a wave may leave in flight when it waits for a tile: those of
+    // the NSA - 2 A tiles and NSB - 2 B tiles issued after it (each
+    // iteration issues its A copies, then its B copies)
+    constexpr int AHEAD = (NSA - 2) * S::NCA + (NSB - 2) * S::NCB;
+    auto aoff = [&](int t) { return (t % NSA) * TA; };
+    auto boff = [&](int t) { return NSA * TA + (t % NSB) * TB; };
     // the same memory as an LDS address, for the copies' M0
     const uint32_t l0 = static_cast<uint32_t>(reinterpret_cast<size_t>((__attribute__((address_space(3))) char*)smem));
 
-    // prologue: tiles 0 .. NS - 2, wait for tile 0, barrier, tile NS - 1,
-    // first fragments
+    // prologue: A tiles 0 .. NSA - 2 and B tiles 0 .. NSB - 2 (A, then B,
+    // per tile), wait for tile 0, barrier, A tile NSA - 1 and B tile
+    // NSB - 1, first fragments
 #pragma unroll
-    for (int t = 0; t + 1 < NS; ++t) {
-      ta.issue((kt0 + t) * BK, l0 + aoff(t), wave);
+    for (int t = 0; t + 1 < NSB; ++t) {
+      if (t + 1 < NSA) ta.issue((kt0 + t) * BK, l0 + aoff(t), wave);
       tb.issue((kt0 + t) * BK, l0 + boff(t), wave);
     }
-    dma::vm_wait<(NS - 2) * NC>();
+    dma::vm_wait<AHEAD>();
     dma::wave_barrier();
-    ta.issue((kt0 + NS - 1) * BK, l0 + aoff(NS - 1), wave);
-    tb.issue((kt0 + NS - 1) * BK, l0 + boff(NS - 1), wave);
+    ta.issue((kt0 + NSA - 1) * BK, l0 + aoff(NSA - 1), wave);
+    tb.issue((kt0 + NSB - 1) * BK, l0 + boff(NSB - 1), wave);
     Frags<MB, NB> f[2];
     read(smem + aoff(0), smem + boff(0), wm0, wn0, lane, 0, f[0]);
 
@@ -284,14 +293,15 @@ __global__ void __launch_bounds__(kk::NT, 1)
         __builtin_amdgcn_sched_barrier(0);
       });
       // every wave done reading tile r; tile r + 1 landed (the copies of
-      // tiles r + 2 .. r + NS - 1 may still be in flight)
+      // later tiles may still be in flight)
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      dma::vm_wait<(NS - 2) * NC>();
+      dma::vm_wait<AHEAD>();
       dma::wave_barrier();
       read(smem + aoff(r + 1), smem + boff(r + 1), wm0, wn0, lane, 0, f[0]);
       __builtin_amdgcn_sched_barrier(0);
-      // last k step of tile r; its stage refills with tile r + NS
-      mfma_copies<E>(f[1], acc, ta, tb, (kt0 + r + NS) * BK, l0 + ao, l0 + bo, wave);
+      // last k step of tile r; its stages refill with A tile r + NSA and B
+      // tile r + NSB
+      mfma_copies<E>(f[1], acc, ta, tb, (kt0 + r + NSA) * BK, (kt0 + r + NSB) * BK, l0 + ao, l0 + bo, wave);
     }
     {
       // the last tile; its first fragments are in f[0]
