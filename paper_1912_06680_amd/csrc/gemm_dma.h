@@ -257,6 +257,19 @@ __device__ __forceinline__ void unroll(F&& f) {
 
 }  // namespace dma
 
+// Registers that an epilogue staging its tile through LDS loads ahead of the
+// tile (prefetch, before the last K tile where the engine allows); nothing
+// for the element-wise epilogues.
+template <class Epi, bool = (Epi::kTileSmem > 0)>
+struct EpiPre {
+  struct type {};
+};
+template <class Epi>
+struct EpiPre<Epi, true> {
+  static_assert(Epi::kThreads == dma::NT, "the tile epilogue maps the engines' 8 waves");
+  using type = typename Epi::Pre;
+};
+
 template <class AL, class BL, class Epi>
 __global__ void __launch_bounds__(dma::NT, 1)
     gemm_bf16_dma(AL al, BL bl, Epi epi, int M, int N, int K, int ktiles_per_split) {
@@ -336,8 +349,10 @@ __global__ void __launch_bounds__(dma::NT, 1)
   }
 
   if constexpr (Epi::kTileSmem > 0) {
+    typename EpiPre<Epi>::type pre;
+    epi.prefetch(pre, m0, n0, tid, M);
     wave_barrier();  // every wave is done with the stages
-    epi.template tile<MB, NB>(acc, smem, m0, n0, wave / WAVES_N, wn0, lane, tid, M);
+    epi.template tile<MB, NB>(acc, smem, m0, n0, wave / WAVES_N, wn0, lane, tid, M, pre);
   } else {
     // accumulator layout of a 32 x 32 block: lane holds column (lane & 31);
     // register e holds row 8*(e/4) + 4*(lane/32) + (e%4)

@@ -226,6 +226,7 @@ __global__ void __launch_bounds__(kk::NT, 1)
   constexpr int BM = S::BM, MB = S::MB, NB = S::NB, WM = S::WM, WN = S::WN, WAVES_N = S::WAVES_N;
   constexpr int TA = S::TA, TB = S::TB;
   static_assert(sizeof(E) == 2, "bf16 operands only");
+  static_assert(NT == dma::NT, "tile epilogues assume the 8 waves of both engines");
   static_assert(KSTEPS % 2 == 0, "the fragment double buffer assumes an even number of k steps");
   constexpr int SMEM = Epi::kTileSmem > S::SMEM ? Epi::kTileSmem : S::SMEM;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
@@ -249,6 +250,7 @@ __global__ void __launch_bounds__(kk::NT, 1)
     for (int b = 0; b < NB; ++b)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.0f;
+  typename EpiPre<Epi>::type pre;  // what the epilogue loads ahead
 
   if (n > 0) {
     Tile<E, S::NCA, TWO> ta;
@@ -303,6 +305,9 @@ __global__ void __launch_bounds__(kk::NT, 1)
       // tile r + NSB
       mfma_copies<E>(f[1], acc, ta, tb, (kt0 + r + NSA) * BK, (kt0 + r + NSB) * BK, l0 + ao, l0 + bo, wave);
     }
+    // the epilogue's own loads overlap the last tile's MFMAs (the wait
+    // below covers them)
+    if constexpr (Epi::kTileSmem > 0) epi.prefetch(pre, m0, n0, tid, M);
     {
       // the last tile; its first fragments are in f[0]
       const int ao = aoff(n - 1), bo = boff(n - 1);
@@ -313,11 +318,13 @@ __global__ void __launch_bounds__(kk::NT, 1)
       });
     }
     dma::vm_wait<0>();  // no copy outlives the loop
+  } else if constexpr (Epi::kTileSmem > 0) {
+    epi.prefetch(pre, m0, n0, tid, M);
   }
 
   if constexpr (Epi::kTileSmem > 0) {
     dma::wave_barrier();  // every wave is done with the stages
-    epi.template tile<MB, NB>(acc, smem, m0, n0, wave / WAVES_N, wn0, lane, tid, M);
+    epi.template tile<MB, NB>(acc, smem, m0, n0, wave / WAVES_N, wn0, lane, tid, M, pre);
   } else {
     // accumulator layout of a 32 x 32 block: lane holds column (lane & 31);
     // register e holds row 8*(e/4) + 4*(lane/32) + (e%4)

@@ -104,13 +104,23 @@ __device__ __forceinline__ float4 f4(float a) { return make_float4(a, a, a, a); 
 // two half-waves of a store hit disjoint banks), then every thread reads the
 // four gates of 4 consecutive units in each of its rows and finishes the
 // cell: c, h and the saved gates go straight to HBM in 16- and 8-byte
-// pieces and the pre-activations never do.  The previous cell state of a
-// pass is requested before the accumulators are parked, so its latency is
-// paid once per pass rather than once per row.
+// pieces and the pre-activations never do.  The bias and the previous cell
+// state of both passes are requested before the last K tile's MFMAs
+// (prefetch), so their latency hides behind them.
 template <typename E>
 struct EpiLstmCell {
   static constexpr int kPad = 72;
   static constexpr int kTileSmem = 4 * 128 * kPad * 4;  // 144 KB
+  static constexpr int kThreads = 512;                  // the block of both engines
+  static constexpr int kRS = kThreads / 16;             // rows per sweep
+  static constexpr int kNR = 128 / kRS;                 // sweeps per 128-row pass
+  // thread -> 4 consecutive hidden units (quad tid % 16) of rows tid / 16 +
+  // kRS * i of each pass
+  struct Pre {
+    float4 b[4];          // bias of gates i, f, g, o
+    float4 cp[2][kNR];    // previous cell state
+    int rs[2][kNR];       // the row's reset flag (its previous state counts as zero)
+  };
   const float* bias;
   const float* c_prev;
   const uint8_t* reset_t;
@@ -119,35 +129,40 @@ struct EpiLstmCell {
   E* gates_out;
   int H;
 
-  template <int MB, int NB>
-  __device__ __forceinline__ void tile(f32x16_t (&acc)[MB][NB], char* smem, int m0, int n0, int wm, int wn0, int lane,
-                                       int tid, int M) const {
-    static_assert(MB * 32 == 128, "expects 128-row wave tiles");
-    float* lds = reinterpret_cast<float*>(smem);
-    // thread -> 4 consecutive hidden units (quad uq) of rows rr, rr + RS, ...
-    const int uq = tid & 15;
+  __device__ __forceinline__ void prefetch(Pre& pre, int m0, int n0, int tid, int M) const {
+    const int j = (n0 >> 2) + 4 * (tid & 15);
     const int rr = tid >> 4;
-    const int RS = blockDim.x >> 4;   // rows covered per sweep
-    const int NR = 128 / RS;          // sweeps per 128-row pass (8 with 256 threads)
-    const int j = (n0 >> 2) + 4 * uq;  // first hidden unit of the quad
-    const size_t G = 4 * static_cast<size_t>(H);
-    const float4 bi = *reinterpret_cast<const float4*>(bias + j);
-    const float4 bf = *reinterpret_cast<const float4*>(bias + H + j);
-    const float4 bg = *reinterpret_cast<const float4*>(bias + 2 * H + j);
-    const float4 bo = *reinterpret_cast<const float4*>(bias + 3 * H + j);
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
-      // the previous cell state of this pass, all requests in flight at once
-      float4 cp[8];
+    for (int g = 0; g < 4; ++g) pre.b[g] = *reinterpret_cast<const float4*>(bias + g * H + j);
+    // (the flag and the state are loaded independently; the flag selects
+    // when the tile uses them, so no load waits for another)
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int bidx = m0 + p * 128 + rr + i * RS;
-        cp[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (i < NR && bidx < M) {
-          const bool keep = !(reset_t && reset_t[bidx]);
-          if (keep) cp[i] = *reinterpret_cast<const float4*>(c_prev + static_cast<size_t>(bidx) * H + j);
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+      for (int i = 0; i < kNR; ++i) {
+        const int bidx = m0 + p * 128 + rr + i * kRS;
+        pre.cp[p][i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        pre.rs[p][i] = 0;
+        if (bidx < M) {
+          pre.cp[p][i] = *reinterpret_cast<const float4*>(c_prev + static_cast<size_t>(bidx) * H + j);
+          if (reset_t) pre.rs[p][i] = reset_t[bidx];
         }
       }
+  }
+
+  template <int MB, int NB>
+  __device__ __forceinline__ void tile(f32x16_t (&acc)[MB][NB], char* smem, int m0, int n0, int wm, int wn0, int lane,
+                                       int tid, int M, const Pre& pre) const {
+    static_assert(MB * 32 == 128, "expects 128-row wave tiles");
+    float* lds = reinterpret_cast<float*>(smem);
+    const int uq = tid & 15;
+    const int rr = tid >> 4;
+    const int j = (n0 >> 2) + 4 * uq;  // first hidden unit of the quad
+    const size_t G = 4 * static_cast<size_t>(H);
+    const float4 bi = pre.b[0], bf = pre.b[1], bg = pre.b[2], bo = pre.b[3];
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const float4* cp = pre.cp[p];
       if (wm == p) {
 #pragma unroll
         for (int a = 0; a < MB; ++a)
@@ -162,10 +177,10 @@ struct EpiLstmCell {
       }
       __syncthreads();
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int row = rr + i * RS;
+      for (int i = 0; i < kNR; ++i) {
+        const int row = rr + i * kRS;
         const int bidx = m0 + p * 128 + row;
-        if (i < NR && bidx < M) {
+        if (bidx < M) {
           const float4 ai = *reinterpret_cast<const float4*>(lds + (0 * 128 + row) * kPad + 4 * uq);
           const float4 af = *reinterpret_cast<const float4*>(lds + (1 * 128 + row) * kPad + 4 * uq);
           const float4 ag = *reinterpret_cast<const float4*>(lds + (2 * 128 + row) * kPad + 4 * uq);
@@ -173,7 +188,8 @@ struct EpiLstmCell {
           float4 ig, fg, gg, og, c, h;
           const float* pai = &ai.x; const float* paf = &af.x; const float* pag = &ag.x; const float* pao = &ao.x;
           const float* pbi = &bi.x; const float* pbf = &bf.x; const float* pbg = &bg.x; const float* pbo = &bo.x;
-          const float* pcp = &cp[i].x;
+          const float4 cpi = pre.rs[p][i] ? make_float4(0.f, 0.f, 0.f, 0.f) : cp[i];
+          const float* pcp = &cpi.x;
           float* pig = &ig.x; float* pfg = &fg.x; float* pgg = &gg.x; float* pog = &og.x;
           float* pc = &c.x; float* ph = &h.x;
 #pragma unroll
