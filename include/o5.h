@@ -86,8 +86,9 @@ const char* o5_last_error(void);
  *
  * dt       GEMM input type: x, Wx, Wh and the output h are fp32 (O5_F32) or
  *          bf16 (O5_BF16).
- * T, B     steps and samples, >= 1.  D, H: input width and hidden units,
- *          multiples of 64, <= 65536.
+ * T, B     steps and samples, >= 1, B <= 2097088.  D, H: input width and
+ *          hidden units, multiples of 64, <= 65536.  T*B*4H and T*B*D below
+ *          2^31.
  * x        [T, B, D] dt.   Wx [4H, D] dt.   Wh [4H, H] dt.   b [4H] fp32.
  * h0, c0   [B, H] fp32, the start state of each sample.
  * reset    [T, B] uint8 or NULL (no resets): nonzero zeroes the carried

@@ -30,17 +30,22 @@ void clear_error();
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-#define O5_PTR(p, name)                                                        \
+// Pointer checks; the _IN forms name the entry point fn in the message (for
+// validation helpers shared by several entry points).
+#define O5_PTR_IN(fn, p, name)                                                 \
   do {                                                                         \
-    O5_CHECK((p) != nullptr, O5_E_NULL, "%s: argument '%s' is NULL", __func__, name); \
-    O5_CHECK(::o5::aligned16(p), O5_E_ALIGN, "%s: '%s' is not 16-byte aligned", __func__, name); \
+    O5_CHECK((p) != nullptr, O5_E_NULL, "%s: argument '%s' is NULL", fn, name); \
+    O5_CHECK(::o5::aligned16(p), O5_E_ALIGN, "%s: '%s' is not 16-byte aligned", fn, name); \
   } while (0)
 
-#define O5_OPT_PTR(p, name)                                                    \
+#define O5_OPT_PTR_IN(fn, p, name)                                             \
   do {                                                                         \
     if ((p) != nullptr)                                                        \
-      O5_CHECK(::o5::aligned16(p), O5_E_ALIGN, "%s: '%s' is not 16-byte aligned", __func__, name); \
+      O5_CHECK(::o5::aligned16(p), O5_E_ALIGN, "%s: '%s' is not 16-byte aligned", fn, name); \
   } while (0)
+
+#define O5_PTR(p, name) O5_PTR_IN(__func__, p, name)
+#define O5_OPT_PTR(p, name) O5_OPT_PTR_IN(__func__, p, name)
 
 // Returns O5_OK, or O5_E_HIP with a message if the last launch failed.
 int check_launch(const char* where);

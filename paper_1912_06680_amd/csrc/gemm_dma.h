@@ -1,14 +1,14 @@
 // bf16 MFMA GEMM fed by direct-to-LDS loads (gfx950):
 //   C[i, j] = sum_k A(i, k) * B(j, k)  (+ epilogue), fp32 accumulate.
 //
-// Pipeline: the K loop runs over tiles of 32 k held in a ring of 4 LDS
-// stages.  Tiles are copied global -> LDS by global_load_lds_dwordx4 (16
+// Pipeline: the K loop runs over tiles of 32 k held in a ring of STAGES (5)
+// LDS stages.  Tiles are copied global -> LDS by global_load_lds_dwordx4 (16
 // bytes per lane, written at M0 + 16 * lane), so no registers stage the
-// operands and three tiles are in flight while one is multiplied: each
+// operands and STAGES - 1 tiles are in flight while one is multiplied: each
 // iteration waits (vmcnt) for its own tile only, meets the other waves at one
-// barrier, issues the copy of the tile three steps ahead into the stage that
-// was just freed, and runs its MFMAs.  The four stages are four distinct LDS
-// arrays and the loop is unrolled by four, so the compiler can see that the
+// barrier, issues the copy of the tile STAGES - 1 steps ahead into the stage
+// that was just freed, and runs its MFMAs.  The stages are distinct LDS
+// arrays and the loop is unrolled by STAGES, so the compiler can see that the
 // copies in flight never alias the LDS reads (it would otherwise wait for
 // every copy before each read); the barrier is a bare s_barrier (a fence
 // would also wait for the copies).

@@ -390,7 +390,8 @@ __global__ void __launch_bounds__(256) lstm_bwd_cell(
 // s0[r] for r < split, else s1[r - split], and zero where mask[r] is set.
 // So dst row c is column c of [x] (split = T*B) or of the masked previous
 // hidden state h~ (s0 = h0, s1 = h, split = B, mask = reset).  Tiles of 64
-// columns x 64 source rows pass through LDS; 256 threads, 16-byte accesses.
+// columns x 64 source rows pass through LDS; 256 threads, 16-byte accesses;
+// blockIdx.x is the column tile, the source row tiles stride by gridDim.y.
 template <typename E>
 __global__ void __launch_bounds__(256) transpose_rows(int T, int B, int Bp, int C, const E* __restrict__ s0,
                                                       const E* __restrict__ s1, int split, int lds,
@@ -398,37 +399,51 @@ __global__ void __launch_bounds__(256) transpose_rows(int T, int B, int Bp, int 
                                                       size_t ldd) {
   static_assert(sizeof(E) == 2, "bf16 only");
   __shared__ __attribute__((aligned(16))) uint16_t tile[64][72];
-  const int k0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int c0 = blockIdx.x * 64;
   const int tid = threadIdx.x;
+  const int nkt = static_cast<int>((static_cast<long long>(T) * Bp + 63) / 64);
+  for (int kt = blockIdx.y; kt < nkt; kt += gridDim.y) {
+    const int k0 = kt * 64;
 #pragma unroll
-  for (int hh = 0; hh < 2; ++hh) {
-    const int kl = (tid >> 3) + 32 * hh, ch = tid & 7;
-    const int k = k0 + kl, c = c0 + ch * 8;
-    const int t = k / Bp, b = k - t * Bp;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (t < T && b < B && c < C) {
-      const int r = t * B + b;
-      if (!(mask && mask[r])) {
-        const E* src = r < split ? s0 + static_cast<size_t>(r) * lds : s1 + static_cast<size_t>(r - split) * lds;
-        v = *reinterpret_cast<const uint4*>(src + c);
+    for (int hh = 0; hh < 2; ++hh) {
+      const int kl = (tid >> 3) + 32 * hh, ch = tid & 7;
+      const int k = k0 + kl, c = c0 + ch * 8;
+      const int t = k / Bp, b = k - t * Bp;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (t < T && b < B && c < C) {
+        const int r = t * B + b;
+        if (!(mask && mask[r])) {
+          const E* src = r < split ? s0 + static_cast<size_t>(r) * lds : s1 + static_cast<size_t>(r - split) * lds;
+          v = *reinterpret_cast<const uint4*>(src + c);
+        }
+      }
+      *reinterpret_cast<uint4*>(&tile[kl][ch * 8]) = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int cl = (tid >> 3) + 32 * hh, ch = tid & 7;
+      const int c = c0 + cl;
+      if (c < C) {
+        uint4 v;
+        v.x = tile[ch * 8 + 0][cl] | (static_cast<uint32_t>(tile[ch * 8 + 1][cl]) << 16);
+        v.y = tile[ch * 8 + 2][cl] | (static_cast<uint32_t>(tile[ch * 8 + 3][cl]) << 16);
+        v.z = tile[ch * 8 + 4][cl] | (static_cast<uint32_t>(tile[ch * 8 + 5][cl]) << 16);
+        v.w = tile[ch * 8 + 6][cl] | (static_cast<uint32_t>(tile[ch * 8 + 7][cl]) << 16);
+        *reinterpret_cast<uint4*>(dst + static_cast<size_t>(c) * ldd + k0 + ch * 8) = v;
       }
     }
-    *reinterpret_cast<uint4*>(&tile[kl][ch * 8]) = v;
+    __syncthreads();  // the tile is rewritten by the next row tile
   }
-  __syncthreads();
-#pragma unroll
-  for (int hh = 0; hh < 2; ++hh) {
-    const int cl = (tid >> 3) + 32 * hh, ch = tid & 7;
-    const int c = c0 + cl;
-    if (c < C) {
-      uint4 v;
-      v.x = tile[ch * 8 + 0][cl] | (static_cast<uint32_t>(tile[ch * 8 + 1][cl]) << 16);
-      v.y = tile[ch * 8 + 2][cl] | (static_cast<uint32_t>(tile[ch * 8 + 3][cl]) << 16);
-      v.z = tile[ch * 8 + 4][cl] | (static_cast<uint32_t>(tile[ch * 8 + 5][cl]) << 16);
-      v.w = tile[ch * 8 + 6][cl] | (static_cast<uint32_t>(tile[ch * 8 + 7][cl]) << 16);
-      *reinterpret_cast<uint4*>(dst + static_cast<size_t>(c) * ldd + k0 + ch * 8) = v;
-    }
-  }
+}
+
+// B rounded up to 64, the time padding of the weight gradient's K: column
+// t * Bp + b of [x | h~]^T holds sample b of step t (zero for b >= B).
+static inline int time_pad(int B) { return cdiv(B, 64) * 64; }
+
+// Grid of transpose_rows for C columns and `rows` source rows.
+static inline dim3 transpose_grid(int C, long long rows) {
+  return dim3(cdiv(C, 64), static_cast<unsigned>(std::min<long long>((rows + 63) / 64, 65535)));
 }
 
 // ---------------------------------------------------------------- layouts
@@ -462,7 +477,7 @@ struct BwdWs {
 static BwdWs bwd_ws(o5_dtype dt, int T, int B, int D, int H) {
   BwdWs w;
   const bool bf = dt == O5_BF16;
-  w.Bp = cdiv(B, 64) * 64;
+  w.Bp = time_pad(B);
   w.nbc = w.Bp / kPwRows;  // cell row blocks; those past B only write zeros
   w.ldt = static_cast<size_t>(T) * w.Bp;
   w.plan_dh = plan_gemm(bf, B, H, 4 * H);
@@ -495,9 +510,14 @@ static BwdWs bwd_ws(o5_dtype dt, int T, int B, int D, int H) {
   return w;
 }
 
+constexpr int kMaxLstmB = 32767 * 64;
+
 static int check_dims(const char* fn, o5_dtype dt, int T, int B, int D, int H) {
   O5_CHECK(dt == O5_F32 || dt == O5_BF16, O5_E_DTYPE, "%s: unknown dtype %d", fn, static_cast<int>(dt));
   O5_CHECK(T >= 1 && B >= 1, O5_E_SHAPE, "%s: T=%d and B=%d must be >= 1", fn, T, B);
+  // the cell kernels' grids give a block of 32 rows to each y index (< 65535
+  // after B is padded to 64)
+  O5_CHECK(B <= kMaxLstmB, O5_E_SHAPE, "%s: B=%d exceeds %d", fn, B, kMaxLstmB);
   O5_CHECK(D >= 64 && H >= 64 && D % 64 == 0 && H % 64 == 0 && D <= 65536 && H <= 65536, O5_E_SHAPE,
            "%s: D=%d and H=%d must be positive multiples of 64 (<= 65536)", fn, D, H);
   O5_CHECK(static_cast<long long>(T) * B < (1ll << 31) && static_cast<long long>(T) * B * 4 * H < (1ll << 31) &&
@@ -592,7 +612,7 @@ static int lstm_bptt_impl(int T, int B, int D, int H, const E* x, const E* Wx, c
     if (st != O5_OK) return st;
     h0e = tmp;
     // W_h^T [H][4H]: the recurrent GEMM's second operand, K-contiguous
-    hipLaunchKernelGGL(transpose_rows<E>, dim3(cdiv(H, 64), cdiv(4 * H, 64)), dim3(256), 0, s, 1, 4 * H, 4 * H, H, Wh,
+    hipLaunchKernelGGL(transpose_rows<E>, transpose_grid(H, 4 * H), dim3(256), 0, s, 1, 4 * H, 4 * H, H, Wh,
                        Wh, 4 * H, H, nullptr, WhT, static_cast<size_t>(4 * H));
   } else {
     h0e = h0;
@@ -660,9 +680,9 @@ static int lstm_bptt_impl(int T, int B, int D, int H, const E* x, const E* Wx, c
       // both operands K-contiguous over the time-padded K = T * Bp
       const int K = static_cast<int>(w.ldt);
       const int ldt = static_cast<int>(w.ldt);
-      hipLaunchKernelGGL(transpose_rows<E>, dim3(cdiv(D, 64), K / 64), dim3(256), 0, s, T, B, w.Bp, D, x, x, T * B, D,
+      hipLaunchKernelGGL(transpose_rows<E>, transpose_grid(D, K), dim3(256), 0, s, T, B, w.Bp, D, x, x, T * B, D,
                          nullptr, XHT, w.ldt);
-      hipLaunchKernelGGL(transpose_rows<E>, dim3(cdiv(H, 64), K / 64), dim3(256), 0, s, T, B, w.Bp, H, h0e, h, B, H,
+      hipLaunchKernelGGL(transpose_rows<E>, transpose_grid(H, K), dim3(256), 0, s, T, B, w.Bp, H, h0e, h, B, H,
                          reset, XHT + static_cast<size_t>(D) * w.ldt, w.ldt);
       KRows2<E> al{dGT, nullptr, nullptr, ldt, 0, K, K, 4 * H};
       KRows2<E> bl{XHT, nullptr, nullptr, ldt, 0, K, K, D + H};
@@ -747,21 +767,21 @@ static int bptt_check(const char* fn, o5_dtype dt, int T, int B, int D, int H, c
                       float* db, void* dx, void* ws, size_t ws_bytes, BwdWs* w) {
   int st = check_dims(fn, dt, T, B, D, H);
   if (st != O5_OK) return st;
-  O5_PTR(x, "x");
-  O5_PTR(Wx, "Wx");
-  O5_PTR(Wh, "Wh");
-  O5_PTR(h0, "h0");
-  O5_PTR(c0, "c0");
-  O5_OPT_PTR(reset, "reset");
-  O5_PTR(h, "h");
-  O5_PTR(c, "c");
-  O5_PTR(gates, "gates");
-  O5_OPT_PTR(dhT, "dhT");
-  O5_OPT_PTR(dcT, "dcT");
-  O5_PTR(dWx, "dWx");
-  O5_PTR(dWh, "dWh");
-  O5_PTR(db, "db");
-  O5_OPT_PTR(dx, "dx");
+  O5_PTR_IN(fn, x, "x");
+  O5_PTR_IN(fn, Wx, "Wx");
+  O5_PTR_IN(fn, Wh, "Wh");
+  O5_PTR_IN(fn, h0, "h0");
+  O5_PTR_IN(fn, c0, "c0");
+  O5_OPT_PTR_IN(fn, reset, "reset");
+  O5_PTR_IN(fn, h, "h");
+  O5_PTR_IN(fn, c, "c");
+  O5_PTR_IN(fn, gates, "gates");
+  O5_OPT_PTR_IN(fn, dhT, "dhT");
+  O5_OPT_PTR_IN(fn, dcT, "dcT");
+  O5_PTR_IN(fn, dWx, "dWx");
+  O5_PTR_IN(fn, dWh, "dWh");
+  O5_PTR_IN(fn, db, "db");
+  O5_OPT_PTR_IN(fn, dx, "dx");
   *w = bwd_ws(dt, T, B, D, H);
   O5_CHECK(ws != nullptr && ws_bytes >= w->total, O5_E_WORKSPACE, "%s: workspace needs %zu bytes, got %zu", fn,
            w->total, ws ? ws_bytes : static_cast<size_t>(0));

@@ -867,22 +867,22 @@ static int ppo_check(const char* fn, o5_dtype dt, int N, int H, int K, const int
   if (st != O5_OK) return st;
   O5_CHECK(hp.clip_eps >= 0.0f && hp.clip_eps < 1.0f, O5_E_ARG, "%s: clip_eps=%g must be in [0, 1)", fn,
            hp.clip_eps);
-  O5_PTR(h, "h");
-  O5_PTR(Wp, "Wp");
-  O5_PTR(bp, "bp");
-  O5_PTR(act, "act");
-  O5_PTR(logp_old, "logp_old");
-  O5_PTR(adv, "adv");
-  O5_PTR(ret, "ret");
-  O5_OPT_PTR(head_mask, "head_mask");
-  O5_OPT_PTR(avail, "avail");
+  O5_PTR_IN(fn, h, "h");
+  O5_PTR_IN(fn, Wp, "Wp");
+  O5_PTR_IN(fn, bp, "bp");
+  O5_PTR_IN(fn, act, "act");
+  O5_PTR_IN(fn, logp_old, "logp_old");
+  O5_PTR_IN(fn, adv, "adv");
+  O5_PTR_IN(fn, ret, "ret");
+  O5_OPT_PTR_IN(fn, head_mask, "head_mask");
+  O5_OPT_PTR_IN(fn, avail, "avail");
   if (unit != nullptr) {
     st = check_unit(fn, *hm, unit, true);
     if (st != O5_OK) return st;
   }
-  O5_PTR(stats, "stats");
-  O5_PTR(dWp, "dWp");
-  O5_PTR(dbp, "dbp");
+  O5_PTR_IN(fn, stats, "stats");
+  O5_PTR_IN(fn, dWp, "dWp");
+  O5_PTR_IN(fn, dbp, "dbp");
   *w = unit ? ppo_ws(dt, N, H, hm->A + 1, hm->off[unit->head + 1] - hm->off[unit->head], unit->d)
             : ppo_ws(dt, N, H, hm->A + 1);
   O5_CHECK(ws != nullptr && ws_bytes >= w->total, O5_E_WORKSPACE, "%s: workspace needs %zu bytes, got %zu", fn,

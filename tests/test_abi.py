@@ -55,6 +55,10 @@ def test_host_validation_errors(lib):
     # dtype and LSTM shapes
     assert L.o5_lstm_fwd(9, 1, 1, 64, 64, *([16] * 11), 1 << 20, None) == 3
     assert L.o5_lstm_fwd(0, 1, 1, 60, 64, *([16] * 11), 1 << 20, None) == 2
+    # B is bounded by the cell kernels' grids (32 rows per block, y < 65535)
+    assert L.o5_lstm_fwd_workspace_bytes(1, 1, 32767 * 64, 64, 64) > 0
+    assert L.o5_lstm_fwd_workspace_bytes(1, 1, 32767 * 64 + 1, 64, 64) == 0
+    assert L.o5_lstm_bptt_workspace_bytes(0, 1, 32767 * 64 + 1, 64, 64) == 0
     # workspace too small
     need = L.o5_lstm_fwd_workspace_bytes(1, 16, 8, 64, 128)
     assert need > 0

@@ -279,3 +279,49 @@ def test_lstm_dma_engine_ragged_sampled_rows():
     assert_close_both("gates[rows]", host(got["gates"][:, rows.tolist()]), ref["gates"], plain["gates"], TOL_BF16)
     for k in ("dWx", "dWh", "db"):
         assert_close_both(k, host(got[k]), ref[k], plain[k], TOL_BF16)
+
+
+def test_lstm_largest_batch_sampled_rows():
+    """The largest batch the calls accept (B = 2,097,088, the cell kernels'
+    grid bound) at T = 3, D = H = 64, bf16, with resets: every cell grid at
+    its limit, and T * B rows of [x | h~] that the weight gradient's
+    transposes walk in more row tiles than one grid dimension holds.
+    Checked on sampled rows as in the paper-scale test (the upstream
+    gradient is nonzero only there)."""
+    need_gpu()
+    T, B, D, H = 3, 32767 * 64, 64, 64
+    banner(f"lstm largest batch T={T} B={B} D={D} H={H}")
+    rng = np.random.Generator(np.random.PCG64(17))
+    bound = 1.0 / np.sqrt(H)
+    inp = dict(
+        Wx=((rng.random((4 * H, D), dtype=np.float32) * 2 - 1) * bound).astype(np.float32),
+        Wh=((rng.random((4 * H, H), dtype=np.float32) * 2 - 1) * bound).astype(np.float32),
+        b=((rng.random(4 * H, dtype=np.float32) * 2 - 1) * bound).astype(np.float32),
+        x=rng.standard_normal((T, B, D), dtype=np.float32),
+        h0=(rng.standard_normal((B, H), dtype=np.float32) * 0.1).astype(np.float32),
+        c0=(rng.standard_normal((B, H), dtype=np.float32) * 0.1).astype(np.float32),
+    )
+    rows = np.array([0, 63, 64, 1 << 20, 1_500_001, B - 65, B - 1])
+    reset = np.zeros((T, B), np.uint8)
+    reset[1, rows[1]] = 1
+    reset[2, rows[4]] = 1
+    inp["reset"] = reset
+    dh = np.zeros((T, B, H), np.float32)
+    dh[:, rows] = rng.standard_normal((T, len(rows), H), dtype=np.float32)
+    inp["dh"] = dh
+    inp["dhT"] = None
+    inp["dcT"] = None
+    got = _run_gpu(inp, T, B, D, H, True, with_final=False, want_dx=False)
+    torch.cuda.synchronize()
+    sub = dict(inp)
+    sub["x"] = inp["x"][:, rows]
+    sub["h0"] = inp["h0"][rows]
+    sub["c0"] = inp["c0"][rows]
+    sub["reset"] = reset[:, rows]
+    sub["dh"] = dh[:, rows]
+    ref = _oracle(sub, True, with_final=False)
+    plain = _oracle(sub, True, with_final=False, plain=True)
+    assert_close_both("h[rows]", host(got["h"][:, rows.tolist()]), ref["h"], plain["h"], TOL_BF16)
+    assert_close_both("c[rows]", host(got["c"][:, rows.tolist()]), ref["c"], plain["c"], TOL_BF16)
+    for k in ("dWx", "dWh", "db"):
+        assert_close_both(k, host(got[k]), ref[k], plain[k], TOL_BF16)
