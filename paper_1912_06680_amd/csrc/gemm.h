@@ -370,10 +370,7 @@ constexpr int kGroupM = 4;
 // round-robin to the 8 XCDs, so each XCD first gets a contiguous run of
 // tiles (when the tile count is a multiple of 8); tiles are then numbered in
 // groups of kGroupM M-tiles with the M-tile fastest.
-__device__ __forceinline__ void xcd_tile(int pid, int tiles_m, int tiles_n, int& tm, int& tn) {
-  const int nt = tiles_m * tiles_n;
-  int tile = pid;
-  if ((nt & 7) == 0) tile = (pid & 7) * (nt >> 3) + (pid >> 3);
+__device__ __forceinline__ void group_tile(int tile, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int gsz = kGroupM * tiles_n;
   const int g = tile / gsz;
   const int first_m = g * kGroupM;
@@ -381,6 +378,34 @@ __device__ __forceinline__ void xcd_tile(int pid, int tiles_m, int tiles_n, int&
   const int in = tile - g * gsz;
   tm = first_m + in % gm;
   tn = in / gm;
+}
+
+__device__ __forceinline__ void xcd_tile(int pid, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int nt = tiles_m * tiles_n;
+  int tile = pid;
+  if ((nt & 7) == 0) tile = (pid & 7) * (nt >> 3) + (pid >> 3);
+  group_tile(tile, tiles_m, tiles_n, tm, tn);
+}
+
+// The same for a grid of S K splits, block (x, z) = tile x of split z
+// (dispatched as linear id x + gridDim.x * z).  When S divides 8 the 8 / S
+// XCDs of one split take its tiles in contiguous runs, so the blocks an XCD
+// holds read the same K range and share operand panels in its L2 (with the
+// plain mapping each XCD would hold every split of fewer tiles); otherwise
+// xcd_tile with split z.
+__device__ __forceinline__ void xcd_tile_split(int x, int z, int S, int tiles_m, int tiles_n, int& tm, int& tn,
+                                               int& split) {
+  const int nt = tiles_m * tiles_n;
+  if (S > 1 && 8 % S == 0 && nt % (8 / S) == 0) {
+    const int xs = 8 / S;           // XCDs per split
+    const int L = x + nt * z;       // the dispatch order; XCD = L % 8
+    const int xcd = L & 7, slot = L >> 3;
+    split = xcd / xs;
+    group_tile((xcd % xs) * (nt / xs) + slot, tiles_m, tiles_n, tm, tn);
+  } else {
+    split = z;
+    xcd_tile(x, tiles_m, tiles_n, tm, tn);
+  }
 }
 
 template <int MB, int NB>

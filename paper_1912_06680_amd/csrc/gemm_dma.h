@@ -286,10 +286,9 @@ __global__ void __launch_bounds__(dma::NT, 1)
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm0 = (wave / WAVES_N) * WM, wn0 = (wave % WAVES_N) * WN;
-  int tm, tn;
-  xcd_tile(blockIdx.x, (M + BM - 1) / BM, (N + BN - 1) / BN, tm, tn);
+  int tm, tn, split;
+  xcd_tile_split(blockIdx.x, blockIdx.z, gridDim.z, (M + BM - 1) / BM, (N + BN - 1) / BN, tm, tn, split);
   const int m0 = tm * BM, n0 = tn * BN;
-  const int split = blockIdx.z;
   const int nkt = (K + BK - 1) / BK;
   const int kt0 = split * ktiles_per_split;
   const int kt1 = min(nkt, kt0 + ktiles_per_split);
