@@ -87,10 +87,10 @@ __global__ void __launch_bounds__(256) f32_to_bf16_kernel(size_t n, const float*
     const float4 a = reinterpret_cast<const float4*>(src)[2 * i];
     const float4 b = reinterpret_cast<const float4*>(src)[2 * i + 1];
     uint4 o;
-    o.x = f32_to_bf16_bits(a.x) | (static_cast<uint32_t>(f32_to_bf16_bits(a.y)) << 16);
-    o.y = f32_to_bf16_bits(a.z) | (static_cast<uint32_t>(f32_to_bf16_bits(a.w)) << 16);
-    o.z = f32_to_bf16_bits(b.x) | (static_cast<uint32_t>(f32_to_bf16_bits(b.y)) << 16);
-    o.w = f32_to_bf16_bits(b.z) | (static_cast<uint32_t>(f32_to_bf16_bits(b.w)) << 16);
+    o.x = f32x2_to_bf16x2(a.x, a.y);
+    o.y = f32x2_to_bf16x2(a.z, a.w);
+    o.z = f32x2_to_bf16x2(b.x, b.y);
+    o.w = f32x2_to_bf16x2(b.z, b.w);
     reinterpret_cast<uint4*>(dst)[i] = o;
   }
   // tail (fewer than 8 elements), handled by the first block

@@ -83,10 +83,10 @@ __global__ void __launch_bounds__(256) adam_kernel(size_t n, float* __restrict__
     st_nt(v4 + k, vk);
     if (kBf16Out) {
       uint2 oa, ok;
-      oa.x = f32_to_bf16_bits(pa.x) | (static_cast<uint32_t>(f32_to_bf16_bits(pa.y)) << 16);
-      oa.y = f32_to_bf16_bits(pa.z) | (static_cast<uint32_t>(f32_to_bf16_bits(pa.w)) << 16);
-      ok.x = f32_to_bf16_bits(pk.x) | (static_cast<uint32_t>(f32_to_bf16_bits(pk.y)) << 16);
-      ok.y = f32_to_bf16_bits(pk.z) | (static_cast<uint32_t>(f32_to_bf16_bits(pk.w)) << 16);
+      oa.x = f32x2_to_bf16x2(pa.x, pa.y);
+      oa.y = f32x2_to_bf16x2(pa.z, pa.w);
+      ok.x = f32x2_to_bf16x2(pk.x, pk.y);
+      ok.y = f32x2_to_bf16x2(pk.z, pk.w);
       st_nt(pb2 + i, oa);
       st_nt(pb2 + k, ok);
     }
@@ -99,8 +99,8 @@ __global__ void __launch_bounds__(256) adam_kernel(size_t n, float* __restrict__
     v4[i] = va;
     if (kBf16Out) {
       uint2 oa;
-      oa.x = f32_to_bf16_bits(pa.x) | (static_cast<uint32_t>(f32_to_bf16_bits(pa.y)) << 16);
-      oa.y = f32_to_bf16_bits(pa.z) | (static_cast<uint32_t>(f32_to_bf16_bits(pa.w)) << 16);
+      oa.x = f32x2_to_bf16x2(pa.x, pa.y);
+      oa.y = f32x2_to_bf16x2(pa.z, pa.w);
       pb2[i] = oa;
     }
   }

@@ -80,11 +80,21 @@ inline size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
 
 // ------------------------------------------------------------------ bf16
 // Round-to-nearest-even fp32 -> bf16 bits; NaN keeps a quiet NaN.
+// f32 -> bf16 bits, rounding to nearest even: for every non-NaN pattern u the
+// bits of (u + 0x7fff + ((u >> 16) & 1)) >> 16, and for NaN (u >> 16) | 0x40
+// (sign and top payload kept, quiet).  gfx950 has this conversion as one
+// instruction (v_cvt_pk_bf16_f32, two values at a time); the conversion
+// test checks it against that formula on every sign, exponent and top
+// mantissa pattern with ties, NaN, infinities and subnormals.
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x0040u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
+}
+
+// Two at once: a in the low 16 bits, b in the high.
+__device__ __forceinline__ uint32_t f32x2_to_bf16x2(float a, float b) {
+  typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
+  const bf16x2_v v = {static_cast<__bf16>(a), static_cast<__bf16>(b)};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {

@@ -87,8 +87,8 @@ template <> struct Vec4<uint16_t> {
   }
   __device__ __forceinline__ static void store(uint16_t* p, float4 v) {
     uint2 u;
-    u.x = f32_to_bf16_bits(v.x) | (static_cast<uint32_t>(f32_to_bf16_bits(v.y)) << 16);
-    u.y = f32_to_bf16_bits(v.z) | (static_cast<uint32_t>(f32_to_bf16_bits(v.w)) << 16);
+    u.x = f32x2_to_bf16x2(v.x, v.y);
+    u.y = f32x2_to_bf16x2(v.z, v.w);
     *reinterpret_cast<uint2*>(p) = u;
   }
 };

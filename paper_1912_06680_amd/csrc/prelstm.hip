@@ -111,8 +111,8 @@ __global__ void __launch_bounds__(256) obs_apply(size_t total4, int Do, const fl
   v.w = fminf(fmaxf((x.w - m.w) * s.w, -clip), clip);
   if constexpr (sizeof(E) == 2) {
     uint2 u;
-    u.x = f32_to_bf16_bits(v.x) | (static_cast<uint32_t>(f32_to_bf16_bits(v.y)) << 16);
-    u.y = f32_to_bf16_bits(v.z) | (static_cast<uint32_t>(f32_to_bf16_bits(v.w)) << 16);
+    u.x = f32x2_to_bf16x2(v.x, v.y);
+    u.y = f32x2_to_bf16x2(v.z, v.w);
     *reinterpret_cast<uint2*>(o + i * 4) = u;
   } else {
     *reinterpret_cast<float4*>(o + i * 4) = v;

@@ -198,3 +198,23 @@ def test_f32_to_bf16_matches_oracle_rounding(n):
     o5.o5_f32_to_bf16(n, dev_f32(a), dst)
     got = dst.view(torch.int16).cpu().numpy().view(np.uint16)
     assert np.array_equal(got, bf16_bits(a))
+
+
+def test_f32_to_bf16_every_top_pattern():
+    """Every sign, exponent and top-7-mantissa pattern (all 2^16 upper
+    halves) with lower halves 0, 1, 0x7fff, 0x8000 (the tie), 0x8001 and
+    0xffff: ties to even both ways, carries into the exponent, overflow to
+    infinity, subnormals, infinities and NaN.  Non-NaN inputs give the
+    oracle's bits; NaN gives the input's top half with the quiet bit set."""
+    need_gpu()
+    banner("f32_to_bf16 every top pattern")
+    hi = np.arange(1 << 16, dtype=np.uint32) << 16
+    lo = np.array([0, 1, 0x7FFF, 0x8000, 0x8001, 0xFFFF], dtype=np.uint32)
+    u = (hi[:, None] | lo[None, :]).ravel()
+    a = u.view(np.float32)
+    dst = torch.empty(a.size, dtype=torch.bfloat16, device="cuda")
+    o5.o5_f32_to_bf16(a.size, dev_f32(a), dst)
+    got = dst.view(torch.int16).cpu().numpy().view(np.uint16)
+    nan = np.isnan(a)
+    assert np.array_equal(got[~nan], bf16_bits(a[~nan]))
+    assert np.array_equal(got[nan], ((u[nan] >> 16) | 0x40).astype(np.uint16))
