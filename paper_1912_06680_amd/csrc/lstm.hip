@@ -116,8 +116,12 @@ struct EpiLstmCell {
   static constexpr int kNR = 128 / kRS;                 // sweeps per 128-row pass
   // thread -> 4 consecutive hidden units (quad tid % 16) of rows tid / 16 +
   // kRS * i of each pass
+  // exp(x) = 2^(x log2 e): the activations take their exponent as one FMA
+  // of the pre-activation with the bias scaled here (-log2 e for the
+  // sigmoids of i, f, o; 2 log2 e for tanh of g)
+  static constexpr float kL2E = 1.44269504088896341f;
   struct Pre {
-    float4 b[4];          // bias of gates i, f, g, o
+    float4 b[4];          // scaled bias of gates i, f, g, o
     float4 cp[2][kNR];    // previous cell state
     int rs[2][kNR];       // the row's reset flag (its previous state counts as zero)
   };
@@ -133,7 +137,11 @@ struct EpiLstmCell {
     const int j = (n0 >> 2) + 4 * (tid & 15);
     const int rr = tid >> 4;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) pre.b[g] = *reinterpret_cast<const float4*>(bias + g * H + j);
+    for (int g = 0; g < 4; ++g) {
+      const float s = g == 2 ? 2.0f * kL2E : -kL2E;
+      const float4 v = *reinterpret_cast<const float4*>(bias + g * H + j);
+      pre.b[g] = make_float4(v.x * s, v.y * s, v.z * s, v.w * s);
+    }
     // (the flag and the state are loaded independently; the flag selects
     // when the tile uses them, so no load waits for another)
 #pragma unroll
@@ -158,7 +166,8 @@ struct EpiLstmCell {
     const int uq = tid & 15;
     const int rr = tid >> 4;
     const int j = (n0 >> 2) + 4 * uq;  // first hidden unit of the quad
-    const size_t G = 4 * static_cast<size_t>(H);
+    const uint32_t base_hc = static_cast<uint32_t>(m0 + rr) * H + j;
+    const uint32_t base_g = static_cast<uint32_t>(m0 + rr) * 4 * H + j;
     const float4 bi = pre.b[0], bf = pre.b[1], bg = pre.b[2], bo = pre.b[3];
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
@@ -180,6 +189,10 @@ struct EpiLstmCell {
       for (int i = 0; i < kNR; ++i) {
         const int row = rr + i * kRS;
         const int bidx = m0 + p * 128 + row;
+        // element offsets (B * 4H < 2^31): h and c at bidx * H + j, the gates
+        // at bidx * 4H + j; the row step is uniform
+        const uint32_t ohc = base_hc + static_cast<uint32_t>((p * 128 + i * kRS) * H);
+        const uint32_t ogt = base_g + static_cast<uint32_t>((p * 128 + i * kRS) * 4 * H);
         if (bidx < M) {
           const float4 ai = *reinterpret_cast<const float4*>(lds + (0 * 128 + row) * kPad + 4 * uq);
           const float4 af = *reinterpret_cast<const float4*>(lds + (1 * 128 + row) * kPad + 4 * uq);
@@ -194,18 +207,19 @@ struct EpiLstmCell {
           float* pc = &c.x; float* ph = &h.x;
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            pig[q] = sigmoid_f(pai[q] + pbi[q]);
-            pfg[q] = sigmoid_f(paf[q] + pbf[q]);
-            pgg[q] = tanh_f(pag[q] + pbg[q]);
-            pog[q] = sigmoid_f(pao[q] + pbo[q]);
+            // sigma(a + b) = 1 / (1 + 2^(-(a + b) log2 e)), tanh(a + b) =
+            // 1 - 2 / (1 + 2^(2 (a + b) log2 e)), as sigmoid_f and tanh_f
+            pig[q] = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(fmaf(pai[q], -kL2E, pbi[q])));
+            pfg[q] = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(fmaf(paf[q], -kL2E, pbf[q])));
+            pgg[q] = 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(fmaf(pag[q], 2.0f * kL2E, pbg[q])));
+            pog[q] = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(fmaf(pao[q], -kL2E, pbo[q])));
             pc[q] = pfg[q] * pcp[q] + pig[q] * pgg[q];
             ph[q] = pog[q] * tanh_f(pc[q]);
           }
-          const size_t hj = static_cast<size_t>(bidx) * H + j;
-          *reinterpret_cast<float4*>(c_out + hj) = c;
-          Vec4<E>::store(h_out + hj, h);
+          *reinterpret_cast<float4*>(c_out + ohc) = c;
+          Vec4<E>::store(h_out + ohc, h);
           if (gates_out) {
-            E* gp = gates_out + static_cast<size_t>(bidx) * G + j;
+            E* gp = gates_out + ogt;
             Vec4<E>::store(gp, ig);
             Vec4<E>::store(gp + H, fg);
             Vec4<E>::store(gp + 2 * H, gg);
