@@ -84,8 +84,7 @@ inline size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
 // bits of (u + 0x7fff + ((u >> 16) & 1)) >> 16, and for NaN (u >> 16) | 0x40
 // (sign and top payload kept, quiet).  gfx950 has this conversion as one
 // instruction (v_cvt_pk_bf16_f32, two values at a time); the conversion
-// test checks it against that formula on every sign, exponent and top
-// mantissa pattern with ties, NaN, infinities and subnormals.
+// tests check it against that formula on all 2^32 inputs.
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
   return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }

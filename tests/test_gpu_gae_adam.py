@@ -200,6 +200,28 @@ def test_f32_to_bf16_matches_oracle_rounding(n):
     assert np.array_equal(got, bf16_bits(a))
 
 
+def test_f32_to_bf16_every_bit_pattern():
+    """All 2^32 float32 bit patterns through the conversion kernel, in chunks
+    of 2^28, against round-to-nearest-even written out on the bits (torch
+    integer arithmetic): (u + 0x7fff + ((u >> 16) & 1)) >> 16, and for NaN
+    the top half with the quiet bit set."""
+    need_gpu()
+    banner("f32_to_bf16 all 2^32 patterns")
+    chunk = 1 << 28
+    dst = torch.empty(chunk, dtype=torch.bfloat16, device="cuda")
+    for c0 in range(0, 1 << 32, chunk):
+        u = torch.arange(c0, c0 + chunk, dtype=torch.int64, device="cuda")
+        src = torch.where(u >= (1 << 31), u - (1 << 32), u).to(torch.int32).view(torch.float32)
+        o5.o5_f32_to_bf16(chunk, src, dst)
+        got = dst.view(torch.int16).to(torch.int64) & 0xFFFF
+        nan = (u & 0x7FFFFFFF) > 0x7F800000
+        exp = torch.where(nan, (u >> 16) | 0x40, (u + 0x7FFF + ((u >> 16) & 1)) >> 16) & 0xFFFF
+        bad = int((got != exp).sum())
+        assert bad == 0, f"chunk {c0:#x}: {bad} patterns differ"
+        del u, src, got, nan, exp
+    torch.cuda.synchronize()
+
+
 def test_f32_to_bf16_every_top_pattern():
     """Every sign, exponent and top-7-mantissa pattern (all 2^16 upper
     halves) with lower halves 0, 1, 0x7fff, 0x8000 (the tie), 0x8001 and
