@@ -33,6 +33,8 @@
 //    its own slice (the caller reduces the slices in a fixed order).
 #pragma once
 
+#include <type_traits>
+
 #include "common.h"
 
 namespace o5 {
@@ -282,6 +284,12 @@ struct EpiStoreF32 {
   __device__ __forceinline__ void operator()(int i, int j, float v, int split) const {
     c[split * sstride + static_cast<size_t>(i) * ldc + j] = v;
   }
+  // where the 32-column block from (i0, j0) goes and its row pitch
+  __device__ __forceinline__ bool blocks_ok() const { return true; }
+  __device__ __forceinline__ float* block(int i0, int j0, int split, int& ld) const {
+    ld = ldc;
+    return c + split * sstride + static_cast<size_t>(i0) * ldc + j0;
+  }
 };
 
 // Store into one of two fp32 matrices split by column: j < J0 -> c0[i*ld0 + j],
@@ -297,6 +305,12 @@ struct EpiStoreF32Split2 {
     else
       c1[static_cast<size_t>(i) * ld1 + (j - J0)] = v;
   }
+  // (a 32-column block lies in one matrix when J0 is a multiple of 32)
+  __device__ __forceinline__ bool blocks_ok() const { return J0 % 32 == 0; }
+  __device__ __forceinline__ float* block(int i0, int j0, int, int& ld) const {
+    ld = j0 < J0 ? ld0 : ld1;
+    return j0 < J0 ? c0 + static_cast<size_t>(i0) * ld0 + j0 : c1 + static_cast<size_t>(i0) * ld1 + (j0 - J0);
+  }
 };
 
 // Store converted to the element type E (dx in the GEMM input type).
@@ -309,6 +323,48 @@ struct EpiStoreElem {
     c[static_cast<size_t>(i) * ldc + j] = elem<E>::from_f32(v);
   }
 };
+
+// Epilogues that store 32 x 32 accumulator blocks row by row (block(),
+// blocks_ok()): the stores of a full tile take a uniform block base and a
+// per-lane 32-bit offset, with no per-element bounds test or 64-bit index.
+template <class Epi, class = void>
+struct HasBlockStore : std::false_type {};
+template <class Epi>
+struct HasBlockStore<Epi, std::void_t<decltype(&Epi::blocks_ok)>> : std::true_type {};
+
+// The element epilogue of an MB x NB set of 32 x 32 MFMA accumulator blocks
+// at (i0, j0) of an M x N result.  Accumulator layout of a block: lane holds
+// column (lane & 31); register e holds row 8*(e/4) + 4*(lane/32) + (e%4).
+// `full`: the block tile lies inside M x N.
+template <int MB, int NB, class Epi>
+__device__ __forceinline__ void store_acc(const Epi& epi, const f32x16_t (&acc)[MB][NB], int i0, int j0, int lane,
+                                          int split, int M, int N, bool full) {
+  if constexpr (HasBlockStore<Epi>::value) {
+    if (full && epi.blocks_ok()) {
+#pragma unroll
+      for (int a = 0; a < MB; ++a)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          int ld;
+          float* base = epi.block(i0 + a * 32, j0 + b * 32, split, ld);
+          const int lo = 4 * (lane >> 5) * ld + (lane & 31);
+#pragma unroll
+          for (int e = 0; e < 16; ++e) base[lo + (8 * (e >> 2) + (e & 3)) * ld] = acc[a][b][e];
+        }
+      return;
+    }
+  }
+#pragma unroll
+  for (int a = 0; a < MB; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int i = i0 + a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        const int j = j0 + b * 32 + (lane & 31);
+        if (full || (i < M && j < N)) epi(i, j, acc[a][b][e], split);
+      }
+}
 
 // ------------------------------------------------------ fp32 FMA engine
 // 64 x 64 tile, K tile 16, 256 threads, 4 x 4 outputs per thread.

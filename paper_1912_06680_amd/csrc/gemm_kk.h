@@ -325,19 +325,7 @@ __global__ void __launch_bounds__(kk::NT, 1)
     dma::wave_barrier();  // every wave is done with the stages
     epi.template tile<MB, NB>(acc, smem, m0, n0, wave / WAVES_N, wn0, lane, tid, M, pre);
   } else {
-    // accumulator layout of a 32 x 32 block: lane holds column (lane & 31);
-    // register e holds row 8*(e/4) + 4*(lane/32) + (e%4)
-    const bool full = m0 + BM <= M && n0 + BN <= N;
-#pragma unroll
-    for (int a = 0; a < MB; ++a)
-#pragma unroll
-      for (int b = 0; b < NB; ++b)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int i = m0 + wm0 + a * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-          const int j = n0 + wn0 + b * 32 + (lane & 31);
-          if (full || (i < M && j < N)) epi(i, j, acc[a][b][e], split);
-        }
+    store_acc<MB, NB>(epi, acc, m0 + wm0, n0 + wn0, lane, split, M, N, m0 + BM <= M && n0 + BN <= N);
   }
 }
 
