@@ -399,55 +399,58 @@ __global__ void __launch_bounds__(256) lstm_bwd_cell(
 }
 
 // Transposed, time-padded operand for the weight-gradient GEMM.  Column
-// k = t * Bp + b of dst (Bp = B rounded up to the cell's row block) holds
-// source row t * B + b; columns with b >= B are zero.  Source row r is
-// s0[r] for r < split, else s1[r - split], and zero where mask[r] is set.
-// So dst row c is column c of [x] (split = T*B) or of the masked previous
-// hidden state h~ (s0 = h0, s1 = h, split = B, mask = reset).  Tiles of 64
-// columns x 64 source rows pass through LDS; 256 threads, 16-byte accesses;
-// blockIdx.x is the column tile, the source row tiles stride by gridDim.y.
+// k = t * Bp + b of dst (Bp = B rounded up to 64) holds source row t * B + b;
+// columns with b >= B are zero.  Source row r is s0[r] for r < split, else
+// s1[r - split], and zero where mask[r] is set.  So dst row c is column c of
+// [x] (split = T*B) or of the masked previous hidden state h~ (s0 = h0, s1 =
+// h, split = B, mask = reset).  Each wave moves 64 source rows x 64 columns
+// with no LDS: lane (rb, cb) loads the 8 x 8 block of rows 8 rb .. + 7,
+// columns 8 cb .. + 7 (eight 16-byte loads in flight), transposes it in
+// registers and stores 8 rows of 16 bytes, so every load and store
+// instruction of a wave covers whole 128-byte lines.  A block is 4 waves
+// side by side in c; the source row tiles stride by gridDim.y.  Requires C
+// and Bp multiples of 64.
 template <typename E>
 __global__ void __launch_bounds__(256) transpose_rows(int T, int B, int Bp, int C, const E* __restrict__ s0,
                                                       const E* __restrict__ s1, int split, int lds,
                                                       const uint8_t* __restrict__ mask, E* __restrict__ dst,
                                                       size_t ldd) {
   static_assert(sizeof(E) == 2, "bf16 only");
-  __shared__ __attribute__((aligned(16))) uint16_t tile[64][72];
-  const int c0 = blockIdx.x * 64;
-  const int tid = threadIdx.x;
-  const int nkt = static_cast<int>((static_cast<long long>(T) * Bp + 63) / 64);
+  const int lane = threadIdx.x & 63;
+  const int c0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * 64;
+  if (c0 >= C) return;  // a whole wave; the kernel has no barrier
+  const int rb = lane >> 3, cb = lane & 7;
+  const int c = c0 + 8 * cb;
+  const int nkt = static_cast<int>((static_cast<long long>(T) * Bp) / 64);
   for (int kt = blockIdx.y; kt < nkt; kt += gridDim.y) {
     const int k0 = kt * 64;
+    const int t = k0 / Bp;  // one step per 64-row tile (Bp is a multiple of 64)
+    const int b0 = k0 - t * Bp + 8 * rb;
+    uint4 v[8];
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int kl = (tid >> 3) + 32 * hh, ch = tid & 7;
-      const int k = k0 + kl, c = c0 + ch * 8;
-      const int t = k / Bp, b = k - t * Bp;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (t < T && b < B && c < C) {
+    for (int i = 0; i < 8; ++i) {
+      v[i] = make_uint4(0, 0, 0, 0);
+      const int b = b0 + i;
+      if (b < B) {
         const int r = t * B + b;
         if (!(mask && mask[r])) {
           const E* src = r < split ? s0 + static_cast<size_t>(r) * lds : s1 + static_cast<size_t>(r - split) * lds;
-          v = *reinterpret_cast<const uint4*>(src + c);
+          v[i] = *reinterpret_cast<const uint4*>(src + c);
         }
       }
-      *reinterpret_cast<uint4*>(&tile[kl][ch * 8]) = v;
     }
-    __syncthreads();
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int cl = (tid >> 3) + 32 * hh, ch = tid & 7;
-      const int c = c0 + cl;
-      if (c < C) {
-        uint4 v;
-        v.x = tile[ch * 8 + 0][cl] | (static_cast<uint32_t>(tile[ch * 8 + 1][cl]) << 16);
-        v.y = tile[ch * 8 + 2][cl] | (static_cast<uint32_t>(tile[ch * 8 + 3][cl]) << 16);
-        v.z = tile[ch * 8 + 4][cl] | (static_cast<uint32_t>(tile[ch * 8 + 5][cl]) << 16);
-        v.w = tile[ch * 8 + 6][cl] | (static_cast<uint32_t>(tile[ch * 8 + 7][cl]) << 16);
-        *reinterpret_cast<uint4*>(dst + static_cast<size_t>(c) * ldd + k0 + ch * 8) = v;
+    for (int j = 0; j < 8; ++j) {
+      // column c + j: 16-bit half (j & 1) of word j / 2 of each of the 8 rows
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t lo = (&v[2 * e].x)[j >> 1], hi = (&v[2 * e + 1].x)[j >> 1];
+        w[e] = (j & 1) ? (lo >> 16) | (hi & 0xffff0000u) : (lo & 0xffffu) | (hi << 16);
       }
+      *reinterpret_cast<uint4*>(dst + static_cast<size_t>(c + j) * ldd + k0 + 8 * rb) =
+          make_uint4(w[0], w[1], w[2], w[3]);
     }
-    __syncthreads();  // the tile is rewritten by the next row tile
   }
 }
 
@@ -457,7 +460,7 @@ static inline int time_pad(int B) { return cdiv(B, 64) * 64; }
 
 // Grid of transpose_rows for C columns and `rows` source rows.
 static inline dim3 transpose_grid(int C, long long rows) {
-  return dim3(cdiv(C, 64), static_cast<unsigned>(std::min<long long>((rows + 63) / 64, 65535)));
+  return dim3(cdiv(C, 256), static_cast<unsigned>(std::min<long long>((rows + 63) / 64, 65535)));
 }
 
 // ---------------------------------------------------------------- layouts
