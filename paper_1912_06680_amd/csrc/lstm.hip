@@ -98,15 +98,17 @@ __device__ __forceinline__ float4 f4(float a) { return make_float4(a, a, a, a); 
 // The forward cell fused into the epilogue of the step's GEMM.  The GEMM's B
 // tile is gate-gathered (256 columns = gates i, f, g, o of 64 hidden units),
 // so a wave whose tile starts at column wn0 holds gate (column / 64) of unit
-// (column % 64) for 128 rows.  In two passes of 128 rows the waves of one row
-// half park their
-// accumulators in LDS ([gate][row][unit], rows padded to 72 floats so the
-// two half-waves of a store hit disjoint banks), then every thread reads the
-// four gates of 4 consecutive units in each of its rows and finishes the
-// cell: c, h and the saved gates go straight to HBM in 16- and 8-byte
-// pieces and the pre-activations never do.  The bias and the previous cell
-// state of both passes are requested before the last K tile's MFMAs
-// (prefetch), so their latency hides behind them.
+// (column % 64) for 128 rows.  In two passes of 128 rows the waves of one
+// row half park their accumulators in LDS ([gate][row][unit], rows padded to
+// 72 floats so the two half-waves of a store hit disjoint banks), then every
+// thread reads the four gates of 4 consecutive units in each of its rows and
+// finishes the cell: c, h and the saved gates go straight to HBM in 16- and
+// 8-byte pieces and the pre-activations never do.  The bias and the previous
+// cell state of both passes are requested before the last K tile's MFMAs
+// (prefetch), so their latency hides behind them.  The epilogue is bound by
+// vector instruction issue (the MFMA units idle meanwhile), hence the
+// hardware bf16 rounding, the bias folded into the exponent's FMA and the
+// 32-bit offsets.
 template <typename E>
 struct EpiLstmCell {
   static constexpr int kPad = 72;
@@ -114,11 +116,11 @@ struct EpiLstmCell {
   static constexpr int kThreads = 512;                  // the block of both engines
   static constexpr int kRS = kThreads / 16;             // rows per sweep
   static constexpr int kNR = 128 / kRS;                 // sweeps per 128-row pass
-  // thread -> 4 consecutive hidden units (quad tid % 16) of rows tid / 16 +
-  // kRS * i of each pass
+  // (thread -> 4 consecutive hidden units, quad tid % 16, of rows tid / 16 +
+  // kRS * i of each pass)
   // exp(x) = 2^(x log2 e): the activations take their exponent as one FMA
-  // of the pre-activation with the bias scaled here (-log2 e for the
-  // sigmoids of i, f, o; 2 log2 e for tanh of g)
+  // of the pre-activation with the bias scaled in prefetch (by -log2 e for
+  // the sigmoids of i, f, o; by 2 log2 e for tanh of g)
   static constexpr float kL2E = 1.44269504088896341f;
   struct Pre {
     float4 b[4];          // scaled bias of gates i, f, g, o
