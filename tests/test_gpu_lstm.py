@@ -325,3 +325,33 @@ def test_lstm_largest_batch_sampled_rows():
     assert_close_both("c[rows]", host(got["c"][:, rows.tolist()]), ref["c"], plain["c"], TOL_BF16)
     for k in ("dWx", "dWh", "db"):
         assert_close_both(k, host(got[k]), ref[k], plain[k], TOL_BF16)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_lstm_saturated_gates(bf16):
+    """Pre-activations far beyond the range where exp over- or underflows in
+    fp32: biases of +-100 and +-150 on four gate rows in five (|a| > 89),
+    the weights at their usual scale so the GEMM sums stay well conditioned.
+    Those gates saturate to 0 or 1 (tanh to -1 or 1) through the
+    exponential's infinity or zero, with nothing non-finite, and the forward
+    pass and BPTT still match the oracle (whose logistic function is
+    evaluated without overflow)."""
+    need_gpu()
+    T, B, D, H = 3, 130, 128, 128
+    banner(f"lstm saturated gates T={T} B={B} D={D} H={H} bf16={bf16}")
+    inp = _inputs(T, B, D, H, 23, p_reset=0.1)
+    rng = np.random.Generator(np.random.PCG64(24))
+    inp["b"] = rng.choice(np.array([-150.0, -100.0, 0.0, 100.0, 150.0], np.float32), 4 * H).astype(np.float32)
+    got = _run_gpu(inp, T, B, D, H, bf16)
+    torch.cuda.synchronize()
+    for k in ("h", "c", "gates", "dWx", "dWh", "db", "dx"):
+        assert bool(torch.isfinite(got[k].float()).all()), k
+    ref = _oracle(inp, bf16)
+    tol = TOL_BF16 if bf16 else TOL_F32
+    if bf16:
+        plain = _oracle(inp, bf16, plain=True)
+        for k in ("h", "c", "gates", "dWx", "dWh", "db", "dx"):
+            assert_close_both(k, host(got[k]), ref[k], plain[k], tol)
+    else:
+        for k in ("h", "c", "gates", "dWx", "dWh", "db", "dx"):
+            assert_close(k, host(got[k]), ref[k], tol)

@@ -35,12 +35,12 @@ def _avail(rng, N, heads, mask):
     return av.astype(np.uint8), act
 
 
-def _inputs(N, H, heads, seed, bf16, with_mask, with_avail=False):
+def _inputs(N, H, heads, seed, bf16, with_mask, with_avail=False, wscale=4.0):
     rng = np.random.Generator(np.random.PCG64(seed))
     A1 = sum(heads) + 1
     bound = 1.0 / np.sqrt(H)
     h = np.tanh(rng.standard_normal((N, H), dtype=np.float32)).astype(np.float32)
-    Wp = ((rng.random((A1, H), dtype=np.float32) * 2 - 1) * bound * 4).astype(np.float32)
+    Wp = ((rng.random((A1, H), dtype=np.float32) * 2 - 1) * bound * wscale).astype(np.float32)
     bp = ((rng.random(A1, dtype=np.float32) * 2 - 1) * bound).astype(np.float32)
     act = np.stack([rng.integers(0, n, N) for n in heads], axis=1).astype(np.int32)
     adv = rng.standard_normal(N, dtype=np.float32)
@@ -113,6 +113,48 @@ def test_ppo_loss_grad_matches_oracle(name, N, H, heads, bf16, with_mask, with_a
                         mask, 0.2, 1.0, 0.01, stats, dh, dWp, dbp, ws, avail=avail)
     tol = TOL_BF16 if bf16 else TOL_F32
     st = host(stats)
+    for i, name_ in enumerate(STAT_NAMES):
+        ref = stats_ref[name_]
+        e = abs(st[i] - ref) / max(abs(ref), 1e-6)
+        print(f"    stat {name_}: gpu={st[i]:.6g} ref={ref:.6g} rel={e:.2e}", flush=True)
+        assert e <= tol, name_
+    assert_close("dh", host(dh), dh_ref, tol)
+    assert_close("dWp", host(dWp), dWp_ref, tol)
+    assert_close("dbp", host(dbp), dbp_ref, tol)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_ppo_peaked_softmax(bf16):
+    """Logits 35 times the usual scale (spreads above 120 within the first
+    head): each softmax is one-hot to fp32 precision, the probabilities of
+    the far logits underflow (e^-104 is below the smallest fp32 subnormal),
+    and log-probabilities away from the argmax reach a hundred and more
+    below zero; the statistics and gradients stay finite and match the
+    oracle.  (At 100x the usual scale, log-probabilities near -1000, fp32
+    rounding alone puts the fp32 path's policy-gradient statistic 1.0e-4
+    from the oracle, the edge of a tolerance meant for logits of order 1.)"""
+    need_gpu()
+    N, H, heads = 500, 128, HEADS
+    banner(f"ppo peaked softmax N={N} H={H} bf16={bf16}")
+    inp = _inputs(N, H, heads, seed=29, bf16=bf16, with_mask=True, wscale=140.0)
+    z = heads_forward(inp["hh"], inp["ww"], inp["bp"])
+    assert np.ptp(z[:, :heads[0]], axis=1).min() > 120
+    stats_ref, dh_ref, dWp_ref, dbp_ref, _ = ppo_loss_grad(
+        inp["hh"], inp["ww"], inp["bp"], inp["act"], inp["logp_old"], inp["adv"], inp["ret"], heads,
+        0.2, 1.0, 0.01, inp["mask"])
+    dt = o5.O5_BF16 if bf16 else o5.O5_F32
+    A1 = sum(heads) + 1
+    stats = torch.empty(8, dtype=torch.float32, device="cuda")
+    dh = torch.empty((N, H), dtype=torch.float32, device="cuda")
+    dWp = torch.empty((A1, H), dtype=torch.float32, device="cuda")
+    dbp = torch.empty(A1, dtype=torch.float32, device="cuda")
+    ws = workspace(o5.o5_ppo_loss_grad_workspace_bytes(dt, N, H, heads))
+    o5.o5_ppo_loss_grad(dt, N, H, heads, dev_dt(inp["h"], bf16), dev_dt(inp["Wp"], bf16), dev_f32(inp["bp"]),
+                        dev(inp["act"]), dev_f32(inp["logp_old"]), dev_f32(inp["adv"]), dev_f32(inp["ret"]),
+                        dev(inp["mask"]), 0.2, 1.0, 0.01, stats, dh, dWp, dbp, ws)
+    tol = TOL_BF16 if bf16 else TOL_F32
+    st = host(stats)
+    assert np.isfinite(st).all() and st[7] == 0.0
     for i, name_ in enumerate(STAT_NAMES):
         ref = stats_ref[name_]
         e = abs(st[i] - ref) / max(abs(ref), 1e-6)
