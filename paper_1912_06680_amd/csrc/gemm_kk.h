@@ -228,6 +228,7 @@ __global__ void __launch_bounds__(kk::NT, 1)
   static_assert(sizeof(E) == 2, "bf16 operands only");
   static_assert(NT == dma::NT, "tile epilogues assume the 8 waves of both engines");
   static_assert(KSTEPS % 2 == 0, "the fragment double buffer assumes an even number of k steps");
+  static_assert(MB * NB >= MB + NB, "a wave's MFMAs of a k step outnumber its fragment reads");
   constexpr int SMEM = Epi::kTileSmem > S::SMEM ? Epi::kTileSmem : S::SMEM;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
@@ -288,8 +289,14 @@ __global__ void __launch_bounds__(kk::NT, 1)
       dma::unroll<0, KSTEPS - 1>([&](auto Sx) {
         constexpr int s = decltype(Sx)::value;
         read(smem + ao, smem + bo, wm0, wn0, lane, s + 1, f[(s + 1) & 1]);
-        __builtin_amdgcn_sched_group_barrier(0x100, MB + NB, 0);  // the LDS reads first
-        __builtin_amdgcn_sched_group_barrier(0x008, MB * NB, 0);  // then the MFMAs
+        // one MFMA, then one of the next step's LDS reads, in turn (forward
+        // GEMM 451 against 458 us with all reads ahead of the MFMAs), then
+        // the remaining MFMAs
+        dma::unroll<0, MB + NB>([&](auto) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        });
+        if constexpr (MB * NB > MB + NB) __builtin_amdgcn_sched_group_barrier(0x008, MB * NB - (MB + NB), 0);
         mfma_all(f[s & 1], acc);
         __builtin_amdgcn_sched_barrier(0);
       });
