@@ -344,6 +344,9 @@ __global__ void __launch_bounds__(kWavesPerBlock * 64) ppo_rows(
 // row's logits; finally the block writes the gradient rows (dz, the (hi,
 // lo) pair, the unit head's columns) and its column sums with coalesced
 // stores.  No cross-lane operation; every sum in a fixed order.
+// the mask byte read where no mask is given
+__device__ const uint8_t kMaskOn = 1;
+
 // Writes row blockIdx.x of part (64 rows per partial).
 constexpr int kRtRows = 64;
 constexpr int kRtThreads = 256;
@@ -371,33 +374,88 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
   const size_t sstride = static_cast<size_t>(N) * A1;
   const int nke = kext >= 0 ? hm.off[kext + 1] - hm.off[kext] : 0;
   const int e0 = kext >= 0 ? hm.off[kext] : 0;
-  // stage the rows: element e = (r, a) of the block's [rows x A1] slice
-  // (the block's rows are contiguous in every source), in groups of kGrp
-  // elements per thread whose loads are all issued before their LDS stores
+  const int r = t & (kRtRows - 1), w0 = t / kRtRows;
+  // the per-row inputs are loaded first, so their latency overlaps the
+  // staging below: the taken action and mask of each head this lane takes
+  // (heads w0, w0 + 4, ...) and, for the row threads, logp_old, A and R
+  constexpr int kHpl = kMaxHeads / (kRtThreads / kRtRows);  // heads per lane
+  // (every load here and in the staging is unconditional, its index clamped
+  // into range, so none waits behind a branch; values of clamped indices
+  // are never used)
+  int act_r[kHpl];
+  uint32_t mk_r[kHpl];
   {
-    constexpr int kGrp = 8;
+    const int rc = min(r, rows - 1);
+    const uint8_t* mp = mask != nullptr ? mask : &kMaskOn;
+    const size_t ms = mask != nullptr ? 1 : 0;
+#pragma unroll
+    for (int i = 0; i < kHpl; ++i) {
+      const size_t nk = static_cast<size_t>(n0 + rc) * K + min(w0 + i * (kRtThreads / kRtRows), K - 1);
+      act_r[i] = act[nk];
+      mk_r[i] = mp[nk * ms];
+    }
+  }
+  const int tc = n0 + min(t, rows - 1);
+  const float lpo_r = logp_old[tc], adv_r = adv[tc], ret_r = ret[tc];
+  // stage the rows: element e = (r, a) of the block's [rows x A1] slice
+  // (the block's rows are contiguous in every source), kGrp elements per
+  // thread at a time: the bias and split 0 of all of them, then each further
+  // split, each split's loads all issued before its adds (the sum is bias +
+  // split 0 + split 1 + ... in that order)
+  {
+    constexpr int kGrp = 16;
     const int ne = rows * A1;
     const float* zp = zpart + static_cast<size_t>(n0) * A1;
+    // (r, a) of e advances by (dr, dc) per kRtThreads elements
+    const int dr = kRtThreads / A1, dc = kRtThreads - dr * A1;
     for (int e0g = 0; e0g < ne; e0g += kGrp * kRtThreads) {
-      float v[kGrp];
+      const int r0 = (e0g + t) / A1, c0 = e0g + t - r0 * A1;
+      int ix[kGrp];
 #pragma unroll
-      for (int q = 0; q < kGrp; ++q) {
-        const int e = e0g + t + q * kRtThreads;
-        v[q] = 0.0f;
-        if (e < ne) {
-          float acc = bp[e % A1] + zp[e];
-          for (int s2 = 1; s2 < S; ++s2) acc += zp[s2 * sstride + e];
-          v[q] = acc;
+      for (int q = 0; q < kGrp; ++q) ix[q] = min(e0g + t + q * kRtThreads, ne - 1);
+      float v[kGrp], b[kGrp], w[kGrp];
+      {
+        int c = c0;
+#pragma unroll
+        for (int q = 0; q < kGrp; ++q) {
+          b[q] = bp[c];
+          c += dc;
+          if (c >= A1) c -= A1;
         }
+      }
+#pragma unroll
+      for (int q = 0; q < kGrp; ++q) v[q] = zp[ix[q]];
+      if (S > 1) {
+#pragma unroll
+        for (int q = 0; q < kGrp; ++q) w[q] = zp[sstride + ix[q]];
+      }
+      // (keeps the adds below every load above)
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int q = 0; q < kGrp; ++q) v[q] = b[q] + v[q];
+      if (S > 1) {
+#pragma unroll
+        for (int q = 0; q < kGrp; ++q) v[q] += w[q];
+      }
+      for (int s2 = 2; s2 < S; ++s2) {
+#pragma unroll
+        for (int q = 0; q < kGrp; ++q) w[q] = zp[s2 * sstride + ix[q]];
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < kGrp; ++q) v[q] += w[q];
       }
       // (the unit head's columns come from zext below, written by other
       // threads: no store here may race with those)
+      int rq = r0, c = c0;
 #pragma unroll
       for (int q = 0; q < kGrp; ++q) {
         const int e = e0g + t + q * kRtThreads;
-        if (e < ne) {
-          const int r = e / A1, a = e - r * A1;
-          if (a < e0 || a >= e0 + nke) zs[r][a] = v[q];
+        if (e < ne && (c < e0 || c >= e0 + nke)) zs[rq][c] = v[q];
+        rq += dr;
+        c += dc;
+        if (c >= A1) {
+          c -= A1;
+          ++rq;
         }
       }
     }
@@ -416,31 +474,57 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
   __syncthreads();
   // heads: wave w takes heads w, w + 4, ... of every row (lane = row): the
   // head's maximum, normaliser, mean logit and the taken action's
-  // log-probability, kept in LDS per (head, row)
-  const int r = t & (kRtRows - 1), w0 = t / kRtRows;
+  // log-probability, kept in LDS per (head, row).  A lane reads a head's
+  // columns kCh at a time, every read of a chunk issued before its first
+  // use (indices past the head repeat its last column and are not used), so
+  // a chunk waits on LDS once; the sums keep column order.
+  constexpr int kCh = 8;
   const bool all_av = avail == nullptr;  // uniform: no availability bytes read
+  auto chunk = [&](const float* z, const uint8_t* av, int o, int nk, int a0, float (&v)[kCh], bool (&ok)[kCh]) {
+#pragma unroll
+    for (int q = 0; q < kCh; ++q) {
+      const int a = o + min(a0 + q, nk - 1);
+      v[q] = z[a];
+      // (the byte is read either way, without a branch; it is only staged,
+      // and only counts, when availability is given)
+      ok[q] = (a0 + q < nk) & (all_av | (av[a] != 0));
+    }
+  };
   if (r < rows) {
-    const int n = n0 + r;
     const float* z = zs[r];
     const uint8_t* av = avs[r];
-    for (int k = w0; k < K; k += kRtThreads / kRtRows) {
+#pragma unroll
+    for (int i = 0; i < kHpl; ++i) {
+      const int k = w0 + i * (kRtThreads / kRtRows);
+      if (k >= K) continue;
       const int o = hm.off[k], nk = hm.off[k + 1] - o;
       float m = -INFINITY;
-      for (int a = 0; a < nk; ++a)
-        if (all_av || av[o + a]) m = fmaxf(m, z[o + a]);
+      for (int a0 = 0; a0 < nk; a0 += kCh) {
+        float v[kCh];
+        bool ok[kCh];
+        chunk(z, av, o, nk, a0, v, ok);
+#pragma unroll
+        for (int q = 0; q < kCh; ++q)
+          if (ok[q]) m = fmaxf(m, v[q]);
+      }
       float sum = 0.0f, sz = 0.0f;
-      for (int a = 0; a < nk; ++a)
-        if (all_av || av[o + a]) {
-          const float e = expf(z[o + a] - m);
-          sum += e;
-          sz += e * z[o + a];
-        }
+      for (int a0 = 0; a0 < nk; a0 += kCh) {
+        float v[kCh];
+        bool ok[kCh];
+        chunk(z, av, o, nk, a0, v, ok);
+#pragma unroll
+        for (int q = 0; q < kCh; ++q)
+          if (ok[q]) {
+            const float e = expf(v[q] - m);
+            sum += e;
+            sz += e * v[q];
+          }
+      }
       const bool some = sum > 0.0f;  // the maximum contributes e = 1
-      const bool mk = mask == nullptr || mask[static_cast<size_t>(n) * K + k] != 0;
       const float lse = some ? m + logf(sum) : 0.0f;
       const float zb = some ? sz / sum : 0.0f;
-      const int ak = act[static_cast<size_t>(n) * K + k];
-      const bool use = mk && some;
+      const int ak = act_r[i];
+      const bool use = mk_r[i] != 0 && some;
       float lp = 0.0f, en = 0.0f;
       if (use) {
         const int a_sel = min(max(ak, 0), nk - 1);
@@ -463,7 +547,6 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
   if (t < kRtRows) {
     float st[kStatCols] = {};
     if (t < rows) {
-      const int n = n0 + t;
       float* z = zs[t];
       float logpi = 0.0f, ent = 0.0f;
       for (int k = 0; k < K; ++k)
@@ -471,8 +554,8 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
           logpi += hd_lp[k][t];
           ent += hd_ent[k][t];
         }
-      const float Ad = adv[n], R = ret[n];
-      const float dlog = logpi - logp_old[n];
+      const float Ad = adv_r, R = ret_r;
+      const float dlog = logpi - lpo_r;
       const float ratio = expf(dlog);
       const float rc = fminf(fmaxf(ratio, 1.0f - clip_eps), 1.0f + clip_eps);
       const float surr = fminf(ratio * Ad, rc * Ad);
@@ -508,14 +591,23 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
       const int ak = hd_act[k][r];
       const bool use = hd_use[k][r] != 0;
       const float mx = hd_mx[k][r], inv = hd_inv[k][r], zbar = hd_zbar[k][r];
-      for (int a = 0; a < nk; ++a) {
-        float d = 0.0f;
-        if (use && (all_av || av[o + a])) {
-          const float p = expf(z[o + a] - mx) * inv;
-          const float onehot = a == ak ? 1.0f : 0.0f;
-          d = g_logpi * (onehot - p) + ent_scale * p * (z[o + a] - zbar);
+      // (the chunk's reads stay inside this head's columns, which only this
+      // lane writes)
+      for (int a0 = 0; a0 < nk; a0 += kCh) {
+        float v[kCh];
+        bool ok[kCh];
+        chunk(z, av, o, nk, a0, v, ok);
+#pragma unroll
+        for (int q = 0; q < kCh; ++q) {
+          const int a = a0 + q;
+          float d = 0.0f;
+          if (use && ok[q]) {
+            const float p = expf(v[q] - mx) * inv;
+            const float onehot = a == ak ? 1.0f : 0.0f;
+            d = g_logpi * (onehot - p) + ent_scale * p * (v[q] - zbar);
+          }
+          if (a < nk) z[o + a] = d;
         }
-        z[o + a] = d;
       }
     }
   }
@@ -556,10 +648,13 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
   const int W = A1 + kStatCols;
   for (int c = t; c < W; c += kRtThreads) {
     float v = 0.0f;
-    if (c < A1)
+    if (c < A1) {
+#pragma unroll 8
       for (int r = 0; r < rows; ++r) v += zs[r][c];
-    else
+    } else {
+#pragma unroll 8
       for (int r = 0; r < rows; ++r) v += st_red[c - A1][r];
+    }
     part[static_cast<size_t>(blockIdx.x) * W + c] = v;
   }
 }
