@@ -182,6 +182,20 @@ __device__ __forceinline__ void read(const char* as, const char* bs, int wm0, in
   read_rows<NB>(bs, wn0, lane, s, f.b);
 }
 
+// Fragment I alone of the same: A block I for I < MB, else B block I - MB.
+template <int I, int MB, int NB>
+__device__ __forceinline__ void read_one(const char* as, const char* bs, int wm0, int wn0, int lane, int s,
+                                         Frags<MB, NB>& f) {
+  const int c = s * 2 + (lane >> 5);
+  if constexpr (I < MB) {
+    const int r = wm0 + I * 32 + (lane & 31);
+    f.a[I] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(as + r * ROW_BYTES + slot(r, c) * 16));
+  } else {
+    const int r = wn0 + (I - MB) * 32 + (lane & 31);
+    f.b[I - MB] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(bs + r * ROW_BYTES + slot(r, c) * 16));
+  }
+}
+
 template <int MB, int NB>
 __device__ __forceinline__ void mfma_all(const Frags<MB, NB>& f, f32x16_t (&acc)[MB][NB]) {
 #pragma unroll
@@ -191,17 +205,21 @@ __device__ __forceinline__ void mfma_all(const Frags<MB, NB>& f, f32x16_t (&acc)
 }
 
 // The same MFMAs with the wave's copies of one A and one B tile (k0, stages
-// as and bs) spread evenly among them (the order is pinned by scheduling
-// barriers).
+// as and bs) spread evenly among them, and after each of the first MB + NB
+// MFMAs one LDS read of the next tile's first fragments (from na and nb into
+// nf; forward GEMM 446 against 451 us with those reads ahead of the MFMAs);
+// the order is pinned by scheduling barriers.
 template <typename E, int MB, int NB, int NCA, int NCB, bool TWO>
 __device__ __forceinline__ void mfma_copies(const Frags<MB, NB>& f, f32x16_t (&acc)[MB][NB],
                                             const Tile<E, NCA, TWO>& ta, const Tile<E, NCB, TWO>& tb, int k0a,
-                                            int k0b, uint32_t as, uint32_t bs, int wave) {
+                                            int k0b, uint32_t as, uint32_t bs, int wave, const char* na,
+                                            const char* nb, int wm0, int wn0, int lane, Frags<MB, NB>& nf) {
   constexpr int NQ = NCA + NCB;
   dma::unroll<0, MB * NB>([&](auto I) {
     constexpr int m = decltype(I)::value;
     constexpr int a = m / NB, b = m % NB;
     acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[a], f.b[b], acc[a][b], 0, 0, 0);
+    if constexpr (m < MB + NB) read_one<m>(na, nb, wm0, wn0, lane, 0, nf);
     // copies after MFMA m: those q with floor(q * MB * NB / NQ) == m
     dma::unroll<0, NQ>([&](auto J) {
       constexpr int q = decltype(J)::value;
@@ -305,11 +323,11 @@ __global__ void __launch_bounds__(kk::NT, 1)
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       dma::vm_wait<AHEAD>();
       dma::wave_barrier();
-      read(smem + aoff(r + 1), smem + boff(r + 1), wm0, wn0, lane, 0, f[0]);
       __builtin_amdgcn_sched_barrier(0);
-      // last k step of tile r; its stages refill with A tile r + NSA and B
-      // tile r + NSB
-      mfma_copies<E>(f[1], acc, ta, tb, (kt0 + r + NSA) * BK, (kt0 + r + NSB) * BK, l0 + ao, l0 + bo, wave);
+      // last k step of tile r, reading tile r + 1's first fragments; its
+      // stages refill with A tile r + NSA and B tile r + NSB
+      mfma_copies<E>(f[1], acc, ta, tb, (kt0 + r + NSA) * BK, (kt0 + r + NSB) * BK, l0 + ao, l0 + bo, wave,
+                     smem + aoff(r + 1), smem + boff(r + 1), wm0, wn0, lane, f[0]);
     }
     // the epilogue's own loads overlap the last tile's MFMAs (the wait
     // below covers them)
