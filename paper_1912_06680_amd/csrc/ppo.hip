@@ -367,6 +367,9 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
   __shared__ float hd_mx[kMaxHeads][kRtRows], hd_inv[kMaxHeads][kRtRows], hd_zbar[kMaxHeads][kRtRows];
   __shared__ float hd_lp[kMaxHeads][kRtRows], hd_ent[kMaxHeads][kRtRows], row_g[kRtRows];
   __shared__ int hd_act[kMaxHeads][kRtRows], hd_use[kMaxHeads][kRtRows];
+  // the byte the head loops read in place of an availability byte when no
+  // availability is given (avs is then never written)
+  __shared__ uint8_t av_all;
   const int t = threadIdx.x;
   const int n0 = blockIdx.x * kRtRows;
   const int rows = min(kRtRows, N - n0);
@@ -469,6 +472,8 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
         const int r = e / A, a = e - r * A;
         avs[r][a] = avail[static_cast<size_t>(n0) * A + e];
       }
+    } else if (t == 0) {
+      av_all = 1;
     }
   }
   __syncthreads();
@@ -485,9 +490,9 @@ __global__ void __launch_bounds__(kRtThreads) ppo_rows_t(
     for (int q = 0; q < kCh; ++q) {
       const int a = o + min(a0 + q, nk - 1);
       v[q] = z[a];
-      // (the byte is read either way, without a branch; it is only staged,
-      // and only counts, when availability is given)
-      ok[q] = (a0 + q < nk) & (all_av | (av[a] != 0));
+      // (a byte is read either way, without a branch: the column's, or
+      // av_all = 1 when no availability is given)
+      ok[q] = (a0 + q < nk) & (*(all_av ? &av_all : av + a) != 0);
     }
   };
   if (r < rows) {
