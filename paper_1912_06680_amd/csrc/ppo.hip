@@ -673,14 +673,29 @@ __global__ void __launch_bounds__(256) pair_weights_t(int A1, int A1p, int ldh, 
                                                       uint16_t* __restrict__ wT) {
   __shared__ uint16_t t[64][66];
   const int j0 = blockIdx.x * 64, k0 = blockIdx.y * 64;
-  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-    const int kk = e >> 6, jj = e & 63, k = k0 + kk, j = j0 + jj;
-    uint16_t v = 0;
-    if (k < A1)
-      v = Wp[static_cast<size_t>(k) * H + j];
-    else if (Wq != nullptr && k >= A1p && k < A1p + d)
-      v = Wq[static_cast<size_t>(k - A1p) * H + j];
-    t[kk][jj] = v;
+  // every load unconditional (rows outside both sources read row 0 of Wp
+  // and are replaced by 0), so all 16 of a thread's loads are in flight
+  // together
+  constexpr int kPer = 64 * 64 / 256;
+  const bool hasq = Wq != nullptr;
+  uint16_t v[kPer];
+  bool in[kPer];
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int e = threadIdx.x + 256 * i, kk = e >> 6, jj = e & 63, k = k0 + kk;
+    const bool inp = k < A1;
+    const bool inq = hasq & (k >= A1p) & (k < A1p + d);
+    in[i] = inp | inq;
+    const uint16_t* base = inq ? Wq : Wp;
+    const int row = inp ? k : inq ? k - A1p : 0;
+    v[i] = base[static_cast<size_t>(row) * H + j0 + jj];
+  }
+  // (keeps the LDS stores below every load above)
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int e = threadIdx.x + 256 * i;
+    t[e >> 6][e & 63] = in[i] ? v[i] : static_cast<uint16_t>(0);
   }
   __syncthreads();
   for (int e = threadIdx.x; e < 64 * 64; e += 256) {
