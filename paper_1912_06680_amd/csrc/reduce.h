@@ -5,6 +5,24 @@
 
 namespace o5 {
 
+// at(0) + at(1) + ... + at(n - 1), added in that order onto 0; the terms'
+// loads are issued eight at a time before their adds, so a run of eight
+// waits on memory once.
+template <class F>
+__device__ __forceinline__ float ordered_sum(int n, F&& at) {
+  float s = 0.0f;
+  int p = 0;
+  for (; p + 8 <= n; p += 8) {
+    float v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = at(p + q);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) s += v[q];
+  }
+  for (; p < n; ++p) s += at(p);
+  return s;
+}
+
 // part[c, n] = sum of src[r, n] over rows r in chunk c = [c*rows_per_chunk, ...).
 static __global__ void __launch_bounds__(256) colsum_chunks(int R, int N, int rows_per_chunk, const float* __restrict__ src,
                                                            float* __restrict__ part) {
@@ -12,18 +30,16 @@ static __global__ void __launch_bounds__(256) colsum_chunks(int R, int N, int ro
   if (n >= N) return;
   const int r0 = blockIdx.y * rows_per_chunk;
   const int r1 = min(R, r0 + rows_per_chunk);
-  float s = 0.0f;
-  for (int r = r0; r < r1; ++r) s += src[static_cast<size_t>(r) * N + n];
-  part[static_cast<size_t>(blockIdx.y) * N + n] = s;
+  const float* col = src + static_cast<size_t>(r0) * N + n;
+  part[static_cast<size_t>(blockIdx.y) * N + n] =
+      ordered_sum(r1 - r0, [&](int i) { return col[static_cast<size_t>(i) * N]; });
 }
 
 // out[n] = sum over the P rows of part (fixed order).
 static __global__ void __launch_bounds__(256) colsum_rows(int P, int N, const float* __restrict__ part, float* __restrict__ out) {
   const int n = blockIdx.x * blockDim.x + threadIdx.x;
   if (n >= N) return;
-  float s = 0.0f;
-  for (int p = 0; p < P; ++p) s += part[static_cast<size_t>(p) * N + n];
-  out[n] = s;
+  out[n] = ordered_sum(P, [&](int p) { return part[static_cast<size_t>(p) * N + n]; });
 }
 
 // out[n] = sum over the P rows of part for many rows and few columns: a
@@ -37,7 +53,7 @@ static __global__ void __launch_bounds__(256) colsum_rows4(int P, int N, const f
   const int n = blockIdx.x * 64 + c;
   float s = 0.0f;
   if (n < N)
-    for (int p = g; p < P; p += 4) s += part[static_cast<size_t>(p) * N + n];
+    s = ordered_sum((P - g + 3) / 4, [&](int i) { return part[static_cast<size_t>(g + 4 * i) * N + n]; });
   red[g][c] = s;
   __syncthreads();
   if (g == 0 && n < N) out[n] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
@@ -51,9 +67,8 @@ static __global__ void __launch_bounds__(256) colsum_tree(int P, int N, const fl
                                                         float* __restrict__ out) {
   __shared__ float red[256];
   const int n = blockIdx.x;
-  float s = 0.0f;
-  for (int p = threadIdx.x; p < P; p += 256) s += part[static_cast<size_t>(p) * N + n];
-  red[threadIdx.x] = s;
+  const int t = threadIdx.x;
+  red[t] = ordered_sum((P - t + 255) / 256, [&](int i) { return part[static_cast<size_t>(t + 256 * i) * N + n]; });
   __syncthreads();
   for (int w = 128; w > 0; w >>= 1) {
     if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
