@@ -163,16 +163,19 @@ struct Frags {
   bf16x8_t a[MB], b[NB];
 };
 
-// Fragments of k step s (16 k) for NBLK 32-row blocks from row0: lane l holds
-// row (l & 31) of each block and the 8 k values 8 * (l >> 5) .. + 7.
+// The fragment of k step s (16 k) for the 32-row block at row0: lane l holds
+// row row0 + (l & 31) and the 8 k values 8 * (l >> 5) .. + 7 of the step.
+__device__ __forceinline__ bf16x8_t read_frag(const char* stage, int row0, int lane, int s) {
+  const int c = s * 2 + (lane >> 5);
+  const int r = row0 + (lane & 31);
+  return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(stage + r * ROW_BYTES + slot(r, c) * 16));
+}
+
+// The same for NBLK 32-row blocks from row0.
 template <int NBLK>
 __device__ __forceinline__ void read_rows(const char* stage, int row0, int lane, int s, bf16x8_t (&f)[NBLK]) {
-  const int c = s * 2 + (lane >> 5);
 #pragma unroll
-  for (int b = 0; b < NBLK; ++b) {
-    const int r = row0 + b * 32 + (lane & 31);
-    f[b] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(stage + r * ROW_BYTES + slot(r, c) * 16));
-  }
+  for (int b = 0; b < NBLK; ++b) f[b] = read_frag(stage, row0 + b * 32, lane, s);
 }
 
 template <int MB, int NB>
@@ -186,14 +189,10 @@ __device__ __forceinline__ void read(const char* as, const char* bs, int wm0, in
 template <int I, int MB, int NB>
 __device__ __forceinline__ void read_one(const char* as, const char* bs, int wm0, int wn0, int lane, int s,
                                          Frags<MB, NB>& f) {
-  const int c = s * 2 + (lane >> 5);
-  if constexpr (I < MB) {
-    const int r = wm0 + I * 32 + (lane & 31);
-    f.a[I] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(as + r * ROW_BYTES + slot(r, c) * 16));
-  } else {
-    const int r = wn0 + (I - MB) * 32 + (lane & 31);
-    f.b[I - MB] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(bs + r * ROW_BYTES + slot(r, c) * 16));
-  }
+  if constexpr (I < MB)
+    f.a[I] = read_frag(as, wm0 + I * 32, lane, s);
+  else
+    f.b[I - MB] = read_frag(bs, wn0 + (I - MB) * 32, lane, s);
 }
 
 template <int MB, int NB>

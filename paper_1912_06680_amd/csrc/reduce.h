@@ -71,10 +71,10 @@ static __global__ void __launch_bounds__(256) colsum_tree(int P, int N, const fl
   red[t] = ordered_sum((P - t + 255) / 256, [&](int i) { return part[static_cast<size_t>(t + 256 * i) * N + n]; });
   __syncthreads();
   for (int w = 128; w > 0; w >>= 1) {
-    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    if (t < w) red[t] += red[t + w];
     __syncthreads();
   }
-  if (threadIdx.x == 0) out[n] = red[0];
+  if (t == 0) out[n] = red[0];
 }
 
 // ------------------------------------------------------ wave reductions

@@ -48,7 +48,7 @@ __device__ __forceinline__ void load8(const float* p, float (&f)[8]) {
 // z[n, u] = sum_j (q[n, j] + bq[j]) E[n, u, j]: per-chunk partial sums, then
 // a butterfly over the unit's C lanes.
 template <typename E>
-__global__ void __launch_bounds__(256) unit_logits(int N, int nk, int d, const float* __restrict__ q,
+__global__ void __launch_bounds__(256) unit_logits(int nk, int d, const float* __restrict__ q,
                                                    const float* __restrict__ bq, const E* __restrict__ emb,
                                                    float* __restrict__ z) {
   const int n = blockIdx.x;
@@ -78,7 +78,7 @@ __global__ void __launch_bounds__(256) unit_logits(int N, int nk, int d, const f
 // chunk over the units it visits, then the 256 / C threads of a chunk are
 // summed in order through LDS.
 template <typename E>
-__global__ void __launch_bounds__(256) unit_dq(int N, int nk, int d, const float* __restrict__ dz,
+__global__ void __launch_bounds__(256) unit_dq(int nk, int d, const float* __restrict__ dz,
                                                const E* __restrict__ emb, float* __restrict__ dq) {
   __shared__ float red[256][9];
   const int n = blockIdx.x;
@@ -202,13 +202,13 @@ void unit_forward(o5_dtype dt, int N, int H, int nk, const o5_unit_head& u, cons
     KRows2<uint16_t> al{static_cast<const uint16_t*>(h), nullptr, nullptr, H, 0, H, H, N};
     KRows2<uint16_t> bl{static_cast<const uint16_t*>(u.Wq), nullptr, nullptr, H, 0, H, H, d};
     run_gemm(plan, al, bl, EpiStoreF32{q, d, 0}, N, d, H, s);
-    hipLaunchKernelGGL(unit_logits<uint16_t>, grid, dim3(256), 0, s, N, nk, d, q, u.bq,
+    hipLaunchKernelGGL(unit_logits<uint16_t>, grid, dim3(256), 0, s, nk, d, q, u.bq,
                        static_cast<const uint16_t*>(u.E), zext);
   } else {
     KRows2<float> al{static_cast<const float*>(h), nullptr, nullptr, H, 0, H, H, N};
     KRows2<float> bl{static_cast<const float*>(u.Wq), nullptr, nullptr, H, 0, H, H, d};
     run_gemm(plan, al, bl, EpiStoreF32{q, d, 0}, N, d, H, s);
-    hipLaunchKernelGGL(unit_logits<float>, grid, dim3(256), 0, s, N, nk, d, q, u.bq, static_cast<const float*>(u.E),
+    hipLaunchKernelGGL(unit_logits<float>, grid, dim3(256), 0, s, nk, d, q, u.bq, static_cast<const float*>(u.E),
                        zext);
   }
 }
@@ -221,10 +221,10 @@ void unit_grad(o5_dtype dt, int N, int H, int nk, const o5_unit_head& u, const v
   float* wpart = reinterpret_cast<float*>(ws + w.wpart);
   const int d = w.d, dp = w.dp;
   if (dt == O5_BF16)
-    hipLaunchKernelGGL(unit_dq<uint16_t>, dim3(N), dim3(256), 0, s, N, nk, d, dzext, static_cast<const uint16_t*>(u.E),
+    hipLaunchKernelGGL(unit_dq<uint16_t>, dim3(N), dim3(256), 0, s, nk, d, dzext, static_cast<const uint16_t*>(u.E),
                        dq);
   else
-    hipLaunchKernelGGL(unit_dq<float>, dim3(N), dim3(256), 0, s, N, nk, d, dzext, static_cast<const float*>(u.E), dq);
+    hipLaunchKernelGGL(unit_dq<float>, dim3(N), dim3(256), 0, s, nk, d, dzext, static_cast<const float*>(u.E), dq);
   // dbq: fixed-order column sums of dq (chunks of 64 rows, then a block per
   // column over the chunk sums: dq is narrow, so a thread per column alone
   // would walk too many rows)
